@@ -1,0 +1,183 @@
+/*
+ * conv2d.h -- C ABI of the MI355X (gfx950) conv2d forward library.
+ *
+ * The library computes the 2D convolution forward primitive that ConvBench
+ * benchmarks (Sec. I, Sec. III-B: the Conv2d layers of TIMM / torchvision
+ * models, with stride, zero padding, dilation, groups and rectangular
+ * filters), on one GPU, with three algorithm families and a per-phase time
+ * breakdown in the nomenclature of ConvBench's timing tool (Sec. III-A):
+ *
+ *   y[n,k,ho,wo] = b[k] + sum_{c<C/g, r<R, s<S}
+ *                  x[n, gi*C/g + c, ho*sh - ph + r*dh, wo*sw - pw + s*dw] * w[k,c,r,s]
+ *   gi = k / (K/g); taps outside the input read zero (no filter flip);
+ *   Ho = floor((H + 2*ph - dh*(R-1) - 1)/sh) + 1, likewise Wo.
+ *
+ * Conventions for every function below:
+ *   - The return value is a status: CONV2D_OK (0) or a negative CONV2D_E_*.
+ *     No function aborts or prints.
+ *   - Device pointers (x, w, bias, y) are owned by the caller, must stay valid
+ *     until the work queued on `stream` has finished, and hold dense,
+ *     contiguous tensors in the layouts stated below.
+ *   - `stream` is a hipStream_t passed as void*; NULL means the null stream.
+ *   - A descriptor must not be used by two host threads at once; distinct
+ *     descriptors are independent.
+ */
+#ifndef CONV2D_H
+#define CONV2D_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+enum {
+    CONV2D_OK = 0,
+    CONV2D_E_INVALID = -1,     /* a parameter is out of range (dims < 1, C % g != 0, ...) */
+    CONV2D_E_SHAPE = -2,       /* the filter window does not fit: Ho < 1 or Wo < 1 */
+    CONV2D_E_UNSUPPORTED = -3, /* valid convolution, but this dtype / layout / algo / size is not offered */
+    CONV2D_E_NULL = -4,        /* a required pointer is NULL */
+    CONV2D_E_ALLOC = -5,       /* workspace could not be allocated within the limit */
+    CONV2D_E_HIP = -6,         /* a HIP runtime call or kernel launch failed */
+    CONV2D_E_NO_DATA = -7      /* breakdown requested before any timed call */
+};
+
+/* Layout of x and y.  w is always K x C/g x R x S (row-major). */
+enum { CONV2D_NCHW = 0, CONV2D_NHWC = 1 };
+
+/* Element types.  x and w share a type; bias is always fp32. */
+enum { CONV2D_F32 = 0, CONV2D_BF16 = 1 };
+
+/* Algorithm families (ConvBench's main and baseline methods, Sec. III-C). */
+enum {
+    CONV2D_ALGO_AUTO = 0,          /* planner's choice */
+    CONV2D_ALGO_IMPLICIT_GEMM = 1, /* sliced direct convolution: im2col slices gathered into LDS, MFMA */
+    CONV2D_ALGO_IM2COL_GEMM = 2,   /* explicit im2col pack, MFMA GEMM, unpack (ConvBench's default baseline) */
+    CONV2D_ALGO_DIRECT = 3,        /* direct VALU kernel for depthwise / small-group convolutions */
+    CONV2D_ALGO_COUNT = 4
+};
+
+/* Processing steps of the timing tool (Sec. III-A): pre-convolution analysis and
+ * reordering; in-convolution tiling, packing, microkernel and unpacking;
+ * post-convolution reordering. */
+enum {
+    CONV2D_PH_PRE_ANALYSIS = 0,
+    CONV2D_PH_PRE_REORDER = 1,
+    CONV2D_PH_IN_TILING = 2,
+    CONV2D_PH_IN_PACKING = 3,
+    CONV2D_PH_IN_MICROKERNEL = 4,
+    CONV2D_PH_IN_UNPACKING = 5,
+    CONV2D_PH_POST_REORDER = 6,
+    CONV2D_PH_COUNT = 7
+};
+
+/* Timing modes of a descriptor.  OFF records nothing; TOTAL records one
+ * event pair around each conv2d_fwd (Operation Time only); PHASES records one
+ * event pair around every phase launch.  The initial mode comes from the
+ * environment variable CONV2D_TIMING = off | total | phases (default: phases). */
+enum { CONV2D_TIMING_OFF = 0, CONV2D_TIMING_TOTAL = 1, CONV2D_TIMING_PHASES = 2 };
+
+typedef struct conv2d_desc conv2d_desc; /* opaque, owned by the library */
+
+/* One convolution.  n,c,h,w: input dims; k: output channels; r,s: filter
+ * height and width.  Padding is symmetric zero padding (pad_h rows above and
+ * below, pad_w columns left and right).  has_bias != 0 means a K-element fp32
+ * bias is added once per output channel. */
+typedef struct {
+    int64_t n, c, h, w, k, r, s;
+    int32_t stride_h, stride_w, pad_h, pad_w, dil_h, dil_w, groups;
+    int32_t layout;   /* CONV2D_NCHW or CONV2D_NHWC, for x and y */
+    int32_t x_dtype;  /* CONV2D_F32 or CONV2D_BF16; the type of x and w */
+    int32_t y_dtype;  /* CONV2D_F32, or CONV2D_BF16 when x_dtype is BF16 */
+    int32_t has_bias;
+} conv2d_params;
+
+/* Accumulated phase times of one algorithm on one descriptor.  ms[p] is the
+ * summed GPU time (hipEvent) of phase p over `calls[p]` launches, except
+ * PRE_ANALYSIS, which is the host time of conv2d_desc_create (calls = 1).
+ * fused_mask has bit p set when phase p runs inside another phase's kernel
+ * (its time is included there).  operation_ms is the sum of all phases
+ * (the timing tool's Operation Time); convolution_ms is the sum of the
+ * in-convolution phases (its Convolution Time).  pack_is_preconv = 1 marks
+ * that the explicit path's im2col is booked as IN_PACKING although the paper
+ * also calls it a pre-convolution reordering.  total_ms / total_calls hold
+ * the event pairs of TIMING_TOTAL mode (whole conv2d_fwd calls). */
+typedef struct {
+    double ms[CONV2D_PH_COUNT];
+    int64_t calls[CONV2D_PH_COUNT];
+    uint32_t fused_mask;
+    int32_t algo;
+    int32_t pack_is_preconv;
+    int64_t fwd_calls;
+    double operation_ms;
+    double convolution_ms;
+    double total_ms;
+    int64_t total_calls;
+} conv2d_breakdown_t;
+
+/* What the planner decided for one algorithm (for reports and tests). */
+typedef struct {
+    int32_t algo;             /* resolved algorithm (never AUTO) */
+    int32_t tile_m, tile_n;   /* GEMM block tile (output channels x output pixels); 0 for DIRECT */
+    int32_t kred, kred_pad;   /* reduction length (C/g)*R*S and its padded length */
+    int64_t workspace_bytes;  /* device workspace this algorithm uses per chunk */
+    int64_t chunks;           /* explicit path: number of pack/GEMM/unpack chunks */
+    int32_t needs_reorder;    /* 1 when pre/post layout reorders run (NHWC through an NCHW kernel) */
+    int32_t op_class;         /* bit 0 pointwise, 1 grouped, 2 depthwise, 3 dilated, 4 rectangular, 5 strided */
+} conv2d_plan_info;
+
+/* Validate params, compute the output size, classify the operation and plan
+ * every algorithm (operation analysis, Sec. III-A).  Host only: needs no GPU.
+ * On success *out receives a new descriptor.  Errors: E_NULL, E_INVALID,
+ * E_SHAPE, E_UNSUPPORTED (fp32 x with bf16 y, unknown layout/dtype). */
+int conv2d_desc_create(const conv2d_params* params, conv2d_desc** out);
+
+/* Free the descriptor, its events and its workspace.  Waits for nothing:
+ * the caller must make sure no work using it is still queued.  NULL is OK. */
+int conv2d_desc_destroy(conv2d_desc* desc);
+
+/* out_nkhw = {N, K, Ho, Wo} (logical dims; the memory layout is the
+ * descriptor's layout). */
+int conv2d_output_shape(const conv2d_desc* desc, int64_t out_nkhw[4]);
+
+/* Queue one forward convolution on `stream` and return without waiting.
+ *   x    : N x C x H x W (NCHW) or N x H x W x C (NHWC), x_dtype
+ *   w    : K x C/g x R x S, x_dtype
+ *   bias : K floats, or NULL when has_bias == 0 (ignored then)
+ *   y    : N x K x Ho x Wo (NCHW) or N x Ho x Wo x K (NHWC), y_dtype
+ *   algo : CONV2D_ALGO_*; AUTO lets the planner choose.
+ * Errors: E_NULL (x, w, y or a required bias missing), E_INVALID (bad algo),
+ * E_UNSUPPORTED (algo cannot run this op), E_ALLOC (explicit path workspace
+ * over CONV2D_WORKSPACE_LIMIT_BYTES, default 1 GiB, even after chunking),
+ * E_HIP (a launch failed).  Faults inside kernels surface at the next
+ * synchronisation.  Results are bitwise reproducible for a fixed algo. */
+int conv2d_fwd(conv2d_desc* desc, const void* x, const void* w, const float* bias, void* y,
+               int algo, void* stream);
+
+/* Synchronise on the descriptor's recorded events, fold them into the
+ * per-algorithm totals and copy the totals of `algo` (AUTO: the algorithm
+ * of the last conv2d_fwd) into *out.  E_NO_DATA when that algorithm has never
+ * been run. */
+int conv2d_breakdown(conv2d_desc* desc, int algo, conv2d_breakdown_t* out);
+
+/* Discard all accumulated phase times (PRE_ANALYSIS is kept). */
+int conv2d_breakdown_reset(conv2d_desc* desc);
+
+/* Set the timing mode (CONV2D_TIMING_*).  Pending events are folded first. */
+int conv2d_set_timing(conv2d_desc* desc, int mode);
+
+/* Planner decisions for `algo` (AUTO: the algorithm AUTO resolves to). */
+int conv2d_plan_query(const conv2d_desc* desc, int algo, conv2d_plan_info* out);
+
+/* Static text for a status code; never NULL. */
+const char* conv2d_status_string(int status);
+
+/* Version of the HIP runtime this library is bound to (hipRuntimeGetVersion). */
+int conv2d_runtime_version(int* hip_runtime_version);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CONV2D_H */

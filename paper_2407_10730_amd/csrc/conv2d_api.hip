@@ -1,0 +1,692 @@
+// conv2d_api.hip -- C ABI, planner, dispatcher and phase timer of the conv2d library.
+//
+// The planner is the library's "operation analysis" step (Sec. III-A, a
+// pre-convolution routine): it validates the operation, derives the output
+// size, classifies it the way the paper's operation set is described
+// (pointwise, grouped, dilated, rectangular, regular; Sec. III-B), chooses the
+// algorithm and GEMM tile, builds the per-reduction-index tap table used by
+// both GEMM paths, and sizes the explicit path's workspace.  Its host time is
+// booked once per descriptor as PRE_ANALYSIS.
+//
+// The timer mirrors the paper's timing tool (Sec. III-A): every phase launch
+// is enclosed by a pair of HIP events on the caller's stream; elapsed time and
+// call counts accumulate per phase and per algorithm; Operation Time is the
+// sum of all phases and Convolution Time the sum of the in-convolution ones.
+#include <algorithm>
+#include <chrono>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "conv2d_internal.h"
+
+using namespace cv;
+
+namespace {
+
+constexpr int64_t kBufferLimit = 0x7fffffffLL;  // raw buffer offsets are 32-bit; keep tensors below 2 GiB
+
+struct PhaseAcc {
+    double ms[CONV2D_PH_COUNT];
+    int64_t calls[CONV2D_PH_COUNT];
+    int64_t fwd_calls;
+    double total_ms;
+    int64_t total_calls;
+    bool used;
+};
+
+struct EvRec {
+    int algo;
+    int phase;  // -1: whole-call pair of TIMING_TOTAL
+    hipEvent_t a, b;
+};
+
+struct GemmPlan {
+    int tile = TILE_64x128;
+    int bm = 64, bn = 128;
+    int nstages = 0;
+};
+
+struct ExplicitPlan {
+    GemmPlan gemm;
+    int64_t rows_per_chunk = 0;  // rows of the (n, ho) output grid per chunk
+    int64_t chunks = 0;
+    int64_t col_bytes = 0;       // per chunk
+    int64_t c_bytes = 0;         // per chunk
+    int status = CONV2D_OK;
+};
+
+int64_t elem_size(int dt) { return dt == CONV2D_BF16 ? 2 : 4; }
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+int64_t env_int64(const char* name, int64_t dflt) {
+    const char* s = std::getenv(name);
+    if (!s || !*s) return dflt;
+    char* end = nullptr;
+    long long v = std::strtoll(s, &end, 10);
+    if (end == s) return dflt;
+    return (int64_t)v;
+}
+
+int env_timing() {
+    const char* s = std::getenv("CONV2D_TIMING");
+    if (!s) return CONV2D_TIMING_PHASES;
+    if (!std::strcmp(s, "off")) return CONV2D_TIMING_OFF;
+    if (!std::strcmp(s, "total")) return CONV2D_TIMING_TOTAL;
+    return CONV2D_TIMING_PHASES;
+}
+
+// Choose the GEMM block tile: fewest rounds of full-chip tile waves, weighted by
+// the MFMA efficiency of each wave tile (64x64 per wave is the reference).
+GemmPlan choose_tile(int64_t M, int64_t P, int64_t G, int64_t kred, int xdt) {
+    struct Cand { int tile; double eff; };
+    const Cand cands[] = {{TILE_64x256, 1.0}, {TILE_128x128, 1.0}, {TILE_64x128, 0.85},
+                          {TILE_128x64, 0.85}, {TILE_64x64, 0.7}};
+    const int cus = 256;
+    GemmPlan best;
+    double best_cost = 1e300;
+    for (const Cand& c : cands) {
+        const TileShape ts = kTileShapes[c.tile];
+        const int64_t tiles = ceil_div(M, ts.bm) * ceil_div(P, ts.bn) * G;
+        const double rounds = (double)ceil_div(tiles, cus);
+        const double cost = rounds * ts.bm * ts.bn / c.eff;
+        if (cost < best_cost) {
+            best_cost = cost;
+            best.tile = c.tile;
+            best.bm = ts.bm;
+            best.bn = ts.bn;
+        }
+    }
+    const int bk = xdt == CONV2D_BF16 ? 32 : 16;
+    best.nstages = (int)ceil_div(kred, bk);
+    return best;
+}
+
+}  // namespace
+
+struct conv2d_desc {
+    conv2d_params prm;
+    Geometry g;
+    uint32_t opclass = 0;
+    int auto_algo = CONV2D_ALGO_IMPLICIT_GEMM;
+    bool implicit_ok = false, direct_ok = false;
+    GemmPlan implicit;
+    ExplicitPlan expl;
+    std::vector<KTabEntry> ktab_host;
+
+    int device = -1;
+    KTabEntry* ktab_dev = nullptr;
+    void* ws = nullptr;
+    int64_t ws_bytes = 0;
+    void* xr = nullptr;  // NCHW copy of an NHWC input
+    int64_t xr_bytes = 0;
+    void* yr = nullptr;  // NCHW result before the NHWC reorder
+    int64_t yr_bytes = 0;
+
+    int timing = CONV2D_TIMING_PHASES;
+    double analysis_ms = 0.0;
+    PhaseAcc acc[CONV2D_ALGO_COUNT];
+    int last_algo = -1;
+    std::vector<hipEvent_t> free_events;
+    std::vector<EvRec> pending;
+};
+
+namespace {
+
+int validate(const conv2d_params* p, Geometry* g) {
+    if (p->n < 1 || p->c < 1 || p->h < 1 || p->w < 1 || p->k < 1 || p->r < 1 || p->s < 1)
+        return CONV2D_E_INVALID;
+    if (p->stride_h < 1 || p->stride_w < 1 || p->dil_h < 1 || p->dil_w < 1) return CONV2D_E_INVALID;
+    if (p->pad_h < 0 || p->pad_w < 0 || p->groups < 1) return CONV2D_E_INVALID;
+    if (p->c % p->groups || p->k % p->groups) return CONV2D_E_INVALID;
+    if (p->layout != CONV2D_NCHW && p->layout != CONV2D_NHWC) return CONV2D_E_INVALID;
+    if (p->x_dtype != CONV2D_F32 && p->x_dtype != CONV2D_BF16) return CONV2D_E_INVALID;
+    if (p->y_dtype != CONV2D_F32 && p->y_dtype != CONV2D_BF16) return CONV2D_E_INVALID;
+    if (p->x_dtype == CONV2D_F32 && p->y_dtype == CONV2D_BF16) return CONV2D_E_UNSUPPORTED;
+    // window extents: the last window start must lie inside the padded input
+    const int64_t span_h = p->h + 2 * (int64_t)p->pad_h - (int64_t)p->dil_h * (p->r - 1) - 1;
+    const int64_t span_w = p->w + 2 * (int64_t)p->pad_w - (int64_t)p->dil_w * (p->s - 1) - 1;
+    if (span_h < 0 || span_w < 0) return CONV2D_E_SHAPE;
+    Geometry& G = *g;
+    G.N = p->n; G.C = p->c; G.H = p->h; G.W = p->w; G.K = p->k; G.R = p->r; G.S = p->s;
+    G.sh = p->stride_h; G.sw = p->stride_w; G.ph = p->pad_h; G.pw = p->pad_w;
+    G.dh = p->dil_h; G.dw = p->dil_w; G.G = p->groups;
+    G.Ho = span_h / p->stride_h + 1;
+    G.Wo = span_w / p->stride_w + 1;
+    G.Cg = p->c / p->groups;
+    G.Kg = p->k / p->groups;
+    G.Kred = G.Cg * G.R * G.S;
+    G.P = G.N * G.Ho * G.Wo;
+    G.layout = p->layout; G.xdt = p->x_dtype; G.ydt = p->y_dtype; G.has_bias = p->has_bias ? 1 : 0;
+    G.x_elems = G.N * G.C * G.H * G.W;
+    G.w_elems = G.K * G.Kred;
+    G.y_elems = G.N * G.K * G.Ho * G.Wo;
+    return CONV2D_OK;
+}
+
+uint32_t classify(const Geometry& g) {
+    uint32_t c = 0;
+    if (g.R == 1 && g.S == 1) c |= OPC_POINTWISE;
+    if (g.G > 1) c |= OPC_GROUPED;
+    if (g.G > 1 && g.Cg == 1) c |= OPC_DEPTHWISE;
+    if (g.dh > 1 || g.dw > 1) c |= OPC_DILATED;
+    if (g.R != g.S) c |= OPC_RECTANGULAR;
+    if (g.sh > 1 || g.sw > 1) c |= OPC_STRIDED;
+    return c;
+}
+
+void build_ktab(conv2d_desc* d) {
+    const Geometry& g = d->g;
+    const int64_t len = ceil_div(g.Kred, KTAB_ALIGN) * KTAB_ALIGN;
+    d->ktab_host.assign((size_t)len, KTabEntry{0, KTAB_DEAD, 0, 0});
+    int64_t kr = 0;
+    for (int64_t c = 0; c < g.Cg; ++c)
+        for (int64_t r = 0; r < g.R; ++r)
+            for (int64_t s = 0; s < g.S; ++s, ++kr) {
+                KTabEntry& e = d->ktab_host[(size_t)kr];
+                e.roff = (int32_t)(r * g.dh);
+                e.soff = (int32_t)(s * g.dw);
+                e.coff = (int32_t)(c * g.H * g.W + e.roff * g.W + e.soff);
+                e.pad = 0;
+            }
+}
+
+void plan_explicit(conv2d_desc* d) {
+    const Geometry& g = d->g;
+    ExplicitPlan& e = d->expl;
+    const int64_t xs = elem_size(g.xdt);
+    const int64_t row_col = g.Wo * g.G * g.Kred * xs;  // col bytes of one output row (all groups)
+    const int64_t row_c = g.Wo * g.G * g.Kg * 4;        // GEMM result bytes of one output row
+    int64_t cap = env_int64("CONV2D_WORKSPACE_LIMIT_BYTES", (int64_t)1 << 30);
+    if (cap < 0) cap = 0;
+    const int64_t total_rows = g.N * g.Ho;
+    int64_t rows = cap / (row_col + row_c);
+    rows = std::min<int64_t>(rows, kBufferLimit / row_col);
+    rows = std::min<int64_t>(rows, kBufferLimit / row_c);
+    rows = std::min<int64_t>(rows, total_rows);
+    if (rows < 1) {
+        e.status = CONV2D_E_ALLOC;
+        e.rows_per_chunk = 0;
+        e.chunks = 0;
+        return;
+    }
+    e.status = CONV2D_OK;
+    e.rows_per_chunk = rows;
+    e.chunks = ceil_div(total_rows, rows);
+    e.col_bytes = rows * row_col;
+    e.c_bytes = rows * row_c;
+    e.gemm = choose_tile(g.Kg, rows * g.Wo, g.G, g.Kred, g.xdt);
+}
+
+// ------------------------------------------------------------------ events
+hipError_t get_event(conv2d_desc* d, hipEvent_t* ev) {
+    if (!d->free_events.empty()) {
+        *ev = d->free_events.back();
+        d->free_events.pop_back();
+        return hipSuccess;
+    }
+    return hipEventCreate(ev);
+}
+
+int harvest(conv2d_desc* d) {
+    int st = CONV2D_OK;
+    for (const EvRec& r : d->pending) {
+        float ms = 0.0f;
+        if (hipEventSynchronize(r.b) != hipSuccess || hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) {
+            st = CONV2D_E_HIP;
+        } else {
+            PhaseAcc& a = d->acc[r.algo];
+            if (r.phase < 0) {
+                a.total_ms += ms;
+                a.total_calls += 1;
+            } else {
+                a.ms[r.phase] += ms;
+                a.calls[r.phase] += 1;
+            }
+        }
+        d->free_events.push_back(r.a);
+        d->free_events.push_back(r.b);
+    }
+    d->pending.clear();
+    return st;
+}
+
+// Encloses one phase launch (PHASES mode) or a whole call (TOTAL mode).
+struct Scope {
+    conv2d_desc* d;
+    int algo, phase;
+    hipStream_t s;
+    hipEvent_t a = nullptr;
+    bool active;
+    Scope(conv2d_desc* d_, int algo_, int phase_, hipStream_t s_, bool active_)
+        : d(d_), algo(algo_), phase(phase_), s(s_), active(active_) {}
+    ~Scope() {
+        if (a) d->free_events.push_back(a);  // an error path left the pair open
+    }
+    int begin() {
+        if (!active) return CONV2D_OK;
+        if (get_event(d, &a) != hipSuccess || hipEventRecord(a, s) != hipSuccess) return CONV2D_E_HIP;
+        return CONV2D_OK;
+    }
+    int end() {
+        if (!active || !a) return CONV2D_OK;
+        hipEvent_t b = nullptr;
+        if (get_event(d, &b) != hipSuccess || hipEventRecord(b, s) != hipSuccess) return CONV2D_E_HIP;
+        d->pending.push_back(EvRec{algo, phase, a, b});
+        a = nullptr;
+        return CONV2D_OK;
+    }
+};
+
+// ------------------------------------------------------------------ device resources
+int ensure_device(conv2d_desc* d, hipStream_t s) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return CONV2D_E_HIP;
+    if (d->device >= 0 && d->device != dev) return CONV2D_E_UNSUPPORTED;
+    if (d->device < 0) {
+        d->device = dev;
+        const size_t bytes = d->ktab_host.size() * sizeof(KTabEntry);
+        if (hipMalloc(&d->ktab_dev, bytes) != hipSuccess) {
+            d->ktab_dev = nullptr;
+            d->device = -1;
+            return CONV2D_E_ALLOC;
+        }
+        if (hipMemcpyAsync(d->ktab_dev, d->ktab_host.data(), bytes, hipMemcpyHostToDevice, s) != hipSuccess)
+            return CONV2D_E_HIP;
+    }
+    return CONV2D_OK;
+}
+
+int ensure_buffer(void** buf, int64_t* have, int64_t need) {
+    if (*have >= need) return CONV2D_OK;
+    if (*buf) {
+        // the old buffer may still be read by queued work
+        if (hipDeviceSynchronize() != hipSuccess) return CONV2D_E_HIP;
+        hipFree(*buf);
+        *buf = nullptr;
+        *have = 0;
+    }
+    if (hipMalloc(buf, (size_t)need) != hipSuccess) {
+        *buf = nullptr;
+        return CONV2D_E_ALLOC;
+    }
+    *have = need;
+    return CONV2D_OK;
+}
+
+#define CV_TRY(expr)                 \
+    do {                             \
+        int _st = (expr);            \
+        if (_st != CONV2D_OK) return _st; \
+    } while (0)
+
+#define CV_HIP(expr)                                   \
+    do {                                               \
+        if ((expr) != hipSuccess) return CONV2D_E_HIP; \
+    } while (0)
+
+// ------------------------------------------------------------------ algorithms (NCHW tensors)
+int run_implicit(conv2d_desc* d, const void* x, const void* w, const float* bias, void* y, hipStream_t s,
+                 bool ph) {
+    const Geometry& g = d->g;
+    const GemmPlan& gp = d->implicit;
+    GemmArgs a{};
+    a.a = w;
+    a.a_bytes = (uint32_t)(g.w_elems * elem_size(g.xdt));
+    a.lda = (int32_t)g.Kred;
+    a.a_gstride = g.Kg * g.Kred;
+    a.b = x;
+    a.b_bytes = (uint32_t)(g.x_elems * elem_size(g.xdt));
+    a.b_gstride = g.Cg * g.H * g.W;
+    a.ktab = d->ktab_dev;
+    a.H = (int32_t)g.H; a.W = (int32_t)g.W; a.Ho = (int32_t)g.Ho; a.Wo = (int32_t)g.Wo;
+    a.sh = g.sh; a.sw = g.sw; a.ph = g.ph; a.pw = g.pw;
+    a.x_nstride = g.C * g.H * g.W;
+    a.M = (int32_t)g.Kg;
+    a.Kred = (int32_t)g.Kred;
+    a.P = (int32_t)g.P;
+    a.nstages = gp.nstages;
+    a.grid_m = (int32_t)ceil_div(g.Kg, gp.bm);
+    a.grid_p = (int32_t)ceil_div(g.P, gp.bn);
+    a.y = y;
+    a.y_bytes = (uint32_t)(g.y_elems * elem_size(g.ydt));
+    a.bias = g.has_bias ? bias : nullptr;
+    a.y_nstride = g.K * g.Ho * g.Wo;
+    a.HoWo = (int32_t)(g.Ho * g.Wo);
+    Scope sc(d, CONV2D_ALGO_IMPLICIT_GEMM, CONV2D_PH_IN_MICROKERNEL, s, ph);
+    CV_TRY(sc.begin());
+    CV_HIP(launch_gemm(a, gp.tile, BSRC_IMPLICIT_NCHW, EPI_NCHW, g.xdt, g.ydt, (int)g.G, s));
+    return sc.end();
+}
+
+int run_explicit(conv2d_desc* d, const void* x, const void* w, const float* bias, void* y, hipStream_t s,
+                 bool ph) {
+    const Geometry& g = d->g;
+    const ExplicitPlan& e = d->expl;
+    if (e.status != CONV2D_OK) return e.status;
+    CV_TRY(ensure_buffer(&d->ws, &d->ws_bytes, e.col_bytes + e.c_bytes));
+    char* col = static_cast<char*>(d->ws);
+    float* cbuf = reinterpret_cast<float*>(col + e.col_bytes);
+    const int64_t total_rows = g.N * g.Ho;
+    for (int64_t r0 = 0; r0 < total_rows; r0 += e.rows_per_chunk) {
+        const int64_t rows = std::min<int64_t>(e.rows_per_chunk, total_rows - r0);
+        const int64_t pc = rows * g.Wo;
+        const int64_t p_begin = r0 * g.Wo;
+        {
+            Im2colArgs a{};
+            a.x = x;
+            a.col = col;
+            a.col_bytes = (uint32_t)(g.G * g.Kred * pc * elem_size(g.xdt));
+            a.ktab = d->ktab_dev;
+            a.H = (int32_t)g.H; a.W = (int32_t)g.W; a.Ho = (int32_t)g.Ho; a.Wo = (int32_t)g.Wo;
+            a.sh = g.sh; a.sw = g.sw; a.ph = g.ph; a.pw = g.pw;
+            a.x_nstride = g.C * g.H * g.W;
+            a.x_gstride = g.Cg * g.H * g.W;
+            a.Kred = (int32_t)g.Kred;
+            a.pc = (int32_t)pc;
+            a.p_begin = p_begin;
+            Scope sc(d, CONV2D_ALGO_IM2COL_GEMM, CONV2D_PH_IN_PACKING, s, ph);
+            CV_TRY(sc.begin());
+            CV_HIP(launch_im2col(a, g.xdt, (int)g.G, s));
+            CV_TRY(sc.end());
+        }
+        {
+            const GemmPlan& gp = e.gemm;
+            GemmArgs a{};
+            a.a = w;
+            a.a_bytes = (uint32_t)(g.w_elems * elem_size(g.xdt));
+            a.lda = (int32_t)g.Kred;
+            a.a_gstride = g.Kg * g.Kred;
+            a.b = col;
+            a.b_bytes = (uint32_t)(g.G * g.Kred * pc * elem_size(g.xdt));
+            a.b_gstride = g.Kred * pc;
+            a.ldb = (int32_t)pc;
+            a.M = (int32_t)g.Kg;
+            a.Kred = (int32_t)g.Kred;
+            a.P = (int32_t)pc;
+            a.nstages = (int32_t)ceil_div(g.Kred, g.xdt == CONV2D_BF16 ? 32 : 16);
+            a.grid_m = (int32_t)ceil_div(g.Kg, gp.bm);
+            a.grid_p = (int32_t)ceil_div(pc, gp.bn);
+            a.y = cbuf;
+            a.y_bytes = (uint32_t)(g.G * g.Kg * pc * 4);
+            a.ldc = (int32_t)pc;
+            a.c_gstride = g.Kg * pc;
+            a.HoWo = (int32_t)(g.Ho * g.Wo);
+            Scope sc(d, CONV2D_ALGO_IM2COL_GEMM, CONV2D_PH_IN_MICROKERNEL, s, ph);
+            CV_TRY(sc.begin());
+            CV_HIP(launch_gemm(a, gp.tile, BSRC_DENSE, EPI_DENSE, g.xdt, CONV2D_F32, (int)g.G, s));
+            CV_TRY(sc.end());
+        }
+        {
+            UnpackArgs a{};
+            a.c = cbuf;
+            a.y = y;
+            a.y_bytes = (uint32_t)(g.y_elems * elem_size(g.ydt));
+            a.bias = g.has_bias ? bias : nullptr;
+            a.Kg = (int32_t)g.Kg;
+            a.pc = (int32_t)pc;
+            a.HoWo = (int32_t)(g.Ho * g.Wo);
+            a.p_begin = p_begin;
+            a.y_nstride = g.K * g.Ho * g.Wo;
+            Scope sc(d, CONV2D_ALGO_IM2COL_GEMM, CONV2D_PH_IN_UNPACKING, s, ph);
+            CV_TRY(sc.begin());
+            CV_HIP(launch_unpack(a, g.ydt, (int)g.G, s));
+            CV_TRY(sc.end());
+        }
+    }
+    return CONV2D_OK;
+}
+
+int run_direct(conv2d_desc* d, const void* x, const void* w, const float* bias, void* y, hipStream_t s,
+               bool ph) {
+    const Geometry& g = d->g;
+    DirectArgs a{};
+    a.x = x; a.w = w; a.bias = g.has_bias ? bias : nullptr; a.y = y;
+    a.x_bytes = (uint32_t)(g.x_elems * elem_size(g.xdt));
+    a.y_bytes = (uint32_t)(g.y_elems * elem_size(g.ydt));
+    a.C = (int32_t)g.C; a.H = (int32_t)g.H; a.W = (int32_t)g.W; a.K = (int32_t)g.K;
+    a.Ho = (int32_t)g.Ho; a.Wo = (int32_t)g.Wo; a.R = (int32_t)g.R; a.S = (int32_t)g.S;
+    a.sh = g.sh; a.sw = g.sw; a.ph = g.ph; a.pw = g.pw; a.dh = g.dh; a.dw = g.dw;
+    a.Cg = (int32_t)g.Cg; a.Kg = (int32_t)g.Kg; a.N = (int32_t)g.N;
+    Scope sc(d, CONV2D_ALGO_DIRECT, CONV2D_PH_IN_MICROKERNEL, s, ph);
+    CV_TRY(sc.begin());
+    CV_HIP(launch_direct(a, g.xdt, g.ydt, s));
+    return sc.end();
+}
+
+bool direct_supported(const Geometry& g) {
+    if (g.x_elems * elem_size(g.xdt) > kBufferLimit || g.y_elems * elem_size(g.ydt) > kBufferLimit)
+        return false;
+    if (g.Wo > 1024 || g.N * g.K > 0x7fffffffLL) return false;
+    const int64_t in_cols = (g.Wo - 1) * g.sw + (g.S - 1) * g.dw + 1;
+    const int64_t in_rows = (g.R - 1) * g.dh + 1;
+    return in_rows * in_cols <= 12288;
+}
+
+bool implicit_supported(const Geometry& g) {
+    return g.x_elems * elem_size(g.xdt) <= kBufferLimit && g.y_elems * elem_size(g.ydt) <= kBufferLimit &&
+           g.w_elems * elem_size(g.xdt) <= kBufferLimit && g.P <= 0x7fffffffLL && g.Kred <= 0x7fffffffLL;
+}
+
+}  // namespace
+
+// ====================================================================== C ABI
+extern "C" {
+
+int conv2d_desc_create(const conv2d_params* params, conv2d_desc** out) {
+    const auto t0 = std::chrono::steady_clock::now();
+    if (!params || !out) return CONV2D_E_NULL;
+    *out = nullptr;
+    Geometry g{};
+    const int st = validate(params, &g);
+    if (st != CONV2D_OK) return st;
+    conv2d_desc* d = new (std::nothrow) conv2d_desc();
+    if (!d) return CONV2D_E_ALLOC;
+    d->prm = *params;
+    d->g = g;
+    d->opclass = classify(g);
+    std::memset(d->acc, 0, sizeof(d->acc));
+    d->timing = env_timing();
+    d->implicit_ok = implicit_supported(g);
+    d->direct_ok = direct_supported(g);
+    d->implicit = choose_tile(g.Kg, g.P, g.G, g.Kred, g.xdt);
+    build_ktab(d);
+    plan_explicit(d);
+    if (d->direct_ok && g.G > 1 && g.Cg <= 8)
+        d->auto_algo = CONV2D_ALGO_DIRECT;
+    else if (d->implicit_ok)
+        d->auto_algo = CONV2D_ALGO_IMPLICIT_GEMM;
+    else if (d->expl.status == CONV2D_OK && g.y_elems * elem_size(g.ydt) <= kBufferLimit)
+        d->auto_algo = CONV2D_ALGO_IM2COL_GEMM;
+    else if (d->direct_ok)
+        d->auto_algo = CONV2D_ALGO_DIRECT;
+    else
+        d->auto_algo = CONV2D_ALGO_IMPLICIT_GEMM;  // conv2d_fwd will report E_UNSUPPORTED
+    const auto t1 = std::chrono::steady_clock::now();
+    d->analysis_ms = std::chrono::duration<double, std::milli>(t1 - t0).count();
+    *out = d;
+    return CONV2D_OK;
+}
+
+int conv2d_desc_destroy(conv2d_desc* d) {
+    if (!d) return CONV2D_OK;
+    for (const EvRec& r : d->pending) {
+        hipEventDestroy(r.a);
+        hipEventDestroy(r.b);
+    }
+    for (hipEvent_t e : d->free_events) hipEventDestroy(e);
+    if (d->ktab_dev) hipFree(d->ktab_dev);
+    if (d->ws) hipFree(d->ws);
+    if (d->xr) hipFree(d->xr);
+    if (d->yr) hipFree(d->yr);
+    delete d;
+    return CONV2D_OK;
+}
+
+int conv2d_output_shape(const conv2d_desc* d, int64_t out_nkhw[4]) {
+    if (!d || !out_nkhw) return CONV2D_E_NULL;
+    out_nkhw[0] = d->g.N;
+    out_nkhw[1] = d->g.K;
+    out_nkhw[2] = d->g.Ho;
+    out_nkhw[3] = d->g.Wo;
+    return CONV2D_OK;
+}
+
+int conv2d_fwd(conv2d_desc* d, const void* x, const void* w, const float* bias, void* y, int algo,
+               void* stream) {
+    if (!d || !x || !w || !y) return CONV2D_E_NULL;
+    if (d->g.has_bias && !bias) return CONV2D_E_NULL;
+    if (algo < 0 || algo >= CONV2D_ALGO_COUNT) return CONV2D_E_INVALID;
+    if (algo == CONV2D_ALGO_AUTO) algo = d->auto_algo;
+    const Geometry& g = d->g;
+    if (algo == CONV2D_ALGO_IMPLICIT_GEMM && !d->implicit_ok) return CONV2D_E_UNSUPPORTED;
+    if (algo == CONV2D_ALGO_DIRECT && !d->direct_ok) return CONV2D_E_UNSUPPORTED;
+    if (algo == CONV2D_ALGO_IM2COL_GEMM) {
+        if (d->expl.status != CONV2D_OK) return d->expl.status;
+        if (g.y_elems * elem_size(g.ydt) > kBufferLimit) return CONV2D_E_UNSUPPORTED;
+    }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    CV_TRY(ensure_device(d, s));
+    if (d->pending.size() > 8192) CV_TRY(harvest(d));
+
+    const bool ph = d->timing == CONV2D_TIMING_PHASES;
+    Scope total(d, algo, -1, s, d->timing == CONV2D_TIMING_TOTAL);
+    CV_TRY(total.begin());
+
+    const void* xin = x;
+    void* yout = y;
+    const bool nhwc = g.layout == CONV2D_NHWC;
+    if (nhwc) {
+        const int64_t xb = g.x_elems * elem_size(g.xdt), yb = g.y_elems * elem_size(g.ydt);
+        CV_TRY(ensure_buffer(&d->xr, &d->xr_bytes, xb));
+        CV_TRY(ensure_buffer(&d->yr, &d->yr_bytes, yb));
+        Scope sc(d, algo, CONV2D_PH_PRE_REORDER, s, ph);
+        CV_TRY(sc.begin());
+        CV_HIP(launch_nhwc_to_nchw(x, d->xr, g.N, g.C, g.H * g.W, (int)elem_size(g.xdt), s));
+        CV_TRY(sc.end());
+        xin = d->xr;
+        yout = d->yr;
+    }
+    int st = CONV2D_OK;
+    switch (algo) {
+        case CONV2D_ALGO_IMPLICIT_GEMM: st = run_implicit(d, xin, w, bias, yout, s, ph); break;
+        case CONV2D_ALGO_IM2COL_GEMM: st = run_explicit(d, xin, w, bias, yout, s, ph); break;
+        case CONV2D_ALGO_DIRECT: st = run_direct(d, xin, w, bias, yout, s, ph); break;
+        default: st = CONV2D_E_INVALID;
+    }
+    if (st != CONV2D_OK) return st;
+    if (nhwc) {
+        Scope sc(d, algo, CONV2D_PH_POST_REORDER, s, ph);
+        CV_TRY(sc.begin());
+        CV_HIP(launch_nchw_to_nhwc(d->yr, y, g.N, g.K, g.Ho * g.Wo, (int)elem_size(g.ydt), s));
+        CV_TRY(sc.end());
+    }
+    CV_TRY(total.end());
+    d->acc[algo].fwd_calls += 1;
+    d->acc[algo].used = true;
+    d->last_algo = algo;
+    return CONV2D_OK;
+}
+
+int conv2d_breakdown(conv2d_desc* d, int algo, conv2d_breakdown_t* out) {
+    if (!d || !out) return CONV2D_E_NULL;
+    if (algo < 0 || algo >= CONV2D_ALGO_COUNT) return CONV2D_E_INVALID;
+    if (algo == CONV2D_ALGO_AUTO) algo = d->last_algo;
+    if (algo < 0) return CONV2D_E_NO_DATA;
+    const int hst = harvest(d);
+    const PhaseAcc& a = d->acc[algo];
+    if (!a.used) return CONV2D_E_NO_DATA;
+    std::memset(out, 0, sizeof(*out));
+    for (int p = 0; p < CONV2D_PH_COUNT; ++p) {
+        out->ms[p] = a.ms[p];
+        out->calls[p] = a.calls[p];
+    }
+    out->ms[CONV2D_PH_PRE_ANALYSIS] = d->analysis_ms;
+    out->calls[CONV2D_PH_PRE_ANALYSIS] = 1;
+    if (algo == CONV2D_ALGO_IMPLICIT_GEMM)
+        out->fused_mask = (1u << CONV2D_PH_IN_TILING) | (1u << CONV2D_PH_IN_PACKING) | (1u << CONV2D_PH_IN_UNPACKING);
+    else if (algo == CONV2D_ALGO_IM2COL_GEMM)
+        out->fused_mask = (1u << CONV2D_PH_IN_TILING);
+    else
+        out->fused_mask = (1u << CONV2D_PH_IN_TILING) | (1u << CONV2D_PH_IN_PACKING);
+    out->algo = algo;
+    out->pack_is_preconv = algo == CONV2D_ALGO_IM2COL_GEMM ? 1 : 0;
+    out->fwd_calls = a.fwd_calls;
+    double op = 0.0, conv = 0.0;
+    for (int p = 0; p < CONV2D_PH_COUNT; ++p) {
+        op += out->ms[p];
+        if (p >= CONV2D_PH_IN_TILING && p <= CONV2D_PH_IN_UNPACKING) conv += out->ms[p];
+    }
+    out->operation_ms = op;
+    out->convolution_ms = conv;
+    out->total_ms = a.total_ms;
+    out->total_calls = a.total_calls;
+    return hst;
+}
+
+int conv2d_breakdown_reset(conv2d_desc* d) {
+    if (!d) return CONV2D_E_NULL;
+    const int st = harvest(d);
+    std::memset(d->acc, 0, sizeof(d->acc));
+    d->last_algo = -1;
+    return st;
+}
+
+int conv2d_set_timing(conv2d_desc* d, int mode) {
+    if (!d) return CONV2D_E_NULL;
+    if (mode < CONV2D_TIMING_OFF || mode > CONV2D_TIMING_PHASES) return CONV2D_E_INVALID;
+    const int st = harvest(d);
+    d->timing = mode;
+    return st;
+}
+
+int conv2d_plan_query(const conv2d_desc* d, int algo, conv2d_plan_info* out) {
+    if (!d || !out) return CONV2D_E_NULL;
+    if (algo < 0 || algo >= CONV2D_ALGO_COUNT) return CONV2D_E_INVALID;
+    if (algo == CONV2D_ALGO_AUTO) algo = d->auto_algo;
+    std::memset(out, 0, sizeof(*out));
+    const Geometry& g = d->g;
+    out->algo = algo;
+    out->kred = (int32_t)g.Kred;
+    out->kred_pad = (int32_t)(ceil_div(g.Kred, g.xdt == CONV2D_BF16 ? 32 : 16) * (g.xdt == CONV2D_BF16 ? 32 : 16));
+    out->needs_reorder = g.layout == CONV2D_NHWC ? 1 : 0;
+    out->op_class = (int32_t)d->opclass;
+    out->chunks = 1;
+    if (algo == CONV2D_ALGO_IMPLICIT_GEMM) {
+        out->tile_m = d->implicit.bm;
+        out->tile_n = d->implicit.bn;
+        if (!d->implicit_ok) return CONV2D_E_UNSUPPORTED;
+    } else if (algo == CONV2D_ALGO_IM2COL_GEMM) {
+        out->tile_m = d->expl.gemm.bm;
+        out->tile_n = d->expl.gemm.bn;
+        out->workspace_bytes = d->expl.col_bytes + d->expl.c_bytes;
+        out->chunks = d->expl.chunks;
+        if (d->expl.status != CONV2D_OK) return d->expl.status;
+    } else if (!d->direct_ok) {
+        return CONV2D_E_UNSUPPORTED;
+    }
+    return CONV2D_OK;
+}
+
+const char* conv2d_status_string(int status) {
+    switch (status) {
+        case CONV2D_OK: return "ok";
+        case CONV2D_E_INVALID: return "invalid parameter";
+        case CONV2D_E_SHAPE: return "filter window does not fit the padded input";
+        case CONV2D_E_UNSUPPORTED: return "unsupported combination";
+        case CONV2D_E_NULL: return "null pointer";
+        case CONV2D_E_ALLOC: return "workspace allocation failed or exceeds the limit";
+        case CONV2D_E_HIP: return "HIP runtime error";
+        case CONV2D_E_NO_DATA: return "no timing data recorded";
+        default: return "unknown status";
+    }
+}
+
+int conv2d_runtime_version(int* v) {
+    if (!v) return CONV2D_E_NULL;
+    return hipRuntimeGetVersion(v) == hipSuccess ? CONV2D_OK : CONV2D_E_HIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,116 @@
+// conv2d_internal.h -- shared declarations of the gfx950 conv2d library (host side).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <vector>
+
+#include "conv2d.h"
+
+namespace cv {
+
+// Operation classes (bit positions of conv2d_plan_info::op_class).
+enum { OPC_POINTWISE = 1, OPC_GROUPED = 2, OPC_DEPTHWISE = 4, OPC_DILATED = 8,
+       OPC_RECTANGULAR = 16, OPC_STRIDED = 32 };
+
+// Everything the kernels need to know about one convolution, in logical NCHW terms.
+struct Geometry {
+    int64_t N, C, H, W, K, R, S, Ho, Wo;
+    int32_t sh, sw, ph, pw, dh, dw, G;
+    int64_t Cg, Kg, Kred, P;   // P = N*Ho*Wo output pixels
+    int32_t layout, xdt, ydt, has_bias;
+    int64_t x_elems, w_elems, y_elems;
+};
+
+// Tile configurations of the MFMA GEMM kernels.
+enum TileCfg { TILE_64x64 = 0, TILE_64x128 = 1, TILE_64x256 = 2, TILE_128x128 = 3,
+               TILE_128x64 = 4, TILE_COUNT = 5 };
+struct TileShape { int bm, bn; };
+static const TileShape kTileShapes[TILE_COUNT] = {{64, 64}, {64, 128}, {64, 256}, {128, 128}, {128, 64}};
+
+// Source of the GEMM's B operand (the im2col matrix, Kred x P).
+enum BSrc { BSRC_IMPLICIT_NCHW = 0, BSRC_DENSE = 1 };
+// Destination of the GEMM result.
+enum Epi { EPI_NCHW = 0, EPI_DENSE = 1 };
+
+// Per reduction index kr (one im2col row) of an NCHW input: the element offset
+// of tap (c, r, s) relative to the window origin, and the row / column shifts
+// used for the zero-padding test.  Rows beyond Kred carry roff = KTAB_DEAD so
+// every bounds test fails and they read zero.
+struct KTabEntry { int32_t coff, roff, soff, pad; };
+constexpr int32_t KTAB_DEAD = -(1 << 29);
+constexpr int KTAB_ALIGN = 64;   // table length is Kred rounded up to this
+
+// Arguments of one MFMA GEMM launch (both algorithm families).
+struct GemmArgs {
+    const void* a;        // weights, [G][Kg][lda] in x dtype
+    uint32_t a_bytes;
+    int32_t lda;
+    int64_t a_gstride;    // elements between groups
+    const void* b;        // implicit: x (NCHW); dense: col [G][Kred][ldb]
+    uint32_t b_bytes;
+    int64_t b_gstride;    // elements between groups
+    int32_t ldb;
+    const KTabEntry* ktab;
+    int32_t H, W, Ho, Wo, sh, sw, ph, pw;
+    int64_t x_nstride;    // C*H*W
+    int32_t M, Kred, P, nstages;
+    int32_t grid_p, grid_m;
+    void* y;              // NCHW y, or dense C [G][M][ldc] (fp32)
+    uint32_t y_bytes;
+    const float* bias;    // may be NULL
+    int64_t y_nstride;    // K*Ho*Wo
+    int32_t HoWo;
+    int32_t ldc;
+    int64_t c_gstride;
+    int32_t p_offset;     // global index of column 0 (explicit chunks)
+};
+
+hipError_t launch_gemm(const GemmArgs& a, int tile, int bsrc, int epi, int xdt, int ydt, int groups,
+                       hipStream_t stream);
+
+// im2col of a chunk of output pixels [p_begin, p_begin + pc): col[g][kr][pl].
+struct Im2colArgs {
+    const void* x;
+    void* col;
+    uint32_t col_bytes;
+    const KTabEntry* ktab;
+    int32_t H, W, Ho, Wo, sh, sw, ph, pw;
+    int64_t x_nstride, x_gstride;
+    int32_t Kred, pc;
+    int64_t p_begin;
+};
+hipError_t launch_im2col(const Im2colArgs& a, int xdt, int groups, hipStream_t stream);
+
+// unpack C[g][m][pl] (fp32) to NCHW y (+bias, cast).
+struct UnpackArgs {
+    const float* c;
+    void* y;
+    uint32_t y_bytes;
+    const float* bias;
+    int32_t Kg, pc, HoWo;
+    int64_t p_begin;
+    int64_t y_nstride;
+};
+hipError_t launch_unpack(const UnpackArgs& a, int ydt, int groups, hipStream_t stream);
+
+// direct convolution (NCHW) for depthwise / small-group layers.
+struct DirectArgs {
+    const void* x;
+    const void* w;
+    const float* bias;
+    void* y;
+    uint32_t x_bytes, y_bytes;
+    int32_t C, H, W, K, Ho, Wo, R, S, sh, sw, ph, pw, dh, dw, Cg, Kg;
+    int32_t N;
+};
+hipError_t launch_direct(const DirectArgs& a, int xdt, int ydt, hipStream_t stream);
+
+// layout transforms between NHWC and NCHW (one image = a [HW x C] <-> [C x HW] transpose).
+hipError_t launch_nhwc_to_nchw(const void* src, void* dst, int64_t n, int64_t c, int64_t hw,
+                               int elem_bytes, hipStream_t stream);
+hipError_t launch_nchw_to_nhwc(const void* src, void* dst, int64_t n, int64_t c, int64_t hw,
+                               int elem_bytes, hipStream_t stream);
+
+}  // namespace cv

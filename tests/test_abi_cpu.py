@@ -1,0 +1,150 @@
+"""The C ABI on the CPU: the library loads, exports what the header declares,
+and its host-only planning and validation behave (no GPU needed)."""
+import os
+import re
+import subprocess
+
+import pytest
+
+import datagen
+import oracle
+import paper_2407_10730_amd as cv
+from paper_2407_10730_amd import binding as B
+from paper_2407_10730_amd.runner import params_for
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "conv2d.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\**(conv2d_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_library_exports_every_declared_function():
+    decl = _declared_functions()
+    assert set(decl) == set(B.EXPORTS), decl
+    lib = cv.load()
+    for name in decl:
+        assert hasattr(lib, name)
+    out = subprocess.run(["nm", "-D", "--defined-only", B.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    exported = set(re.findall(r"\bT (conv2d_\w+)", out))
+    assert set(decl) <= exported
+
+
+def _params(**kw):
+    base = dict(n=2, c=4, h=9, w=9, k=6, r=3, s=3, stride_h=1, stride_w=1, pad_h=1, pad_w=1,
+                dil_h=1, dil_w=1, groups=1, layout=0, x_dtype=0, y_dtype=0, has_bias=1)
+    base.update(kw)
+    return B.conv2d_params(**base)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n=0), B.CONV2D_E_INVALID), (dict(k=-1), B.CONV2D_E_INVALID),
+    (dict(stride_h=0), B.CONV2D_E_INVALID), (dict(dil_w=0), B.CONV2D_E_INVALID),
+    (dict(pad_h=-1), B.CONV2D_E_INVALID), (dict(groups=0), B.CONV2D_E_INVALID),
+    (dict(groups=3), B.CONV2D_E_INVALID), (dict(layout=2), B.CONV2D_E_INVALID),
+    (dict(x_dtype=5), B.CONV2D_E_INVALID),
+    (dict(x_dtype=0, y_dtype=1), B.CONV2D_E_UNSUPPORTED),
+    (dict(h=2, pad_h=0), B.CONV2D_E_SHAPE), (dict(w=3, s=2, dil_w=3, pad_w=0), B.CONV2D_E_SHAPE),
+])
+def test_create_rejects(kw, code):
+    with pytest.raises(B.Conv2dError) as ei:
+        B.conv2d_desc_create(_params(**kw))
+    assert ei.value.status == code
+
+
+def test_null_pointers_rejected():
+    lib = cv.load()
+    assert lib.conv2d_desc_create(None, None) == B.CONV2D_E_NULL
+    d = B.conv2d_desc_create(_params())
+    try:
+        assert lib.conv2d_fwd(d, None, None, None, None, 0, None) == B.CONV2D_E_NULL
+        assert lib.conv2d_fwd(d, 1, 1, None, 1, 0, None) == B.CONV2D_E_NULL  # bias missing
+        assert lib.conv2d_fwd(d, 1, 1, 1, 1, 9, None) == B.CONV2D_E_INVALID
+    finally:
+        B.conv2d_desc_destroy(d)
+    assert lib.conv2d_desc_destroy(None) == 0
+
+
+def test_output_shape_matches_oracle_over_a_grid():
+    checked = 0
+    for h in (1, 2, 5, 8, 13):
+        for r in (1, 2, 3, 5):
+            for st in (1, 2, 3):
+                for pd in (0, 1, 3):
+                    for dl in (1, 2):
+                        kw = dict(h=h, w=h + 1, r=r, s=max(1, r - 1), stride_h=st, stride_w=st,
+                                  pad_h=pd, pad_w=pd, dil_h=dl, dil_w=dl)
+                        try:
+                            ref = oracle.output_dims((2, 4, h, h + 1), (6, 4, r, max(1, r - 1)),
+                                                     (st, st), (pd, pd), (dl, dl))
+                        except oracle.OracleError:
+                            with pytest.raises(B.Conv2dError):
+                                B.conv2d_desc_create(_params(**kw))
+                            continue
+                        d = B.conv2d_desc_create(_params(**kw))
+                        assert B.conv2d_output_shape(d) == (2, 6) + ref
+                        B.conv2d_desc_destroy(d)
+                        checked += 1
+    assert checked > 200
+
+
+def test_breakdown_before_any_call():
+    d = B.conv2d_desc_create(_params())
+    try:
+        with pytest.raises(B.Conv2dError) as ei:
+            B.conv2d_breakdown(d, B.CONV2D_ALGO_IMPLICIT_GEMM)
+        assert ei.value.status == B.CONV2D_E_NO_DATA
+        with pytest.raises(B.Conv2dError) as ei:
+            B.conv2d_breakdown(d, B.CONV2D_ALGO_AUTO)
+        assert ei.value.status == B.CONV2D_E_NO_DATA
+        B.conv2d_set_timing(d, B.CONV2D_TIMING_TOTAL)
+        with pytest.raises(B.Conv2dError):
+            B.conv2d_set_timing(d, 7)
+        B.conv2d_breakdown_reset(d)
+    finally:
+        B.conv2d_desc_destroy(d)
+
+
+def test_auto_algorithm_choice_and_classes():
+    dw = datagen.CONFIGS["dw"]
+    d = B.conv2d_desc_create(params_for(dw))
+    info = B.conv2d_plan_query(d)
+    assert info.algo == B.CONV2D_ALGO_DIRECT and info.op_class & 4 and info.op_class & 2
+    B.conv2d_desc_destroy(d)
+    d = B.conv2d_desc_create(params_for(datagen.CONFIGS["cfg2"]))
+    info = B.conv2d_plan_query(d)
+    assert info.algo == B.CONV2D_ALGO_IMPLICIT_GEMM and info.kred == 576 and info.op_class == 0
+    B.conv2d_desc_destroy(d)
+    d = B.conv2d_desc_create(params_for(datagen.CONFIGS["cfg3b"]))
+    assert B.conv2d_plan_query(d).op_class == 1 | 32
+    B.conv2d_desc_destroy(d)
+
+
+def test_explicit_workspace_chunking(monkeypatch):
+    cs = datagen.CONFIGS["cfg4"]
+    d = B.conv2d_desc_create(params_for(cs))
+    info = B.conv2d_plan_query(d, B.CONV2D_ALGO_IM2COL_GEMM)
+    # col (147 x 401408 fp32) + result (64 x 401408 fp32) fits the 1 GiB default in one chunk
+    assert info.chunks == 1 and info.workspace_bytes == 401408 * (147 + 64) * 4
+    B.conv2d_desc_destroy(d)
+    monkeypatch.setenv("CONV2D_WORKSPACE_LIMIT_BYTES", str(64 << 20))
+    d = B.conv2d_desc_create(params_for(cs))
+    info = B.conv2d_plan_query(d, B.CONV2D_ALGO_IM2COL_GEMM)
+    assert info.chunks > 1 and info.workspace_bytes <= 64 << 20
+    B.conv2d_desc_destroy(d)
+    monkeypatch.setenv("CONV2D_WORKSPACE_LIMIT_BYTES", "0")
+    d = B.conv2d_desc_create(params_for(cs))
+    with pytest.raises(B.Conv2dError) as ei:
+        B.conv2d_plan_query(d, B.CONV2D_ALGO_IM2COL_GEMM)
+    assert ei.value.status == B.CONV2D_E_ALLOC
+    B.conv2d_desc_destroy(d)
+
+
+def test_status_strings():
+    for code in range(-8, 1):
+        assert isinstance(B.conv2d_status_string(code), str)
+    assert B.conv2d_status_string(0) == "ok"

@@ -1,0 +1,237 @@
+"""Parity of the HIP conv2d library against the fp64 CPU oracle (needs the GPU).
+
+Gates (per-output normalised error |y - y_ref| / (|b| + sum |x*w|)):
+fp32 inputs 1e-5, bf16 inputs 1e-2 (fp32 accumulation; the oracle reads the
+same bf16-rounded values).  Integer-valued data (every partial sum exact in
+fp32) must match the oracle bit for bit, for every algorithm and dtype.
+"""
+import os
+
+import numpy as np
+import pytest
+
+import datagen
+import oracle
+from paper_2407_10730_amd import binding as B
+from paper_2407_10730_amd.runner import DeviceConv
+
+pytestmark = pytest.mark.gpu
+
+GATE = {"f32": 1e-5, "bf16": 1e-2}
+IMPLICIT, IM2COL, DIRECT = B.CONV2D_ALGO_IMPLICIT_GEMM, B.CONV2D_ALGO_IM2COL_GEMM, B.CONV2D_ALGO_DIRECT
+ALGO_IDS = {IMPLICIT: "implicit", IM2COL: "im2col", DIRECT: "direct", B.CONV2D_ALGO_AUTO: "auto"}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.load()
+    yield
+    torch.cuda.synchronize()
+
+
+_ORACLE_CACHE = {}
+
+
+def _reference(cs, mode, inputs):
+    key = (cs, mode)
+    if key not in _ORACLE_CACHE:
+        x, w, b = inputs
+        _ORACLE_CACHE[key] = oracle.conv2d(x, w, b if cs.has_bias else None, cs.stride, cs.pad,
+                                           cs.dil, cs.groups)
+    return _ORACLE_CACHE[key]
+
+
+def _run(cs, algo, mode="random"):
+    import torch
+    print(f"\n[case] {cs} algo={ALGO_IDS[algo]} mode={mode}", flush=True)
+    dc = DeviceConv(cs, mode)
+    try:
+        dc.run(algo)
+        torch.cuda.synchronize()
+        y = dc.y_nchw()
+    finally:
+        dc.close()
+    return y, (dc.x_host, dc.w_host, dc.b_host)
+
+
+def _check(cs, algo, mode="random"):
+    y, inputs = _run(cs, algo, mode)
+    y_ref, a_ref = _reference(cs, mode, inputs)
+    assert y.shape == y_ref.shape
+    if mode == "integer" and cs.y_dtype == "f32":
+        bad = np.argwhere(y != y_ref)
+        assert bad.size == 0, f"{len(bad)} mismatches, first at {bad[0]}: {y[tuple(bad[0])]} vs {y_ref[tuple(bad[0])]}"
+        return 0.0
+    lit, pt = oracle.normalised_errors(y, y_ref, a_ref)
+    gate = GATE[cs.x_dtype]
+    if cs.y_dtype == "bf16":
+        gate = max(gate, 2.0 ** -8)
+    assert pt <= gate, f"per-point error {pt:.3e} > {gate} (literal {lit:.3e})"
+    return pt
+
+
+# ------------------------------------------------------------------ the fixed workloads
+
+FULL = ["cfg1", "cfg2", "cfg3a", "cfg3b", "cfg4", "cfg4_bf16"]
+
+
+@pytest.mark.parametrize("algo", [IMPLICIT, IM2COL], ids=lambda a: ALGO_IDS[a])
+@pytest.mark.parametrize("name", FULL)
+def test_config_parity(name, algo):
+    _check(datagen.CONFIGS[name], algo)
+
+
+@pytest.mark.parametrize("algo", [DIRECT, IMPLICIT, IM2COL], ids=lambda a: ALGO_IDS[a])
+def test_depthwise_config_parity(algo):
+    _check(datagen.CONFIGS["dw"], algo)
+
+
+@pytest.mark.parametrize("name", ["cfg1", "cfg2", "cfg3b", "cfg4", "dw"])
+def test_config_exact_integer(name):
+    cs = datagen.CONFIGS[name].with_(w_scale=None)
+    algos = [DIRECT] if name == "dw" else [IMPLICIT, IM2COL]
+    for algo in algos:
+        _check(cs, algo, "integer")
+        _check(cs.with_(x_dtype="bf16"), algo, "integer")
+
+
+# ------------------------------------------------------------------ edge grid
+
+def _shape(n, c, h, w, k, r, s, st=(1, 1), pd=(0, 0), dl=(1, 1), g=1, seed=100, bias=True):
+    return datagen.ConvShape(n=n, c=c, h=h, w=w, k=k, r=r, s=s, stride=st, pad=pd, dil=dl, groups=g,
+                             seed=seed, has_bias=bias)
+
+
+EDGE = [
+    _shape(1, 3, 5, 7, 5, 3, 3, pd=(1, 1)),
+    _shape(2, 5, 11, 9, 7, 5, 3, st=(2, 1), pd=(2, 1), dl=(1, 2)),
+    _shape(3, 6, 8, 8, 6, 3, 3, pd=(1, 1), g=6),
+    _shape(1, 4, 7, 7, 8, 2, 2, g=2),
+    _shape(2, 8, 9, 10, 70, 1, 1),
+    _shape(1, 3, 6, 6, 4, 7, 7, pd=(3, 3)),
+    _shape(1, 2, 4, 4, 3, 3, 3, st=(3, 3), pd=(3, 3), dl=(2, 2)),
+    _shape(2, 64, 14, 14, 130, 3, 3, st=(2, 2), pd=(1, 1)),
+    _shape(1, 1, 1, 1, 1, 1, 1),
+    _shape(1, 3, 17, 1, 5, 3, 1, pd=(1, 0)),
+    _shape(2, 16, 9, 9, 32, 3, 3, pd=(2, 2), dl=(2, 2), g=4),
+    _shape(3, 19, 23, 23, 70, 3, 3, pd=(1, 1)),
+    _shape(1, 150, 6, 6, 33, 3, 3, pd=(1, 1), bias=False),
+    _shape(2, 3, 30, 30, 64, 7, 7, st=(2, 2), pd=(3, 3)),
+    _shape(1, 8, 5, 13, 9, 1, 5, st=(1, 3), pd=(0, 2)),
+    _shape(4, 12, 7, 7, 12, 3, 3, st=(2, 2), pd=(1, 1), g=12),
+    _shape(1, 256, 7, 7, 512, 3, 3, pd=(1, 1)),
+]
+VARIANTS = [("nchw", "f32", "f32"), ("nhwc", "f32", "f32"), ("nchw", "bf16", "bf16"),
+            ("nhwc", "bf16", "f32")]
+
+
+@pytest.mark.parametrize("algo", [IMPLICIT, IM2COL, DIRECT], ids=lambda a: ALGO_IDS[a])
+@pytest.mark.parametrize("var", VARIANTS, ids=lambda v: "-".join(v))
+@pytest.mark.parametrize("idx", range(len(EDGE)))
+def test_edge_grid(idx, var, algo):
+    layout, xdt, ydt = var
+    cs = EDGE[idx].with_(layout=layout, x_dtype=xdt, y_dtype=ydt)
+    _check(cs, algo, "random")
+    _check(cs.with_(y_dtype="f32"), algo, "integer")
+
+
+# ------------------------------------------------------------------ behaviour
+
+@pytest.mark.parametrize("algo", [IMPLICIT, IM2COL, DIRECT], ids=lambda a: ALGO_IDS[a])
+def test_run_to_run_bitwise_determinism(algo):
+    import torch
+    cs = _shape(2, 24, 15, 15, 40, 3, 3, pd=(1, 1), seed=7)
+    dc = DeviceConv(cs)
+    try:
+        dc.run(algo)
+        torch.cuda.synchronize()
+        y1 = dc.y.clone()
+        for _ in range(3):
+            dc.run(algo)
+        torch.cuda.synchronize()
+        assert torch.equal(y1, dc.y)
+    finally:
+        dc.close()
+
+
+def test_families_agree_with_each_other():
+    import torch
+    cs = datagen.CONFIGS["cfg2"].with_(n=4)
+    dc = DeviceConv(cs)
+    try:
+        dc.run(IMPLICIT)
+        torch.cuda.synchronize()
+        y_imp = dc.y_nchw()
+        dc.run(IM2COL)
+        torch.cuda.synchronize()
+        y_exp = dc.y_nchw()
+    finally:
+        dc.close()
+    _, a_ref = oracle.conv2d(dc.x_host, dc.w_host, dc.b_host, cs.stride, cs.pad, cs.dil, cs.groups)
+    _, pt = oracle.normalised_errors(y_imp, y_exp, a_ref)
+    assert pt <= 2e-5
+
+
+def test_chunked_explicit_path(monkeypatch):
+    monkeypatch.setenv("CONV2D_WORKSPACE_LIMIT_BYTES", str(3 << 20))
+    cs = _shape(3, 16, 33, 31, 24, 3, 3, st=(1, 2), pd=(1, 1), seed=9)
+    import torch
+    dc = DeviceConv(cs)
+    try:
+        assert dc.plan(IM2COL).chunks > 2
+        dc.run(IM2COL)
+        torch.cuda.synchronize()
+        y = dc.y_nchw()
+        bd = dc.breakdown(IM2COL)
+        assert bd["calls"]["in_packing"] == dc.plan(IM2COL).chunks
+    finally:
+        dc.close()
+    y_ref, a_ref = oracle.conv2d(dc.x_host, dc.w_host, dc.b_host, cs.stride, cs.pad, cs.dil, cs.groups)
+    assert oracle.normalised_errors(y, y_ref, a_ref)[1] <= 1e-5
+
+
+def test_breakdown_phases_and_invariants():
+    import torch
+    cs = datagen.CONFIGS["cfg1"].with_(layout="nhwc")
+    dc = DeviceConv(cs)
+    try:
+        for algo in (IMPLICIT, IM2COL, DIRECT):
+            for _ in range(3):
+                dc.run(algo)
+        torch.cuda.synchronize()
+        for algo in (IMPLICIT, IM2COL, DIRECT):
+            bd = dc.breakdown(algo)
+            ms, calls = bd["ms"], bd["calls"]
+            assert bd["fwd_calls"] == 3 and calls["pre_analysis"] == 1
+            assert calls["in_microkernel"] == 3
+            assert calls["pre_reorder"] == 3 and calls["post_reorder"] == 3
+            assert all(v >= 0 for v in ms.values())
+            assert bd["operation_ms"] == pytest.approx(sum(ms.values()))
+            assert bd["convolution_ms"] == pytest.approx(
+                ms["in_tiling"] + ms["in_packing"] + ms["in_microkernel"] + ms["in_unpacking"])
+            if algo == IM2COL:
+                assert calls["in_packing"] == 3 and calls["in_unpacking"] == 3
+                assert bd["pack_is_preconv"] == 1
+            else:
+                assert "in_packing" in bd["fused"]
+        assert dc.breakdown(B.CONV2D_ALGO_AUTO)["algo"] == "direct"
+        B.conv2d_breakdown_reset(dc.desc)
+        with pytest.raises(B.Conv2dError):
+            dc.breakdown(IMPLICIT)
+        B.conv2d_set_timing(dc.desc, B.CONV2D_TIMING_TOTAL)
+        dc.run(IMPLICIT)
+        torch.cuda.synchronize()
+        bd = dc.breakdown(IMPLICIT)
+        assert bd["total_calls"] == 1 and bd["calls"]["in_microkernel"] == 0
+    finally:
+        dc.close()
+
+
+def test_shared_hip_runtime_with_torch():
+    import torch
+    v = B.conv2d_runtime_version()
+    major, minor = (int(t) for t in torch.version.hip.split(".")[:2])
+    assert v // 10000000 == major and (v // 100000) % 100 == minor
