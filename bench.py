@@ -1,0 +1,275 @@
+"""Benchmark of the conv2d forward primitive on one MI355X.
+
+Default workload: fp32 NCHW conv2d, N=32, C=K=64, 56x56, 3x3, stride 1, pad 1
+(the contraction-bound square-channel layer), AUTO algorithm (implicit GEMM).
+A step is one conv2d_fwd over the whole batch with inputs resident in HBM.
+
+Prints ONE JSON line with the throughput (TFLOP/s), the dominant kernel's
+roofline position (its duration from the HIP events that enclose every phase
+launch in the timed region), the per-phase breakdown of the timed region, the
+explicit im2col path's pack-phase time share on the same workload, and the
+CPU oracle timed on a bounded sample of the same workload.
+
+    python bench.py [--gpus 1] [--steps 50] [--warmup 10] [--workload cfg2] [--no-cpu]
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "conv2d TFLOP/s and % of MFMA/HBM roofline per shape; pack-phase time share"
+PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}   # dense MFMA
+PEAK_HBM_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+KERNEL_SOURCES = {
+    "implicit_gemm": ["paper_2407_10730_amd/csrc/gemm_mfma.hip"],
+    "im2col_gemm": ["paper_2407_10730_amd/csrc/gemm_mfma.hip", "paper_2407_10730_amd/csrc/pack_kernels.hip"],
+    "direct": ["paper_2407_10730_amd/csrc/direct_kernels.hip"],
+}
+
+
+def kernel_hash(algo_name):
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES[algo_name]:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def describe(cs):
+    return (f"conv2d fwd {cs.layout.upper()} {cs.x_dtype}->{cs.y_dtype} N{cs.n} C{cs.c} {cs.h}x{cs.w} "
+            f"K{cs.k} {cs.r}x{cs.s} s{cs.stride[0]}x{cs.stride[1]} p{cs.pad[0]}x{cs.pad[1]} "
+            f"d{cs.dil[0]}x{cs.dil[1]} g{cs.groups}{' +bias' if cs.has_bias else ''}")
+
+
+def algorithmic_bytes(cs, nkhw):
+    """Bytes the operation must move at least once: the input pixels its windows touch,
+    the weights, the bias and the output."""
+    n, k, ho, wo = nkhw
+    xs = 2 if cs.x_dtype == "bf16" else 4
+    ys = 2 if cs.y_dtype == "bf16" else 4
+    rows = set()
+    for o in range(ho):
+        for r in range(cs.r):
+            h = o * cs.stride[0] - cs.pad[0] + r * cs.dil[0]
+            if 0 <= h < cs.h:
+                rows.add(h)
+    cols = set()
+    for o in range(wo):
+        for s in range(cs.s):
+            w = o * cs.stride[1] - cs.pad[1] + s * cs.dil[1]
+            if 0 <= w < cs.w:
+                cols.add(w)
+    x_touched = n * cs.c * len(rows) * len(cols) * xs
+    w_bytes = k * (cs.c // cs.groups) * cs.r * cs.s * xs
+    b_bytes = 4 * k if cs.has_bias else 0
+    return x_touched + w_bytes + b_bytes + n * k * ho * wo * ys
+
+
+def load_traffic(workload, algo_name):
+    try:
+        with open(TRAFFIC_FILE) as f:
+            data = json.load(f)
+    except (OSError, ValueError):
+        return None
+    ent = data.get(f"{workload}:{algo_name}")
+    if not ent or ent.get("kernel_hash") != kernel_hash(algo_name):
+        return None
+    return ent.get("bytes_per_launch")
+
+
+def cpu_baseline(cs, x, w, b, y_gpu, flops_per_image, target_s=10.0):
+    """Time the fp64 oracle on the first images of the batch (host cores) and
+    compare the GPU output on them."""
+    import numpy as np
+    import oracle
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or len(os.sched_getaffinity(0))
+    threads = max(1, min(threads, len(os.sched_getaffinity(0))))
+    bias = b if cs.has_bias else None
+    t0 = time.perf_counter()
+    oracle.conv2d(x[:1], w, bias, cs.stride, cs.pad, cs.dil, cs.groups, nthreads=threads, want_abs=False)
+    t1 = time.perf_counter() - t0
+    n_img = int(max(1, min(cs.n, round(target_s / max(t1, 1e-6)))))
+    t0 = time.perf_counter()
+    y_ref, a_ref = oracle.conv2d(x[:n_img], w, bias, cs.stride, cs.pad, cs.dil, cs.groups, nthreads=threads)
+    dt = time.perf_counter() - t0
+    lit, pt = oracle.normalised_errors(y_gpu[:n_img], y_ref, a_ref)
+    res = {
+        "value": flops_per_image * n_img / dt / 1e12,
+        "unit": "TFLOP/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": f"fp64 seven-loop oracle over the first {n_img} of {cs.n} images (all outputs), "
+                  f"{dt:.2f} s wall",
+        "seconds": dt,
+        "cpu_model": _cpu_model(),
+    }
+    return res, {"images": n_img, "err_per_point": pt, "err_literal": lit}
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def time_algo(dc, algo, steps, warmup, B, torch):
+    """Warm up, then time exactly `steps` calls bracketed by device synchronisation;
+    phase events are on (they enclose every kernel launch on the stream)."""
+    stream = torch.cuda.current_stream()
+    B.conv2d_set_timing(dc.desc, B.CONV2D_TIMING_PHASES)
+    for _ in range(warmup):
+        dc.run(algo, stream)
+    torch.cuda.synchronize()
+    B.conv2d_breakdown_reset(dc.desc)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        dc.run(algo, stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    bd = dc.breakdown(algo)
+    return wall, bd
+
+
+def cold_median(dc, algo, runs, B, torch):
+    """Median of single calls with the 256 MB last-level cache flushed before each
+    (flush outside the timed events)."""
+    stream = torch.cuda.current_stream()
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    B.conv2d_set_timing(dc.desc, B.CONV2D_TIMING_TOTAL)
+    B.conv2d_breakdown_reset(dc.desc)
+    times = []
+    for _ in range(runs):
+        flush.fill_(1)
+        torch.cuda.synchronize()
+        before = dc.breakdown(algo)["total_ms"] if times else 0.0
+        dc.run(algo, stream)
+        torch.cuda.synchronize()
+        after = dc.breakdown(algo)["total_ms"]
+        times.append(after - before)
+    del flush
+    times.sort()
+    return times[len(times) // 2]
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="cfg2")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cold-runs", type=int, default=20)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              f"(the conv2d library runs on a single MI355X)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import datagen
+    from paper_2407_10730_amd import binding as B
+    from paper_2407_10730_amd.runner import DeviceConv
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    B.load()
+    cs = datagen.CONFIGS[args.workload]
+    print(f"[bench] workload {args.workload}: {describe(cs)}", file=sys.stderr, flush=True)
+    dc = DeviceConv(cs)
+    nkhw = dc.out_nkhw
+    n, k, ho, wo = nkhw
+    flops = 2 * n * k * (cs.c // cs.groups) * cs.r * cs.s * ho * wo
+    algo = dc.plan(B.CONV2D_ALGO_AUTO).algo
+    algo_name = B.ALGO_NAMES[algo]
+
+    wall, bd = time_algo(dc, algo, args.steps, args.warmup, B, torch)
+    ms_per_step = wall * 1e3 / args.steps
+    tflops = flops / (ms_per_step * 1e-3) / 1e12
+    mk_calls = bd["calls"]["in_microkernel"]
+    kern_ms = bd["ms"]["in_microkernel"] / max(mk_calls, 1) * (mk_calls / args.steps)
+    kern_launch_ms = bd["ms"]["in_microkernel"] / max(mk_calls, 1)
+    print(f"[bench] {algo_name}: {ms_per_step*1e3:.1f} us/step, {tflops:.1f} TFLOP/s, kernel "
+          f"{kern_launch_ms*1e3:.1f} us/launch", file=sys.stderr, flush=True)
+    y_gpu = dc.y_nchw()
+
+    xdt = cs.x_dtype
+    alg_bytes = algorithmic_bytes(cs, nkhw)
+    ai = flops / alg_bytes
+    ridge = PEAK_TFLOPS[xdt] * 1e12 / (PEAK_HBM_GBS * 1e9)
+    if ai >= ridge:
+        achieved = flops / (kern_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": PEAK_TFLOPS[xdt], "unit": "TFLOP/s",
+                "frac": achieved / PEAK_TFLOPS[xdt]}
+    else:
+        achieved = alg_bytes / (kern_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": achieved / PEAK_HBM_GBS}
+    roof["kernel"] = f"{algo_name} microkernel"
+    roof["kernel_us_per_launch"] = kern_launch_ms * 1e3
+    roof["launches_per_step"] = mk_calls / args.steps
+    roof["algorithmic_bytes"] = alg_bytes
+    roof["algorithmic_flops"] = flops
+    roof["traffic"] = load_traffic(args.workload, algo_name)
+
+    # explicit im2col baseline on the same workload: pack-phase share
+    wall_e, bd_e = time_algo(dc, B.CONV2D_ALGO_IM2COL_GEMM, max(5, args.steps // 5), 3, B, torch)
+    ms_e = wall_e * 1e3 / max(5, args.steps // 5)
+    opsum = bd_e["ms"]["in_packing"] + bd_e["ms"]["in_microkernel"] + bd_e["ms"]["in_unpacking"]
+    explicit = {
+        "ms_per_step": ms_e,
+        "tflops": flops / (ms_e * 1e-3) / 1e12,
+        "phase_ms_per_step": {p: v / bd_e["fwd_calls"] for p, v in bd_e["ms"].items() if p != "pre_analysis"},
+        "pack_share": bd_e["ms"]["in_packing"] / opsum if opsum > 0 else None,
+        "t_explicit_over_t_implicit": ms_e / ms_per_step,
+    }
+    cold = cold_median(dc, algo, args.cold_runs, B, torch)
+
+    out = {
+        "metric": METRIC,
+        "value": tflops,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": {"f32": "f32", "bf16": "bf16"}[xdt],
+        "data": "synthetic (seeded U[-1,1])",
+        "config": {"workload": f"{args.workload}: {describe(cs)}", "algo": algo_name,
+                   "flops": flops, "arith_intensity": ai},
+        "roofline": roof,
+        "breakdown_ms_per_step": {p: v / bd["fwd_calls"] for p, v in bd["ms"].items()
+                                  if p != "pre_analysis"},
+        "fused_phases": bd["fused"],
+        "pre_analysis_ms_once": bd["ms"]["pre_analysis"],
+        "explicit_im2col": explicit,
+        "cold_cache_ms_median": cold,
+        "cold_cache_tflops": flops / (cold * 1e-3) / 1e12,
+    }
+    if not args.no_cpu:
+        x = dc.x_host
+        cb, parity = cpu_baseline(cs, x, dc.w_host, dc.b_host, y_gpu, flops // n)
+        out["cpu_baseline"] = cb
+        out["parity_on_cpu_sample"] = parity
+    dc.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

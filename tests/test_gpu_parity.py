@@ -176,7 +176,7 @@ def test_families_agree_with_each_other():
 
 
 def test_chunked_explicit_path(monkeypatch):
-    monkeypatch.setenv("CONV2D_WORKSPACE_LIMIT_BYTES", str(3 << 20))
+    monkeypatch.setenv("CONV2D_WORKSPACE_LIMIT_BYTES", "200000")
     cs = _shape(3, 16, 33, 31, 24, 3, 3, st=(1, 2), pd=(1, 1), seed=9)
     import torch
     dc = DeviceConv(cs)
