@@ -27,7 +27,7 @@ PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}   # dense MFMA
 PEAK_HBM_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 KERNEL_SOURCES = {
-    "implicit_gemm": ["paper_2407_10730_amd/csrc/gemm_mfma.hip"],
+    "implicit_gemm": ["paper_2407_10730_amd/csrc/gemm_mfma.hip", "paper_2407_10730_amd/csrc/pack_kernels.hip"],
     "im2col_gemm": ["paper_2407_10730_amd/csrc/gemm_mfma.hip", "paper_2407_10730_amd/csrc/pack_kernels.hip"],
     "direct": ["paper_2407_10730_amd/csrc/direct_kernels.hip"],
 }
@@ -123,11 +123,12 @@ def _cpu_model():
     return "unknown"
 
 
-def time_algo(dc, algo, steps, warmup, B, torch):
-    """Warm up, then time exactly `steps` calls bracketed by device synchronisation;
-    phase events are on (they enclose every kernel launch on the stream)."""
+def time_algo(dc, algo, steps, warmup, B, torch, timing):
+    """Warm up, then time exactly `steps` calls bracketed by device synchronisation.
+    timing = CONV2D_TIMING_OFF for the headline loop (no events between kernels), or
+    CONV2D_TIMING_PHASES for the breakdown loop (an event pair around every phase launch)."""
     stream = torch.cuda.current_stream()
-    B.conv2d_set_timing(dc.desc, B.CONV2D_TIMING_PHASES)
+    B.conv2d_set_timing(dc.desc, timing)
     for _ in range(warmup):
         dc.run(algo, stream)
     torch.cuda.synchronize()
@@ -138,7 +139,7 @@ def time_algo(dc, algo, steps, warmup, B, torch):
         dc.run(algo, stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    bd = dc.breakdown(algo)
+    bd = dc.breakdown(algo) if timing == B.CONV2D_TIMING_PHASES else None
     return wall, bd
 
 
@@ -163,6 +164,77 @@ def cold_median(dc, algo, runs, B, torch):
     return times[len(times) // 2]
 
 
+PROFILE_COMMANDS = {
+    "trace": "rocprofv3 --kernel-trace --stats -f csv -d {d}/trace -o run -- python -u bench.py --no-cpu --workload {w}",
+    "pmc1": "rocprofv3 --pmc SQ_WAVES SQ_BUSY_CYCLES SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU SQ_INSTS_MFMA "
+            "SQ_LDS_BANK_CONFLICT GRBM_GUI_ACTIVE -f csv -d {d}/pmc1 -o run -- python -u bench.py --no-cpu "
+            "--steps 5 --warmup 1 --cold-runs 1 --workload {w}",
+    "pmc2": "rocprofv3 --pmc FETCH_SIZE -f csv -d {d}/pmc2 -o run -- python -u bench.py --no-cpu --steps 5 "
+            "--warmup 1 --cold-runs 1 --calibrate-copy --workload {w}",
+    "pmc3": "rocprofv3 --pmc WRITE_SIZE -f csv -d {d}/pmc3 -o run -- python -u bench.py --no-cpu --steps 5 "
+            "--warmup 1 --cold-runs 1 --calibrate-copy --workload {w}",
+}
+
+
+def summarize_profiles(d, workload, algo_name="implicit_gemm"):
+    """Turn the rocprofv3 CSV outputs of PROFILE_COMMANDS into the short text summaries
+    kept under profiles/ and the per-launch HBM traffic in profiles/traffic.json."""
+    import csv
+    import collections
+
+    def rows(path):
+        with open(path) as f:
+            return list(csv.DictReader(f))
+
+    def short(name):
+        return name.split("(")[0].replace("void ", "")[:90]
+
+    lines = [f"# rocprofv3 summary: workload {workload}", ""]
+    stats = rows(os.path.join(d, "trace", "run_kernel_stats.csv"))
+    lines += ["## kernel trace (--kernel-trace --stats)", "",
+              "command (from the repository root on the GPU box): `"
+              + PROFILE_COMMANDS["trace"].format(d="gpurun_out/<dir>", w=workload) + "`", "",
+              "| kernel | calls | avg us | min us | max us | share % |", "|---|---|---|---|---|---|"]
+    for r in stats:
+        lines.append(f"| `{short(r['Name'])}` | {r['Calls']} | {float(r['AverageNs'])/1e3:.1f} | "
+                     f"{float(r['MinNs'])/1e3:.1f} | {float(r['MaxNs'])/1e3:.1f} | {float(r['Percentage']):.1f} |")
+    counters = collections.defaultdict(lambda: collections.defaultdict(list))
+    for sub in ("pmc1", "pmc2", "pmc3"):
+        path = os.path.join(d, sub, "run_counter_collection.csv")
+        if not os.path.exists(path):
+            continue
+        for r in rows(path):
+            counters[(r["Kernel_Name"], r["Grid_Size"])][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    # calibration: the 1 GiB device copy
+    cal_f = cal_w = None
+    for (name, grid), cs in counters.items():
+        if "copyBuffer" in name and cs.get("FETCH_SIZE") and max(cs["FETCH_SIZE"]) > 400000:
+            cal_f = (1 << 20) / (sum(cs["FETCH_SIZE"]) / len(cs["FETCH_SIZE"]))
+        if "copyBuffer" in name and cs.get("WRITE_SIZE") and max(cs["WRITE_SIZE"]) > 400000:
+            cal_w = (1 << 20) / (sum(cs["WRITE_SIZE"]) / len(cs["WRITE_SIZE"]))
+    lines += ["", "## counters per kernel (mean per dispatch)", ""]
+    for k in ("pmc1", "pmc2", "pmc3"):
+        lines.append("command: `" + PROFILE_COMMANDS[k].format(d="gpurun_out/<dir>", w=workload) + "`")
+    lines += ["", f"HBM byte scale factors from the 1 GiB device copy: FETCH_SIZE x {cal_f}, WRITE_SIZE x {cal_w}"
+              " (counters are in KiB per dispatch)", ""]
+    traffic = {}
+    for (name, grid), cs in sorted(counters.items()):
+        if "cv::" not in name:
+            continue
+        mean = {c: sum(v) / len(v) for c, v in cs.items()}
+        txt = ", ".join(f"{c}={v:.0f}" for c, v in sorted(mean.items()))
+        lines.append(f"- `{short(name)}` grid {grid}: {txt}")
+        if "FETCH_SIZE" in mean and "WRITE_SIZE" in mean and cal_f and cal_w:
+            b = mean["FETCH_SIZE"] * 1024 * cal_f + mean["WRITE_SIZE"] * 1024 * cal_w
+            traffic[short(name)] = b
+            lines.append(f"  - HBM traffic per dispatch: {b/1e6:.2f} MB (fetch {mean['FETCH_SIZE']*1024*cal_f/1e6:.2f}"
+                         f" + write {mean['WRITE_SIZE']*1024*cal_w/1e6:.2f})")
+        if "SQ_VALU_MFMA_BUSY_CYCLES" in mean and "GRBM_GUI_ACTIVE" in mean:
+            busy = mean["SQ_VALU_MFMA_BUSY_CYCLES"] / 1024 / (mean["GRBM_GUI_ACTIVE"] / 8)
+            lines.append(f"  - MFMA busy fraction (busy cycles per SIMD / active cycles per XCD): {busy:.3f}")
+    return "\n".join(lines) + "\n", traffic
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -171,7 +243,32 @@ def main():
     ap.add_argument("--workload", default="cfg2")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cold-runs", type=int, default=20)
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run a plain 1 GiB device copy (reference kernel for HBM byte counters)")
+    ap.add_argument("--summarize-profiles", metavar="DIR",
+                    help="write the text summary of rocprofv3 outputs in DIR (no GPU needed) and exit")
+    ap.add_argument("--traffic-kernel", default=None,
+                    help="with --summarize-profiles: kernel whose traffic goes to profiles/traffic.json")
     args = ap.parse_args()
+    if args.summarize_profiles:
+        text, traffic = summarize_profiles(args.summarize_profiles, args.workload)
+        print(text)
+        if args.traffic_kernel:
+            key = [k for k in traffic if args.traffic_kernel in k]
+            if len(key) != 1:
+                sys.exit(f"traffic kernel {args.traffic_kernel!r} matches {key}")
+            try:
+                with open(TRAFFIC_FILE) as f:
+                    data = json.load(f)
+            except (OSError, ValueError):
+                data = {}
+            algo_name = "im2col_gemm" if "DENSE" in key[0] else "implicit_gemm"
+            data[f"{args.workload}:implicit_gemm"] = {
+                "kernel": key[0], "bytes_per_launch": traffic[key[0]],
+                "kernel_hash": kernel_hash("implicit_gemm")}
+            with open(TRAFFIC_FILE, "w") as f:
+                json.dump(data, f, indent=1)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               f"(the conv2d library runs on a single MI355X)", file=sys.stderr)
@@ -196,9 +293,12 @@ def main():
     algo = dc.plan(B.CONV2D_ALGO_AUTO).algo
     algo_name = B.ALGO_NAMES[algo]
 
-    wall, bd = time_algo(dc, algo, args.steps, args.warmup, B, torch)
+    # headline: no events inside the timed region
+    wall, _ = time_algo(dc, algo, args.steps, args.warmup, B, torch, B.CONV2D_TIMING_OFF)
     ms_per_step = wall * 1e3 / args.steps
     tflops = flops / (ms_per_step * 1e-3) / 1e12
+    # the same loop again with an event pair around every phase launch: kernel durations
+    wall_ph, bd = time_algo(dc, algo, args.steps, 2, B, torch, B.CONV2D_TIMING_PHASES)
     mk_calls = bd["calls"]["in_microkernel"]
     kern_ms = bd["ms"]["in_microkernel"] / max(mk_calls, 1) * (mk_calls / args.steps)
     kern_launch_ms = bd["ms"]["in_microkernel"] / max(mk_calls, 1)
@@ -226,8 +326,10 @@ def main():
     roof["traffic"] = load_traffic(args.workload, algo_name)
 
     # explicit im2col baseline on the same workload: pack-phase share
-    wall_e, bd_e = time_algo(dc, B.CONV2D_ALGO_IM2COL_GEMM, max(5, args.steps // 5), 3, B, torch)
-    ms_e = wall_e * 1e3 / max(5, args.steps // 5)
+    ne = max(5, args.steps // 5)
+    wall_e, _ = time_algo(dc, B.CONV2D_ALGO_IM2COL_GEMM, ne, 3, B, torch, B.CONV2D_TIMING_OFF)
+    _, bd_e = time_algo(dc, B.CONV2D_ALGO_IM2COL_GEMM, ne, 1, B, torch, B.CONV2D_TIMING_PHASES)
+    ms_e = wall_e * 1e3 / ne
     opsum = bd_e["ms"]["in_packing"] + bd_e["ms"]["in_microkernel"] + bd_e["ms"]["in_unpacking"]
     explicit = {
         "ms_per_step": ms_e,
@@ -256,6 +358,7 @@ def main():
         "roofline": roof,
         "breakdown_ms_per_step": {p: v / bd["fwd_calls"] for p, v in bd["ms"].items()
                                   if p != "pre_analysis"},
+        "phase_events_overhead_ms_per_step": (wall_ph - wall) * 1e3 / args.steps,
         "fused_phases": bd["fused"],
         "pre_analysis_ms_once": bd["ms"]["pre_analysis"],
         "explicit_im2col": explicit,
@@ -268,6 +371,15 @@ def main():
         out["cpu_baseline"] = cb
         out["parity_on_cpu_sample"] = parity
     dc.close()
+    if args.calibrate_copy:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        src.fill_(3)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        out["copy_calibration_bytes"] = 1 << 30
+        del src, dst
     print(json.dumps(out), flush=True)
 
 

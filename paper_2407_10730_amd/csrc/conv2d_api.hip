@@ -14,6 +14,7 @@
 // sum of all phases and Convolution Time the sum of the in-convolution ones.
 #include <algorithm>
 #include <chrono>
+#include <cstdio>
 #include <cstdlib>
 #include <cstring>
 #include <new>
@@ -43,8 +44,11 @@ struct EvRec {
 };
 
 struct GemmPlan {
+    int kind = 0;  // 0: 32x32-MFMA kernels (tile config)
     int tile = TILE_64x128;
-    int bm = 64, bn = 128;
+    int bm = 64, bn = 128, u = 0;
+    int bk = 16;   // reduction rows per stage
+    int pf = 1;    // register prefetch distance (fp32 32x32 kernels)
     int nstages = 0;
 };
 
@@ -78,30 +82,53 @@ int env_timing() {
     return CONV2D_TIMING_PHASES;
 }
 
-// Choose the GEMM block tile: fewest rounds of full-chip tile waves, weighted by
-// the MFMA efficiency of each wave tile (64x64 per wave is the reference).
-GemmPlan choose_tile(int64_t M, int64_t P, int64_t G, int64_t kred, int xdt) {
-    struct Cand { int tile; double eff; };
-    const Cand cands[] = {{TILE_64x256, 1.0}, {TILE_128x128, 1.0}, {TILE_64x128, 0.85},
-                          {TILE_128x64, 0.85}, {TILE_64x64, 0.7}};
+// Choose the GEMM kernel and block tile.  Cost = (most tiles any CU runs) x
+// (work of one tile) / (MFMA efficiency of its wave tile): with many more tiles
+// than CUs the tiles are dealt out evenly, so the busiest CU sets the time.
+// CONV2D_GEMM = "k32:TILE[:BK[:PF]]" overrides the choice for tuning.
+GemmPlan choose_tile(int64_t M, int64_t P, int64_t G, int64_t kred, int xdt, int64_t cg) {
     const int cus = 256;
     GemmPlan best;
     double best_cost = 1e300;
+    // Candidate block tiles of the 32x32-MFMA kernels, with the measured MFMA efficiency of
+    // their wave tiles relative to 64x128 (fp32, MI355X).
+    struct Cand { int tile; double eff; };
+    const Cand cands[] = {{TILE_64x128, 1.0}, {TILE_64x256, 0.8}, {TILE_64x64, 0.85},
+                          {TILE_128x64, 0.9}, {TILE_128x128, 0.85}};
     for (const Cand& c : cands) {
         const TileShape ts = kTileShapes[c.tile];
         const int64_t tiles = ceil_div(M, ts.bm) * ceil_div(P, ts.bn) * G;
-        const double rounds = (double)ceil_div(tiles, cus);
-        const double cost = rounds * ts.bm * ts.bn / c.eff;
+        const double cost = (double)ceil_div(tiles, cus) * ts.bm * ts.bn / c.eff;
         if (cost < best_cost) {
             best_cost = cost;
+            best.kind = 0;
             best.tile = c.tile;
             best.bm = ts.bm;
             best.bn = ts.bn;
         }
     }
-    const int bk = xdt == CONV2D_BF16 ? 32 : 16;
-    best.nstages = (int)ceil_div(kred, bk);
+    (void)cg;
+    if (best.kind == 0) best.bk = xdt == CONV2D_BF16 ? 32 : 16;
+    const char* ov = std::getenv("CONV2D_GEMM");
+    if (ov) {
+        int a = 0, b = 0, c = 16;
+        if (std::sscanf(ov, "k32:%d:%d:%d", &a, &b, &c) >= 1 && a >= 0 && a < TILE_COUNT) {
+            int bk = xdt == CONV2D_BF16 ? 32 : (std::strchr(ov + 4, ':') ? b : 16);
+            int pf = std::strchr(ov + 4, ':') && std::strchr(std::strchr(ov + 4, ':') + 1, ':') ? c : 1;
+            if (xdt == CONV2D_BF16 || gemm32_f32_supported(a, bk, pf)) {
+                best.kind = 0; best.tile = a; best.bm = kTileShapes[a].bm; best.bn = kTileShapes[a].bn;
+                best.bk = bk;
+                best.pf = xdt == CONV2D_BF16 ? 1 : pf;
+            }
+        }
+    }
+    best.nstages = (int)ceil_div(kred, best.bk);
     return best;
+}
+
+hipError_t dispatch_gemm(const GemmPlan& gp, const GemmArgs& a, int bsrc, int epi, int xdt, int ydt,
+                         int groups, hipStream_t s) {
+    return launch_gemm(a, gp.tile, gp.bk, gp.pf, bsrc, epi, xdt, ydt, groups, s);
 }
 
 }  // namespace
@@ -112,6 +139,7 @@ struct conv2d_desc {
     uint32_t opclass = 0;
     int auto_algo = CONV2D_ALGO_IMPLICIT_GEMM;
     bool implicit_ok = false, direct_ok = false;
+    bool implicit_tap = false;  // tap-major gather (C/g a multiple of the stage depth)
     GemmPlan implicit;
     ExplicitPlan expl;
     std::vector<KTabEntry> ktab_host;
@@ -124,6 +152,8 @@ struct conv2d_desc {
     int64_t xr_bytes = 0;
     void* yr = nullptr;  // NCHW result before the NHWC reorder
     int64_t yr_bytes = 0;
+    void* wr = nullptr;  // weights in tap-major order for the implicit GEMM
+    int64_t wr_bytes = 0;
 
     int timing = CONV2D_TIMING_PHASES;
     double analysis_ms = 0.0;
@@ -217,7 +247,7 @@ void plan_explicit(conv2d_desc* d) {
     e.chunks = ceil_div(total_rows, rows);
     e.col_bytes = rows * row_col;
     e.c_bytes = rows * row_c;
-    e.gemm = choose_tile(g.Kg, rows * g.Wo, g.G, g.Kred, g.xdt);
+    e.gemm = choose_tile(g.Kg, rows * g.Wo, g.G, g.Kred, g.xdt, g.Cg);
 }
 
 // ------------------------------------------------------------------ events
@@ -332,6 +362,16 @@ int run_implicit(conv2d_desc* d, const void* x, const void* w, const float* bias
                  bool ph) {
     const Geometry& g = d->g;
     const GemmPlan& gp = d->implicit;
+    if (d->implicit_tap && g.R * g.S > 1) {
+        // pre-convolution reordering of the filters into the tap-major reduction order
+        const int64_t wb = g.w_elems * elem_size(g.xdt);
+        CV_TRY(ensure_buffer(&d->wr, &d->wr_bytes, wb));
+        Scope sc(d, CONV2D_ALGO_IMPLICIT_GEMM, CONV2D_PH_PRE_REORDER, s, ph);
+        CV_TRY(sc.begin());
+        CV_HIP(launch_repack_tap_major(w, d->wr, g.K, g.Cg, g.R * g.S, (int)elem_size(g.xdt), s));
+        CV_TRY(sc.end());
+        w = d->wr;
+    }
     GemmArgs a{};
     a.a = w;
     a.a_bytes = (uint32_t)(g.w_elems * elem_size(g.xdt));
@@ -343,6 +383,9 @@ int run_implicit(conv2d_desc* d, const void* x, const void* w, const float* bias
     a.ktab = d->ktab_dev;
     a.H = (int32_t)g.H; a.W = (int32_t)g.W; a.Ho = (int32_t)g.Ho; a.Wo = (int32_t)g.Wo;
     a.sh = g.sh; a.sw = g.sw; a.ph = g.ph; a.pw = g.pw;
+    a.dh = g.dh; a.dw = g.dw; a.R = (int32_t)g.R; a.S = (int32_t)g.S; a.RS = (int32_t)(g.R * g.S);
+    a.Cg = (int32_t)g.Cg;
+    a.HW = (int32_t)(g.H * g.W);
     a.x_nstride = g.C * g.H * g.W;
     a.M = (int32_t)g.Kg;
     a.Kred = (int32_t)g.Kred;
@@ -357,7 +400,8 @@ int run_implicit(conv2d_desc* d, const void* x, const void* w, const float* bias
     a.HoWo = (int32_t)(g.Ho * g.Wo);
     Scope sc(d, CONV2D_ALGO_IMPLICIT_GEMM, CONV2D_PH_IN_MICROKERNEL, s, ph);
     CV_TRY(sc.begin());
-    CV_HIP(launch_gemm(a, gp.tile, BSRC_IMPLICIT_NCHW, EPI_NCHW, g.xdt, g.ydt, (int)g.G, s));
+    const int bsrc = d->implicit_tap ? BSRC_IMPLICIT_TAP : BSRC_IMPLICIT_NCHW;
+    CV_HIP(dispatch_gemm(gp, a, bsrc, EPI_NCHW, g.xdt, g.ydt, (int)g.G, s));
     return sc.end();
 }
 
@@ -406,7 +450,7 @@ int run_explicit(conv2d_desc* d, const void* x, const void* w, const float* bias
             a.M = (int32_t)g.Kg;
             a.Kred = (int32_t)g.Kred;
             a.P = (int32_t)pc;
-            a.nstages = (int32_t)ceil_div(g.Kred, g.xdt == CONV2D_BF16 ? 32 : 16);
+            a.nstages = gp.nstages;
             a.grid_m = (int32_t)ceil_div(g.Kg, gp.bm);
             a.grid_p = (int32_t)ceil_div(pc, gp.bn);
             a.y = cbuf;
@@ -416,7 +460,7 @@ int run_explicit(conv2d_desc* d, const void* x, const void* w, const float* bias
             a.HoWo = (int32_t)(g.Ho * g.Wo);
             Scope sc(d, CONV2D_ALGO_IM2COL_GEMM, CONV2D_PH_IN_MICROKERNEL, s, ph);
             CV_TRY(sc.begin());
-            CV_HIP(launch_gemm(a, gp.tile, BSRC_DENSE, EPI_DENSE, g.xdt, CONV2D_F32, (int)g.G, s));
+            CV_HIP(dispatch_gemm(gp, a, BSRC_DENSE, EPI_DENSE, g.xdt, CONV2D_F32, (int)g.G, s));
             CV_TRY(sc.end());
         }
         {
@@ -491,7 +535,8 @@ int conv2d_desc_create(const conv2d_params* params, conv2d_desc** out) {
     d->timing = env_timing();
     d->implicit_ok = implicit_supported(g);
     d->direct_ok = direct_supported(g);
-    d->implicit = choose_tile(g.Kg, g.P, g.G, g.Kred, g.xdt);
+    d->implicit = choose_tile(g.Kg, g.P, g.G, g.Kred, g.xdt, g.Cg);
+    d->implicit_tap = g.Cg % d->implicit.bk == 0;
     build_ktab(d);
     plan_explicit(d);
     if (d->direct_ok && g.G > 1 && g.Cg <= 8)
@@ -521,6 +566,7 @@ int conv2d_desc_destroy(conv2d_desc* d) {
     if (d->ws) hipFree(d->ws);
     if (d->xr) hipFree(d->xr);
     if (d->yr) hipFree(d->yr);
+    if (d->wr) hipFree(d->wr);
     delete d;
     return CONV2D_OK;
 }
@@ -650,7 +696,8 @@ int conv2d_plan_query(const conv2d_desc* d, int algo, conv2d_plan_info* out) {
     const Geometry& g = d->g;
     out->algo = algo;
     out->kred = (int32_t)g.Kred;
-    out->kred_pad = (int32_t)(ceil_div(g.Kred, g.xdt == CONV2D_BF16 ? 32 : 16) * (g.xdt == CONV2D_BF16 ? 32 : 16));
+    const int bk = algo == CONV2D_ALGO_IM2COL_GEMM ? d->expl.gemm.bk : d->implicit.bk;
+    out->kred_pad = (int32_t)(ceil_div(g.Kred, bk) * bk);
     out->needs_reorder = g.layout == CONV2D_NHWC ? 1 : 0;
     out->op_class = (int32_t)d->opclass;
     out->chunks = 1;

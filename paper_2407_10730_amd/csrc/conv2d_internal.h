@@ -30,7 +30,11 @@ struct TileShape { int bm, bn; };
 static const TileShape kTileShapes[TILE_COUNT] = {{64, 64}, {64, 128}, {64, 256}, {128, 128}, {128, 64}};
 
 // Source of the GEMM's B operand (the im2col matrix, Kred x P).
-enum BSrc { BSRC_IMPLICIT_NCHW = 0, BSRC_DENSE = 1 };
+//  IMPLICIT_NCHW : gathered from NCHW x, reduction index kr = (c, r, s) looked up in the tap table
+//  DENSE         : read from a packed column matrix [G][Kred][ldb]
+//  IMPLICIT_TAP  : gathered from NCHW x in tap-major order kr' = (r, s, c); one filter tap per
+//                  stage, so needs C/g to be a multiple of the stage depth (no table)
+enum BSrc { BSRC_IMPLICIT_NCHW = 0, BSRC_DENSE = 1, BSRC_IMPLICIT_TAP = 2 };
 // Destination of the GEMM result.
 enum Epi { EPI_NCHW = 0, EPI_DENSE = 1 };
 
@@ -54,6 +58,7 @@ struct GemmArgs {
     int32_t ldb;
     const KTabEntry* ktab;
     int32_t H, W, Ho, Wo, sh, sw, ph, pw;
+    int32_t dh, dw, R, S, RS, Cg, HW;  // tap-major gather: filter dims, R*S, channels per group, H*W
     int64_t x_nstride;    // C*H*W
     int32_t M, Kred, P, nstages;
     int32_t grid_p, grid_m;
@@ -67,8 +72,12 @@ struct GemmArgs {
     int32_t p_offset;     // global index of column 0 (explicit chunks)
 };
 
-hipError_t launch_gemm(const GemmArgs& a, int tile, int bsrc, int epi, int xdt, int ydt, int groups,
-                       hipStream_t stream);
+// 32x32-MFMA kernels.  fp32: stage depth bk in {16, 32}, register prefetch distance pf in {1, 2};
+// bf16: bk = 32, pf = 1 (arguments ignored).
+bool gemm32_f32_supported(int tile, int bk, int pf);
+hipError_t launch_gemm(const GemmArgs& a, int tile, int bk, int pf, int bsrc, int epi, int xdt, int ydt,
+                       int groups, hipStream_t stream);
+
 
 // im2col of a chunk of output pixels [p_begin, p_begin + pc): col[g][kr][pl].
 struct Im2colArgs {
@@ -106,6 +115,10 @@ struct DirectArgs {
     int32_t N;
 };
 hipError_t launch_direct(const DirectArgs& a, int xdt, int ydt, hipStream_t stream);
+
+// weight repack to tap-major order: w [K][C/g][R*S] -> wr [K][R*S][C/g].
+hipError_t launch_repack_tap_major(const void* w, void* wr, int64_t k, int64_t cg, int64_t rs, int elem_bytes,
+                                   hipStream_t stream);
 
 // layout transforms between NHWC and NCHW (one image = a [HW x C] <-> [C x HW] transpose).
 hipError_t launch_nhwc_to_nchw(const void* src, void* dst, int64_t n, int64_t c, int64_t hw,

@@ -17,120 +17,31 @@
 // Every global access goes through a raw buffer resource: loads outside the
 // buffer return zero and stores outside it are dropped, and masked elements
 // use an offset beyond any valid record.
-#include "conv2d_internal.h"
+#include "device_common.h"
 
 namespace cv {
 
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
-#define OOB_OFF 0x80000000u
-#define RSRC_WORD3 0x00020000
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, RSRC_WORD3);
-}
-
-__device__ __forceinline__ float ld_f32(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
-}
-__device__ __forceinline__ uint16_t ld_u16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-    return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
-}
-__device__ __forceinline__ void st_f32(__amdgpu_buffer_rsrc_t r, uint32_t off, float v) {
-    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), r, off, 0, 0);
-}
-__device__ __forceinline__ void st_u16(__amdgpu_buffer_rsrc_t r, uint32_t off, uint16_t v) {
-    __builtin_amdgcn_raw_buffer_store_b16(v, r, off, 0, 0);
-}
-
-// fp32 -> bf16 bits, round to nearest even (inputs are finite).
-__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
-    uint32_t u = __builtin_bit_cast(uint32_t, f);
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return (uint16_t)(u >> 16);
-}
-
-template <typename TOut>
-__device__ __forceinline__ void store_out(__amdgpu_buffer_rsrc_t r, uint32_t elem_off_valid, bool ok,
-                                          float v);
-template <>
-__device__ __forceinline__ void store_out<float>(__amdgpu_buffer_rsrc_t r, uint32_t e, bool ok, float v) {
-    st_f32(r, ok ? e * 4u : OOB_OFF, v);
-}
-template <>
-__device__ __forceinline__ void store_out<uint16_t>(__amdgpu_buffer_rsrc_t r, uint32_t e, bool ok,
-                                                    float v) {
-    st_u16(r, ok ? e * 2u : OOB_OFF, f32_to_bf16_rne(v));
-}
-
-// Linear block id -> tile id such that consecutive tile ids land on the same
-// XCD (workgroups are handed to the 8 XCDs round-robin), so the M tiles of one
-// pixel tile and neighbouring pixel tiles share an L2.
-__device__ __forceinline__ int xcd_remap(int bid, int nb) {
-    const int per = nb >> 3, rem = nb & 7;
-    const int xcd = bid & 7, slot = bid >> 3;
-    return xcd < rem ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
-}
-
-// Per-column state of the implicit gather: window origin and base offset.
-struct ColState {
-    int64_t base;  // element offset of x[n, gi*Cg, hi0, wi0] (may be "negative" in padding)
-    int32_t hi0, wi0;
-};
-
-__device__ __forceinline__ ColState col_state(const GemmArgs& A, int p, int gi) {
-    ColState s;
-    if (p < A.P) {
-        const int n = p / A.HoWo;
-        const int hw = p - n * A.HoWo;
-        const int ho = hw / A.Wo;
-        const int wo = hw - ho * A.Wo;
-        s.hi0 = ho * A.sh - A.ph;
-        s.wi0 = wo * A.sw - A.pw;
-        s.base = (int64_t)n * A.x_nstride + (int64_t)gi * A.b_gstride + (int64_t)s.hi0 * A.W + s.wi0;
-    } else {
-        s.hi0 = KTAB_DEAD;
-        s.wi0 = 0;
-        s.base = 0;
-    }
-    return s;
-}
-
-// Byte offset of B[kr][col] for the implicit gather (or OOB_OFF for a zero tap).
-template <int ESIZE>
-__device__ __forceinline__ uint32_t implicit_off(const GemmArgs& A, const ColState& cs, const KTabEntry& e) {
-    const int hi = cs.hi0 + e.roff;
-    const int wi = cs.wi0 + e.soff;
-    const bool ok = ((unsigned)hi < (unsigned)A.H) & ((unsigned)wi < (unsigned)A.W);
-    return ok ? (uint32_t)((cs.base + e.coff) * ESIZE) : OOB_OFF;
-}
-
-// Scalar (wave-uniform) read of one table entry.
-__device__ __forceinline__ KTabEntry ktab_at(const KTabEntry* t, int kr) {
-    kr = __builtin_amdgcn_readfirstlane(kr);
-    return t[kr];
-}
-
 // ============================================================================ fp32
 // Block: 256 threads = 4 waves arranged WM x WN over a BM x BN tile; each wave
-// owns (BM/WM) x (BN/WN) = TM x TN MFMA 32x32x2 tiles.  BK = 16 reduction rows
-// per stage, double-buffered in LDS (k-major, so one MFMA operand read is 32
-// consecutive floats per half-wave).
-template <int BM, int BN, int WM, int WN, int BSRC, int EPI, typename TOut>
+// owns (BM/WM) x (BN/WN) = TM x TN MFMA 32x32x2 tiles.  BK reduction rows per
+// stage, double-buffered in LDS (k-major, so one MFMA operand read is 32
+// consecutive floats per half-wave).  PF = 1: the global loads of stage s+1
+// are issued before the MFMAs of stage s; PF = 2: two register sets, the loads
+// of stage s+2 are issued before the MFMAs of stage s, so a load has two
+// stages of MFMA work to land.
+template <int BM, int BN, int WM, int WN, int BK, int PF, int BSRC, int EPI, typename TOut>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs A) {
-    constexpr int BK = 16;
     constexpr int WTM = BM / WM, WTN = BN / WN;
     constexpr int TM = WTM / 32, TN = WTN / 32;
     static_assert(WM * WN == 4 && TM >= 1 && TN >= 1, "bad wave layout");
+    static_assert(PF == 1 || PF == 2, "prefetch distance");
     constexpr int BNT = BN < 256 ? BN : 256;  // threads along pixels in the B loader
     constexpr int BKT = 256 / BNT;            // threads along k
     constexpr int BCOLS = BN / BNT;           // pixel columns per thread
     constexpr int BROWS = BK / BKT;           // k rows per thread
     constexpr int AROWS = BM * BK / 256;      // A elements per thread
     static_assert(BNT >= 64, "B loader needs wave-uniform k rows");
+    static_assert(256 % BK == 0 && AROWS >= 4 && AROWS % 4 == 0, "A loader layout");
 
     __shared__ float As[2][BK][BM + 1];
     __shared__ float Bs[2][BK][BN];
@@ -153,54 +64,109 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs A) {
     const int tn = t % BNT;
     const int tk = __builtin_amdgcn_readfirstlane(t / BNT);
     ColState cs[BCOLS];
-    int pcol[BCOLS];
+    uint32_t dvb[BCOLS];  // dense: byte offset of column j in row 0 of this group, or OOB
 #pragma unroll
     for (int j = 0; j < BCOLS; ++j) {
-        pcol[j] = p0 + tn + j * BNT;
-        if (BSRC == BSRC_IMPLICIT_NCHW) cs[j] = col_state(A, pcol[j], gi);
+        const int p = p0 + tn + j * BNT;
+        if (BSRC != BSRC_DENSE) cs[j] = col_state(A, p, gi);
+        dvb[j] = p < A.P ? (uint32_t)(((int64_t)gi * A.b_gstride + p) * 4) : OOB_OFF;
     }
     // ---- A loader state: element (m = am + i*(256/BK), k = ak)
     const int ak = t % BK;
     const int am = t / BK;
     const int64_t a_base = (int64_t)gi * A.a_gstride;
 
-    float breg[BROWS][BCOLS];
-    float areg[AROWS];
+    float breg0[BROWS][BCOLS], breg1[BROWS][BCOLS];
+    float areg0[AROWS], areg1[AROWS];
+    // tap-major cursor of the next stage to load.  Channel blocks outermost, filter
+    // taps innermost: the taps of one channel block re-read the same input lines,
+    // which then hit in L1.
+    int cur_c0 = 0, cur_r = 0, cur_s = 0;
 
-    auto load_stage = [&](int stage) {
+    auto load_stage = [&](int stage, float (&breg)[BROWS][BCOLS], float (&areg)[AROWS]) {
         const int k0 = stage * BK;
+        if constexpr (BSRC == BSRC_IMPLICIT_TAP) {
+            const int roff = cur_r * A.dh, soff = cur_s * A.dw;
+            const int tapoff = roff * A.W + soff;
+            uint32_t vb[BCOLS];
 #pragma unroll
-        for (int i = 0; i < BROWS; ++i) {
-            const int kr = k0 + tk + i * BKT;
-            if (BSRC == BSRC_IMPLICIT_NCHW) {
-                const KTabEntry e = ktab_at(A.ktab, kr);
+            for (int j = 0; j < BCOLS; ++j) {
+                const int hi = cs[j].hi0 + roff, wi = cs[j].wi0 + soff;
+                const bool ok = ((unsigned)hi < (unsigned)A.H) & ((unsigned)wi < (unsigned)A.W);
+                vb[j] = ok ? (uint32_t)(((int32_t)cs[j].base + tapoff) * 4) : OOB_OFF;
+            }
 #pragma unroll
-                for (int j = 0; j < BCOLS; ++j) breg[i][j] = ld_f32(rb, implicit_off<4>(A, cs[j], e));
-            } else {
+            for (int i = 0; i < BROWS; ++i) {
+                const uint32_t cofs = (uint32_t)((cur_c0 + tk + i * BKT) * A.HW) * 4u;
 #pragma unroll
-                for (int j = 0; j < BCOLS; ++j) {
-                    const bool ok = (kr < A.Kred) & (pcol[j] < A.P);
-                    const int64_t e = (int64_t)gi * A.b_gstride + (int64_t)kr * A.ldb + pcol[j];
-                    breg[i][j] = ld_f32(rb, ok ? (uint32_t)(e * 4) : OOB_OFF);
+                for (int j = 0; j < BCOLS; ++j) breg[i][j] = ld_f32(rb, vb[j] + cofs);
+            }
+            // weights in tap-major order [K][R*S][C/g]: 4 consecutive channels per 16-byte load
+            const int tap = cur_r * A.S + cur_s;
+#pragma unroll
+            for (int i = 0; i < AROWS / 4; ++i) {
+                const int q = t + i * 256;
+                const int m = m0 + q / (BK / 4);
+                const int64_t e = a_base + (int64_t)m * A.lda + (int64_t)tap * A.Cg + cur_c0 + 4 * (q % (BK / 4));
+                // bit-cast the whole vector: casting its elements one by one made this
+                // compiler emit a single-dword load
+                const f32x4 v = __builtin_bit_cast(
+                    f32x4, __builtin_amdgcn_raw_buffer_load_b128(ra, m < A.M ? (uint32_t)(e * 4) : OOB_OFF, 0, 0));
+#pragma unroll
+                for (int j = 0; j < 4; ++j) areg[4 * i + j] = v[j];
+            }
+            if (++cur_s == A.S) {
+                cur_s = 0;
+                if (++cur_r == A.R) {
+                    cur_r = 0;
+                    cur_c0 += BK;
                 }
             }
-        }
+        } else {
+            if constexpr (BSRC == BSRC_IMPLICIT_NCHW) {
+                KTabEntry e[BROWS];
 #pragma unroll
-        for (int i = 0; i < AROWS; ++i) {
-            const int m = m0 + am + i * (256 / BK);
-            const int kr = k0 + ak;
-            const bool ok = (m < A.M) & (kr < A.Kred);
-            const int64_t e = a_base + (int64_t)m * A.lda + kr;
-            areg[i] = ld_f32(ra, ok ? (uint32_t)(e * 4) : OOB_OFF);
+                for (int i = 0; i < BROWS; ++i) e[i] = ktab_at(A.ktab, k0 + tk + i * BKT);
+#pragma unroll
+                for (int i = 0; i < BROWS; ++i)
+#pragma unroll
+                    for (int j = 0; j < BCOLS; ++j) breg[i][j] = ld_f32(rb, implicit_off<4>(A, cs[j], e[i]));
+            } else {
+#pragma unroll
+                for (int i = 0; i < BROWS; ++i) {
+                    const int kr = k0 + tk + i * BKT;
+                    const bool kok = kr < A.Kred;
+#pragma unroll
+                    for (int j = 0; j < BCOLS; ++j)
+                        breg[i][j] = ld_f32(rb, kok ? dvb[j] + (uint32_t)kr * (uint32_t)A.ldb * 4u : OOB_OFF);
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < AROWS; ++i) {
+                const int m = m0 + am + i * (256 / BK);
+                const int kr = k0 + ak;
+                const bool ok = (m < A.M) & (kr < A.Kred);
+                const int64_t e = a_base + (int64_t)m * A.lda + kr;
+                areg[i] = ld_f32(ra, ok ? (uint32_t)(e * 4) : OOB_OFF);
+            }
         }
     };
-    auto store_stage = [&](int buf) {
+    auto store_stage = [&](int buf, const float (&breg)[BROWS][BCOLS], const float (&areg)[AROWS]) {
 #pragma unroll
         for (int i = 0; i < BROWS; ++i)
 #pragma unroll
             for (int j = 0; j < BCOLS; ++j) Bs[buf][tk + i * BKT][tn + j * BNT] = breg[i][j];
+        if constexpr (BSRC == BSRC_IMPLICIT_TAP) {
 #pragma unroll
-        for (int i = 0; i < AROWS; ++i) As[buf][ak][am + i * (256 / BK)] = areg[i];
+            for (int i = 0; i < AROWS / 4; ++i) {
+                const int q = t + i * 256;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) As[buf][4 * (q % (BK / 4)) + j][q / (BK / 4)] = areg[4 * i + j];
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < AROWS; ++i) As[buf][ak][am + i * (256 / BK)] = areg[i];
+        }
     };
 
     f32x16 acc[TM][TN];
@@ -216,13 +182,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs A) {
     const int lrow = lane >> 5;  // which of the two k rows this half-wave feeds
     const int lcol = lane & 31;
 
-    load_stage(0);
-    store_stage(0);
-    __syncthreads();
-    for (int st = 0; st < A.nstages; ++st) {
-        const int buf = st & 1;
-        const bool more = st + 1 < A.nstages;
-        if (more) load_stage(st + 1);
+    auto compute = [&](int buf) {
 #pragma unroll
         for (int ks = 0; ks < BK / 2; ++ks) {
             float a[TM], b[TN];
@@ -236,8 +196,39 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs A) {
                 for (int j = 0; j < TN; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
         }
-        if (more) store_stage(buf ^ 1);
+    };
+
+    const int n = A.nstages;
+    if constexpr (PF == 1) {
+        load_stage(0, breg0, areg0);
+        store_stage(0, breg0, areg0);
         __syncthreads();
+        for (int st = 0; st < n; ++st) {
+            const int buf = st & 1;
+            const bool more = st + 1 < n;
+            if (more) load_stage(st + 1, breg0, areg0);
+            compute(buf);
+            if (more) store_stage(buf ^ 1, breg0, areg0);
+            __syncthreads();
+        }
+    } else {
+        load_stage(0, breg0, areg0);
+        if (n > 1) load_stage(1, breg1, areg1);
+        store_stage(0, breg0, areg0);
+        __syncthreads();
+        for (int st = 0; st < n; st += 2) {
+            // even stage: set 0 is free, set 1 holds stage st+1
+            if (st + 2 < n) load_stage(st + 2, breg0, areg0);
+            compute(0);
+            if (st + 1 < n) store_stage(1, breg1, areg1);
+            __syncthreads();
+            if (st + 1 >= n) break;
+            // odd stage: set 1 is free, set 0 holds stage st+2
+            if (st + 3 < n) load_stage(st + 3, breg1, areg1);
+            compute(1);
+            if (st + 2 < n) store_stage(0, breg0, areg0);
+            __syncthreads();
+        }
     }
 
     // ---- epilogue.  Accumulator v of lane l holds row 8*(v/4) + 4*(l/32) + v%4, column l%32.
@@ -248,9 +239,9 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs A) {
         const bool pok = p < A.P;
         int64_t ybase;
         if (EPI == EPI_NCHW) {
-            const int n = p / A.HoWo;
-            const int hw = p - n * A.HoWo;
-            ybase = (int64_t)n * A.y_nstride + (int64_t)gi * A.M * A.HoWo + hw;
+            const int n_img = p / A.HoWo;
+            const int hw = p - n_img * A.HoWo;
+            ybase = (int64_t)n_img * A.y_nstride + (int64_t)gi * A.M * A.HoWo + hw;
         } else {
             ybase = (int64_t)gi * A.c_gstride + p;
         }
@@ -309,50 +300,85 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs A) {
     const int bkc0 = __builtin_amdgcn_readfirstlane(t / BN);
     const int pcol = p0 + bn;
     ColState cs;
-    if (BSRC == BSRC_IMPLICIT_NCHW) cs = col_state(A, pcol, gi);
+    if (BSRC != BSRC_DENSE) cs = col_state(A, pcol, gi);
+    const uint32_t dvb = pcol < A.P ? (uint32_t)(((int64_t)gi * A.b_gstride + pcol) * 2) : OOB_OFF;
     // A: unit u = t + i*256 -> row m = u / 4, k chunk kc = u % 4
     const int64_t a_base = (int64_t)gi * A.a_gstride;
 
     u32x4 breg[BUNITS];
     u32x4 areg[AUNITS];
+    int cur_c0 = 0, cur_r = 0, cur_s = 0;  // tap-major cursor of the next stage
 
     auto load_stage = [&](int stage) {
         const int k0 = stage * BK;
+        uint16_t h[8];
+        if constexpr (BSRC == BSRC_IMPLICIT_TAP) {
+            const int roff = cur_r * A.dh, soff = cur_s * A.dw;
+            const int hi = cs.hi0 + roff, wi = cs.wi0 + soff;
+            const bool ok = ((unsigned)hi < (unsigned)A.H) & ((unsigned)wi < (unsigned)A.W);
+            const uint32_t vb = ok ? (uint32_t)(((int32_t)cs.base + roff * A.W + soff) * 2) : OOB_OFF;
 #pragma unroll
-        for (int i = 0; i < BUNITS; ++i) {
-            const int kc = bkc0 + i * (256 / BN);
-            uint16_t h[8];
+            for (int i = 0; i < BUNITS; ++i) {
+                const int kc = bkc0 + i * (256 / BN);
 #pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                const int kr = k0 + kc * 8 + q;
-                uint32_t off;
-                if (BSRC == BSRC_IMPLICIT_NCHW) {
-                    off = implicit_off<2>(A, cs, ktab_at(A.ktab, kr));
-                } else {
-                    const bool ok = (kr < A.Kred) & (pcol < A.P);
-                    const int64_t e = (int64_t)gi * A.b_gstride + (int64_t)kr * A.ldb + pcol;
-                    off = ok ? (uint32_t)(e * 2) : OOB_OFF;
+                for (int q = 0; q < 8; ++q)
+                    h[q] = ld_u16(rb, vb + (uint32_t)((cur_c0 + kc * 8 + q) * A.HW) * 2u);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) breg[i][q] = (uint32_t)h[2 * q] | ((uint32_t)h[2 * q + 1] << 16);
+            }
+            // weights in tap-major order [K][R*S][C/g]: 8 consecutive channels per 16-byte load
+            const int tap = cur_r * A.S + cur_s;
+#pragma unroll
+            for (int i = 0; i < AUNITS; ++i) {
+                const int u = t + i * 256;
+                const int m = m0 + u / (BK / 8);
+                const int kc = u % (BK / 8);
+                const int64_t e0 = a_base + (int64_t)m * A.lda + (int64_t)tap * A.Cg + cur_c0 + kc * 8;
+                areg[i] = __builtin_amdgcn_raw_buffer_load_b128(ra, m < A.M ? (uint32_t)(e0 * 2) : OOB_OFF, 0, 0);
+            }
+            cur_c0 += BK;
+            if (cur_c0 >= A.Cg) {
+                cur_c0 = 0;
+                if (++cur_s == A.S) {
+                    cur_s = 0;
+                    ++cur_r;
                 }
-                h[q] = ld_u16(rb, off);
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < BUNITS; ++i) {
+                const int kc = bkc0 + i * (256 / BN);
+                if constexpr (BSRC == BSRC_IMPLICIT_NCHW) {
+                    KTabEntry e[8];
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) e[q] = ktab_at(A.ktab, k0 + kc * 8 + q);
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) h[q] = ld_u16(rb, implicit_off<2>(A, cs, e[q]));
+                } else {
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) {
+                        const int kr = k0 + kc * 8 + q;
+                        h[q] = ld_u16(rb, kr < A.Kred ? dvb + (uint32_t)kr * (uint32_t)A.ldb * 2u : OOB_OFF);
+                    }
+                }
+#pragma unroll
+                for (int q = 0; q < 4; ++q) breg[i][q] = (uint32_t)h[2 * q] | ((uint32_t)h[2 * q + 1] << 16);
             }
 #pragma unroll
-            for (int q = 0; q < 4; ++q) breg[i][q] = (uint32_t)h[2 * q] | ((uint32_t)h[2 * q + 1] << 16);
-        }
+            for (int i = 0; i < AUNITS; ++i) {
+                const int u = t + i * 256;
+                const int m = m0 + u / (BK / 8);
+                const int kc = u % (BK / 8);
 #pragma unroll
-        for (int i = 0; i < AUNITS; ++i) {
-            const int u = t + i * 256;
-            const int m = m0 + u / (BK / 8);
-            const int kc = u % (BK / 8);
-            uint16_t h[8];
+                for (int q = 0; q < 8; ++q) {
+                    const int kr = k0 + kc * 8 + q;
+                    const bool ok = (m < A.M) & (kr < A.Kred);
+                    const int64_t e = a_base + (int64_t)m * A.lda + kr;
+                    h[q] = ld_u16(ra, ok ? (uint32_t)(e * 2) : OOB_OFF);
+                }
 #pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                const int kr = k0 + kc * 8 + q;
-                const bool ok = (m < A.M) & (kr < A.Kred);
-                const int64_t e = a_base + (int64_t)m * A.lda + kr;
-                h[q] = ld_u16(ra, ok ? (uint32_t)(e * 2) : OOB_OFF);
+                for (int q = 0; q < 4; ++q) areg[i][q] = (uint32_t)h[2 * q] | ((uint32_t)h[2 * q + 1] << 16);
             }
-#pragma unroll
-            for (int q = 0; q < 4; ++q) areg[i][q] = (uint32_t)h[2 * q] | ((uint32_t)h[2 * q + 1] << 16);
         }
     };
     auto store_stage = [&](int buf) {
@@ -439,40 +465,74 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs A) {
 }
 
 // ============================================================================ dispatch
-template <int BM, int BN, int WM, int WN>
-static hipError_t launch_tile(const GemmArgs& a, int bsrc, int epi, int xdt, int ydt, int groups,
-                              hipStream_t stream) {
+template <int BM, int BN, int WM, int WN, int BK, int PF>
+static hipError_t launch_f32(const GemmArgs& a, int bsrc, int epi, int groups, hipStream_t stream) {
     dim3 grid((unsigned)(a.grid_p * a.grid_m), 1, (unsigned)groups);
-    dim3 block(256);
-#define CV_LAUNCH(KER, BS, EP, TO) hipLaunchKernelGGL((KER<BM, BN, WM, WN, BS, EP, TO>), grid, block, 0, stream, a)
-    if (xdt == CONV2D_F32) {
-        if (bsrc == BSRC_IMPLICIT_NCHW && epi == EPI_NCHW) CV_LAUNCH(gemm_f32_kernel, BSRC_IMPLICIT_NCHW, EPI_NCHW, float);
-        else if (bsrc == BSRC_DENSE && epi == EPI_DENSE) CV_LAUNCH(gemm_f32_kernel, BSRC_DENSE, EPI_DENSE, float);
-        else return hipErrorInvalidValue;
-    } else {
-        if (bsrc == BSRC_IMPLICIT_NCHW && epi == EPI_NCHW) {
-            if (ydt == CONV2D_BF16) CV_LAUNCH(gemm_bf16_kernel, BSRC_IMPLICIT_NCHW, EPI_NCHW, uint16_t);
-            else CV_LAUNCH(gemm_bf16_kernel, BSRC_IMPLICIT_NCHW, EPI_NCHW, float);
-        } else if (bsrc == BSRC_DENSE && epi == EPI_DENSE) {
-            CV_LAUNCH(gemm_bf16_kernel, BSRC_DENSE, EPI_DENSE, float);
-        } else {
-            return hipErrorInvalidValue;
-        }
-    }
-#undef CV_LAUNCH
+#define CV_F32(BS, EP) \
+    hipLaunchKernelGGL((gemm_f32_kernel<BM, BN, WM, WN, BK, PF, BS, EP, float>), grid, dim3(256), 0, stream, a)
+    if (bsrc == BSRC_IMPLICIT_NCHW && epi == EPI_NCHW) CV_F32(BSRC_IMPLICIT_NCHW, EPI_NCHW);
+    else if (bsrc == BSRC_IMPLICIT_TAP && epi == EPI_NCHW) CV_F32(BSRC_IMPLICIT_TAP, EPI_NCHW);
+    else if (bsrc == BSRC_DENSE && epi == EPI_DENSE) CV_F32(BSRC_DENSE, EPI_DENSE);
+    else return hipErrorInvalidValue;
+#undef CV_F32
     return hipGetLastError();
 }
 
-hipError_t launch_gemm(const GemmArgs& a, int tile, int bsrc, int epi, int xdt, int ydt, int groups,
-                       hipStream_t stream) {
-    switch (tile) {
-        case TILE_64x64: return launch_tile<64, 64, 2, 2>(a, bsrc, epi, xdt, ydt, groups, stream);
-        case TILE_64x128: return launch_tile<64, 128, 1, 4>(a, bsrc, epi, xdt, ydt, groups, stream);
-        case TILE_64x256: return launch_tile<64, 256, 1, 4>(a, bsrc, epi, xdt, ydt, groups, stream);
-        case TILE_128x128: return launch_tile<128, 128, 2, 2>(a, bsrc, epi, xdt, ydt, groups, stream);
-        case TILE_128x64: return launch_tile<128, 64, 2, 2>(a, bsrc, epi, xdt, ydt, groups, stream);
-        default: return hipErrorInvalidValue;
+template <int BM, int BN, int WM, int WN>
+static hipError_t launch_bf16(const GemmArgs& a, int bsrc, int epi, int ydt, int groups, hipStream_t stream) {
+    dim3 grid((unsigned)(a.grid_p * a.grid_m), 1, (unsigned)groups);
+#define CV_BF(BS, EP, TO) \
+    hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, BS, EP, TO>), grid, dim3(256), 0, stream, a)
+    if (bsrc == BSRC_IMPLICIT_NCHW && epi == EPI_NCHW) {
+        if (ydt == CONV2D_BF16) CV_BF(BSRC_IMPLICIT_NCHW, EPI_NCHW, uint16_t);
+        else CV_BF(BSRC_IMPLICIT_NCHW, EPI_NCHW, float);
+    } else if (bsrc == BSRC_IMPLICIT_TAP && epi == EPI_NCHW) {
+        if (ydt == CONV2D_BF16) CV_BF(BSRC_IMPLICIT_TAP, EPI_NCHW, uint16_t);
+        else CV_BF(BSRC_IMPLICIT_TAP, EPI_NCHW, float);
+    } else if (bsrc == BSRC_DENSE && epi == EPI_DENSE) {
+        CV_BF(BSRC_DENSE, EPI_DENSE, float);
+    } else {
+        return hipErrorInvalidValue;
     }
+#undef CV_BF
+    return hipGetLastError();
+}
+
+bool gemm32_f32_supported(int tile, int bk, int pf) {
+    if (tile < 0 || tile >= TILE_COUNT || (pf != 1 && pf != 2)) return false;
+    if (bk == 16) return true;
+    return bk == 32 && (tile == TILE_64x64 || tile == TILE_64x128);
+}
+
+hipError_t launch_gemm(const GemmArgs& a, int tile, int bk, int pf, int bsrc, int epi, int xdt, int ydt,
+                       int groups, hipStream_t stream) {
+    if (xdt == CONV2D_BF16) {
+        switch (tile) {
+            case TILE_64x64: return launch_bf16<64, 64, 2, 2>(a, bsrc, epi, ydt, groups, stream);
+            case TILE_64x128: return launch_bf16<64, 128, 1, 4>(a, bsrc, epi, ydt, groups, stream);
+            case TILE_64x256: return launch_bf16<64, 256, 1, 4>(a, bsrc, epi, ydt, groups, stream);
+            case TILE_128x128: return launch_bf16<128, 128, 2, 2>(a, bsrc, epi, ydt, groups, stream);
+            case TILE_128x64: return launch_bf16<128, 64, 2, 2>(a, bsrc, epi, ydt, groups, stream);
+            default: return hipErrorInvalidValue;
+        }
+    }
+    if (!gemm32_f32_supported(tile, bk, pf)) return hipErrorInvalidValue;
+#define CV_T(TL, BMV, BNV, WMV, WNV)                                                          \
+    if (tile == TL) {                                                                        \
+        if (bk == 16 && pf == 1) return launch_f32<BMV, BNV, WMV, WNV, 16, 1>(a, bsrc, epi, groups, stream); \
+        if (bk == 16 && pf == 2) return launch_f32<BMV, BNV, WMV, WNV, 16, 2>(a, bsrc, epi, groups, stream); \
+    }
+    CV_T(TILE_64x64, 64, 64, 2, 2)
+    CV_T(TILE_64x128, 64, 128, 1, 4)
+    CV_T(TILE_64x256, 64, 256, 1, 4)
+    CV_T(TILE_128x128, 128, 128, 2, 2)
+    CV_T(TILE_128x64, 128, 64, 2, 2)
+#undef CV_T
+    if (tile == TILE_64x64 && bk == 32 && pf == 1) return launch_f32<64, 64, 2, 2, 32, 1>(a, bsrc, epi, groups, stream);
+    if (tile == TILE_64x64 && bk == 32 && pf == 2) return launch_f32<64, 64, 2, 2, 32, 2>(a, bsrc, epi, groups, stream);
+    if (tile == TILE_64x128 && bk == 32 && pf == 1) return launch_f32<64, 128, 1, 4, 32, 1>(a, bsrc, epi, groups, stream);
+    if (tile == TILE_64x128 && bk == 32 && pf == 2) return launch_f32<64, 128, 1, 4, 32, 2>(a, bsrc, epi, groups, stream);
+    return hipErrorInvalidValue;
 }
 
 }  // namespace cv
