@@ -44,9 +44,9 @@ struct EvRec {
 };
 
 struct GemmPlan {
-    int kind = 0;  // 0: 32x32-MFMA kernels (tile config)
+    int kind = 0;  // 0: 32x32-MFMA tile kernels (tile config)
     int tile = TILE_64x128;
-    int bm = 64, bn = 128, u = 0;
+    int bm = 64, bn = 128;
     int bk = 16;   // reduction rows per stage
     int pf = 1;    // register prefetch distance (fp32 32x32 kernels)
     int nstages = 0;
@@ -91,9 +91,9 @@ GemmPlan choose_tile(int64_t M, int64_t P, int64_t G, int64_t kred, int xdt, int
     GemmPlan best;
     double best_cost = 1e300;
     // Candidate block tiles of the 32x32-MFMA kernels, with the measured MFMA efficiency of
-    // their wave tiles relative to 64x128 (fp32, MI355X).
+    // their wave tiles relative to 64x64 (fp32, MI355X).
     struct Cand { int tile; double eff; };
-    const Cand cands[] = {{TILE_64x128, 1.0}, {TILE_64x256, 0.8}, {TILE_64x64, 0.85},
+    const Cand cands[] = {{TILE_64x64, 1.0}, {TILE_64x128, 1.0}, {TILE_64x256, 0.8},
                           {TILE_128x64, 0.9}, {TILE_128x128, 0.85}};
     for (const Cand& c : cands) {
         const TileShape ts = kTileShapes[c.tile];
@@ -126,8 +126,9 @@ GemmPlan choose_tile(int64_t M, int64_t P, int64_t G, int64_t kred, int xdt, int
     return best;
 }
 
-hipError_t dispatch_gemm(const GemmPlan& gp, const GemmArgs& a, int bsrc, int epi, int xdt, int ydt,
+hipError_t dispatch_gemm(const GemmPlan& gp, const GemmArgs& a_in, int bsrc, int epi, int xdt, int ydt,
                          int groups, hipStream_t s) {
+    const GemmArgs& a = a_in;
     return launch_gemm(a, gp.tile, gp.bk, gp.pf, bsrc, epi, xdt, ydt, groups, s);
 }
 

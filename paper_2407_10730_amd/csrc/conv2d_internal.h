@@ -61,7 +61,7 @@ struct GemmArgs {
     int32_t dh, dw, R, S, RS, Cg, HW;  // tap-major gather: filter dims, R*S, channels per group, H*W
     int64_t x_nstride;    // C*H*W
     int32_t M, Kred, P, nstages;
-    int32_t grid_p, grid_m;
+    int32_t grid_p, grid_m;   // pixel tiles x channel tiles
     void* y;              // NCHW y, or dense C [G][M][ldc] (fp32)
     uint32_t y_bytes;
     const float* bias;    // may be NULL

@@ -123,6 +123,11 @@ EDGE = [
     _shape(1, 8, 5, 13, 9, 1, 5, st=(1, 3), pd=(0, 2)),
     _shape(4, 12, 7, 7, 12, 3, 3, st=(2, 2), pd=(1, 1), g=12),
     _shape(1, 256, 7, 7, 512, 3, 3, pd=(1, 1)),
+    # channel blocks of 16/32 (tap-major gather) with padding, dilation and rectangular filters
+    _shape(2, 32, 9, 12, 40, 3, 3, pd=(1, 1)),
+    _shape(1, 16, 6, 4, 8, 3, 3, st=(2, 1), pd=(1, 2), dl=(1, 2)),
+    _shape(3, 48, 5, 8, 70, 5, 5, pd=(2, 2)),
+    _shape(1, 16, 3, 20, 16, 1, 7, pd=(0, 3)),
 ]
 VARIANTS = [("nchw", "f32", "f32"), ("nhwc", "f32", "f32"), ("nchw", "bf16", "bf16"),
             ("nhwc", "bf16", "f32")]
