@@ -8,6 +8,9 @@
 // needs for one input channel are staged once in LDS with a zero halo, then
 // each thread sums R*S taps per output from LDS.  Filter taps are
 // block-uniform and come through the scalar cache.
+#include <cstdlib>
+#include <type_traits>
+
 #include "conv2d_internal.h"
 
 namespace cv {
@@ -29,6 +32,9 @@ __device__ __forceinline__ float dk_load(__amdgpu_buffer_rsrc_t r, bool ok, int6
     const uint32_t h = __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
     return __builtin_bit_cast(float, h << 16);
 }
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ uint16_t dk_f32_to_bf16(float f) {
     uint32_t u = __builtin_bit_cast(uint32_t, f);
@@ -114,6 +120,267 @@ __global__ __launch_bounds__(DIRECT_THREADS) void direct_kernel(DirectArgs A, in
     }
 }
 
+// ------------------------------------------------------------------ depthwise (C/g = 1)
+// Every output plane (n, k) reads one input plane (n, k / (K/g)).  A block stages
+// whole input rows of one or more planes into LDS with a zero halo (16-byte loads
+// when W % 4 == 0), then each thread produces strips of 4 consecutive outputs of
+// one row: for stride 1 / dilation 1 the S + 3 input values of a filter row are
+// read once and reused by the 4 outputs.  HBM traffic is one read of x and one
+// write of y; filter taps and bias of the block's planes sit in LDS.
+constexpr int DW_LDS_FLOATS = 8192;   // 32 KiB input tile
+constexpr int DW_MAX_PLANES = 64;
+
+struct DwPlan {
+    int32_t PB, TH, IR, LDW, LPAD, nbands, WS;
+};
+
+// One block per work item (a group of PB planes x a band of TH output rows).  The input
+// tile lives in dynamic LDS sized to the item, so many blocks fit on a CU and their tile
+// loads overlap (the kernel is bound by HBM bandwidth, which needs many bytes in flight).
+constexpr int DWP_TILE = 4096;                           // max floats of one tile (16 KiB)
+constexpr int DWP_VMAX = DWP_TILE / 4 / DIRECT_THREADS;  // 16-byte loads per thread
+constexpr int DWP_SMAX = DWP_TILE / DIRECT_THREADS;      // 4-byte loads per thread
+
+template <int R, int S, int ST, int DL, typename TX, typename TY>
+__global__ __launch_bounds__(DIRECT_THREADS) void dw_kernel(DirectArgs A, DwPlan P) {
+    extern __shared__ __attribute__((aligned(16))) float tile[];  // PB * IR * LDW floats
+    __shared__ float wsh[DW_MAX_PLANES * R * S];
+    __shared__ float bsh[DW_MAX_PLANES];
+    __shared__ int32_t pbase[DW_MAX_PLANES];  // element offset of the input plane of local plane lp
+    const int t = threadIdx.x;
+    const int planes_total = A.N * A.K;
+    const int band = blockIdx.x % P.nbands;
+    const int pl0 = (blockIdx.x / P.nbands) * P.PB;
+    const int npl = min(P.PB, planes_total - pl0);
+    const int oh0 = band * P.TH;
+    const int nrows = min(P.TH, A.Ho - oh0);
+    const int hi_base = oh0 * A.sh - A.ph;
+    const __amdgpu_buffer_rsrc_t rx = dk_rsrc(A.x, A.x_bytes);
+    const __amdgpu_buffer_rsrc_t ry = dk_rsrc(A.y, A.y_bytes);
+    const TX* wp = reinterpret_cast<const TX*>(A.w);
+
+    for (int i = t; i < npl * R * S; i += DIRECT_THREADS) {
+        const int k = (pl0 + i / (R * S)) % A.K;
+        const TX v = wp[(int64_t)k * R * S + i % (R * S)];
+        if constexpr (sizeof(TX) == 4) wsh[i] = __builtin_bit_cast(float, v);
+        else wsh[i] = __builtin_bit_cast(float, (uint32_t)v << 16);
+    }
+    for (int i = t; i < npl; i += DIRECT_THREADS) {
+        const int pl = pl0 + i;
+        const int n = pl / A.K;
+        const int k = pl - n * A.K;
+        bsh[i] = A.bias ? A.bias[k] : 0.0f;
+        pbase[i] = (int32_t)(((int64_t)n * A.C + k / A.Kg) * A.H * A.W);
+    }
+    __syncthreads();
+
+    // input tile: row tr of local plane lp holds input row hi_base + tr, input column w sits at
+    // w + LPAD.  All of a thread's loads are issued before any is written to LDS.
+    {
+        const int VW = (A.W & 3) == 0 ? 4 : 1;
+        const int LDWV = P.LDW / VW;
+        const int total = npl * P.IR * LDWV;
+        const int srow = DIRECT_THREADS / LDWV, scol = DIRECT_THREADS - srow * LDWV;
+        int row = t / LDWV;
+        int cg = t - row * LDWV;
+        int lp = row / P.IR;
+        int tr = row - lp * P.IR;
+        auto step = [&]() {
+            cg += scol;
+            int adv = srow;
+            if (cg >= LDWV) {
+                cg -= LDWV;
+                ++adv;
+            }
+            tr += adv;
+            while (tr >= P.IR) {
+                tr -= P.IR;
+                ++lp;
+            }
+        };
+        if (VW == 4) {
+            f32x4 vreg[DWP_VMAX];
+#pragma unroll
+            for (int u = 0; u < DWP_VMAX; ++u) {
+                const int e = t + u * DIRECT_THREADS;
+                const int hi = hi_base + tr;
+                const int w0 = 4 * cg - P.LPAD;
+                const bool ok = (e < total) & ((unsigned)hi < (unsigned)A.H) & ((unsigned)w0 < (unsigned)A.W);
+                const int32_t idx = ok ? pbase[lp] + hi * A.W + w0 : 0;
+                if constexpr (sizeof(TX) == 4) {
+                    vreg[u] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                           rx, ok ? (uint32_t)idx * 4u : OOB_OFF, 0, 0));
+                } else {
+                    typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+                    const u32x2 h = __builtin_bit_cast(
+                        u32x2, __builtin_amdgcn_raw_buffer_load_b64(rx, ok ? (uint32_t)idx * 2u : OOB_OFF, 0, 0));
+                    vreg[u] = f32x4{__builtin_bit_cast(float, h[0] << 16), __builtin_bit_cast(float, h[0] & 0xFFFF0000u),
+                                    __builtin_bit_cast(float, h[1] << 16), __builtin_bit_cast(float, h[1] & 0xFFFF0000u)};
+                }
+                step();
+            }
+#pragma unroll
+            for (int u = 0; u < DWP_VMAX; ++u) {
+                const int e = t + u * DIRECT_THREADS;
+                if (e < total) *reinterpret_cast<f32x4*>(&tile[4 * e]) = vreg[u];
+            }
+        } else {
+            float sreg[DWP_SMAX];
+#pragma unroll
+            for (int u = 0; u < DWP_SMAX; ++u) {
+                const int e = t + u * DIRECT_THREADS;
+                const int hi = hi_base + tr;
+                const int w = cg - P.LPAD;
+                const bool ok = (e < total) & ((unsigned)hi < (unsigned)A.H) & ((unsigned)w < (unsigned)A.W);
+                sreg[u] = dk_load(rx, ok, ok ? pbase[lp] + hi * A.W + w : 0, (TX*)nullptr);
+                step();
+            }
+#pragma unroll
+            for (int u = 0; u < DWP_SMAX; ++u) {
+                const int e = t + u * DIRECT_THREADS;
+                if (e < total) tile[e] = sreg[u];
+            }
+        }
+    }
+    __syncthreads();
+
+    // outputs: each thread computes a vertical strip of VR outputs of one column (consecutive
+    // lanes on consecutive columns, so LDS reads hit consecutive banks); the NR x S input
+    // values under the strip are read once and shared by its VR outputs.
+    constexpr int VR = 4;
+    constexpr int NR = (VR - 1) * ST + (R - 1) * DL + 1;
+    auto compute = [&](auto uniform_w) {
+        constexpr bool UW = decltype(uniform_w)::value;
+        const int nrb = (nrows + VR - 1) / VR;
+        const int per_plane = nrb * A.Wo;
+        const int strips = npl * per_plane;
+        const int st_a = DIRECT_THREADS / per_plane;
+        const int st_r = DIRECT_THREADS - st_a * per_plane;
+        const int st_b = st_r / A.Wo, st_c = st_r - st_b * A.Wo;
+        int lp = t / per_plane;
+        int rb = (t - lp * per_plane) / A.Wo;
+        int ow = t - lp * per_plane - rb * A.Wo;
+        float wreg[R * S];
+        if constexpr (UW) {
+#pragma unroll
+            for (int i = 0; i < R * S; ++i) wreg[i] = wsh[i];
+        }
+        for (int q = t; q < strips; q += DIRECT_THREADS) {
+            if constexpr (!UW) {
+#pragma unroll
+                for (int i = 0; i < R * S; ++i) wreg[i] = wsh[lp * R * S + i];
+            }
+            const float bias = bsh[lp];
+            const int orow0 = rb * VR;
+            const float* rp = &tile[(lp * P.IR + orow0 * ST) * P.LDW + P.LPAD - A.pw + ow * ST];
+            float xv[NR][S];
+#pragma unroll
+            for (int rr = 0; rr < NR; ++rr)
+#pragma unroll
+                for (int sx = 0; sx < S; ++sx) xv[rr][sx] = rp[rr * P.LDW + sx * DL];
+            const int64_t o0 = ((int64_t)(pl0 + lp) * A.Ho + oh0 + orow0) * A.Wo + ow;
+#pragma unroll
+            for (int v = 0; v < VR; ++v) {
+                float acc = bias;
+#pragma unroll
+                for (int r = 0; r < R; ++r)
+#pragma unroll
+                    for (int sx = 0; sx < S; ++sx) acc = __builtin_fmaf(xv[v * ST + r * DL][sx], wreg[r * S + sx], acc);
+                const bool ok = orow0 + v < nrows;
+                const int64_t o = o0 + (int64_t)v * A.Wo;
+                if constexpr (sizeof(TY) == 4)
+                    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, acc), ry,
+                                                          ok ? (uint32_t)(o * 4) : OOB_OFF, 0, 0);
+                else
+                    __builtin_amdgcn_raw_buffer_store_b16(dk_f32_to_bf16(acc), ry, ok ? (uint32_t)(o * 2) : OOB_OFF,
+                                                          0, 0);
+            }
+            ow += st_c;
+            rb += st_b;
+            lp += st_a;
+            if (ow >= A.Wo) {
+                ow -= A.Wo;
+                ++rb;
+            }
+            if (rb >= nrb) {
+                rb -= nrb;
+                ++lp;
+            }
+        }
+    };
+    if (npl == 1) compute(std::true_type{});
+    else compute(std::false_type{});
+}
+
+// Host plan of the depthwise kernel; returns false when the shape needs the generic kernel.
+static bool dw_plan(const DirectArgs& a, int sw_t, int dw_t, DwPlan* p) {
+    const int WS = (a.Wo + 3) / 4;
+    const int LPAD = (a.pw + 3) / 4 * 4;
+    const int maxcol = LPAD - a.pw + (a.Wo - 1) * sw_t + (a.S - 1) * dw_t;
+    int LDW = (maxcol + 1 + 3) / 4 * 4;
+    if (LDW < LPAD + a.W) LDW = (LPAD + a.W + 3) / 4 * 4;
+    // rows of the tile: TH output rows rounded up to whole strips of 4
+    auto ir = [&](int th) { return (((th + 3) / 4) * 4 - 1) * a.sh + (a.R - 1) * a.dh + 1; };
+    int TH, PB;
+    if (a.Ho * WS <= 1024) {
+        TH = a.Ho;
+        PB = 1024 / (a.Ho * WS);
+        if (PB < 1) PB = 1;
+        if (PB > DW_MAX_PLANES) PB = DW_MAX_PLANES;
+        while (PB > 1 && PB * ir(TH) * LDW > DWP_TILE) --PB;
+    } else {
+        PB = 1;
+        TH = 1024 / WS;
+        if (TH < 1) TH = 1;
+        if (TH > a.Ho) TH = a.Ho;
+    }
+    while (TH > 1 && PB * ir(TH) * LDW > DWP_TILE) --TH;
+    if (PB * ir(TH) * LDW > DWP_TILE) return false;
+    p->PB = PB;
+    p->TH = TH;
+    p->IR = ir(TH);
+    p->LDW = LDW;
+    p->LPAD = LPAD;
+    p->nbands = (a.Ho + TH - 1) / TH;
+    p->WS = WS;
+    return true;
+}
+
+template <int R, int S, int ST, int DL>
+static hipError_t launch_dw_t(const DirectArgs& a, const DwPlan& p, int xdt, int ydt, hipStream_t stream) {
+    const int64_t planes = (int64_t)a.N * a.K;
+    const int64_t nblocks = (planes + p.PB - 1) / p.PB * p.nbands;
+    if (nblocks > 0x7fffffff) return hipErrorInvalidConfiguration;
+    dim3 grid((unsigned)nblocks);
+    const size_t lds = (size_t)p.PB * p.IR * p.LDW * sizeof(float);
+    if (xdt == CONV2D_F32)
+        hipLaunchKernelGGL((dw_kernel<R, S, ST, DL, float, float>), grid, dim3(DIRECT_THREADS), lds, stream, a, p);
+    else if (ydt == CONV2D_BF16)
+        hipLaunchKernelGGL((dw_kernel<R, S, ST, DL, uint16_t, uint16_t>), grid, dim3(DIRECT_THREADS), lds, stream, a, p);
+    else
+        hipLaunchKernelGGL((dw_kernel<R, S, ST, DL, uint16_t, float>), grid, dim3(DIRECT_THREADS), lds, stream, a, p);
+    return hipGetLastError();
+}
+
+// Depthwise fast path: square 1/3/5/7 filters, equal strides of 1 or 2, equal dilations of 1 or 2.
+static hipError_t try_launch_dw(const DirectArgs& a, int xdt, int ydt, hipStream_t stream, bool* launched) {
+    *launched = false;
+    if (a.Cg != 1 || a.R != a.S || (a.sw != 1 && a.sw != 2) || (a.dw != 1 && a.dw != 2)) return hipSuccess;
+    if (a.sh != a.sw || a.dh != a.dw) return hipSuccess;
+    if (a.R != 1 && a.R != 3 && a.R != 5 && a.R != 7) return hipSuccess;
+    DwPlan p;
+    if (!dw_plan(a, a.sw, a.dw, &p)) return hipSuccess;
+    *launched = true;
+#define CV_DW(RV, SWV, DWV) \
+    if (a.R == RV && a.sw == SWV && a.dw == DWV) return launch_dw_t<RV, RV, SWV, DWV>(a, p, xdt, ydt, stream);
+#define CV_DW4(RV) CV_DW(RV, 1, 1) CV_DW(RV, 1, 2) CV_DW(RV, 2, 1) CV_DW(RV, 2, 2)
+    CV_DW4(1) CV_DW4(3) CV_DW4(5) CV_DW4(7)
+#undef CV_DW4
+#undef CV_DW
+    *launched = false;
+    return hipSuccess;
+}
+
 // Output rows per block: as many as fit both the LDS window and 4 outputs per thread.
 static int direct_rows(const DirectArgs& a, int* in_rows, int* in_cols) {
     const int ic = (a.Wo - 1) * a.sw + (a.S - 1) * a.dw + 1;
@@ -126,6 +393,11 @@ static int direct_rows(const DirectArgs& a, int* in_rows, int* in_cols) {
 }
 
 hipError_t launch_direct(const DirectArgs& a, int xdt, int ydt, hipStream_t stream) {
+    if (!std::getenv("CONV2D_DW_GENERIC")) {
+        bool launched = false;
+        const hipError_t e = try_launch_dw(a, xdt, ydt, stream, &launched);
+        if (launched || e != hipSuccess) return e;
+    }
     int in_rows = 0, in_cols = 0;
     const int rows = direct_rows(a, &in_rows, &in_cols);
     if (rows < 1 || a.Wo > 4 * DIRECT_THREADS || in_rows * in_cols > DIRECT_LDS_FLOATS)

@@ -128,6 +128,13 @@ EDGE = [
     _shape(1, 16, 6, 4, 8, 3, 3, st=(2, 1), pd=(1, 2), dl=(1, 2)),
     _shape(3, 48, 5, 8, 70, 5, 5, pd=(2, 2)),
     _shape(1, 16, 3, 20, 16, 1, 7, pd=(0, 3)),
+    # depthwise: multiplier 2, 5x5 dilated, 7x7 stride 2, widths with and without W % 4 == 0,
+    # planes taller than one band
+    _shape(2, 8, 12, 12, 16, 3, 3, pd=(1, 1), g=8),
+    _shape(1, 5, 13, 16, 5, 5, 5, pd=(4, 4), dl=(2, 2), g=5),
+    _shape(2, 6, 19, 17, 6, 7, 7, st=(2, 2), pd=(3, 3), g=6),
+    _shape(1, 3, 150, 124, 3, 3, 3, st=(1, 2), pd=(1, 1), g=3),
+    _shape(3, 4, 7, 7, 4, 1, 1, g=4),
 ]
 VARIANTS = [("nchw", "f32", "f32"), ("nhwc", "f32", "f32"), ("nchw", "bf16", "bf16"),
             ("nhwc", "bf16", "f32")]
