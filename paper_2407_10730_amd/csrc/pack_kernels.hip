@@ -25,46 +25,97 @@ __device__ __forceinline__ uint16_t pk_f32_to_bf16(float f) {
 }
 
 // ------------------------------------------------------------------ im2col
-// grid (ceil(pc/256), ceil(Kred/KR_PER_BLOCK), G), 256 threads, one pixel per thread.
-constexpr int KR_PER_BLOCK = 16;
+// grid (ceil(pc / 1024), ceil(Kred / KR_PER_BLOCK), G), 256 threads.  A thread packs 4
+// consecutive pixels for KR_PER_BLOCK reduction rows: all its gathers are issued first,
+// then each row's 4 values go out as one 16-byte (fp32) or 8-byte (bf16) store when the
+// column matrix rows are aligned (pc % 4 == 0).
+constexpr int KR_PER_BLOCK = 8;
+constexpr int PIX_PER_THREAD = 4;
 
 template <typename T>
 __global__ __launch_bounds__(256) void im2col_kernel(Im2colArgs A) {
-    const int pl = blockIdx.x * 256 + threadIdx.x;
     const int gi = blockIdx.z;
     const int kr0 = blockIdx.y * KR_PER_BLOCK;
-    if (pl >= A.pc) return;
-    const int64_t p = A.p_begin + pl;
-    const int64_t howo = (int64_t)A.Ho * A.Wo;
-    const int64_t n = p / howo;
-    const int hw = (int)(p - n * howo);
-    const int ho = hw / A.Wo;
-    const int wo = hw - ho * A.Wo;
-    const int hi0 = ho * A.sh - A.ph;
-    const int wi0 = wo * A.sw - A.pw;
-    const T* xb = reinterpret_cast<const T*>(A.x) + n * A.x_nstride + gi * A.x_gstride +
-                  (int64_t)hi0 * A.W + wi0;
+    const int pl0 = (blockIdx.x * 256 + threadIdx.x) * PIX_PER_THREAD;
+    if (pl0 >= A.pc) return;
     const __amdgpu_buffer_rsrc_t rc = pk_rsrc(A.col, A.col_bytes);
-    const int kr_end = min(kr0 + KR_PER_BLOCK, A.Kred);
-    for (int kr = kr0; kr < kr_end; ++kr) {
-        const KTabEntry e = A.ktab[__builtin_amdgcn_readfirstlane(kr)];
-        const int hi = hi0 + e.roff;
-        const int wi = wi0 + e.soff;
-        T v = T(0);
-        if ((unsigned)hi < (unsigned)A.H && (unsigned)wi < (unsigned)A.W) v = xb[e.coff];
-        const int64_t off = ((int64_t)gi * A.Kred + kr) * A.pc + pl;
-        if constexpr (sizeof(T) == 4)
-            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), rc,
-                                                  (uint32_t)(off * 4), 0, 0);
-        else
-            __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(uint16_t, v), rc,
-                                                  (uint32_t)(off * 2), 0, 0);
+    // window origins of the 4 pixels (consecutive in (n, ho, wo) order)
+    int hi0[PIX_PER_THREAD], wi0[PIX_PER_THREAD];
+    int64_t xb[PIX_PER_THREAD];
+    bool pv[PIX_PER_THREAD];
+    {
+        const int64_t p = A.p_begin + pl0;
+        const int64_t howo = (int64_t)A.Ho * A.Wo;
+        int64_t n = p / howo;
+        int hw = (int)(p - n * howo);
+        int ho = hw / A.Wo;
+        int wo = hw - ho * A.Wo;
+#pragma unroll
+        for (int j = 0; j < PIX_PER_THREAD; ++j) {
+            pv[j] = pl0 + j < A.pc;
+            hi0[j] = ho * A.sh - A.ph;
+            wi0[j] = wo * A.sw - A.pw;
+            xb[j] = n * A.x_nstride + gi * A.x_gstride + (int64_t)hi0[j] * A.W + wi0[j];
+            if (++wo == A.Wo) {
+                wo = 0;
+                if (++ho == A.Ho) {
+                    ho = 0;
+                    ++n;
+                }
+            }
+        }
+    }
+    const T* x = reinterpret_cast<const T*>(A.x);
+    KTabEntry e[KR_PER_BLOCK];
+#pragma unroll
+    for (int i = 0; i < KR_PER_BLOCK; ++i) e[i] = A.ktab[__builtin_amdgcn_readfirstlane(min(kr0 + i, A.Kred - 1))];
+    T v[KR_PER_BLOCK][PIX_PER_THREAD];
+#pragma unroll
+    for (int i = 0; i < KR_PER_BLOCK; ++i)
+#pragma unroll
+        for (int j = 0; j < PIX_PER_THREAD; ++j) {
+            const int hi = hi0[j] + e[i].roff;
+            const int wi = wi0[j] + e[i].soff;
+            const bool ok = pv[j] & ((unsigned)hi < (unsigned)A.H) & ((unsigned)wi < (unsigned)A.W);
+            v[i][j] = ok ? x[xb[j] + e[i].coff] : T(0);
+        }
+    const bool vec = ((A.pc & 3) == 0) & (pl0 + PIX_PER_THREAD <= A.pc);
+#pragma unroll
+    for (int i = 0; i < KR_PER_BLOCK; ++i) {
+        const int kr = kr0 + i;
+        if (kr >= A.Kred) break;
+        const int64_t off = ((int64_t)gi * A.Kred + kr) * A.pc + pl0;
+        if constexpr (sizeof(T) == 4) {
+            if (vec) {
+                typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+                const u32x4 q = {__builtin_bit_cast(uint32_t, v[i][0]), __builtin_bit_cast(uint32_t, v[i][1]),
+                                 __builtin_bit_cast(uint32_t, v[i][2]), __builtin_bit_cast(uint32_t, v[i][3])};
+                __builtin_amdgcn_raw_buffer_store_b128(q, rc, (uint32_t)(off * 4), 0, 0);
+            } else {
+#pragma unroll
+                for (int j = 0; j < PIX_PER_THREAD; ++j)
+                    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v[i][j]), rc,
+                                                          pv[j] ? (uint32_t)((off + j) * 4) : OOB_OFF, 0, 0);
+            }
+        } else {
+            if (vec) {
+                typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+                const u32x2 q = {(uint32_t)v[i][0] | ((uint32_t)v[i][1] << 16),
+                                 (uint32_t)v[i][2] | ((uint32_t)v[i][3] << 16)};
+                __builtin_amdgcn_raw_buffer_store_b64(q, rc, (uint32_t)(off * 2), 0, 0);
+            } else {
+#pragma unroll
+                for (int j = 0; j < PIX_PER_THREAD; ++j)
+                    __builtin_amdgcn_raw_buffer_store_b16(v[i][j], rc, pv[j] ? (uint32_t)((off + j) * 2) : OOB_OFF, 0, 0);
+            }
+        }
     }
 }
 
 hipError_t launch_im2col(const Im2colArgs& a, int xdt, int groups, hipStream_t stream) {
-    dim3 grid((unsigned)((a.pc + 255) / 256), (unsigned)((a.Kred + KR_PER_BLOCK - 1) / KR_PER_BLOCK),
-              (unsigned)groups);
+    const int per_block = 256 * PIX_PER_THREAD;
+    dim3 grid((unsigned)((a.pc + per_block - 1) / per_block),
+              (unsigned)((a.Kred + KR_PER_BLOCK - 1) / KR_PER_BLOCK), (unsigned)groups);
     if (xdt == CONV2D_F32)
         hipLaunchKernelGGL(im2col_kernel<float>, grid, dim3(256), 0, stream, a);
     else
@@ -73,29 +124,54 @@ hipError_t launch_im2col(const Im2colArgs& a, int xdt, int groups, hipStream_t s
 }
 
 // ------------------------------------------------------------------ unpack
-// grid (ceil(pc/256), Kg, G): C[g][m][pl] -> y[n][g*Kg + m][hw] (+ bias[g*Kg + m]).
+// grid (ceil(pc / 1024), Kg, G): C[g][m][pl] -> y[n][g*Kg + m][hw] (+ bias[g*Kg + m]).
+// A thread moves 4 consecutive pixels; with HoWo % 4 == 0 and pc % 4 == 0 they are one
+// 16-byte load and one 16-byte (fp32) or 8-byte (bf16) store.
 template <bool BF16OUT>
 __global__ __launch_bounds__(256) void unpack_kernel(UnpackArgs A) {
-    const int pl = blockIdx.x * 256 + threadIdx.x;
+    const int pl0 = (blockIdx.x * 256 + threadIdx.x) * 4;
     const int m = blockIdx.y;
     const int gi = blockIdx.z;
-    if (pl >= A.pc) return;
-    const int64_t p = A.p_begin + pl;
+    if (pl0 >= A.pc) return;
+    const int ch = gi * A.Kg + m;
+    const float bias = A.bias ? A.bias[ch] : 0.0f;
+    const float* crow = A.c + ((int64_t)gi * A.Kg + m) * A.pc;
+    const __amdgpu_buffer_rsrc_t ry = pk_rsrc(A.y, A.y_bytes);
+    const int64_t p = A.p_begin + pl0;
     const int64_t n = p / A.HoWo;
     const int64_t hw = p - n * A.HoWo;
-    const int ch = gi * A.Kg + m;
-    float v = A.c[((int64_t)gi * A.Kg + m) * A.pc + pl];
-    if (A.bias) v += A.bias[ch];
     const int64_t off = n * A.y_nstride + (int64_t)ch * A.HoWo + hw;
-    const __amdgpu_buffer_rsrc_t ry = pk_rsrc(A.y, A.y_bytes);
-    if (BF16OUT)
-        __builtin_amdgcn_raw_buffer_store_b16(pk_f32_to_bf16(v), ry, (uint32_t)(off * 2), 0, 0);
-    else
-        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), ry, (uint32_t)(off * 4), 0, 0);
+    const bool vec = ((A.HoWo & 3) == 0) & ((A.pc & 3) == 0) & ((A.p_begin & 3) == 0) & (pl0 + 4 <= A.pc);
+    if (vec) {
+        typedef float f32x4 __attribute__((ext_vector_type(4)));
+        const f32x4 c = *reinterpret_cast<const f32x4*>(crow + pl0);
+        if (BF16OUT) {
+            typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+            const u32x2 q = {(uint32_t)pk_f32_to_bf16(c[0] + bias) | ((uint32_t)pk_f32_to_bf16(c[1] + bias) << 16),
+                             (uint32_t)pk_f32_to_bf16(c[2] + bias) | ((uint32_t)pk_f32_to_bf16(c[3] + bias) << 16)};
+            __builtin_amdgcn_raw_buffer_store_b64(q, ry, (uint32_t)(off * 2), 0, 0);
+        } else {
+            typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+            const u32x4 q = {__builtin_bit_cast(uint32_t, c[0] + bias), __builtin_bit_cast(uint32_t, c[1] + bias),
+                             __builtin_bit_cast(uint32_t, c[2] + bias), __builtin_bit_cast(uint32_t, c[3] + bias)};
+            __builtin_amdgcn_raw_buffer_store_b128(q, ry, (uint32_t)(off * 4), 0, 0);
+        }
+        return;
+    }
+    for (int j = 0; j < 4 && pl0 + j < A.pc; ++j) {
+        const int64_t pj = p + j;
+        const int64_t nj = pj / A.HoWo;
+        const int64_t o = nj * A.y_nstride + (int64_t)ch * A.HoWo + (pj - nj * A.HoWo);
+        const float v = crow[pl0 + j] + bias;
+        if (BF16OUT)
+            __builtin_amdgcn_raw_buffer_store_b16(pk_f32_to_bf16(v), ry, (uint32_t)(o * 2), 0, 0);
+        else
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), ry, (uint32_t)(o * 4), 0, 0);
+    }
 }
 
 hipError_t launch_unpack(const UnpackArgs& a, int ydt, int groups, hipStream_t stream) {
-    dim3 grid((unsigned)((a.pc + 255) / 256), (unsigned)a.Kg, (unsigned)groups);
+    dim3 grid((unsigned)((a.pc + 1023) / 1024), (unsigned)a.Kg, (unsigned)groups);
     if (ydt == CONV2D_BF16)
         hipLaunchKernelGGL(unpack_kernel<true>, grid, dim3(256), 0, stream, a);
     else
