@@ -207,3 +207,107 @@ CONFIGS = {
     "dw": _cfg("dw", n=32, c=256, h=56, w=56, k=256, r=3, s=3, pad=(1, 1), groups=256, seed=6),
 }
 
+
+
+# ---------------------------------------------------------------- device-side generation
+
+def _i64(v: int) -> int:
+    """A 64-bit pattern as a signed int64 value (torch has no uint64 arithmetic)."""
+    v &= _MASK
+    return v - (1 << 64) if v >= (1 << 63) else v
+
+
+def _lsr(z, k: int):
+    """Logical right shift of int64 bit patterns."""
+    return (z >> k) & ((1 << (64 - k)) - 1)
+
+
+def raw_stream_torch(seed: int, tensor_id: int, count: int, device="cpu", chunk: int = 1 << 26):
+    """The uint64 stream of raw_stream() as int64 bit patterns, computed with torch on
+    `device` (wrapping int64 arithmetic gives the same bits as uint64)."""
+    import torch
+    start = _i64(stream_start(seed, tensor_id))
+    gamma, m1, m2 = _i64(GAMMA), _i64(_M1), _i64(_M2)
+    out = torch.empty(count, dtype=torch.int64, device=device)
+    for lo in range(0, count, chunk):
+        hi = min(count, lo + chunk)
+        z = torch.arange(lo + 1, hi + 1, dtype=torch.int64, device=device) * gamma + start
+        z = (z ^ _lsr(z, 30)) * m1
+        z = (z ^ _lsr(z, 27)) * m2
+        out[lo:hi] = z ^ _lsr(z, 31)
+    return out
+
+
+def draw_torch(seed: int, tensor_id: int, shape, mode: str = "random", const: float = 1.0,
+               scale: float = 1.0, device="cpu"):
+    """draw() computed on a torch device; returns float32 values bit-identical to draw()."""
+    import torch
+    count = 1
+    for d in shape:
+        count *= int(d)
+    if mode == "constant":
+        v = torch.full((count,), float(const), dtype=torch.float64, device=device)
+    else:
+        z = raw_stream_torch(seed, tensor_id, count, device)
+        u = _lsr(z, 40).to(torch.float64) * (2.0 ** -24)
+        del z
+        if mode == "random":
+            v = 2.0 * u - 1.0
+        elif mode == "integer":
+            v = torch.floor(9.0 * u) - 4.0
+        else:
+            raise ValueError(f"unknown data mode {mode!r}")
+    if scale != 1.0:
+        v = v * scale
+    return v.to(torch.float32).reshape(tuple(shape))
+
+
+def round_bf16_torch(t):
+    """Round fp32 values to bf16 (RNE) on the tensor's device; returns torch.bfloat16."""
+    import torch
+    return t.to(torch.bfloat16)
+
+
+# ---------------------------------------------------------------- the random sweep
+
+SWEEP_CHANNELS = (3, 16, 32, 64, 128, 256, 512, 1024, 2048)
+SWEEP_SIZES = (7, 14, 28, 56, 112, 224)
+
+
+def sweep_shapes(out_hw, count: int = 500, master_seed: int = 1000, max_bytes: int = 2 << 30,
+                 max_flops: float = 2e13):
+    """The seeded random sweep of convolutions.
+
+    Draw i (in order): dtype fp32 for even i and bf16 for odd i (y in the same type);
+    depthwise with probability 0.2 (then K = C = groups); N in {1, 8, 32}; C and K in
+    SWEEP_CHANNELS; H = W in SWEEP_SIZES; R = S in {1, 3, 5, 7}; stride in {1, 2};
+    dilation in {1, 2}; 'same' padding p = d*(R-1)/2.  A draw whose fp32 |x| + |y| exceeds
+    max_bytes or whose FLOP count exceeds max_flops is rejected and redrawn.  Input seed of
+    convolution i is master_seed + i.  `out_hw(shape) -> (Ho, Wo)` is supplied by the caller
+    (this module holds no convolution arithmetic).  Returns (shapes, rejected_count).
+    """
+    rng = np.random.default_rng(master_seed)
+    shapes, rejected = [], 0
+    while len(shapes) < count:
+        i = len(shapes)
+        dw = bool(rng.random() < 0.2)
+        n = int(rng.choice((1, 8, 32)))
+        c = int(rng.choice(SWEEP_CHANNELS))
+        k = c if dw else int(rng.choice(SWEEP_CHANNELS))
+        h = int(rng.choice(SWEEP_SIZES))
+        r = int(rng.choice((1, 3, 5, 7)))
+        st = int(rng.choice((1, 2)))
+        dl = int(rng.choice((1, 2)))
+        p = dl * (r - 1) // 2
+        dt = "f32" if i % 2 == 0 else "bf16"
+        cs = ConvShape(n=n, c=c, h=h, w=h, k=k, r=r, s=r, stride=(st, st), pad=(p, p), dil=(dl, dl),
+                       groups=c if dw else 1, x_dtype=dt, y_dtype=dt, seed=master_seed + i,
+                       name=f"sweep{i:03d}")
+        ho, wo = out_hw(cs)
+        xy = 4 * (n * c * h * h + n * k * ho * wo)
+        fl = 2.0 * n * k * (c // cs.groups) * r * r * ho * wo
+        if xy > max_bytes or fl > max_flops:
+            rejected += 1
+            continue
+        shapes.append(cs)
+    return shapes, rejected

@@ -63,19 +63,25 @@ def from_device(t) -> np.ndarray:
 class DeviceConv:
     """One operation on one device: inputs, descriptor, output."""
 
-    def __init__(self, cs, mode: str = "random", device: str = "cuda:0", inputs=None):
+    def __init__(self, cs, mode: str = "random", device: str = "cuda:0", inputs=None, device_inputs=None):
+        """inputs: host float32 (x NCHW, w, b) to upload; device_inputs: tensors already on the
+        device in the layout and dtype of `cs` (then x_host etc. are not kept)."""
         import torch
         self.cs = cs
         self.device = torch.device(device)
-        if inputs is None:
-            inputs = _datagen().make_inputs(cs, mode)
-        self.x_host, self.w_host, self.b_host = inputs   # NCHW / KCRS float32 values
-        x_dev = self.x_host
-        if cs.layout == "nhwc":
-            x_dev = np.ascontiguousarray(self.x_host.transpose(0, 2, 3, 1))
-        self.x = to_device(x_dev, cs.x_dtype, self.device)
-        self.w = to_device(self.w_host, cs.x_dtype, self.device)
-        self.b = torch.from_numpy(self.b_host).to(self.device) if cs.has_bias else None
+        if device_inputs is not None:
+            self.x, self.w, self.b = device_inputs
+            self.x_host = self.w_host = self.b_host = None
+        else:
+            if inputs is None:
+                inputs = _datagen().make_inputs(cs, mode)
+            self.x_host, self.w_host, self.b_host = inputs   # NCHW / KCRS float32 values
+            x_dev = self.x_host
+            if cs.layout == "nhwc":
+                x_dev = np.ascontiguousarray(self.x_host.transpose(0, 2, 3, 1))
+            self.x = to_device(x_dev, cs.x_dtype, self.device)
+            self.w = to_device(self.w_host, cs.x_dtype, self.device)
+            self.b = torch.from_numpy(self.b_host).to(self.device) if cs.has_bias else None
         self.desc = B.conv2d_desc_create(params_for(cs))
         n, k, ho, wo = B.conv2d_output_shape(self.desc)
         self.out_nkhw = (n, k, ho, wo)
