@@ -235,6 +235,81 @@ def summarize_profiles(d, workload, algo_name="implicit_gemm"):
     return "\n".join(lines) + "\n", traffic
 
 
+def run_sweep(report_path, B, torch):
+    """Time every convolution of the 500-convolution sweep with the planner's algorithm and
+    report, per class, the fraction of the MFMA roofline (contraction-bound: arithmetic
+    intensity at or above the ridge) or of the HBM roofline (the rest)."""
+    import datagen
+    from paper_2407_10730_amd.runner import DeviceConv, params_for
+
+    def out_hw(cs):
+        d = B.conv2d_desc_create(params_for(cs))
+        try:
+            return B.conv2d_output_shape(d)[2:]
+        finally:
+            B.conv2d_desc_destroy(d)
+
+    shapes, rejected = datagen.sweep_shapes(out_hw)
+    dev = torch.device("cuda:0")
+    rows = []
+    for cs in shapes:
+        x = datagen.draw_torch(cs.seed, datagen.TENSOR_X, cs.x_shape(), device=dev)
+        w = datagen.draw_torch(cs.seed, datagen.TENSOR_W, cs.w_shape(), device=dev)
+        b = datagen.draw_torch(cs.seed, datagen.TENSOR_B, (cs.k,), device=dev)
+        if cs.x_dtype == "bf16":
+            x, w = x.to(torch.bfloat16), w.to(torch.bfloat16)
+        dc = DeviceConv(cs, device_inputs=(x, w, b))
+        B.conv2d_set_timing(dc.desc, B.CONV2D_TIMING_OFF)
+        stream = torch.cuda.current_stream()
+        dc.run(B.CONV2D_ALGO_AUTO, stream)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        dc.run(B.CONV2D_ALGO_AUTO, stream)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter() - t0
+        runs = int(min(20, max(3, 0.05 / max(t1, 1e-6))))
+        t0 = time.perf_counter()
+        for _ in range(runs):
+            dc.run(B.CONV2D_ALGO_AUTO, stream)
+        torch.cuda.synchronize()
+        sec = (time.perf_counter() - t0) / runs
+        n, k, ho, wo = dc.out_nkhw
+        flops = 2 * n * k * (cs.c // cs.groups) * cs.r * cs.s * ho * wo
+        nbytes = algorithmic_bytes(cs, dc.out_nkhw)
+        ai = flops / nbytes
+        peak = PEAK_TFLOPS[cs.x_dtype]
+        ridge = peak * 1e12 / (PEAK_HBM_GBS * 1e9)
+        tf = flops / sec / 1e12
+        gbs = nbytes / sec / 1e9
+        bound = "mfma" if ai >= ridge else "hbm"
+        frac = tf / peak if bound == "mfma" else gbs / PEAK_HBM_GBS
+        algo = B.ALGO_NAMES[dc.plan(B.CONV2D_ALGO_AUTO).algo]
+        rows.append({"name": cs.name, "dtype": cs.x_dtype, "n": cs.n, "c": cs.c, "hw": cs.h, "k": cs.k,
+                     "r": cs.r, "stride": cs.stride[0], "dil": cs.dil[0], "groups": cs.groups,
+                     "algo": algo, "us": sec * 1e6, "tflops": tf, "gbs": gbs, "ai": ai, "bound": bound,
+                     "frac": frac, "depthwise": cs.groups > 1})
+        dc.close()
+        del x, w, b
+    def summary(sel):
+        if not sel:
+            return None
+        fr = sorted(r["frac"] for r in sel)
+        return {"count": len(sel), "median_frac": fr[len(fr) // 2], "min_frac": fr[0], "max_frac": fr[-1]}
+    out = {
+        "rejected_draws": rejected,
+        "contraction_bound_f32": summary([r for r in rows if r["bound"] == "mfma" and r["dtype"] == "f32"]),
+        "contraction_bound_bf16": summary([r for r in rows if r["bound"] == "mfma" and r["dtype"] == "bf16"]),
+        "depthwise": summary([r for r in rows if r["depthwise"]]),
+        "hbm_bound_other": summary([r for r in rows if r["bound"] == "hbm" and not r["depthwise"]]),
+        "depthwise_at_70pct_hbm": sum(1 for r in rows if r["depthwise"] and r["frac"] >= 0.7),
+        "contraction_at_60pct_mfma": sum(1 for r in rows if r["bound"] == "mfma" and r["frac"] >= 0.6),
+        "total_seconds_one_pass": sum(r["us"] for r in rows) * 1e-6,
+    }
+    with open(report_path, "w") as f:
+        json.dump({"summary": out, "convs": rows}, f, indent=1)
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -249,6 +324,8 @@ def main():
                     help="write the text summary of rocprofv3 outputs in DIR (no GPU needed) and exit")
     ap.add_argument("--traffic-kernel", default=None,
                     help="with --summarize-profiles: kernel whose traffic goes to profiles/traffic.json")
+    ap.add_argument("--sweep", metavar="REPORT",
+                    help="time the 500-convolution sweep, write per-convolution rows to REPORT and exit")
     args = ap.parse_args()
     if args.summarize_profiles:
         text, traffic = summarize_profiles(args.summarize_profiles, args.workload)
@@ -284,6 +361,9 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     B.load()
+    if args.sweep:
+        print(json.dumps(run_sweep(args.sweep, B, torch)), flush=True)
+        return
     cs = datagen.CONFIGS[args.workload]
     print(f"[bench] workload {args.workload}: {describe(cs)}", file=sys.stderr, flush=True)
     dc = DeviceConv(cs)
