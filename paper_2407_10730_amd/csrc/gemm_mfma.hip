@@ -21,30 +21,83 @@
 
 namespace cv {
 
+// Epilogue of both kernels.  Accumulator v of lane l holds row 8*(v/4) + 4*(l/32) + v%4,
+// column l%32 of its 32x32 tile.  All bias values of the rows a lane writes are loaded
+// before its first store, so the stores leave back to back behind one wait (a load
+// between two stores would make each store wait for the previous one).
+template <int TM, int TN, int EPI, typename TOut>
+__device__ __forceinline__ void store_tile(const GemmArgs& A, f32x16 (&acc)[TM][TN], int gi, int mb, int pb,
+                                           int lrow, int lcol) {
+    if (EPI == EPI_NCHW && A.bias != nullptr) {
+        const __amdgpu_buffer_rsrc_t rbias = make_rsrc(A.bias, (uint32_t)(gridDim.z * A.M * 4));
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int m = mb + i * 32 + 8 * (v >> 2) + 4 * lrow + (v & 3);
+                const float bv = ld_f32(rbias, m < A.M ? (uint32_t)((gi * A.M + m) * 4) : OOB_OFF);
+#pragma unroll
+                for (int j = 0; j < TN; ++j) acc[i][j][v] += bv;
+            }
+    }
+    const __amdgpu_buffer_rsrc_t ry = make_rsrc(A.y, A.y_bytes);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int p = pb + j * 32 + lcol;
+        const bool pok = p < A.P;
+        int64_t ybase;
+        if (EPI == EPI_NCHW) {
+            const int n_img = p / A.HoWo;
+            const int hw = p - n_img * A.HoWo;
+            ybase = (int64_t)n_img * A.y_nstride + (int64_t)gi * A.M * A.HoWo + hw;
+        } else {
+            ybase = (int64_t)gi * A.c_gstride + p;
+        }
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int m = mb + i * 32 + 8 * (v >> 2) + 4 * lrow + (v & 3);
+                const bool ok = pok & (m < A.M);
+                if (EPI == EPI_NCHW)
+                    store_out<TOut>(ry, (uint32_t)(ybase + (int64_t)m * A.HoWo), ok, acc[i][j][v]);
+                else
+                    store_out<float>(ry, (uint32_t)(ybase + (int64_t)m * A.ldc), ok, acc[i][j][v]);
+            }
+    }
+}
+
 // ============================================================================ fp32
 // Block: 256 threads = 4 waves arranged WM x WN over a BM x BN tile; each wave
 // owns (BM/WM) x (BN/WN) = TM x TN MFMA 32x32x2 tiles.  BK reduction rows per
-// stage, double-buffered in LDS (k-major, so one MFMA operand read is 32
-// consecutive floats per half-wave).  PF = 1: the global loads of stage s+1
-// are issued before the MFMAs of stage s; PF = 2: two register sets, the loads
-// of stage s+2 are issued before the MFMAs of stage s, so a load has two
-// stages of MFMA work to land.
+// stage, double-buffered in LDS.  Both operands sit in LDS row-per-output
+// ([m][k] and [p][k]) with the BK values of a row contiguous: the MFMA of step
+// ks takes reduction index ks from lanes 0-31 and ks + BK/2 from lanes 32-63,
+// so a lane reads its BK/2 operand values of a stage with 16-byte LDS loads,
+// and a loader thread that holds 4 consecutive reduction rows of one output
+// writes them with one 16-byte store.  The row pitch is BK + 4 floats.
+// PF = 1: the global loads of stage s+1 are issued before the MFMAs of stage s;
+// PF = 2: two register sets, the loads of stage s+2 are issued before the
+// MFMAs of stage s, so a load has two stages of MFMA work to land.
 template <int BM, int BN, int WM, int WN, int BK, int PF, int BSRC, int EPI, typename TOut>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs A) {
     constexpr int WTM = BM / WM, WTN = BN / WN;
     constexpr int TM = WTM / 32, TN = WTN / 32;
     static_assert(WM * WN == 4 && TM >= 1 && TN >= 1, "bad wave layout");
     static_assert(PF == 1 || PF == 2, "prefetch distance");
+    static_assert(BK == 16 || BK == 32, "stage depth");
+    constexpr int LDK = BK + 4;               // LDS row pitch in floats (16-byte aligned rows)
+    constexpr int KH = BK / 2;                // reduction values per lane per stage
     constexpr int BNT = BN < 256 ? BN : 256;  // threads along pixels in the B loader
-    constexpr int BKT = 256 / BNT;            // threads along k
+    constexpr int BKT = 256 / BNT;            // threads along k (each owns runs of 4 rows)
     constexpr int BCOLS = BN / BNT;           // pixel columns per thread
-    constexpr int BROWS = BK / BKT;           // k rows per thread
-    constexpr int AROWS = BM * BK / 256;      // A elements per thread
+    constexpr int BRUNS = BK / (4 * BKT);     // runs of 4 consecutive k rows per thread
+    constexpr int ARUNS = BM * BK / 1024;     // runs of 4 consecutive k of one A row per thread
     static_assert(BNT >= 64, "B loader needs wave-uniform k rows");
-    static_assert(256 % BK == 0 && AROWS >= 4 && AROWS % 4 == 0, "A loader layout");
+    static_assert(BRUNS >= 1 && ARUNS >= 1, "loader layout");
 
-    __shared__ float As[2][BK][BM + 1];
-    __shared__ float Bs[2][BK][BN];
+    __shared__ __attribute__((aligned(16))) float As[2][BM][LDK];
+    __shared__ __attribute__((aligned(16))) float Bs[2][BN][LDK];
 
     const int t = threadIdx.x;
     const int lane = t & 63;
@@ -60,7 +113,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs A) {
     const __amdgpu_buffer_rsrc_t ra = make_rsrc(A.a, A.a_bytes);
     const __amdgpu_buffer_rsrc_t rb = make_rsrc(A.b, A.b_bytes);
 
-    // ---- B loader state
+    // ---- B loader: thread (tn, tk) loads pixels tn + j*BNT, k rows 4*(g*BKT + tk) + i
     const int tn = t % BNT;
     const int tk = __builtin_amdgcn_readfirstlane(t / BNT);
     ColState cs[BCOLS];
@@ -71,19 +124,17 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs A) {
         if (BSRC != BSRC_DENSE) cs[j] = col_state(A, p, gi);
         dvb[j] = p < A.P ? (uint32_t)(((int64_t)gi * A.b_gstride + p) * 4) : OOB_OFF;
     }
-    // ---- A loader state: element (m = am + i*(256/BK), k = ak)
-    const int ak = t % BK;
-    const int am = t / BK;
+    // ---- A loader: run g of thread t is row (t + g*256) / (BK/4), k 4*((t + g*256) % (BK/4)) + i
     const int64_t a_base = (int64_t)gi * A.a_gstride;
 
-    float breg0[BROWS][BCOLS], breg1[BROWS][BCOLS];
-    float areg0[AROWS], areg1[AROWS];
+    f32x4 breg0[BRUNS][BCOLS], breg1[BRUNS][BCOLS];
+    f32x4 areg0[ARUNS], areg1[ARUNS];
     // tap-major cursor of the next stage to load.  Channel blocks outermost, filter
     // taps innermost: the taps of one channel block re-read the same input lines,
     // which then hit in L1.
     int cur_c0 = 0, cur_r = 0, cur_s = 0;
 
-    auto load_stage = [&](int stage, float (&breg)[BROWS][BCOLS], float (&areg)[AROWS]) {
+    auto load_stage = [&](int stage, f32x4 (&breg)[BRUNS][BCOLS], f32x4 (&areg)[ARUNS]) {
         const int k0 = stage * BK;
         if constexpr (BSRC == BSRC_IMPLICIT_TAP) {
             const int roff = cur_r * A.dh, soff = cur_s * A.dw;
@@ -96,24 +147,24 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs A) {
                 vb[j] = ok ? (uint32_t)(((int32_t)cs[j].base + tapoff) * 4) : OOB_OFF;
             }
 #pragma unroll
-            for (int i = 0; i < BROWS; ++i) {
-                const uint32_t cofs = (uint32_t)((cur_c0 + tk + i * BKT) * A.HW) * 4u;
+            for (int g = 0; g < BRUNS; ++g)
 #pragma unroll
-                for (int j = 0; j < BCOLS; ++j) breg[i][j] = ld_f32(rb, vb[j] + cofs);
-            }
+                for (int i = 0; i < 4; ++i) {
+                    const uint32_t cofs = (uint32_t)((cur_c0 + 4 * (g * BKT + tk) + i) * A.HW) * 4u;
+#pragma unroll
+                    for (int j = 0; j < BCOLS; ++j) breg[g][j][i] = ld_f32(rb, vb[j] + cofs);
+                }
             // weights in tap-major order [K][R*S][C/g]: 4 consecutive channels per 16-byte load
             const int tap = cur_r * A.S + cur_s;
 #pragma unroll
-            for (int i = 0; i < AROWS / 4; ++i) {
-                const int q = t + i * 256;
+            for (int g = 0; g < ARUNS; ++g) {
+                const int q = t + g * 256;
                 const int m = m0 + q / (BK / 4);
                 const int64_t e = a_base + (int64_t)m * A.lda + (int64_t)tap * A.Cg + cur_c0 + 4 * (q % (BK / 4));
                 // bit-cast the whole vector: casting its elements one by one made this
                 // compiler emit a single-dword load
-                const f32x4 v = __builtin_bit_cast(
+                areg[g] = __builtin_bit_cast(
                     f32x4, __builtin_amdgcn_raw_buffer_load_b128(ra, m < A.M ? (uint32_t)(e * 4) : OOB_OFF, 0, 0));
-#pragma unroll
-                for (int j = 0; j < 4; ++j) areg[4 * i + j] = v[j];
             }
             if (++cur_s == A.S) {
                 cur_s = 0;
@@ -123,49 +174,52 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs A) {
                 }
             }
         } else {
-            if constexpr (BSRC == BSRC_IMPLICIT_NCHW) {
-                KTabEntry e[BROWS];
 #pragma unroll
-                for (int i = 0; i < BROWS; ++i) e[i] = ktab_at(A.ktab, k0 + tk + i * BKT);
+            for (int g = 0; g < BRUNS; ++g) {
+                const int kb = k0 + 4 * (g * BKT + tk);
+                if constexpr (BSRC == BSRC_IMPLICIT_NCHW) {
+                    KTabEntry e[4];
 #pragma unroll
-                for (int i = 0; i < BROWS; ++i)
+                    for (int i = 0; i < 4; ++i) e[i] = ktab_at(A.ktab, kb + i);
 #pragma unroll
-                    for (int j = 0; j < BCOLS; ++j) breg[i][j] = ld_f32(rb, implicit_off<4>(A, cs[j], e[i]));
-            } else {
+                    for (int i = 0; i < 4; ++i)
 #pragma unroll
-                for (int i = 0; i < BROWS; ++i) {
-                    const int kr = k0 + tk + i * BKT;
-                    const bool kok = kr < A.Kred;
+                        for (int j = 0; j < BCOLS; ++j) breg[g][j][i] = ld_f32(rb, implicit_off<4>(A, cs[j], e[i]));
+                } else {
 #pragma unroll
-                    for (int j = 0; j < BCOLS; ++j)
-                        breg[i][j] = ld_f32(rb, kok ? dvb[j] + (uint32_t)kr * (uint32_t)A.ldb * 4u : OOB_OFF);
+                    for (int i = 0; i < 4; ++i) {
+                        const int kr = kb + i;
+                        const bool kok = kr < A.Kred;
+#pragma unroll
+                        for (int j = 0; j < BCOLS; ++j)
+                            breg[g][j][i] = ld_f32(rb, kok ? dvb[j] + (uint32_t)kr * (uint32_t)A.ldb * 4u : OOB_OFF);
+                    }
                 }
             }
 #pragma unroll
-            for (int i = 0; i < AROWS; ++i) {
-                const int m = m0 + am + i * (256 / BK);
-                const int kr = k0 + ak;
-                const bool ok = (m < A.M) & (kr < A.Kred);
-                const int64_t e = a_base + (int64_t)m * A.lda + kr;
-                areg[i] = ld_f32(ra, ok ? (uint32_t)(e * 4) : OOB_OFF);
+            for (int g = 0; g < ARUNS; ++g) {
+                const int q = t + g * 256;
+                const int m = m0 + q / (BK / 4);
+                const int kb = k0 + 4 * (q % (BK / 4));
+                const int64_t e = a_base + (int64_t)m * A.lda + kb;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const bool ok = (m < A.M) & (kb + i < A.Kred);
+                    areg[g][i] = ld_f32(ra, ok ? (uint32_t)((e + i) * 4) : OOB_OFF);
+                }
             }
         }
     };
-    auto store_stage = [&](int buf, const float (&breg)[BROWS][BCOLS], const float (&areg)[AROWS]) {
+    auto store_stage = [&](int buf, const f32x4 (&breg)[BRUNS][BCOLS], const f32x4 (&areg)[ARUNS]) {
 #pragma unroll
-        for (int i = 0; i < BROWS; ++i)
+        for (int g = 0; g < BRUNS; ++g)
 #pragma unroll
-            for (int j = 0; j < BCOLS; ++j) Bs[buf][tk + i * BKT][tn + j * BNT] = breg[i][j];
-        if constexpr (BSRC == BSRC_IMPLICIT_TAP) {
+            for (int j = 0; j < BCOLS; ++j)
+                *reinterpret_cast<f32x4*>(&Bs[buf][tn + j * BNT][4 * (g * BKT + tk)]) = breg[g][j];
 #pragma unroll
-            for (int i = 0; i < AROWS / 4; ++i) {
-                const int q = t + i * 256;
-#pragma unroll
-                for (int j = 0; j < 4; ++j) As[buf][4 * (q % (BK / 4)) + j][q / (BK / 4)] = areg[4 * i + j];
-            }
-        } else {
-#pragma unroll
-            for (int i = 0; i < AROWS; ++i) As[buf][ak][am + i * (256 / BK)] = areg[i];
+        for (int g = 0; g < ARUNS; ++g) {
+            const int q = t + g * 256;
+            *reinterpret_cast<f32x4*>(&As[buf][q / (BK / 4)][4 * (q % (BK / 4))]) = areg[g];
         }
     };
 
@@ -179,23 +233,29 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs A) {
 
     const int wm0 = (wave % WM) * WTM;
     const int wn0 = (wave / WM) * WTN;
-    const int lrow = lane >> 5;  // which of the two k rows this half-wave feeds
+    const int lrow = lane >> 5;  // 0: first half of the stage's reduction rows, 1: second half
     const int lcol = lane & 31;
 
     auto compute = [&](int buf) {
+        f32x4 a[TM][KH / 4], b[TN][KH / 4];
 #pragma unroll
-        for (int ks = 0; ks < BK / 2; ++ks) {
-            float a[TM], b[TN];
+        for (int i = 0; i < TM; ++i)
 #pragma unroll
-            for (int i = 0; i < TM; ++i) a[i] = As[buf][2 * ks + lrow][wm0 + i * 32 + lcol];
+            for (int v = 0; v < KH / 4; ++v)
+                a[i][v] = *reinterpret_cast<const f32x4*>(&As[buf][wm0 + i * 32 + lcol][KH * lrow + 4 * v]);
 #pragma unroll
-            for (int j = 0; j < TN; ++j) b[j] = Bs[buf][2 * ks + lrow][wn0 + j * 32 + lcol];
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int v = 0; v < KH / 4; ++v)
+                b[j][v] = *reinterpret_cast<const f32x4*>(&Bs[buf][wn0 + j * 32 + lcol][KH * lrow + 4 * v]);
+#pragma unroll
+        for (int ks = 0; ks < KH; ++ks)
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
-        }
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][ks / 4][ks % 4], b[j][ks / 4][ks % 4],
+                                                                     acc[i][j], 0, 0, 0);
     };
 
     const int n = A.nstages;
@@ -231,36 +291,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs A) {
         }
     }
 
-    // ---- epilogue.  Accumulator v of lane l holds row 8*(v/4) + 4*(l/32) + v%4, column l%32.
-    const __amdgpu_buffer_rsrc_t ry = make_rsrc(A.y, A.y_bytes);
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-        const int p = p0 + wn0 + j * 32 + lcol;
-        const bool pok = p < A.P;
-        int64_t ybase;
-        if (EPI == EPI_NCHW) {
-            const int n_img = p / A.HoWo;
-            const int hw = p - n_img * A.HoWo;
-            ybase = (int64_t)n_img * A.y_nstride + (int64_t)gi * A.M * A.HoWo + hw;
-        } else {
-            ybase = (int64_t)gi * A.c_gstride + p;
-        }
-#pragma unroll
-        for (int i = 0; i < TM; ++i) {
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int m = m0 + wm0 + i * 32 + 8 * (v >> 2) + 4 * lrow + (v & 3);
-                const bool ok = pok & (m < A.M);
-                float val = acc[i][j][v];
-                if (EPI == EPI_NCHW) {
-                    if (A.bias != nullptr && ok) val += A.bias[gi * A.M + m];
-                    store_out<TOut>(ry, (uint32_t)(ybase + (int64_t)m * A.HoWo), ok, val);
-                } else {
-                    store_out<float>(ry, (uint32_t)(ybase + (int64_t)m * A.ldc), ok, val);
-                }
-            }
-        }
-    }
+    store_tile<TM, TN, EPI, TOut>(A, acc, gi, m0 + wm0, p0 + wn0, lrow, lcol);
 }
 
 // ============================================================================ bf16
@@ -433,35 +464,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs A) {
         __syncthreads();
     }
 
-    const __amdgpu_buffer_rsrc_t ry = make_rsrc(A.y, A.y_bytes);
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-        const int p = p0 + wn0 + j * 32 + lcol;
-        const bool pok = p < A.P;
-        int64_t ybase;
-        if (EPI == EPI_NCHW) {
-            const int n = p / A.HoWo;
-            const int hw = p - n * A.HoWo;
-            ybase = (int64_t)n * A.y_nstride + (int64_t)gi * A.M * A.HoWo + hw;
-        } else {
-            ybase = (int64_t)gi * A.c_gstride + p;
-        }
-#pragma unroll
-        for (int i = 0; i < TM; ++i) {
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int m = m0 + wm0 + i * 32 + 8 * (v >> 2) + 4 * lrow + (v & 3);
-                const bool ok = pok & (m < A.M);
-                float val = acc[i][j][v];
-                if (EPI == EPI_NCHW) {
-                    if (A.bias != nullptr && ok) val += A.bias[gi * A.M + m];
-                    store_out<TOut>(ry, (uint32_t)(ybase + (int64_t)m * A.HoWo), ok, val);
-                } else {
-                    store_out<float>(ry, (uint32_t)(ybase + (int64_t)m * A.ldc), ok, val);
-                }
-            }
-        }
-    }
+    store_tile<TM, TN, EPI, TOut>(A, acc, gi, m0 + wm0, p0 + wn0, lrow, lcol);
 }
 
 // ============================================================================ dispatch

@@ -184,26 +184,28 @@ hipError_t launch_unpack(const UnpackArgs& a, int ydt, int groups, hipStream_t s
 // reduction, so one stage's weights (one tap, consecutive channels) are contiguous.
 template <typename T>
 __global__ __launch_bounds__(256) void repack_tap_major_kernel(const T* __restrict__ w, T* __restrict__ wr,
-                                                              int64_t total, int cg, int rs) {
-    const int64_t o = (int64_t)blockIdx.x * 256 + threadIdx.x;
+                                                              uint32_t total, uint32_t cg, uint32_t rs) {
+    // 32-bit index arithmetic: the host guarantees total < 2^31
+    const uint32_t o = blockIdx.x * 256u + threadIdx.x;
     if (o >= total) return;
-    const int c = (int)(o % cg);
-    const int64_t kt = o / cg;
-    const int tap = (int)(kt % rs);
-    const int64_t k = kt / rs;
+    const uint32_t c = o % cg;
+    const uint32_t kt = o / cg;
+    const uint32_t tap = kt % rs;
+    const uint32_t k = kt / rs;
     wr[o] = w[(k * cg + c) * rs + tap];
 }
 
 hipError_t launch_repack_tap_major(const void* w, void* wr, int64_t k, int64_t cg, int64_t rs, int elem_bytes,
                                    hipStream_t stream) {
     const int64_t total = k * cg * rs;
+    if (total <= 0 || total >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
     dim3 grid((unsigned)((total + 255) / 256));
     if (elem_bytes == 4)
         hipLaunchKernelGGL(repack_tap_major_kernel<uint32_t>, grid, dim3(256), 0, stream, (const uint32_t*)w,
-                           (uint32_t*)wr, total, (int)cg, (int)rs);
+                           (uint32_t*)wr, (uint32_t)total, (uint32_t)cg, (uint32_t)rs);
     else
         hipLaunchKernelGGL(repack_tap_major_kernel<uint16_t>, grid, dim3(256), 0, stream, (const uint16_t*)w,
-                           (uint16_t*)wr, total, (int)cg, (int)rs);
+                           (uint16_t*)wr, (uint32_t)total, (uint32_t)cg, (uint32_t)rs);
     return hipGetLastError();
 }
 
