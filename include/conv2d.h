@@ -116,6 +116,12 @@ typedef struct {
     int64_t total_calls;
 } conv2d_breakdown_t;
 
+/* Microkernels behind the algorithms.  IMPLICIT_GEMM runs either the tiled MFMA
+ * GEMM that gathers im2col slices into LDS (GEMM) or, for short reductions
+ * (C/g * R * S), the sliced direct kernel that keeps the input rows of a run of
+ * output pixels in LDS and reads the columns from there (SLICE). */
+enum { CONV2D_KERNEL_GEMM = 0, CONV2D_KERNEL_SLICE = 1, CONV2D_KERNEL_DIRECT = 2 };
+
 /* What the planner decided for one algorithm (for reports and tests). */
 typedef struct {
     int32_t algo;             /* resolved algorithm (never AUTO) */
@@ -125,6 +131,7 @@ typedef struct {
     int64_t chunks;           /* explicit path: number of pack/GEMM/unpack chunks */
     int32_t needs_reorder;    /* 1 when pre/post layout reorders run (NHWC through an NCHW kernel) */
     int32_t op_class;         /* bit 0 pointwise, 1 grouped, 2 depthwise, 3 dilated, 4 rectangular, 5 strided */
+    int32_t kernel;           /* microkernel that runs: CONV2D_KERNEL_* */
 } conv2d_plan_info;
 
 /* Validate params, compute the output size, classify the operation and plan

@@ -34,6 +34,8 @@ PHASE_NAMES = ["pre_analysis", "pre_reorder", "in_tiling", "in_packing", "in_mic
                "in_unpacking", "post_reorder"]
 CONV2D_PH_COUNT = 7
 CONV2D_TIMING_OFF, CONV2D_TIMING_TOTAL, CONV2D_TIMING_PHASES = 0, 1, 2
+CONV2D_KERNEL_GEMM, CONV2D_KERNEL_SLICE, CONV2D_KERNEL_DIRECT = 0, 1, 2
+KERNEL_NAMES = {CONV2D_KERNEL_GEMM: "gemm", CONV2D_KERNEL_SLICE: "slice", CONV2D_KERNEL_DIRECT: "direct"}
 
 # every function the header declares
 EXPORTS = ("conv2d_desc_create", "conv2d_desc_destroy", "conv2d_output_shape", "conv2d_fwd",
@@ -86,7 +88,7 @@ class conv2d_plan_info(ctypes.Structure):
     _fields_ = [("algo", ctypes.c_int32), ("tile_m", ctypes.c_int32), ("tile_n", ctypes.c_int32),
                 ("kred", ctypes.c_int32), ("kred_pad", ctypes.c_int32),
                 ("workspace_bytes", ctypes.c_int64), ("chunks", ctypes.c_int64),
-                ("needs_reorder", ctypes.c_int32), ("op_class", ctypes.c_int32)]
+                ("needs_reorder", ctypes.c_int32), ("op_class", ctypes.c_int32), ("kernel", ctypes.c_int32)]
 
 
 _lib = None

@@ -141,11 +141,14 @@ struct conv2d_desc {
     int auto_algo = CONV2D_ALGO_IMPLICIT_GEMM;
     bool implicit_ok = false, direct_ok = false;
     bool implicit_tap = false;  // tap-major gather (C/g a multiple of the stage depth)
+    bool implicit_slice = false;  // sliced direct MFMA kernel instead of the GEMM
     GemmPlan implicit;
+    SlicePlan slice{};
     ExplicitPlan expl;
     std::vector<KTabEntry> ktab_host;
 
     int device = -1;
+    int cus = 256;  // compute units of that device
     KTabEntry* ktab_dev = nullptr;
     void* ws = nullptr;
     int64_t ws_bytes = 0;
@@ -318,6 +321,9 @@ int ensure_device(conv2d_desc* d, hipStream_t s) {
     if (d->device >= 0 && d->device != dev) return CONV2D_E_UNSUPPORTED;
     if (d->device < 0) {
         d->device = dev;
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cus > 0)
+            d->cus = cus;
         const size_t bytes = d->ktab_host.size() * sizeof(KTabEntry);
         if (hipMalloc(&d->ktab_dev, bytes) != hipSuccess) {
             d->ktab_dev = nullptr;
@@ -359,10 +365,45 @@ int ensure_buffer(void** buf, int64_t* have, int64_t need) {
     } while (0)
 
 // ------------------------------------------------------------------ algorithms (NCHW tensors)
+int run_slice(conv2d_desc* d, const void* x, const void* w, const float* bias, void* y, hipStream_t s, bool ph) {
+    const Geometry& g = d->g;
+    const SlicePlan& sp = d->slice;
+    SliceArgs a{};
+    a.x = x;
+    a.x_bytes = (uint32_t)(g.x_elems * elem_size(g.xdt));
+    a.w = w;
+    a.w_bytes = (uint32_t)(g.w_elems * elem_size(g.xdt));
+    a.bias = g.has_bias ? bias : nullptr;
+    a.y = y;
+    a.y_bytes = (uint32_t)(g.y_elems * elem_size(g.ydt));
+    a.C = (int32_t)g.C; a.H = (int32_t)g.H; a.W = (int32_t)g.W; a.K = (int32_t)g.K;
+    a.Ho = (int32_t)g.Ho; a.Wo = (int32_t)g.Wo; a.R = (int32_t)g.R; a.S = (int32_t)g.S;
+    a.sh = g.sh; a.sw = g.sw; a.ph = g.ph; a.pw = g.pw; a.dh = g.dh; a.dw = g.dw;
+    a.Cg = (int32_t)g.Cg; a.Kg = (int32_t)g.Kg;
+    a.kred = (int32_t)g.Kred;
+    a.kh = sp.kh;
+    a.ph_max = sp.ph_max;
+    a.pwp = sp.pwp;
+    a.N = (int32_t)g.N;
+    a.tiles_px = (int32_t)ceil_div(g.Ho * g.Wo, 256);
+    a.grid_m = (int32_t)ceil_div(g.Kg, 64);
+    a.tiles_total = (int32_t)(g.G * a.grid_m * g.N * a.tiles_px);
+    const int per_cu = std::max(1, std::min(2, (int)((160 << 10) / sp.lds_bytes)));
+    a.nblocks = std::min(a.tiles_total, d->cus * per_cu);
+    a.lds_k_off = sp.lds_k_off;
+    a.lds_x_off = sp.lds_x_off;
+    a.lds_bytes = sp.lds_bytes;
+    Scope sc(d, CONV2D_ALGO_IMPLICIT_GEMM, CONV2D_PH_IN_MICROKERNEL, s, ph);
+    CV_TRY(sc.begin());
+    CV_HIP(launch_slice(a, g.xdt, g.ydt, s));
+    return sc.end();
+}
+
 int run_implicit(conv2d_desc* d, const void* x, const void* w, const float* bias, void* y, hipStream_t s,
                  bool ph) {
     const Geometry& g = d->g;
     const GemmPlan& gp = d->implicit;
+    if (d->implicit_slice) return run_slice(d, x, w, bias, y, s, ph);
     if (d->implicit_tap && g.R * g.S > 1) {
         // pre-convolution reordering of the filters into the tap-major reduction order
         const int64_t wb = g.w_elems * elem_size(g.xdt);
@@ -538,6 +579,14 @@ int conv2d_desc_create(const conv2d_params* params, conv2d_desc** out) {
     d->direct_ok = direct_supported(g);
     d->implicit = choose_tile(g.Kg, g.P, g.G, g.Kred, g.xdt, g.Cg);
     d->implicit_tap = g.Cg % d->implicit.bk == 0;
+    d->slice = slice_plan(g.Cg, g.R, g.S, g.Ho, g.Wo, g.sh, g.sw, g.dh, g.dw, g.xdt);
+    // The sliced kernel replaces the table-driven gather (C/g not a multiple of the stage
+    // depth) when its LDS footprint fits; CONV2D_SLICE=0 / 1 forces the choice for tests.
+    {
+        const int64_t force = env_int64("CONV2D_SLICE", -1);
+        const bool grid_ok = g.G * ceil_div(g.Kg, 64) * g.N * ceil_div(g.Ho * g.Wo, 256) <= 0x7fffffffLL;
+        d->implicit_slice = d->slice.ok && grid_ok && (force < 0 ? !d->implicit_tap : force != 0);
+    }
     build_ktab(d);
     plan_explicit(d);
     if (d->direct_ok && g.G > 1 && g.Cg <= 8)
@@ -705,6 +754,13 @@ int conv2d_plan_query(const conv2d_desc* d, int algo, conv2d_plan_info* out) {
     if (algo == CONV2D_ALGO_IMPLICIT_GEMM) {
         out->tile_m = d->implicit.bm;
         out->tile_n = d->implicit.bn;
+        out->kernel = CONV2D_KERNEL_GEMM;
+        if (d->implicit_slice) {
+            out->tile_m = 64;
+            out->tile_n = 256;
+            out->kred_pad = 2 * d->slice.kh;
+            out->kernel = CONV2D_KERNEL_SLICE;
+        }
         if (!d->implicit_ok) return CONV2D_E_UNSUPPORTED;
     } else if (algo == CONV2D_ALGO_IM2COL_GEMM) {
         out->tile_m = d->expl.gemm.bm;
@@ -712,8 +768,9 @@ int conv2d_plan_query(const conv2d_desc* d, int algo, conv2d_plan_info* out) {
         out->workspace_bytes = d->expl.col_bytes + d->expl.c_bytes;
         out->chunks = d->expl.chunks;
         if (d->expl.status != CONV2D_OK) return d->expl.status;
-    } else if (!d->direct_ok) {
-        return CONV2D_E_UNSUPPORTED;
+    } else {
+        out->kernel = CONV2D_KERNEL_DIRECT;
+        if (!d->direct_ok) return CONV2D_E_UNSUPPORTED;
     }
     return CONV2D_OK;
 }

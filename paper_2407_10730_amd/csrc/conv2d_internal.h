@@ -116,6 +116,37 @@ struct DirectArgs {
 };
 hipError_t launch_direct(const DirectArgs& a, int xdt, int ydt, hipStream_t stream);
 
+// Sliced direct convolution on MFMA (small C/g * R * S): per block the filters of 64 output
+// channels, the input rows of 256 consecutive output pixels of one image and a table of the
+// slice offset of every reduction index sit in LDS (weights at byte 0, then the table at
+// lds_k_off, then the slice at lds_x_off).  Persistent blocks walk the tiles
+// (group x channel tile, image, pixel tile).  NCHW x and y.
+constexpr int64_t SLICE_MAX_KRED = 1024;
+constexpr int64_t SLICE_MAX_LDS = 160 * 1024;
+struct SliceArgs {
+    const void* x;
+    uint32_t x_bytes;
+    const void* w;        // [K][C/g][R][S]
+    uint32_t w_bytes;
+    const float* bias;    // may be NULL
+    void* y;
+    uint32_t y_bytes;
+    int32_t C, H, W, K, Ho, Wo, R, S, sh, sw, ph, pw, dh, dw, Cg, Kg;
+    int32_t kred, kh;     // reduction length; per lane-half length (2*kh >= kred)
+    int32_t ph_max, pwp;  // slice rows per channel (capacity), slice row length
+    int32_t N, tiles_px, grid_m;
+    int32_t tiles_total;  // G * grid_m * N * tiles_px
+    int32_t nblocks;      // persistent grid size
+    int32_t lds_k_off, lds_x_off, lds_bytes;
+};
+struct SlicePlan {
+    bool ok;
+    int32_t kh, ph_max, pwp, lds_k_off, lds_x_off, lds_bytes;
+};
+SlicePlan slice_plan(int64_t Cg, int64_t R, int64_t S, int64_t Ho, int64_t Wo, int sh, int sw, int dh, int dw,
+                     int xdt);
+hipError_t launch_slice(const SliceArgs& a, int xdt, int ydt, hipStream_t stream);
+
 // weight repack to tap-major order: w [K][C/g][R*S] -> wr [K][R*S][C/g].
 hipError_t launch_repack_tap_major(const void* w, void* wr, int64_t k, int64_t cg, int64_t rs, int elem_bytes,
                                    hipStream_t stream);

@@ -1,0 +1,340 @@
+// slice_conv.hip -- sliced direct convolution on MFMA for small reductions.
+//
+// For layers whose reduction C/g * R * S is short (stems: few input channels,
+// large filters), an im2col column of one output pixel is a handful of input
+// values that neighbouring pixels share many times over.  Gathering them from
+// global memory per GEMM stage (the implicit GEMM) spends most of its time in
+// address arithmetic and small loads, and the explicit path writes them all
+// out.  Here one block stages, in LDS,
+//   * the filters of 64 output channels, [64][kred] in the natural (c, r, s)
+//     order with the reduction split into two halves of kh values,
+//   * the input slice those pixels read: every input row a run of 256
+//     consecutive output pixels of one image touches, zero-filled where the
+//     window leaves the image (padding),
+//   * a table of the slice offset of every reduction index,
+// and the MFMA loop then reads each im2col column straight out of the slice
+// (the paper's sliced convolution keeps input slices in fast memory and
+// skips the packing step, Sec. II; this is that idea on the LDS of one CU).
+//
+// A tile is 64 output channels x 256 consecutive output pixels of one image;
+// wave w (of 8, two per SIMD) computes the 64 x 32 tile of pixels 32w..32w+31;
+// lane l covers pixel l%32 and the reduction half l/32, so the weight operand
+// of a lane is a contiguous run of its LDS row (16-byte reads) and the input
+// operand is one LDS read per reduction index at (pixel base + table offset).
+//
+// Blocks are persistent: each walks the tiles blockIdx.x, +gridDim.x, ... in
+// (group, channel tile, image, pixel tile) order and keeps the filters while
+// the channel tile stays the same.  The slice is copied global -> LDS by the
+// buffer unit itself (buffer loads with the LDS bit: no registers, padding
+// comes back as zero from out-of-range offsets), one 4-byte LDS word per
+// element for both dtypes, into the second of two slice buffers while the
+// MFMAs run on the first.
+#include "device_common.h"
+
+namespace cv {
+
+constexpr int SLICE_BM = 64;    // output channels per tile
+constexpr int SLICE_THREADS = 512;  // 8 waves, two per SIMD
+constexpr int SLICE_NPX = 256;      // output pixels per tile (8 waves x 32)
+constexpr int SLICE_UNR = 8;    // loads in flight per thread in the filter copy
+constexpr int SLICE_LP = 256;   // slice line pitch in words (one column per thread)
+constexpr int SLICE_STORES = 32;  // vector stores per lane in the epilogue of a tile
+// s_waitcnt immediate: vmcnt = SLICE_STORES (bits 15:14 and 3:0), expcnt and lgkmcnt not waited on
+constexpr int SLICE_WAIT_ALL_BUT_STORES =
+    ((SLICE_STORES >> 4) << 14) | (0xF << 8) | (0x7 << 4) | (SLICE_STORES & 0xF);
+
+// Buffer load of one element per lane straight into LDS: lane l writes the 4-byte LDS word
+// lds_addr + 4*l (2-byte elements are zero-extended to a word); out-of-range offsets write
+// zero.  Issued as inline assembly so that the compiler does not add a wait for these writes
+// before every later LDS read: the kernel orders them itself (vmcnt wait, then a barrier).
+__device__ __forceinline__ void lds_dma_b32(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t lds_addr) {
+    asm volatile("buffer_load_dword %0, %1, 0 offen lds" ::"v"(voff), "s"(r), "{m0}"(lds_addr) : "memory");
+}
+__device__ __forceinline__ void lds_dma_u16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t lds_addr) {
+    asm volatile("buffer_load_ushort %0, %1, 0 offen lds" ::"v"(voff), "s"(r), "{m0}"(lds_addr) : "memory");
+}
+// Workgroup barrier after this wave's LDS operations complete.  Unlike __syncthreads it does
+// not also wait for outstanding global loads and stores.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+template <typename T> struct SliceTraits;
+template <> struct SliceTraits<float> { static constexpr int wpad = 4; };
+template <> struct SliceTraits<uint16_t> { static constexpr int wpad = 8; };
+
+template <typename T, typename TOut>
+__global__ __launch_bounds__(SLICE_THREADS) void slice_conv_kernel(SliceArgs A) {
+    extern __shared__ __attribute__((aligned(16))) char lds[];
+    constexpr int ES = sizeof(T);
+    const int wpitch = 2 * A.kh + SliceTraits<T>::wpad;  // LDS filter row pitch, elements
+    T* wl = reinterpret_cast<T*>(lds);
+    int32_t* ko = reinterpret_cast<int32_t*>(lds + A.lds_k_off);
+    uint32_t* xs = reinterpret_cast<uint32_t*>(lds + A.lds_x_off);  // slice, one word per element
+
+    const int t = threadIdx.x;
+    const int lane = t & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(t >> 6);  // wave-uniform: keeps the control flow scalar
+    const int lcol = lane & 31;
+    const int lrow = lane >> 5;
+    const int howo = A.Ho * A.Wo;
+    const int per_gz = A.N * A.tiles_px;  // tiles of one (group, channel tile)
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(A.x, A.x_bytes);
+
+    // ---- slice offset of every reduction index (0 for the zero-weight tail)
+    {
+        const int rs = A.R * A.S;
+        for (int k = t; k < 2 * A.kh; k += SLICE_THREADS) {
+            int off = 0;
+            if (k < A.kred) {
+                const int c = k / rs;
+                const int q = k - c * rs;
+                const int r = q / A.S;
+                const int s = q - r * A.S;
+                off = (c * A.ph_max + r * A.dh) * SLICE_LP + s * A.dw;
+            }
+            ko[k] = off;
+        }
+    }
+
+    // Geometry of tile w: image n, first pixel p0, first slice row hi0.
+    struct Tile { int gz, n, p0, oh0, hi0; };
+    auto decode = [&](int w) {
+        Tile tl;
+        tl.gz = w / per_gz;
+        const int rem = w - tl.gz * per_gz;
+        tl.n = rem / A.tiles_px;
+        tl.p0 = (rem - tl.n * A.tiles_px) * SLICE_NPX;
+        tl.oh0 = tl.p0 / A.Wo;
+        tl.hi0 = tl.oh0 * A.sh - A.ph;
+        return tl;
+    };
+
+    // ---- slice of tile w into buffer buf: line u = c*ph_max + row holds input row hi0 + row of
+    // channel c in columns j = wi + pw; lane t of the block copies column t of every line
+    const int slice_words = A.Cg * A.ph_max * SLICE_LP;
+    auto copy_slice = [&](int w, uint32_t* buf) {
+        const Tile tl = decode(w);
+        const int gi = tl.gz / A.grid_m;
+        const int col = t & (SLICE_LP - 1);    // waves 0-3 and 4-7 each cover the 256 columns
+        const int half = wave >> 2;            // ... of the even and the odd lines
+        const int wi = col - A.pw;
+        const bool wok = (col < A.pwp) & ((unsigned)wi < (unsigned)A.W);
+        const uint32_t plane0 = (uint32_t)(tl.n * A.C + gi * A.Cg) * (uint32_t)(A.H * A.W);
+        // LDS byte address of this wave's 64 columns of line 0
+        const uint32_t lds0 = __builtin_amdgcn_readfirstlane(
+            (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint32_t*)(buf + (wave & 3) * 64));
+        const uint32_t hw = (uint32_t)(A.H * A.W);
+        for (int c = 0; c < A.Cg; ++c) {
+            const uint32_t plane = plane0 + (uint32_t)c * hw;
+            for (int row = half; row < A.ph_max; row += 2) {
+                const int hi = tl.hi0 + row;
+                const bool ok = wok & ((unsigned)hi < (unsigned)A.H);
+                const uint32_t e = plane + (uint32_t)(hi * A.W + wi);
+                // lane l of the wave lands in word l of the destination
+                const uint32_t la = lds0 + (uint32_t)((c * A.ph_max + row) * SLICE_LP * 4);
+                if constexpr (ES == 4)
+                    lds_dma_b32(rx, ok ? e * 4u : OOB_OFF, la);
+                else
+                    lds_dma_u16(rx, ok ? e * 2u : OOB_OFF, la);
+            }
+        }
+    };
+
+    f32x16 acc0, acc1;
+    float bv0[16], bv1[16];
+    int cur_gz = -1;
+    if ((int)blockIdx.x < A.tiles_total) copy_slice(blockIdx.x, xs);
+    for (int w = blockIdx.x, it = 0; w < A.tiles_total; w += gridDim.x, ++it) {
+        const Tile tl = decode(w);
+        const int gi = tl.gz / A.grid_m;
+        const int m0 = (tl.gz - gi * A.grid_m) * SLICE_BM;
+        uint32_t* cur = xs + (it & 1) * slice_words;
+        uint32_t* nxt = xs + ((it & 1) ^ 1) * slice_words;
+        if (tl.gz != cur_gz) {
+            // ---- filters of this (group, channel tile): wl[m][k], zero beyond kred or Kg
+            __syncthreads();  // no wave still reads the previous filters
+            cur_gz = tl.gz;
+            const __amdgpu_buffer_rsrc_t rw = make_rsrc(A.w, A.w_bytes);
+            const int kw = 2 * A.kh;
+            const int total = SLICE_BM * kw;
+            for (int base = t; base < total; base += SLICE_THREADS * SLICE_UNR) {
+                T v[SLICE_UNR];
+                int dst[SLICE_UNR];
+#pragma unroll
+                for (int u = 0; u < SLICE_UNR; ++u) {
+                    const int idx = base + u * SLICE_THREADS;
+                    const int m = idx / kw;
+                    const int k = idx - m * kw;
+                    const bool ok = (idx < total) & (m0 + m < A.Kg) & (k < A.kred);
+                    const uint32_t e = (uint32_t)(gi * A.Kg + m0 + m) * (uint32_t)A.kred + (uint32_t)k;
+                    if constexpr (ES == 4)
+                        v[u] = ld_f32(rw, ok ? e * 4u : OOB_OFF);
+                    else
+                        v[u] = ld_u16(rw, ok ? e * 2u : OOB_OFF);
+                    dst[u] = idx < total ? m * wpitch + k : -1;
+                }
+#pragma unroll
+                for (int u = 0; u < SLICE_UNR; ++u)
+                    if (dst[u] >= 0) wl[dst[u]] = v[u];
+            }
+            const __amdgpu_buffer_rsrc_t rbias = make_rsrc(A.bias, A.bias ? (uint32_t)A.K * 4u : 0u);
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int m = m0 + 8 * (v >> 2) + 4 * lrow + (v & 3);
+                bv0[v] = ld_f32(rbias, A.bias && m < A.Kg ? (uint32_t)(gi * A.Kg + m) * 4u : OOB_OFF);
+                bv1[v] = ld_f32(rbias, A.bias && m + 32 < A.Kg ? (uint32_t)(gi * A.Kg + m + 32) * 4u : OOB_OFF);
+            }
+            __builtin_amdgcn_s_waitcnt(0);
+        } else {
+            // The slice of this tile was requested before the previous tile's MFMAs; only the
+            // previous tile's SLICE_STORES stores were issued after it, and vector memory
+            // operations complete in order, so this waits for the slice but not for them.
+            __builtin_amdgcn_s_waitcnt(SLICE_WAIT_ALL_BUT_STORES);
+        }
+        lds_barrier();  // the slice has landed; every wave is done with the other buffer
+        if (w + (int)gridDim.x < A.tiles_total) copy_slice(w + gridDim.x, nxt);
+
+        const int p = tl.p0 + wave * 32 + lcol;
+        int pixbase = 0;  // pixels past the end read a valid (discarded) column
+        if (p < howo) {
+            const int oh = p / A.Wo;
+            const int ow = p - oh * A.Wo;
+            pixbase = (oh - tl.oh0) * A.sh * SLICE_LP + ow * A.sw;
+        }
+        const T* wa0 = wl + lcol * wpitch + lrow * A.kh;
+        const T* wa1 = wa0 + 32 * wpitch;
+        const int32_t* kp = ko + lrow * A.kh;
+        const uint32_t* xp = cur + pixbase;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc0[v] = acc1[v] = 0.0f;
+
+        if constexpr (ES == 4) {
+            // MFMA 32x32x2: step k takes reduction index k of the lane's half.  Software
+            // pipelined: the operands of group kk+4 (and the offsets of kk+8) are read while
+            // the MFMAs of group kk run; reads past the end are clamped to the last group.
+            const int last = A.kh - 4;
+            int4 o = *reinterpret_cast<const int4*>(kp);
+            f32x4 a0 = *reinterpret_cast<const f32x4*>(wa0);
+            f32x4 a1 = *reinterpret_cast<const f32x4*>(wa1);
+            float b0 = __builtin_bit_cast(float, xp[o.x]), b1 = __builtin_bit_cast(float, xp[o.y]),
+                  b2 = __builtin_bit_cast(float, xp[o.z]), b3 = __builtin_bit_cast(float, xp[o.w]);
+            o = *reinterpret_cast<const int4*>(kp + min(4, last));
+            for (int kk = 0; kk < A.kh; kk += 4) {
+                const int kn = min(kk + 4, last);
+                const f32x4 a0n = *reinterpret_cast<const f32x4*>(wa0 + kn);
+                const f32x4 a1n = *reinterpret_cast<const f32x4*>(wa1 + kn);
+                const float c0 = __builtin_bit_cast(float, xp[o.x]), c1 = __builtin_bit_cast(float, xp[o.y]),
+                            c2 = __builtin_bit_cast(float, xp[o.z]), c3 = __builtin_bit_cast(float, xp[o.w]);
+                o = *reinterpret_cast<const int4*>(kp + min(kk + 8, last));
+                // keep the next group's reads ahead of this group's MFMAs
+                __builtin_amdgcn_sched_barrier(0);
+                acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a0[0], b0, acc0, 0, 0, 0);
+                acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[0], b0, acc1, 0, 0, 0);
+                acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a0[1], b1, acc0, 0, 0, 0);
+                acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[1], b1, acc1, 0, 0, 0);
+                acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a0[2], b2, acc0, 0, 0, 0);
+                acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[2], b2, acc1, 0, 0, 0);
+                acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a0[3], b3, acc0, 0, 0, 0);
+                acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[3], b3, acc1, 0, 0, 0);
+                a0 = a0n;
+                a1 = a1n;
+                b0 = c0; b1 = c1; b2 = c2; b3 = c3;
+            }
+        } else {
+            // MFMA 32x32x16 bf16: a step takes 8 consecutive reduction indices of the lane's
+            // half; the raw values of the next step are read before this step's MFMAs and
+            // packed after them.
+            // slice words hold one bf16 each, zero-extended
+            const int last = A.kh - 8;
+            uint32_t h[8];
+            auto gather = [&](const int4& q0, const int4& q1) {
+                h[0] = xp[q0.x]; h[1] = xp[q0.y]; h[2] = xp[q0.z]; h[3] = xp[q0.w];
+                h[4] = xp[q1.x]; h[5] = xp[q1.y]; h[6] = xp[q1.z]; h[7] = xp[q1.w];
+            };
+            auto pack = [&]() {
+                u32x4 bw;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) bw[q] = h[2 * q] | (h[2 * q + 1] << 16);
+                return __builtin_bit_cast(bf16x8, bw);
+            };
+            int4 o0 = *reinterpret_cast<const int4*>(kp);
+            int4 o1 = *reinterpret_cast<const int4*>(kp + 4);
+            bf16x8 a0 = *reinterpret_cast<const bf16x8*>(wa0);
+            bf16x8 a1 = *reinterpret_cast<const bf16x8*>(wa1);
+            gather(o0, o1);
+            bf16x8 b = pack();
+            o0 = *reinterpret_cast<const int4*>(kp + min(8, last));
+            o1 = *reinterpret_cast<const int4*>(kp + min(8, last) + 4);
+            for (int kk = 0; kk < A.kh; kk += 8) {
+                const int kn = min(kk + 8, last);
+                const bf16x8 a0n = *reinterpret_cast<const bf16x8*>(wa0 + kn);
+                const bf16x8 a1n = *reinterpret_cast<const bf16x8*>(wa1 + kn);
+                gather(o0, o1);
+                const int kn2 = min(kk + 16, last);
+                o0 = *reinterpret_cast<const int4*>(kp + kn2);
+                o1 = *reinterpret_cast<const int4*>(kp + kn2 + 4);
+                __builtin_amdgcn_sched_barrier(0);
+                acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b, acc0, 0, 0, 0);
+                acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b, acc1, 0, 0, 0);
+                __builtin_amdgcn_sched_barrier(0);
+                a0 = a0n;
+                a1 = a1n;
+                b = pack();
+            }
+        }
+
+        // ---- epilogue: accumulator v of lane l holds channel 8*(v/4) + 4*(l/32) + v%4 (+32
+        // for acc1) and pixel l%32; the bias sits in registers since the filters were loaded
+        const bool pok = p < howo;
+        const __amdgpu_buffer_rsrc_t ry = make_rsrc(A.y, A.y_bytes);
+        const uint32_t ybase = (uint32_t)(tl.n * A.K + gi * A.Kg) * (uint32_t)howo + (uint32_t)p;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int m = m0 + 8 * (v >> 2) + 4 * lrow + (v & 3);
+            store_out<TOut>(ry, ybase + (uint32_t)m * (uint32_t)howo, pok & (m < A.Kg), acc0[v] + bv0[v]);
+            store_out<TOut>(ry, ybase + (uint32_t)(m + 32) * (uint32_t)howo, pok & (m + 32 < A.Kg),
+                            acc1[v] + bv1[v]);
+        }
+    }
+}
+
+SlicePlan slice_plan(int64_t Cg, int64_t R, int64_t S, int64_t Ho, int64_t Wo, int sh, int sw, int dh, int dw,
+                     int xdt) {
+    SlicePlan sp{};
+    const int64_t es = xdt == CONV2D_BF16 ? 2 : 4;
+    const int64_t step = xdt == CONV2D_BF16 ? 8 : 4;
+    const int64_t kred = Cg * R * S;
+    if (kred > SLICE_MAX_KRED) return sp;
+    const int64_t kh = (kred + 2 * step - 1) / (2 * step) * step;
+    const int64_t wbytes = SLICE_BM * (2 * kh + step) * es;
+    const int64_t kbytes = 2 * kh * 4;
+    int64_t rows = (SLICE_NPX + Wo - 2) / Wo + 1;  // output rows a tile's consecutive pixels can touch
+    if (rows > Ho) rows = Ho;
+    const int64_t ph_max = (rows - 1) * sh + (R - 1) * dh + 1;
+    const int64_t pwp = (Wo - 1) * sw + (S - 1) * dw + 1;
+    if (pwp > SLICE_LP) return sp;  // one column per thread
+    const int64_t xbytes = Cg * ph_max * SLICE_LP * 4;
+    const int64_t total = wbytes + kbytes + 2 * xbytes;  // the slice is double-buffered
+    if (total > SLICE_MAX_LDS) return sp;
+    sp.ok = true;
+    sp.kh = (int32_t)kh;
+    sp.ph_max = (int32_t)ph_max;
+    sp.pwp = (int32_t)pwp;
+    sp.lds_k_off = (int32_t)wbytes;
+    sp.lds_x_off = (int32_t)(wbytes + kbytes);
+    sp.lds_bytes = (int32_t)total;
+    return sp;
+}
+
+hipError_t launch_slice(const SliceArgs& a, int xdt, int ydt, hipStream_t stream) {
+    if (a.nblocks < 1 || a.tiles_total < 1) return hipErrorInvalidValue;
+    dim3 grid((unsigned)a.nblocks);
+    if (xdt == CONV2D_F32)
+        hipLaunchKernelGGL((slice_conv_kernel<float, float>), grid, dim3(SLICE_THREADS), a.lds_bytes, stream, a);
+    else if (ydt == CONV2D_BF16)
+        hipLaunchKernelGGL((slice_conv_kernel<uint16_t, uint16_t>), grid, dim3(SLICE_THREADS), a.lds_bytes, stream, a);
+    else
+        hipLaunchKernelGGL((slice_conv_kernel<uint16_t, float>), grid, dim3(SLICE_THREADS), a.lds_bytes, stream, a);
+    return hipGetLastError();
+}
+
+}  // namespace cv

@@ -124,6 +124,37 @@ def test_auto_algorithm_choice_and_classes():
     B.conv2d_desc_destroy(d)
 
 
+def test_implicit_microkernel_choice(monkeypatch):
+    """Short reductions with C/g off the 16-channel stage grid take the sliced kernel; the
+    rest the tiled GEMM; CONV2D_SLICE forces either where the slice fits in LDS."""
+    def kernel(cs):
+        d = B.conv2d_desc_create(params_for(cs))
+        try:
+            info = B.conv2d_plan_query(d, B.CONV2D_ALGO_IMPLICIT_GEMM)
+            return info.kernel, info.kred_pad
+        finally:
+            B.conv2d_desc_destroy(d)
+    monkeypatch.delenv("CONV2D_SLICE", raising=False)
+    assert kernel(datagen.CONFIGS["cfg4"]) == (B.CONV2D_KERNEL_SLICE, 152)       # 147 -> 2 x 76
+    assert kernel(datagen.CONFIGS["cfg4_bf16"]) == (B.CONV2D_KERNEL_SLICE, 160)  # 147 -> 2 x 80
+    assert kernel(datagen.CONFIGS["cfg1"])[0] == B.CONV2D_KERNEL_SLICE
+    assert kernel(datagen.CONFIGS["cfg2"])[0] == B.CONV2D_KERNEL_GEMM
+    big = datagen.CONFIGS["cfg4"].with_(c=48)                                    # 2352-long reduction
+    assert kernel(big)[0] == B.CONV2D_KERNEL_GEMM
+    c16 = datagen.CONFIGS["cfg2"].with_(c=16, h=130, w=130, r=1, s=1, pad=(0, 0))  # tap-major GEMM
+    assert kernel(c16)[0] == B.CONV2D_KERNEL_GEMM
+    monkeypatch.setenv("CONV2D_SLICE", "0")
+    assert kernel(datagen.CONFIGS["cfg4"])[0] == B.CONV2D_KERNEL_GEMM
+    monkeypatch.setenv("CONV2D_SLICE", "1")
+    assert kernel(c16)[0] == B.CONV2D_KERNEL_SLICE
+    assert kernel(datagen.CONFIGS["cfg2"])[0] == B.CONV2D_KERNEL_GEMM           # 64 x 576 filters overflow LDS
+    assert kernel(datagen.CONFIGS["cfg2"].with_(c=16))[0] == B.CONV2D_KERNEL_GEMM  # 96 slice lines
+    assert kernel(big)[0] == B.CONV2D_KERNEL_GEMM
+    d = B.conv2d_desc_create(params_for(datagen.CONFIGS["dw"]))
+    assert B.conv2d_plan_query(d).kernel == B.CONV2D_KERNEL_DIRECT
+    B.conv2d_desc_destroy(d)
+
+
 def test_explicit_workspace_chunking(monkeypatch):
     cs = datagen.CONFIGS["cfg4"]
     d = B.conv2d_desc_create(params_for(cs))

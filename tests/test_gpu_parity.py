@@ -44,11 +44,34 @@ def _reference(cs, mode, inputs):
     return _ORACLE_CACHE[key]
 
 
-def _run(cs, algo, mode="random"):
+class _Kernel:
+    """Forces the implicit family's microkernel through CONV2D_SLICE while descriptors are
+    created: None = planner's choice, "0" = tiled GEMM, "1" = sliced kernel (when it fits)."""
+
+    def __init__(self, force):
+        self.force, self.old = force, None
+
+    def __enter__(self):
+        self.old = os.environ.get("CONV2D_SLICE")
+        if self.force is not None:
+            os.environ["CONV2D_SLICE"] = self.force
+        return self
+
+    def __exit__(self, *exc):
+        if self.old is None:
+            os.environ.pop("CONV2D_SLICE", None)
+        else:
+            os.environ["CONV2D_SLICE"] = self.old
+
+
+def _run(cs, algo, mode="random", kernel=None):
     import torch
-    print(f"\n[case] {cs} algo={ALGO_IDS[algo]} mode={mode}", flush=True)
-    dc = DeviceConv(cs, mode)
+    print(f"\n[case] {cs} algo={ALGO_IDS[algo]} kernel={kernel} mode={mode}", flush=True)
+    with _Kernel(kernel):
+        dc = DeviceConv(cs, mode)
     try:
+        if kernel == "1" and dc.plan(algo).kernel != B.CONV2D_KERNEL_SLICE:
+            pytest.skip("the sliced kernel does not fit this shape")
         dc.run(algo)
         torch.cuda.synchronize()
         y = dc.y_nchw()
@@ -57,8 +80,8 @@ def _run(cs, algo, mode="random"):
     return y, (dc.x_host, dc.w_host, dc.b_host)
 
 
-def _check(cs, algo, mode="random"):
-    y, inputs = _run(cs, algo, mode)
+def _check(cs, algo, mode="random", kernel=None):
+    y, inputs = _run(cs, algo, mode, kernel)
     y_ref, a_ref = _reference(cs, mode, inputs)
     assert y.shape == y_ref.shape
     if mode == "integer" and cs.y_dtype == "f32":
@@ -82,6 +105,13 @@ FULL = ["cfg1", "cfg2", "cfg3a", "cfg3b", "cfg4", "cfg4_bf16"]
 @pytest.mark.parametrize("name", FULL)
 def test_config_parity(name, algo):
     _check(datagen.CONFIGS[name], algo)
+
+
+@pytest.mark.parametrize("kernel", ["0", "1"], ids=["gemm", "slice"])
+@pytest.mark.parametrize("name", ["cfg1", "cfg4", "cfg4_bf16"])
+def test_config_parity_both_implicit_kernels(name, kernel):
+    _check(datagen.CONFIGS[name], IMPLICIT, kernel=kernel)
+    _check(datagen.CONFIGS[name], IMPLICIT, "integer", kernel=kernel)
 
 
 @pytest.mark.parametrize("algo", [DIRECT, IMPLICIT, IM2COL], ids=lambda a: ALGO_IDS[a])
@@ -140,14 +170,19 @@ VARIANTS = [("nchw", "f32", "f32"), ("nhwc", "f32", "f32"), ("nchw", "bf16", "bf
             ("nhwc", "bf16", "f32")]
 
 
-@pytest.mark.parametrize("algo", [IMPLICIT, IM2COL, DIRECT], ids=lambda a: ALGO_IDS[a])
+EDGE_ALGOS = [("implicit", IMPLICIT, None), ("implicit-gemm", IMPLICIT, "0"), ("implicit-slice", IMPLICIT, "1"),
+              ("im2col", IM2COL, None), ("direct", DIRECT, None)]
+
+
+@pytest.mark.parametrize("algo", EDGE_ALGOS, ids=lambda a: a[0])
 @pytest.mark.parametrize("var", VARIANTS, ids=lambda v: "-".join(v))
 @pytest.mark.parametrize("idx", range(len(EDGE)))
 def test_edge_grid(idx, var, algo):
     layout, xdt, ydt = var
+    _, algo, kernel = algo
     cs = EDGE[idx].with_(layout=layout, x_dtype=xdt, y_dtype=ydt)
-    _check(cs, algo, "random")
-    _check(cs.with_(y_dtype="f32"), algo, "integer")
+    _check(cs, algo, "random", kernel)
+    _check(cs.with_(y_dtype="f32"), algo, "integer", kernel)
 
 
 # ------------------------------------------------------------------ behaviour
