@@ -385,17 +385,17 @@ int run_slice(conv2d_desc* d, const void* x, const void* w, const float* bias, v
     a.ph_max = sp.ph_max;
     a.pwp = sp.pwp;
     a.N = (int32_t)g.N;
-    a.tiles_px = (int32_t)ceil_div(g.Ho * g.Wo, 256);
+    a.tiles_px = (int32_t)ceil_div(g.Ho * g.Wo, 32 * sp.nw);
     a.grid_m = (int32_t)ceil_div(g.Kg, 64);
     a.tiles_total = (int32_t)(g.G * a.grid_m * g.N * a.tiles_px);
-    const int per_cu = std::max(1, std::min(2, (int)((160 << 10) / sp.lds_bytes)));
+    const int per_cu = std::max(1, std::min(16 / sp.nw, (int)((160 << 10) / sp.lds_bytes)));
     a.nblocks = std::min(a.tiles_total, d->cus * per_cu);
     a.lds_k_off = sp.lds_k_off;
     a.lds_x_off = sp.lds_x_off;
     a.lds_bytes = sp.lds_bytes;
     Scope sc(d, CONV2D_ALGO_IMPLICIT_GEMM, CONV2D_PH_IN_MICROKERNEL, s, ph);
     CV_TRY(sc.begin());
-    CV_HIP(launch_slice(a, g.xdt, g.ydt, s));
+    CV_HIP(launch_slice(a, g.xdt, g.ydt, sp.nw, s));
     return sc.end();
 }
 
@@ -579,12 +579,19 @@ int conv2d_desc_create(const conv2d_params* params, conv2d_desc** out) {
     d->direct_ok = direct_supported(g);
     d->implicit = choose_tile(g.Kg, g.P, g.G, g.Kred, g.xdt, g.Cg);
     d->implicit_tap = g.Cg % d->implicit.bk == 0;
-    d->slice = slice_plan(g.Cg, g.R, g.S, g.Ho, g.Wo, g.sh, g.sw, g.dh, g.dw, g.xdt);
+    {
+        // 8 waves (256-pixel tiles) unless an image has at most 128 output pixels;
+        // CONV2D_SLICE_WAVES = 4 or 8 overrides for tests and tuning
+        int nw = g.Ho * g.Wo <= 128 ? 4 : 8;
+        const int64_t force_nw = env_int64("CONV2D_SLICE_WAVES", 0);
+        if (force_nw == 4 || force_nw == 8) nw = (int)force_nw;
+        d->slice = slice_plan(g.Cg, g.R, g.S, g.Ho, g.Wo, g.sh, g.sw, g.dh, g.dw, g.xdt, nw);
+    }
     // The sliced kernel replaces the table-driven gather (C/g not a multiple of the stage
     // depth) when its LDS footprint fits; CONV2D_SLICE=0 / 1 forces the choice for tests.
     {
         const int64_t force = env_int64("CONV2D_SLICE", -1);
-        const bool grid_ok = g.G * ceil_div(g.Kg, 64) * g.N * ceil_div(g.Ho * g.Wo, 256) <= 0x7fffffffLL;
+        const bool grid_ok = g.G * ceil_div(g.Kg, 64) * g.N * ceil_div(g.Ho * g.Wo, 128) <= 0x7fffffffLL;
         d->implicit_slice = d->slice.ok && grid_ok && (force < 0 ? !d->implicit_tap : force != 0);
     }
     build_ktab(d);
@@ -757,7 +764,7 @@ int conv2d_plan_query(const conv2d_desc* d, int algo, conv2d_plan_info* out) {
         out->kernel = CONV2D_KERNEL_GEMM;
         if (d->implicit_slice) {
             out->tile_m = 64;
-            out->tile_n = 256;
+            out->tile_n = 32 * d->slice.nw;
             out->kred_pad = 2 * d->slice.kh;
             out->kernel = CONV2D_KERNEL_SLICE;
         }

@@ -122,7 +122,7 @@ hipError_t launch_direct(const DirectArgs& a, int xdt, int ydt, hipStream_t stre
 // lds_k_off, then the slice at lds_x_off).  Persistent blocks walk the tiles
 // (group x channel tile, image, pixel tile).  NCHW x and y.
 constexpr int64_t SLICE_MAX_KRED = 1024;
-constexpr int64_t SLICE_MAX_LDS = 160 * 1024;
+constexpr int64_t SLICE_MAX_LDS = 80 * 1024;  // two blocks per CU
 struct SliceArgs {
     const void* x;
     uint32_t x_bytes;
@@ -141,11 +141,12 @@ struct SliceArgs {
 };
 struct SlicePlan {
     bool ok;
+    int32_t nw;           // waves per block (tile = 32*nw pixels)
     int32_t kh, ph_max, pwp, lds_k_off, lds_x_off, lds_bytes;
 };
 SlicePlan slice_plan(int64_t Cg, int64_t R, int64_t S, int64_t Ho, int64_t Wo, int sh, int sw, int dh, int dw,
-                     int xdt);
-hipError_t launch_slice(const SliceArgs& a, int xdt, int ydt, hipStream_t stream);
+                     int xdt, int nw);
+hipError_t launch_slice(const SliceArgs& a, int xdt, int ydt, int nw, hipStream_t stream);
 
 // weight repack to tap-major order: w [K][C/g][R*S] -> wr [K][R*S][C/g].
 hipError_t launch_repack_tap_major(const void* w, void* wr, int64_t k, int64_t cg, int64_t rs, int elem_bytes,

@@ -27,21 +27,14 @@
 // the channel tile stays the same.  The slice is copied global -> LDS by the
 // buffer unit itself (buffer loads with the LDS bit: no registers, padding
 // comes back as zero from out-of-range offsets), one 4-byte LDS word per
-// element for both dtypes, into the second of two slice buffers while the
-// MFMAs run on the first.
+// element for both dtypes.
 #include "device_common.h"
 
 namespace cv {
 
 constexpr int SLICE_BM = 64;    // output channels per tile
-constexpr int SLICE_THREADS = 512;  // 8 waves, two per SIMD
-constexpr int SLICE_NPX = 256;      // output pixels per tile (8 waves x 32)
 constexpr int SLICE_UNR = 8;    // loads in flight per thread in the filter copy
 constexpr int SLICE_LP = 256;   // slice line pitch in words (one column per thread)
-constexpr int SLICE_STORES = 32;  // vector stores per lane in the epilogue of a tile
-// s_waitcnt immediate: vmcnt = SLICE_STORES (bits 15:14 and 3:0), expcnt and lgkmcnt not waited on
-constexpr int SLICE_WAIT_ALL_BUT_STORES =
-    ((SLICE_STORES >> 4) << 14) | (0xF << 8) | (0x7 << 4) | (SLICE_STORES & 0xF);
 
 // Buffer load of one element per lane straight into LDS: lane l writes the 4-byte LDS word
 // lds_addr + 4*l (2-byte elements are zero-extended to a word); out-of-range offsets write
@@ -61,8 +54,13 @@ template <typename T> struct SliceTraits;
 template <> struct SliceTraits<float> { static constexpr int wpad = 4; };
 template <> struct SliceTraits<uint16_t> { static constexpr int wpad = 8; };
 
-template <typename T, typename TOut>
-__global__ __launch_bounds__(SLICE_THREADS) void slice_conv_kernel(SliceArgs A) {
+// NW waves per block (4 or 8), tiles of 32*NW pixels.  The slice has one buffer: it is copied
+// between tiles, and a second resident block keeps the MFMAs busy meanwhile (a second buffer
+// would halve the resident blocks, which measured slower).
+template <typename T, typename TOut, int NW>
+__global__ __launch_bounds__(64 * NW) void slice_conv_kernel(SliceArgs A) {
+    constexpr int SLICE_THREADS = 64 * NW;
+    constexpr int SLICE_NPX = 32 * NW;
     extern __shared__ __attribute__((aligned(16))) char lds[];
     constexpr int ES = sizeof(T);
     const int wpitch = 2 * A.kh + SliceTraits<T>::wpad;  // LDS filter row pitch, elements
@@ -72,6 +70,7 @@ __global__ __launch_bounds__(SLICE_THREADS) void slice_conv_kernel(SliceArgs A) 
 
     const int t = threadIdx.x;
     const int lane = t & 63;
+
     const int wave = __builtin_amdgcn_readfirstlane(t >> 6);  // wave-uniform: keeps the control flow scalar
     const int lcol = lane & 31;
     const int lrow = lane >> 5;
@@ -110,12 +109,11 @@ __global__ __launch_bounds__(SLICE_THREADS) void slice_conv_kernel(SliceArgs A) 
 
     // ---- slice of tile w into buffer buf: line u = c*ph_max + row holds input row hi0 + row of
     // channel c in columns j = wi + pw; lane t of the block copies column t of every line
-    const int slice_words = A.Cg * A.ph_max * SLICE_LP;
     auto copy_slice = [&](int w, uint32_t* buf) {
         const Tile tl = decode(w);
         const int gi = tl.gz / A.grid_m;
-        const int col = t & (SLICE_LP - 1);    // waves 0-3 and 4-7 each cover the 256 columns
-        const int half = wave >> 2;            // ... of the even and the odd lines
+        const int col = t & (SLICE_LP - 1);    // each group of 4 waves covers the 256 columns
+        const int half = wave >> 2;            // ... of every (NW/4)-th line
         const int wi = col - A.pw;
         const bool wok = (col < A.pwp) & ((unsigned)wi < (unsigned)A.W);
         const uint32_t plane0 = (uint32_t)(tl.n * A.C + gi * A.Cg) * (uint32_t)(A.H * A.W);
@@ -125,7 +123,7 @@ __global__ __launch_bounds__(SLICE_THREADS) void slice_conv_kernel(SliceArgs A) 
         const uint32_t hw = (uint32_t)(A.H * A.W);
         for (int c = 0; c < A.Cg; ++c) {
             const uint32_t plane = plane0 + (uint32_t)c * hw;
-            for (int row = half; row < A.ph_max; row += 2) {
+            for (int row = half; row < A.ph_max; row += NW / 4) {
                 const int hi = tl.hi0 + row;
                 const bool ok = wok & ((unsigned)hi < (unsigned)A.H);
                 const uint32_t e = plane + (uint32_t)(hi * A.W + wi);
@@ -143,12 +141,10 @@ __global__ __launch_bounds__(SLICE_THREADS) void slice_conv_kernel(SliceArgs A) 
     float bv0[16], bv1[16];
     int cur_gz = -1;
     if ((int)blockIdx.x < A.tiles_total) copy_slice(blockIdx.x, xs);
-    for (int w = blockIdx.x, it = 0; w < A.tiles_total; w += gridDim.x, ++it) {
+    for (int w = blockIdx.x; w < A.tiles_total; w += gridDim.x) {
         const Tile tl = decode(w);
         const int gi = tl.gz / A.grid_m;
         const int m0 = (tl.gz - gi * A.grid_m) * SLICE_BM;
-        uint32_t* cur = xs + (it & 1) * slice_words;
-        uint32_t* nxt = xs + ((it & 1) ^ 1) * slice_words;
         if (tl.gz != cur_gz) {
             // ---- filters of this (group, channel tile): wl[m][k], zero beyond kred or Kg
             __syncthreads();  // no wave still reads the previous filters
@@ -161,16 +157,17 @@ __global__ __launch_bounds__(SLICE_THREADS) void slice_conv_kernel(SliceArgs A) 
                 int dst[SLICE_UNR];
 #pragma unroll
                 for (int u = 0; u < SLICE_UNR; ++u) {
-                    const int idx = base + u * SLICE_THREADS;
+                    const int i0 = base + u * SLICE_THREADS;
+                    const int idx = i0;
                     const int m = idx / kw;
                     const int k = idx - m * kw;
-                    const bool ok = (idx < total) & (m0 + m < A.Kg) & (k < A.kred);
+                    const bool ok = (i0 < total) & (m0 + m < A.Kg) & (k < A.kred);
                     const uint32_t e = (uint32_t)(gi * A.Kg + m0 + m) * (uint32_t)A.kred + (uint32_t)k;
                     if constexpr (ES == 4)
                         v[u] = ld_f32(rw, ok ? e * 4u : OOB_OFF);
                     else
                         v[u] = ld_u16(rw, ok ? e * 2u : OOB_OFF);
-                    dst[u] = idx < total ? m * wpitch + k : -1;
+                    dst[u] = i0 < total ? m * wpitch + k : -1;
                 }
 #pragma unroll
                 for (int u = 0; u < SLICE_UNR; ++u)
@@ -183,15 +180,9 @@ __global__ __launch_bounds__(SLICE_THREADS) void slice_conv_kernel(SliceArgs A) 
                 bv0[v] = ld_f32(rbias, A.bias && m < A.Kg ? (uint32_t)(gi * A.Kg + m) * 4u : OOB_OFF);
                 bv1[v] = ld_f32(rbias, A.bias && m + 32 < A.Kg ? (uint32_t)(gi * A.Kg + m + 32) * 4u : OOB_OFF);
             }
-            __builtin_amdgcn_s_waitcnt(0);
-        } else {
-            // The slice of this tile was requested before the previous tile's MFMAs; only the
-            // previous tile's SLICE_STORES stores were issued after it, and vector memory
-            // operations complete in order, so this waits for the slice but not for them.
-            __builtin_amdgcn_s_waitcnt(SLICE_WAIT_ALL_BUT_STORES);
         }
-        lds_barrier();  // the slice has landed; every wave is done with the other buffer
-        if (w + (int)gridDim.x < A.tiles_total) copy_slice(w + gridDim.x, nxt);
+        __builtin_amdgcn_s_waitcnt(0);  // this wave's slice copies (and filter loads) have landed
+        lds_barrier();                  // ... and every other wave's
 
         const int p = tl.p0 + wave * 32 + lcol;
         int pixbase = 0;  // pixels past the end read a valid (discarded) column
@@ -203,7 +194,7 @@ __global__ __launch_bounds__(SLICE_THREADS) void slice_conv_kernel(SliceArgs A) 
         const T* wa0 = wl + lcol * wpitch + lrow * A.kh;
         const T* wa1 = wa0 + 32 * wpitch;
         const int32_t* kp = ko + lrow * A.kh;
-        const uint32_t* xp = cur + pixbase;
+        const uint32_t* xp = xs + pixbase;
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc0[v] = acc1[v] = 0.0f;
 
@@ -294,12 +285,15 @@ __global__ __launch_bounds__(SLICE_THREADS) void slice_conv_kernel(SliceArgs A) 
             store_out<TOut>(ry, ybase + (uint32_t)(m + 32) * (uint32_t)howo, pok & (m + 32 < A.Kg),
                             acc1[v] + bv1[v]);
         }
+        lds_barrier();  // every wave is done with the slice before it is overwritten
+        if (w + (int)gridDim.x < A.tiles_total) copy_slice(w + gridDim.x, xs);
     }
 }
 
 SlicePlan slice_plan(int64_t Cg, int64_t R, int64_t S, int64_t Ho, int64_t Wo, int sh, int sw, int dh, int dw,
-                     int xdt) {
+                     int xdt, int nw) {
     SlicePlan sp{};
+    const int64_t SLICE_NPX = 32 * nw;
     const int64_t es = xdt == CONV2D_BF16 ? 2 : 4;
     const int64_t step = xdt == CONV2D_BF16 ? 8 : 4;
     const int64_t kred = Cg * R * S;
@@ -313,9 +307,10 @@ SlicePlan slice_plan(int64_t Cg, int64_t R, int64_t S, int64_t Ho, int64_t Wo, i
     const int64_t pwp = (Wo - 1) * sw + (S - 1) * dw + 1;
     if (pwp > SLICE_LP) return sp;  // one column per thread
     const int64_t xbytes = Cg * ph_max * SLICE_LP * 4;
-    const int64_t total = wbytes + kbytes + 2 * xbytes;  // the slice is double-buffered
+    const int64_t total = wbytes + kbytes + xbytes;
     if (total > SLICE_MAX_LDS) return sp;
     sp.ok = true;
+    sp.nw = nw;
     sp.kh = (int32_t)kh;
     sp.ph_max = (int32_t)ph_max;
     sp.pwp = (int32_t)pwp;
@@ -325,15 +320,22 @@ SlicePlan slice_plan(int64_t Cg, int64_t R, int64_t S, int64_t Ho, int64_t Wo, i
     return sp;
 }
 
-hipError_t launch_slice(const SliceArgs& a, int xdt, int ydt, hipStream_t stream) {
-    if (a.nblocks < 1 || a.tiles_total < 1) return hipErrorInvalidValue;
-    dim3 grid((unsigned)a.nblocks);
+template <int NW>
+static void launch_slice_cfg(const SliceArgs& a, int xdt, int ydt, hipStream_t stream) {
+    dim3 grid((unsigned)a.nblocks), block(64 * NW);
     if (xdt == CONV2D_F32)
-        hipLaunchKernelGGL((slice_conv_kernel<float, float>), grid, dim3(SLICE_THREADS), a.lds_bytes, stream, a);
+        hipLaunchKernelGGL((slice_conv_kernel<float, float, NW>), grid, block, a.lds_bytes, stream, a);
     else if (ydt == CONV2D_BF16)
-        hipLaunchKernelGGL((slice_conv_kernel<uint16_t, uint16_t>), grid, dim3(SLICE_THREADS), a.lds_bytes, stream, a);
+        hipLaunchKernelGGL((slice_conv_kernel<uint16_t, uint16_t, NW>), grid, block, a.lds_bytes, stream, a);
     else
-        hipLaunchKernelGGL((slice_conv_kernel<uint16_t, float>), grid, dim3(SLICE_THREADS), a.lds_bytes, stream, a);
+        hipLaunchKernelGGL((slice_conv_kernel<uint16_t, float, NW>), grid, block, a.lds_bytes, stream, a);
+}
+
+hipError_t launch_slice(const SliceArgs& a, int xdt, int ydt, int nw, hipStream_t stream) {
+    if (a.nblocks < 1 || a.tiles_total < 1) return hipErrorInvalidValue;
+    if (nw == 4) launch_slice_cfg<4>(a, xdt, ydt, stream);
+    else if (nw == 8) launch_slice_cfg<8>(a, xdt, ydt, stream);
+    else return hipErrorInvalidValue;
     return hipGetLastError();
 }
 

@@ -45,29 +45,33 @@ def _reference(cs, mode, inputs):
 
 
 class _Kernel:
-    """Forces the implicit family's microkernel through CONV2D_SLICE while descriptors are
-    created: None = planner's choice, "0" = tiled GEMM, "1" = sliced kernel (when it fits)."""
+    """Forces the implicit family's microkernel while descriptors are created: kernel None =
+    planner's choice, "0" = tiled GEMM, "1" = sliced kernel (when it fits); waves = the sliced
+    kernel's waves per block ("4" or "8"; None = planner's choice)."""
 
-    def __init__(self, force):
-        self.force, self.old = force, None
+    def __init__(self, force, waves=None):
+        self.set = {"CONV2D_SLICE": force, "CONV2D_SLICE_WAVES": waves}
+        self.old = {}
 
     def __enter__(self):
-        self.old = os.environ.get("CONV2D_SLICE")
-        if self.force is not None:
-            os.environ["CONV2D_SLICE"] = self.force
+        for k, v in self.set.items():
+            self.old[k] = os.environ.get(k)
+            if v is not None:
+                os.environ[k] = v
         return self
 
     def __exit__(self, *exc):
-        if self.old is None:
-            os.environ.pop("CONV2D_SLICE", None)
-        else:
-            os.environ["CONV2D_SLICE"] = self.old
+        for k, v in self.old.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
 
 
-def _run(cs, algo, mode="random", kernel=None):
+def _run(cs, algo, mode="random", kernel=None, waves=None):
     import torch
-    print(f"\n[case] {cs} algo={ALGO_IDS[algo]} kernel={kernel} mode={mode}", flush=True)
-    with _Kernel(kernel):
+    print(f"\n[case] {cs} algo={ALGO_IDS[algo]} kernel={kernel} waves={waves} mode={mode}", flush=True)
+    with _Kernel(kernel, waves):
         dc = DeviceConv(cs, mode)
     try:
         if kernel == "1" and dc.plan(algo).kernel != B.CONV2D_KERNEL_SLICE:
@@ -80,8 +84,8 @@ def _run(cs, algo, mode="random", kernel=None):
     return y, (dc.x_host, dc.w_host, dc.b_host)
 
 
-def _check(cs, algo, mode="random", kernel=None):
-    y, inputs = _run(cs, algo, mode, kernel)
+def _check(cs, algo, mode="random", kernel=None, waves=None):
+    y, inputs = _run(cs, algo, mode, kernel, waves)
     y_ref, a_ref = _reference(cs, mode, inputs)
     assert y.shape == y_ref.shape
     if mode == "integer" and cs.y_dtype == "f32":
@@ -107,11 +111,11 @@ def test_config_parity(name, algo):
     _check(datagen.CONFIGS[name], algo)
 
 
-@pytest.mark.parametrize("kernel", ["0", "1"], ids=["gemm", "slice"])
+@pytest.mark.parametrize("kernel", [("0", None), ("1", "4"), ("1", "8")], ids=["gemm", "slice4", "slice8"])
 @pytest.mark.parametrize("name", ["cfg1", "cfg4", "cfg4_bf16"])
 def test_config_parity_both_implicit_kernels(name, kernel):
-    _check(datagen.CONFIGS[name], IMPLICIT, kernel=kernel)
-    _check(datagen.CONFIGS[name], IMPLICIT, "integer", kernel=kernel)
+    _check(datagen.CONFIGS[name], IMPLICIT, kernel=kernel[0], waves=kernel[1])
+    _check(datagen.CONFIGS[name], IMPLICIT, "integer", kernel=kernel[0], waves=kernel[1])
 
 
 @pytest.mark.parametrize("algo", [DIRECT, IMPLICIT, IM2COL], ids=lambda a: ALGO_IDS[a])
@@ -170,8 +174,9 @@ VARIANTS = [("nchw", "f32", "f32"), ("nhwc", "f32", "f32"), ("nchw", "bf16", "bf
             ("nhwc", "bf16", "f32")]
 
 
-EDGE_ALGOS = [("implicit", IMPLICIT, None), ("implicit-gemm", IMPLICIT, "0"), ("implicit-slice", IMPLICIT, "1"),
-              ("im2col", IM2COL, None), ("direct", DIRECT, None)]
+EDGE_ALGOS = [("implicit", IMPLICIT, None, None), ("implicit-gemm", IMPLICIT, "0", None),
+              ("implicit-slice4", IMPLICIT, "1", "4"), ("implicit-slice8", IMPLICIT, "1", "8"),
+              ("im2col", IM2COL, None, None), ("direct", DIRECT, None, None)]
 
 
 @pytest.mark.parametrize("algo", EDGE_ALGOS, ids=lambda a: a[0])
@@ -179,10 +184,10 @@ EDGE_ALGOS = [("implicit", IMPLICIT, None), ("implicit-gemm", IMPLICIT, "0"), ("
 @pytest.mark.parametrize("idx", range(len(EDGE)))
 def test_edge_grid(idx, var, algo):
     layout, xdt, ydt = var
-    _, algo, kernel = algo
+    _, algo, kernel, waves = algo
     cs = EDGE[idx].with_(layout=layout, x_dtype=xdt, y_dtype=ydt)
-    _check(cs, algo, "random", kernel)
-    _check(cs.with_(y_dtype="f32"), algo, "integer", kernel)
+    _check(cs, algo, "random", kernel, waves)
+    _check(cs.with_(y_dtype="f32"), algo, "integer", kernel, waves)
 
 
 # ------------------------------------------------------------------ behaviour
