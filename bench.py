@@ -27,7 +27,8 @@ PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}   # dense MFMA
 PEAK_HBM_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 KERNEL_SOURCES = {
-    "implicit_gemm": ["paper_2407_10730_amd/csrc/gemm_mfma.hip", "paper_2407_10730_amd/csrc/pack_kernels.hip"],
+    "implicit_gemm": ["paper_2407_10730_amd/csrc/gemm_mfma.hip", "paper_2407_10730_amd/csrc/pack_kernels.hip",
+                      "paper_2407_10730_amd/csrc/slice_conv.hip"],
     "im2col_gemm": ["paper_2407_10730_amd/csrc/gemm_mfma.hip", "paper_2407_10730_amd/csrc/pack_kernels.hip"],
     "direct": ["paper_2407_10730_amd/csrc/direct_kernels.hip"],
 }
@@ -340,10 +341,14 @@ def main():
                     data = json.load(f)
             except (OSError, ValueError):
                 data = {}
-            algo_name = "im2col_gemm" if "DENSE" in key[0] else "implicit_gemm"
-            data[f"{args.workload}:implicit_gemm"] = {
+            try:
+                with open(os.path.join(args.summarize_profiles, "bench.json")) as f:
+                    algo_name = json.loads(f.read().strip().splitlines()[-1])["config"]["algo"]
+            except (OSError, ValueError, KeyError, IndexError):
+                algo_name = "implicit_gemm"
+            data[f"{args.workload}:{algo_name}"] = {
                 "kernel": key[0], "bytes_per_launch": traffic[key[0]],
-                "kernel_hash": kernel_hash("implicit_gemm")}
+                "kernel_hash": kernel_hash(algo_name)}
             with open(TRAFFIC_FILE, "w") as f:
                 json.dump(data, f, indent=1)
         return
@@ -399,7 +404,8 @@ def main():
         achieved = alg_bytes / (kern_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": achieved / PEAK_HBM_GBS}
-    roof["kernel"] = f"{algo_name} microkernel"
+    plan = dc.plan(algo)
+    roof["kernel"] = f"{algo_name} microkernel ({B.KERNEL_NAMES[plan.kernel]}, tile {plan.tile_m}x{plan.tile_n})"
     roof["kernel_us_per_launch"] = kern_launch_ms * 1e3
     roof["launches_per_step"] = mk_calls / args.steps
     roof["algorithmic_bytes"] = alg_bytes
