@@ -86,19 +86,26 @@ int env_timing() {
 // (work of one tile) / (MFMA efficiency of its wave tile): with many more tiles
 // than CUs the tiles are dealt out evenly, so the busiest CU sets the time.
 // CONV2D_GEMM = "k32:TILE[:BK[:PF]]" overrides the choice for tuning.
-GemmPlan choose_tile(int64_t M, int64_t P, int64_t G, int64_t kred, int xdt, int64_t cg) {
+// nhwc: bf16 with the channel-contiguous gather (BK 64 when C/g allows).
+GemmPlan choose_tile(int64_t M, int64_t P, int64_t G, int64_t kred, int xdt, int64_t cg, bool nhwc = false) {
     const int cus = 256;
     GemmPlan best;
     double best_cost = 1e300;
     // Candidate block tiles of the 32x32-MFMA kernels, with the measured MFMA efficiency of
-    // their wave tiles relative to 64x64 (fp32, MI355X).
+    // their wave tiles relative to 64x64 (fp32, MI355X); with the bf16 16-byte gather the
+    // larger tiles reuse each LDS operand more and win.
     struct Cand { int tile; double eff; };
-    const Cand cands[] = {{TILE_64x64, 1.0}, {TILE_64x128, 1.0}, {TILE_64x256, 0.8},
-                          {TILE_128x64, 0.9}, {TILE_128x128, 0.85}};
-    for (const Cand& c : cands) {
+    const Cand cands_f32[] = {{TILE_64x64, 1.0}, {TILE_64x128, 1.0}, {TILE_64x256, 0.8},
+                              {TILE_128x64, 0.9}, {TILE_128x128, 0.85}};
+    const Cand cands_bf16[] = {{TILE_64x64, 0.7}, {TILE_64x128, 0.8}, {TILE_64x256, 0.6},
+                               {TILE_128x64, 0.85}, {TILE_128x128, 1.0}};
+    // bf16 tiles need two resident blocks per CU to hide their load latency: count rounds
+    // of two blocks per CU (a single block per CU measured well below its share)
+    const int per_round = nhwc ? 2 * cus : cus;
+    for (const Cand& c : nhwc ? cands_bf16 : cands_f32) {
         const TileShape ts = kTileShapes[c.tile];
         const int64_t tiles = ceil_div(M, ts.bm) * ceil_div(P, ts.bn) * G;
-        const double cost = (double)ceil_div(tiles, cus) * ts.bm * ts.bn / c.eff;
+        const double cost = (double)ceil_div(tiles, per_round) * ts.bm * ts.bn / c.eff;
         if (cost < best_cost) {
             best_cost = cost;
             best.kind = 0;
@@ -107,14 +114,15 @@ GemmPlan choose_tile(int64_t M, int64_t P, int64_t G, int64_t kred, int xdt, int
             best.bn = ts.bn;
         }
     }
-    (void)cg;
-    if (best.kind == 0) best.bk = xdt == CONV2D_BF16 ? 32 : 16;
+    if (best.kind == 0) best.bk = xdt == CONV2D_BF16 ? (nhwc && cg % 64 == 0 ? 64 : 32) : 16;
     const char* ov = std::getenv("CONV2D_GEMM");
     if (ov) {
         int a = 0, b = 0, c = 16;
         if (std::sscanf(ov, "k32:%d:%d:%d", &a, &b, &c) >= 1 && a >= 0 && a < TILE_COUNT) {
-            int bk = xdt == CONV2D_BF16 ? 32 : (std::strchr(ov + 4, ':') ? b : 16);
-            int pf = std::strchr(ov + 4, ':') && std::strchr(std::strchr(ov + 4, ':') + 1, ':') ? c : 1;
+            const bool has_bk = std::strchr(ov + 4, ':') != nullptr;
+            int bk = xdt == CONV2D_BF16 ? (nhwc && has_bk && b == 64 && cg % 64 == 0 ? 64 : 32)
+                                        : (has_bk ? b : 16);
+            int pf = has_bk && std::strchr(std::strchr(ov + 4, ':') + 1, ':') ? c : 1;
             if (xdt == CONV2D_BF16 || gemm32_f32_supported(a, bk, pf)) {
                 best.kind = 0; best.tile = a; best.bm = kTileShapes[a].bm; best.bn = kTileShapes[a].bn;
                 best.bk = bk;
@@ -142,6 +150,7 @@ struct conv2d_desc {
     bool implicit_ok = false, direct_ok = false;
     bool implicit_tap = false;  // tap-major gather (C/g a multiple of the stage depth)
     bool implicit_slice = false;  // sliced direct MFMA kernel instead of the GEMM
+    bool implicit_nhwc = false;   // bf16 GEMM gathering from an NHWC copy of x (16-byte loads)
     GemmPlan implicit;
     SlicePlan slice{};
     ExplicitPlan expl;
@@ -152,7 +161,7 @@ struct conv2d_desc {
     KTabEntry* ktab_dev = nullptr;
     void* ws = nullptr;
     int64_t ws_bytes = 0;
-    void* xr = nullptr;  // NCHW copy of an NHWC input
+    void* xr = nullptr;  // NCHW copy of an NHWC input, or NHWC copy of an NCHW one (bf16 NHWC gather)
     int64_t xr_bytes = 0;
     void* yr = nullptr;  // NCHW result before the NHWC reorder
     int64_t yr_bytes = 0;
@@ -404,7 +413,7 @@ int run_implicit(conv2d_desc* d, const void* x, const void* w, const float* bias
     const Geometry& g = d->g;
     const GemmPlan& gp = d->implicit;
     if (d->implicit_slice) return run_slice(d, x, w, bias, y, s, ph);
-    if (d->implicit_tap && g.R * g.S > 1) {
+    if ((d->implicit_tap || d->implicit_nhwc) && g.R * g.S > 1) {
         // pre-convolution reordering of the filters into the tap-major reduction order
         const int64_t wb = g.w_elems * elem_size(g.xdt);
         CV_TRY(ensure_buffer(&d->wr, &d->wr_bytes, wb));
@@ -428,6 +437,7 @@ int run_implicit(conv2d_desc* d, const void* x, const void* w, const float* bias
     a.dh = g.dh; a.dw = g.dw; a.R = (int32_t)g.R; a.S = (int32_t)g.S; a.RS = (int32_t)(g.R * g.S);
     a.Cg = (int32_t)g.Cg;
     a.HW = (int32_t)(g.H * g.W);
+    a.Cx = (int32_t)g.C;
     a.x_nstride = g.C * g.H * g.W;
     a.M = (int32_t)g.Kg;
     a.Kred = (int32_t)g.Kred;
@@ -442,7 +452,7 @@ int run_implicit(conv2d_desc* d, const void* x, const void* w, const float* bias
     a.HoWo = (int32_t)(g.Ho * g.Wo);
     Scope sc(d, CONV2D_ALGO_IMPLICIT_GEMM, CONV2D_PH_IN_MICROKERNEL, s, ph);
     CV_TRY(sc.begin());
-    const int bsrc = d->implicit_tap ? BSRC_IMPLICIT_TAP : BSRC_IMPLICIT_NCHW;
+    const int bsrc = d->implicit_nhwc ? BSRC_NHWC_TAP : d->implicit_tap ? BSRC_IMPLICIT_TAP : BSRC_IMPLICIT_NCHW;
     CV_HIP(dispatch_gemm(gp, a, bsrc, EPI_NCHW, g.xdt, g.ydt, (int)g.G, s));
     return sc.end();
 }
@@ -577,7 +587,16 @@ int conv2d_desc_create(const conv2d_params* params, conv2d_desc** out) {
     d->timing = env_timing();
     d->implicit_ok = implicit_supported(g);
     d->direct_ok = direct_supported(g);
-    d->implicit = choose_tile(g.Kg, g.P, g.G, g.Kred, g.xdt, g.Cg);
+    // bf16 with C/g a multiple of 32: gather 16-byte channel runs from an NHWC copy of x.  The
+    // copy costs 2|x| of HBM traffic (nothing when x is already NHWC), so it is taken when the
+    // convolution does at least 1000 flops per input byte; CONV2D_NHWC_GATHER=0 / 1 forces it.
+    if (g.xdt == CONV2D_BF16 && g.Cg % 32 == 0) {
+        const double flops = 2.0 * (double)g.N * g.K * g.Cg * g.R * g.S * g.Ho * g.Wo;
+        const double xbytes = (double)g.x_elems * 2;
+        const int64_t force = env_int64("CONV2D_NHWC_GATHER", -1);
+        d->implicit_nhwc = force < 0 ? (g.layout == CONV2D_NHWC || flops >= 1000.0 * xbytes) : force != 0;
+    }
+    d->implicit = choose_tile(g.Kg, g.P, g.G, g.Kred, g.xdt, g.Cg, d->implicit_nhwc);
     d->implicit_tap = g.Cg % d->implicit.bk == 0;
     {
         // 8 waves (256-pixel tiles) unless an image has at most 128 output pixels;
@@ -661,15 +680,24 @@ int conv2d_fwd(conv2d_desc* d, const void* x, const void* w, const float* bias, 
     const void* xin = x;
     void* yout = y;
     const bool nhwc = g.layout == CONV2D_NHWC;
-    if (nhwc) {
-        const int64_t xb = g.x_elems * elem_size(g.xdt), yb = g.y_elems * elem_size(g.ydt);
+    // The bf16 NHWC gather reads x channel-contiguous: an NHWC x goes in as it is, an NCHW x is
+    // reordered.  Every other kernel reads NCHW x.
+    const bool x_nhwc = algo == CONV2D_ALGO_IMPLICIT_GEMM && d->implicit_nhwc && !d->implicit_slice;
+    if (nhwc != x_nhwc) {
+        const int64_t xb = g.x_elems * elem_size(g.xdt);
         CV_TRY(ensure_buffer(&d->xr, &d->xr_bytes, xb));
-        CV_TRY(ensure_buffer(&d->yr, &d->yr_bytes, yb));
         Scope sc(d, algo, CONV2D_PH_PRE_REORDER, s, ph);
         CV_TRY(sc.begin());
-        CV_HIP(launch_nhwc_to_nchw(x, d->xr, g.N, g.C, g.H * g.W, (int)elem_size(g.xdt), s));
+        if (nhwc)
+            CV_HIP(launch_nhwc_to_nchw(x, d->xr, g.N, g.C, g.H * g.W, (int)elem_size(g.xdt), s));
+        else
+            CV_HIP(launch_nchw_to_nhwc(x, d->xr, g.N, g.C, g.H * g.W, (int)elem_size(g.xdt), s));
         CV_TRY(sc.end());
         xin = d->xr;
+    }
+    if (nhwc) {
+        const int64_t yb = g.y_elems * elem_size(g.ydt);
+        CV_TRY(ensure_buffer(&d->yr, &d->yr_bytes, yb));
         yout = d->yr;
     }
     int st = CONV2D_OK;
@@ -756,6 +784,7 @@ int conv2d_plan_query(const conv2d_desc* d, int algo, conv2d_plan_info* out) {
     const int bk = algo == CONV2D_ALGO_IM2COL_GEMM ? d->expl.gemm.bk : d->implicit.bk;
     out->kred_pad = (int32_t)(ceil_div(g.Kred, bk) * bk);
     out->needs_reorder = g.layout == CONV2D_NHWC ? 1 : 0;
+    if (algo == CONV2D_ALGO_IMPLICIT_GEMM && d->implicit_nhwc && !d->implicit_slice) out->needs_reorder = 1;
     out->op_class = (int32_t)d->opclass;
     out->chunks = 1;
     if (algo == CONV2D_ALGO_IMPLICIT_GEMM) {

@@ -34,7 +34,8 @@ static const TileShape kTileShapes[TILE_COUNT] = {{64, 64}, {64, 128}, {64, 256}
 //  DENSE         : read from a packed column matrix [G][Kred][ldb]
 //  IMPLICIT_TAP  : gathered from NCHW x in tap-major order kr' = (r, s, c); one filter tap per
 //                  stage, so needs C/g to be a multiple of the stage depth (no table)
-enum BSrc { BSRC_IMPLICIT_NCHW = 0, BSRC_DENSE = 1, BSRC_IMPLICIT_TAP = 2 };
+//  NHWC_TAP      : (bf16) the same order gathered from an NHWC copy of x, 16 bytes per load
+enum BSrc { BSRC_IMPLICIT_NCHW = 0, BSRC_DENSE = 1, BSRC_IMPLICIT_TAP = 2, BSRC_NHWC_TAP = 3 };
 // Destination of the GEMM result.
 enum Epi { EPI_NCHW = 0, EPI_DENSE = 1 };
 
@@ -59,6 +60,7 @@ struct GemmArgs {
     const KTabEntry* ktab;
     int32_t H, W, Ho, Wo, sh, sw, ph, pw;
     int32_t dh, dw, R, S, RS, Cg, HW;  // tap-major gather: filter dims, R*S, channels per group, H*W
+    int32_t Cx;           // NHWC source: channels per pixel (all groups)
     int64_t x_nstride;    // C*H*W
     int32_t M, Kred, P, nstages;
     int32_t grid_p, grid_m;   // pixel tiles x channel tiles
@@ -73,7 +75,7 @@ struct GemmArgs {
 };
 
 // 32x32-MFMA kernels.  fp32: stage depth bk in {16, 32}, register prefetch distance pf in {1, 2};
-// bf16: bk = 32, pf = 1 (arguments ignored).
+// bf16: bk in {32, 64} (64 only with the NHWC source), pf ignored.
 bool gemm32_f32_supported(int tile, int bk, int pf);
 hipError_t launch_gemm(const GemmArgs& a, int tile, int bk, int pf, int bsrc, int epi, int xdt, int ydt,
                        int groups, hipStream_t stream);

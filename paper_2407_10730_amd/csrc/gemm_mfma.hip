@@ -297,17 +297,47 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs A) {
 // ============================================================================ bf16
 // Same structure with MFMA 32x32x16 bf16 (fp32 accumulation).  LDS tiles are
 // m-major / n-major with 8 consecutive k per 16-byte chunk, which is exactly
-// one lane's MFMA operand; rows are padded by 8 elements.
-template <int BM, int BN, int WM, int WN, int BSRC, int EPI, typename TOut>
+// one lane's MFMA operand; rows are padded by 8 elements.  BK = 32 or 64
+// reduction rows per stage.
+//
+// B sources: the NCHW gathers (tap table or tap-major) read one 2-byte element
+// per load, 8 loads per 16-byte chunk.  NHWC_TAP reads a channel-contiguous
+// copy of x (NHWC): in tap-major order one chunk is 8 consecutive channels of
+// one pixel at one tap, a single 16-byte load, and the 4 or 8 chunks of a
+// pixel's stage row come from consecutive threads (one 64- or 128-byte run).
+
+// Window origin of output pixel p in an NHWC input: element offset of
+// x[n, hi0, wi0, gi*Cg] (negative or past the row inside the padding).
+__device__ __forceinline__ ColState col_state_nhwc(const GemmArgs& A, int p, int gi) {
+    ColState s;
+    if (p < A.P) {
+        const int n = p / A.HoWo;
+        const int hw = p - n * A.HoWo;
+        const int ho = hw / A.Wo;
+        const int wo = hw - ho * A.Wo;
+        s.hi0 = ho * A.sh - A.ph;
+        s.wi0 = wo * A.sw - A.pw;
+        s.base = (((int64_t)n * A.H + s.hi0) * A.W + s.wi0) * A.Cx + (int64_t)gi * A.Cg;
+    } else {
+        s.hi0 = KTAB_DEAD;
+        s.wi0 = 0;
+        s.base = 0;
+    }
+    return s;
+}
+
+template <int BM, int BN, int WM, int WN, int BK, int BSRC, int EPI, typename TOut>
 __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs A) {
-    constexpr int BK = 32;
     constexpr int LDK = BK + 8;
     constexpr int WTM = BM / WM, WTN = BN / WN;
     constexpr int TM = WTM / 32, TN = WTN / 32;
+    static_assert(BK == 32 || BK == 64, "stage depth");
     static_assert(WM * WN == 4 && TM >= 1 && TN >= 1, "bad wave layout");
     static_assert(BN <= 256 && 256 % BN == 0 && BN >= 64, "B loader assumes one column per thread");
-    constexpr int BUNITS = BN * (BK / 8) / 256;  // 8-element B chunks per thread
-    constexpr int AUNITS = BM * (BK / 8) / 256;  // 8-element A chunks per thread
+    constexpr int CPR = BK / 8;                  // 16-byte chunks per tile row
+    constexpr int BUNITS = BN * CPR / 256;       // 8-element B chunks per thread
+    constexpr int AUNITS = BM * CPR / 256;       // 8-element A chunks per thread
+    constexpr bool NHWC = BSRC == BSRC_NHWC_TAP;
 
     __shared__ __attribute__((aligned(16))) uint16_t As[2][BM][LDK];
     __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN][LDK];
@@ -326,24 +356,67 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs A) {
     const __amdgpu_buffer_rsrc_t ra = make_rsrc(A.a, A.a_bytes);
     const __amdgpu_buffer_rsrc_t rb = make_rsrc(A.b, A.b_bytes);
 
-    // B: unit u = t + i*256 -> column n = u % BN (same for all i), k chunk kc = u / BN
+    // B, NCHW sources: unit u = t + i*256 -> column n = u % BN (same for all i), chunk u / BN.
+    // B, NHWC: unit u = t + i*256 -> column u / CPR, chunk u % CPR.
     const int bn = t % BN;
     const int bkc0 = __builtin_amdgcn_readfirstlane(t / BN);
     const int pcol = p0 + bn;
     ColState cs;
-    if (BSRC != BSRC_DENSE) cs = col_state(A, pcol, gi);
+    ColState csn[NHWC ? BUNITS : 1];
+    if constexpr (NHWC) {
+#pragma unroll
+        for (int i = 0; i < BUNITS; ++i) csn[i] = col_state_nhwc(A, p0 + (t + i * 256) / CPR, gi);
+    } else if (BSRC != BSRC_DENSE) {
+        cs = col_state(A, pcol, gi);
+    }
     const uint32_t dvb = pcol < A.P ? (uint32_t)(((int64_t)gi * A.b_gstride + pcol) * 2) : OOB_OFF;
-    // A: unit u = t + i*256 -> row m = u / 4, k chunk kc = u % 4
+    // A: unit u = t + i*256 -> row m = u / CPR, k chunk kc = u % CPR
     const int64_t a_base = (int64_t)gi * A.a_gstride;
 
     u32x4 breg[BUNITS];
     u32x4 areg[AUNITS];
     int cur_c0 = 0, cur_r = 0, cur_s = 0;  // tap-major cursor of the next stage
 
+    auto load_weights_tap = [&]() {
+        // weights in tap-major order [K][R*S][C/g]: 8 consecutive channels per 16-byte load
+        const int tap = cur_r * A.S + cur_s;
+#pragma unroll
+        for (int i = 0; i < AUNITS; ++i) {
+            const int u = t + i * 256;
+            const int m = m0 + u / CPR;
+            const int kc = u % CPR;
+            const int64_t e0 = a_base + (int64_t)m * A.lda + (int64_t)tap * A.Cg + cur_c0 + kc * 8;
+            areg[i] = __builtin_amdgcn_raw_buffer_load_b128(ra, m < A.M ? (uint32_t)(e0 * 2) : OOB_OFF, 0, 0);
+        }
+    };
+    auto advance_tap = [&]() {
+        cur_c0 += BK;
+        if (cur_c0 >= A.Cg) {
+            cur_c0 = 0;
+            if (++cur_s == A.S) {
+                cur_s = 0;
+                ++cur_r;
+            }
+        }
+    };
+
     auto load_stage = [&](int stage) {
         const int k0 = stage * BK;
         uint16_t h[8];
-        if constexpr (BSRC == BSRC_IMPLICIT_TAP) {
+        if constexpr (NHWC) {
+            const int roff = cur_r * A.dh, soff = cur_s * A.dw;
+            const int64_t tapoff = ((int64_t)roff * A.W + soff) * A.Cx + cur_c0;
+#pragma unroll
+            for (int i = 0; i < BUNITS; ++i) {
+                const int kc = (t + i * 256) % CPR;
+                const int hi = csn[i].hi0 + roff, wi = csn[i].wi0 + soff;
+                const bool ok = ((unsigned)hi < (unsigned)A.H) & ((unsigned)wi < (unsigned)A.W);
+                const int64_t e = csn[i].base + tapoff + kc * 8;
+                breg[i] = __builtin_amdgcn_raw_buffer_load_b128(rb, ok ? (uint32_t)(e * 2) : OOB_OFF, 0, 0);
+            }
+            load_weights_tap();
+            advance_tap();
+        } else if constexpr (BSRC == BSRC_IMPLICIT_TAP) {
             const int roff = cur_r * A.dh, soff = cur_s * A.dw;
             const int hi = cs.hi0 + roff, wi = cs.wi0 + soff;
             const bool ok = ((unsigned)hi < (unsigned)A.H) & ((unsigned)wi < (unsigned)A.W);
@@ -357,24 +430,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs A) {
 #pragma unroll
                 for (int q = 0; q < 4; ++q) breg[i][q] = (uint32_t)h[2 * q] | ((uint32_t)h[2 * q + 1] << 16);
             }
-            // weights in tap-major order [K][R*S][C/g]: 8 consecutive channels per 16-byte load
-            const int tap = cur_r * A.S + cur_s;
-#pragma unroll
-            for (int i = 0; i < AUNITS; ++i) {
-                const int u = t + i * 256;
-                const int m = m0 + u / (BK / 8);
-                const int kc = u % (BK / 8);
-                const int64_t e0 = a_base + (int64_t)m * A.lda + (int64_t)tap * A.Cg + cur_c0 + kc * 8;
-                areg[i] = __builtin_amdgcn_raw_buffer_load_b128(ra, m < A.M ? (uint32_t)(e0 * 2) : OOB_OFF, 0, 0);
-            }
-            cur_c0 += BK;
-            if (cur_c0 >= A.Cg) {
-                cur_c0 = 0;
-                if (++cur_s == A.S) {
-                    cur_s = 0;
-                    ++cur_r;
-                }
-            }
+            load_weights_tap();
+            advance_tap();
         } else {
 #pragma unroll
             for (int i = 0; i < BUNITS; ++i) {
@@ -398,8 +455,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs A) {
 #pragma unroll
             for (int i = 0; i < AUNITS; ++i) {
                 const int u = t + i * 256;
-                const int m = m0 + u / (BK / 8);
-                const int kc = u % (BK / 8);
+                const int m = m0 + u / CPR;
+                const int kc = u % CPR;
 #pragma unroll
                 for (int q = 0; q < 8; ++q) {
                     const int kr = k0 + kc * 8 + q;
@@ -415,13 +472,18 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs A) {
     auto store_stage = [&](int buf) {
 #pragma unroll
         for (int i = 0; i < BUNITS; ++i) {
-            const int kc = bkc0 + i * (256 / BN);
-            *reinterpret_cast<u32x4*>(&Bs[buf][bn][kc * 8]) = breg[i];
+            if constexpr (NHWC) {
+                const int u = t + i * 256;
+                *reinterpret_cast<u32x4*>(&Bs[buf][u / CPR][(u % CPR) * 8]) = breg[i];
+            } else {
+                const int kc = bkc0 + i * (256 / BN);
+                *reinterpret_cast<u32x4*>(&Bs[buf][bn][kc * 8]) = breg[i];
+            }
         }
 #pragma unroll
         for (int i = 0; i < AUNITS; ++i) {
             const int u = t + i * 256;
-            *reinterpret_cast<u32x4*>(&As[buf][u / (BK / 8)][(u % (BK / 8)) * 8]) = areg[i];
+            *reinterpret_cast<u32x4*>(&As[buf][u / CPR][(u % CPR) * 8]) = areg[i];
         }
     };
 
@@ -481,12 +543,17 @@ static hipError_t launch_f32(const GemmArgs& a, int bsrc, int epi, int groups, h
     return hipGetLastError();
 }
 
-template <int BM, int BN, int WM, int WN>
+template <int BM, int BN, int WM, int WN, int BK>
 static hipError_t launch_bf16(const GemmArgs& a, int bsrc, int epi, int ydt, int groups, hipStream_t stream) {
     dim3 grid((unsigned)(a.grid_p * a.grid_m), 1, (unsigned)groups);
 #define CV_BF(BS, EP, TO) \
-    hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, BS, EP, TO>), grid, dim3(256), 0, stream, a)
-    if (bsrc == BSRC_IMPLICIT_NCHW && epi == EPI_NCHW) {
+    hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, BK, BS, EP, TO>), grid, dim3(256), 0, stream, a)
+    if (bsrc == BSRC_NHWC_TAP && epi == EPI_NCHW) {
+        if (ydt == CONV2D_BF16) CV_BF(BSRC_NHWC_TAP, EPI_NCHW, uint16_t);
+        else CV_BF(BSRC_NHWC_TAP, EPI_NCHW, float);
+    } else if (BK != 32) {
+        return hipErrorInvalidValue;  // the NCHW gathers and the dense source use 32-row stages
+    } else if (bsrc == BSRC_IMPLICIT_NCHW && epi == EPI_NCHW) {
         if (ydt == CONV2D_BF16) CV_BF(BSRC_IMPLICIT_NCHW, EPI_NCHW, uint16_t);
         else CV_BF(BSRC_IMPLICIT_NCHW, EPI_NCHW, float);
     } else if (bsrc == BSRC_IMPLICIT_TAP && epi == EPI_NCHW) {
@@ -510,14 +577,19 @@ bool gemm32_f32_supported(int tile, int bk, int pf) {
 hipError_t launch_gemm(const GemmArgs& a, int tile, int bk, int pf, int bsrc, int epi, int xdt, int ydt,
                        int groups, hipStream_t stream) {
     if (xdt == CONV2D_BF16) {
+        if (bk != 32 && bk != 64) return hipErrorInvalidValue;
+#define CV_TB(BMV, BNV, WMV, WNV) \
+    return bk == 64 ? launch_bf16<BMV, BNV, WMV, WNV, 64>(a, bsrc, epi, ydt, groups, stream) \
+                    : launch_bf16<BMV, BNV, WMV, WNV, 32>(a, bsrc, epi, ydt, groups, stream)
         switch (tile) {
-            case TILE_64x64: return launch_bf16<64, 64, 2, 2>(a, bsrc, epi, ydt, groups, stream);
-            case TILE_64x128: return launch_bf16<64, 128, 1, 4>(a, bsrc, epi, ydt, groups, stream);
-            case TILE_64x256: return launch_bf16<64, 256, 1, 4>(a, bsrc, epi, ydt, groups, stream);
-            case TILE_128x128: return launch_bf16<128, 128, 2, 2>(a, bsrc, epi, ydt, groups, stream);
-            case TILE_128x64: return launch_bf16<128, 64, 2, 2>(a, bsrc, epi, ydt, groups, stream);
+            case TILE_64x64: CV_TB(64, 64, 2, 2);
+            case TILE_64x128: CV_TB(64, 128, 1, 4);
+            case TILE_64x256: CV_TB(64, 256, 1, 4);
+            case TILE_128x128: CV_TB(128, 128, 2, 2);
+            case TILE_128x64: CV_TB(128, 64, 2, 2);
             default: return hipErrorInvalidValue;
         }
+#undef CV_TB
     }
     if (!gemm32_f32_supported(tile, bk, pf)) return hipErrorInvalidValue;
 #define CV_T(TL, BMV, BNV, WMV, WNV)                                                          \

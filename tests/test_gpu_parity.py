@@ -46,11 +46,16 @@ def _reference(cs, mode, inputs):
 
 class _Kernel:
     """Forces the implicit family's microkernel while descriptors are created: kernel None =
-    planner's choice, "0" = tiled GEMM, "1" = sliced kernel (when it fits); waves = the sliced
-    kernel's waves per block ("4" or "8"; None = planner's choice)."""
+    planner's choice, "0" = tiled GEMM, "1" = sliced kernel (when it fits), "nhwc" = tiled
+    GEMM with the bf16 NHWC gather (when C/g allows); waves = the sliced kernel's waves per
+    block ("4" or "8"; None = planner's choice)."""
 
     def __init__(self, force, waves=None):
-        self.set = {"CONV2D_SLICE": force, "CONV2D_SLICE_WAVES": waves}
+        if force == "nhwc":
+            self.set = {"CONV2D_SLICE": "0", "CONV2D_NHWC_GATHER": "1", "CONV2D_SLICE_WAVES": None}
+        else:
+            self.set = {"CONV2D_SLICE": force, "CONV2D_SLICE_WAVES": waves,
+                        "CONV2D_NHWC_GATHER": None if force is None else "0"}
         self.old = {}
 
     def __enter__(self):
@@ -76,6 +81,8 @@ def _run(cs, algo, mode="random", kernel=None, waves=None):
     try:
         if kernel == "1" and dc.plan(algo).kernel != B.CONV2D_KERNEL_SLICE:
             pytest.skip("the sliced kernel does not fit this shape")
+        if kernel == "nhwc" and (cs.x_dtype != "bf16" or (cs.c // cs.groups) % 32):
+            pytest.skip("the NHWC gather needs bf16 and C/g a multiple of 32")
         dc.run(algo)
         torch.cuda.synchronize()
         y = dc.y_nchw()
@@ -174,8 +181,36 @@ VARIANTS = [("nchw", "f32", "f32"), ("nhwc", "f32", "f32"), ("nchw", "bf16", "bf
             ("nhwc", "bf16", "f32")]
 
 
+# bf16 layers the planner sends through the NHWC gather (C/g multiple of 32, high arithmetic
+# intensity): stage depths 32 and 64, stride, dilation, padding, groups, NHWC in and out,
+# ragged pixel and channel tiles
+NHWC_BF16 = [
+    _shape(4, 64, 28, 28, 128, 3, 3, pd=(1, 1), seed=210),
+    _shape(2, 32, 30, 26, 96, 3, 3, st=(2, 2), pd=(1, 1), seed=211),
+    _shape(2, 128, 17, 19, 70, 5, 5, pd=(4, 4), dl=(2, 2), seed=212),
+    _shape(1, 256, 14, 14, 256, 3, 3, pd=(1, 1), g=2, seed=213),
+    _shape(3, 96, 9, 9, 200, 1, 1, seed=214),
+    _shape(2, 64, 23, 23, 64, 7, 7, st=(2, 2), pd=(3, 3), seed=215),
+]
+
+
+@pytest.mark.parametrize("layout", ["nchw", "nhwc"])
+@pytest.mark.parametrize("idx", range(len(NHWC_BF16)))
+def test_bf16_nhwc_gather(idx, layout):
+    cs = NHWC_BF16[idx].with_(layout=layout, x_dtype="bf16", y_dtype="bf16")
+    with _Kernel("nhwc"):
+        dc = DeviceConv(cs, "random")
+    try:
+        assert dc.plan(IMPLICIT).needs_reorder == 1 or layout == "nhwc"
+    finally:
+        dc.close()
+    _check(cs, IMPLICIT, "random", "nhwc")
+    _check(cs.with_(y_dtype="f32"), IMPLICIT, "integer", "nhwc")
+
+
 EDGE_ALGOS = [("implicit", IMPLICIT, None, None), ("implicit-gemm", IMPLICIT, "0", None),
               ("implicit-slice4", IMPLICIT, "1", "4"), ("implicit-slice8", IMPLICIT, "1", "8"),
+              ("implicit-nhwc", IMPLICIT, "nhwc", None),
               ("im2col", IM2COL, None, None), ("direct", DIRECT, None, None)]
 
 
