@@ -127,11 +127,14 @@ typedef struct {
     int32_t algo;             /* resolved algorithm (never AUTO) */
     int32_t tile_m, tile_n;   /* GEMM block tile (output channels x output pixels); 0 for DIRECT */
     int32_t kred, kred_pad;   /* reduction length (C/g)*R*S and its padded length */
-    int64_t workspace_bytes;  /* device workspace this algorithm uses per chunk */
+    int64_t workspace_bytes;  /* device workspace this algorithm uses per chunk (explicit) or for the
+                                 split reduction's partial sums (implicit) */
     int64_t chunks;           /* explicit path: number of pack/GEMM/unpack chunks */
     int32_t needs_reorder;    /* 1 when pre/post layout reorders run (NHWC through an NCHW kernel) */
     int32_t op_class;         /* bit 0 pointwise, 1 grouped, 2 depthwise, 3 dilated, 4 rectangular, 5 strided */
     int32_t kernel;           /* microkernel that runs: CONV2D_KERNEL_* */
+    int32_t ksplit;           /* implicit GEMM: reduction split into this many parts (1 = none);
+                                 the parts' fp32 partial sums are added by the unpack phase */
 } conv2d_plan_info;
 
 /* Validate params, compute the output size, classify the operation and plan

@@ -88,7 +88,8 @@ class conv2d_plan_info(ctypes.Structure):
     _fields_ = [("algo", ctypes.c_int32), ("tile_m", ctypes.c_int32), ("tile_n", ctypes.c_int32),
                 ("kred", ctypes.c_int32), ("kred_pad", ctypes.c_int32),
                 ("workspace_bytes", ctypes.c_int64), ("chunks", ctypes.c_int64),
-                ("needs_reorder", ctypes.c_int32), ("op_class", ctypes.c_int32), ("kernel", ctypes.c_int32)]
+                ("needs_reorder", ctypes.c_int32), ("op_class", ctypes.c_int32), ("kernel", ctypes.c_int32),
+                ("ksplit", ctypes.c_int32)]
 
 
 _lib = None

@@ -50,6 +50,8 @@ struct GemmPlan {
     int bk = 16;   // reduction rows per stage
     int pf = 1;    // register prefetch distance (fp32 32x32 kernels)
     int nstages = 0;
+    int ksplit = 1;        // split reduction (implicit path): partial sums reduced by the unpack kernel
+    int split_stages = 0;  // stages per split
 };
 
 struct ExplicitPlan {
@@ -167,6 +169,8 @@ struct conv2d_desc {
     int64_t yr_bytes = 0;
     void* wr = nullptr;  // weights in tap-major order for the implicit GEMM
     int64_t wr_bytes = 0;
+    void* sk = nullptr;  // partial sums of the split reduction
+    int64_t sk_bytes = 0;
 
     int timing = CONV2D_TIMING_PHASES;
     double analysis_ms = 0.0;
@@ -234,6 +238,30 @@ void build_ktab(conv2d_desc* d) {
                 e.coff = (int32_t)(c * g.H * g.W + e.roff * g.W + e.soff);
                 e.pad = 0;
             }
+}
+
+// Split reduction for layers with too few output tiles to fill the chip (batch 1, small
+// planes, few channels) and a long reduction: split s of S runs a contiguous range of
+// stages and writes fp32 partial sums, and the unpack kernel adds the S partials in split
+// order (deterministic) with the bias.  Aim for two tiles per CU,
+// keep at least 8 stages per split and the partials under 256 MiB.  CONV2D_KSPLIT forces S.
+void plan_split(conv2d_desc* d) {
+    const Geometry& g = d->g;
+    GemmPlan& gp = d->implicit;
+    gp.ksplit = 1;
+    gp.split_stages = gp.nstages;
+    const int64_t tiles = ceil_div(g.Kg, gp.bm) * ceil_div(g.P, gp.bn) * g.G;
+    int64_t S = 1;
+    if (tiles < 512) S = std::min<int64_t>(ceil_div(512, tiles), gp.nstages / 8);
+    const int64_t force = env_int64("CONV2D_KSPLIT", 0);
+    if (force > 0) S = std::min<int64_t>(force, gp.nstages);
+    const int64_t part_bytes = g.G * g.Kg * g.P * 4;
+    while (S > 1 && S * part_bytes > ((int64_t)256 << 20)) --S;
+    if (S > 256) S = 256;
+    if (S < 2 || g.G * S > 65535) return;
+    const int64_t per = ceil_div(gp.nstages, S);
+    gp.ksplit = (int)ceil_div(gp.nstages, per);  // every split non-empty
+    gp.split_stages = (int)per;
 }
 
 void plan_explicit(conv2d_desc* d) {
@@ -450,10 +478,44 @@ int run_implicit(conv2d_desc* d, const void* x, const void* w, const float* bias
     a.bias = g.has_bias ? bias : nullptr;
     a.y_nstride = g.K * g.Ho * g.Wo;
     a.HoWo = (int32_t)(g.Ho * g.Wo);
-    Scope sc(d, CONV2D_ALGO_IMPLICIT_GEMM, CONV2D_PH_IN_MICROKERNEL, s, ph);
-    CV_TRY(sc.begin());
     const int bsrc = d->implicit_nhwc ? BSRC_NHWC_TAP : d->implicit_tap ? BSRC_IMPLICIT_TAP : BSRC_IMPLICIT_NCHW;
-    CV_HIP(dispatch_gemm(gp, a, bsrc, EPI_NCHW, g.xdt, g.ydt, (int)g.G, s));
+    if (gp.ksplit <= 1) {
+        Scope sc(d, CONV2D_ALGO_IMPLICIT_GEMM, CONV2D_PH_IN_MICROKERNEL, s, ph);
+        CV_TRY(sc.begin());
+        CV_HIP(dispatch_gemm(gp, a, bsrc, EPI_NCHW, g.xdt, g.ydt, (int)g.G, s));
+        return sc.end();
+    }
+    // split reduction: partial sums [split][g][m][p] in fp32, then the unpack kernel adds them
+    const int64_t slice = g.G * g.Kg * g.P;  // elements of one split's partials
+    CV_TRY(ensure_buffer(&d->sk, &d->sk_bytes, gp.ksplit * slice * 4));
+    a.y = d->sk;
+    a.y_bytes = (uint32_t)(gp.ksplit * slice * 4);
+    a.ldc = (int32_t)g.P;
+    a.c_gstride = g.Kg * g.P;
+    a.ksplit = gp.ksplit;
+    a.split_stages = gp.split_stages;
+    a.c_sstride = slice;
+    {
+        Scope sc(d, CONV2D_ALGO_IMPLICIT_GEMM, CONV2D_PH_IN_MICROKERNEL, s, ph);
+        CV_TRY(sc.begin());
+        CV_HIP(dispatch_gemm(gp, a, bsrc, EPI_DENSE, g.xdt, CONV2D_F32, (int)g.G, s));
+        CV_TRY(sc.end());
+    }
+    UnpackArgs u{};
+    u.c = static_cast<const float*>(d->sk);
+    u.y = y;
+    u.y_bytes = (uint32_t)(g.y_elems * elem_size(g.ydt));
+    u.bias = g.has_bias ? bias : nullptr;
+    u.Kg = (int32_t)g.Kg;
+    u.pc = (int32_t)g.P;
+    u.HoWo = (int32_t)(g.Ho * g.Wo);
+    u.p_begin = 0;
+    u.y_nstride = g.K * g.Ho * g.Wo;
+    u.splits = gp.ksplit;
+    u.split_stride = slice;
+    Scope sc(d, CONV2D_ALGO_IMPLICIT_GEMM, CONV2D_PH_IN_UNPACKING, s, ph);
+    CV_TRY(sc.begin());
+    CV_HIP(launch_unpack(u, g.ydt, (int)g.G, s));
     return sc.end();
 }
 
@@ -598,6 +660,7 @@ int conv2d_desc_create(const conv2d_params* params, conv2d_desc** out) {
     }
     d->implicit = choose_tile(g.Kg, g.P, g.G, g.Kred, g.xdt, g.Cg, d->implicit_nhwc);
     d->implicit_tap = g.Cg % d->implicit.bk == 0;
+    plan_split(d);
     {
         // 8 waves (256-pixel tiles) unless an image has at most 128 output pixels;
         // CONV2D_SLICE_WAVES = 4 or 8 overrides for tests and tuning
@@ -641,6 +704,7 @@ int conv2d_desc_destroy(conv2d_desc* d) {
     if (d->ktab_dev) hipFree(d->ktab_dev);
     if (d->ws) hipFree(d->ws);
     if (d->xr) hipFree(d->xr);
+    if (d->sk) hipFree(d->sk);
     if (d->yr) hipFree(d->yr);
     if (d->wr) hipFree(d->wr);
     delete d;
@@ -737,7 +801,8 @@ int conv2d_breakdown(conv2d_desc* d, int algo, conv2d_breakdown_t* out) {
     out->ms[CONV2D_PH_PRE_ANALYSIS] = d->analysis_ms;
     out->calls[CONV2D_PH_PRE_ANALYSIS] = 1;
     if (algo == CONV2D_ALGO_IMPLICIT_GEMM)
-        out->fused_mask = (1u << CONV2D_PH_IN_TILING) | (1u << CONV2D_PH_IN_PACKING) | (1u << CONV2D_PH_IN_UNPACKING);
+        out->fused_mask = (1u << CONV2D_PH_IN_TILING) | (1u << CONV2D_PH_IN_PACKING) |
+                          (d->implicit.ksplit > 1 && !d->implicit_slice ? 0u : (1u << CONV2D_PH_IN_UNPACKING));
     else if (algo == CONV2D_ALGO_IM2COL_GEMM)
         out->fused_mask = (1u << CONV2D_PH_IN_TILING);
     else
@@ -791,11 +856,15 @@ int conv2d_plan_query(const conv2d_desc* d, int algo, conv2d_plan_info* out) {
         out->tile_m = d->implicit.bm;
         out->tile_n = d->implicit.bn;
         out->kernel = CONV2D_KERNEL_GEMM;
+        out->ksplit = d->implicit.ksplit;
+        if (d->implicit.ksplit > 1) out->workspace_bytes = d->implicit.ksplit * g.G * g.Kg * g.P * 4;
         if (d->implicit_slice) {
             out->tile_m = 64;
             out->tile_n = 32 * d->slice.nw;
             out->kred_pad = 2 * d->slice.kh;
             out->kernel = CONV2D_KERNEL_SLICE;
+            out->ksplit = 1;
+            out->workspace_bytes = 0;
         }
         if (!d->implicit_ok) return CONV2D_E_UNSUPPORTED;
     } else if (algo == CONV2D_ALGO_IM2COL_GEMM) {

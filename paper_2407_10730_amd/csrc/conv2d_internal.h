@@ -72,6 +72,11 @@ struct GemmArgs {
     int32_t ldc;
     int64_t c_gstride;
     int32_t p_offset;     // global index of column 0 (explicit chunks)
+    // split reduction: blockIdx.z = group * ksplit + split; split s runs stages
+    // [s*split_stages, min((s+1)*split_stages, nstages)) and writes its partial result (dense
+    // epilogue) at offset s*c_sstride.  ksplit 0 or 1: no split.
+    int32_t ksplit, split_stages;
+    int64_t c_sstride;
 };
 
 // 32x32-MFMA kernels.  fp32: stage depth bk in {16, 32}, register prefetch distance pf in {1, 2};
@@ -94,7 +99,8 @@ struct Im2colArgs {
 };
 hipError_t launch_im2col(const Im2colArgs& a, int xdt, int groups, hipStream_t stream);
 
-// unpack C[g][m][pl] (fp32) to NCHW y (+bias, cast).
+// unpack C[g][m][pl] (fp32) to NCHW y (+bias, cast).  With splits > 1 the value is the sum,
+// in split order, of C + s*split_stride over s < splits (a split reduction's partials).
 struct UnpackArgs {
     const float* c;
     void* y;
@@ -103,6 +109,8 @@ struct UnpackArgs {
     int32_t Kg, pc, HoWo;
     int64_t p_begin;
     int64_t y_nstride;
+    int32_t splits;
+    int64_t split_stride;
 };
 hipError_t launch_unpack(const UnpackArgs& a, int ydt, int groups, hipStream_t stream);
 

@@ -26,7 +26,7 @@ namespace cv {
 // before its first store, so the stores leave back to back behind one wait (a load
 // between two stores would make each store wait for the previous one).
 template <int TM, int TN, int EPI, typename TOut>
-__device__ __forceinline__ void store_tile(const GemmArgs& A, f32x16 (&acc)[TM][TN], int gi, int mb, int pb,
+__device__ __forceinline__ void store_tile(const GemmArgs& A, f32x16 (&acc)[TM][TN], int gi, int sp, int mb, int pb,
                                            int lrow, int lcol) {
     if (EPI == EPI_NCHW && A.bias != nullptr) {
         const __amdgpu_buffer_rsrc_t rbias = make_rsrc(A.bias, (uint32_t)(gridDim.z * A.M * 4));
@@ -51,7 +51,7 @@ __device__ __forceinline__ void store_tile(const GemmArgs& A, f32x16 (&acc)[TM][
             const int hw = p - n_img * A.HoWo;
             ybase = (int64_t)n_img * A.y_nstride + (int64_t)gi * A.M * A.HoWo + hw;
         } else {
-            ybase = (int64_t)gi * A.c_gstride + p;
+            ybase = (int64_t)sp * A.c_sstride + (int64_t)gi * A.c_gstride + p;
         }
 #pragma unroll
         for (int i = 0; i < TM; ++i)
@@ -102,7 +102,12 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs A) {
     const int t = threadIdx.x;
     const int lane = t & 63;
     const int wave = t >> 6;
-    const int gi = blockIdx.z;
+    const int ksplit = A.ksplit > 1 ? A.ksplit : 1;
+    const int gi = blockIdx.z / ksplit;
+    const int sp = blockIdx.z - gi * ksplit;
+    // this block's stages [s_begin, s_end)
+    const int s_begin = ksplit > 1 ? sp * A.split_stages : 0;
+    const int s_end = ksplit > 1 ? min(s_begin + A.split_stages, A.nstages) : A.nstages;
 
     const int tile = xcd_remap(blockIdx.x, gridDim.x);
     const int tile_p = tile / A.grid_m;
@@ -133,6 +138,12 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs A) {
     // taps innermost: the taps of one channel block re-read the same input lines,
     // which then hit in L1.
     int cur_c0 = 0, cur_r = 0, cur_s = 0;
+    if constexpr (BSRC == BSRC_IMPLICIT_TAP) {
+        const int tap = s_begin % A.RS;
+        cur_c0 = (s_begin / A.RS) * BK;
+        cur_r = tap / A.S;
+        cur_s = tap - cur_r * A.S;
+    }
 
     auto load_stage = [&](int stage, f32x4 (&breg)[BRUNS][BCOLS], f32x4 (&areg)[ARUNS]) {
         const int k0 = stage * BK;
@@ -258,40 +269,41 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs A) {
                                                                      acc[i][j], 0, 0, 0);
     };
 
-    const int n = A.nstages;
+    // stages s_begin + j, j < n; LDS buffer j & 1
+    const int n = s_end - s_begin;
     if constexpr (PF == 1) {
-        load_stage(0, breg0, areg0);
+        load_stage(s_begin, breg0, areg0);
         store_stage(0, breg0, areg0);
         __syncthreads();
-        for (int st = 0; st < n; ++st) {
-            const int buf = st & 1;
-            const bool more = st + 1 < n;
-            if (more) load_stage(st + 1, breg0, areg0);
+        for (int j = 0; j < n; ++j) {
+            const int buf = j & 1;
+            const bool more = j + 1 < n;
+            if (more) load_stage(s_begin + j + 1, breg0, areg0);
             compute(buf);
             if (more) store_stage(buf ^ 1, breg0, areg0);
             __syncthreads();
         }
     } else {
-        load_stage(0, breg0, areg0);
-        if (n > 1) load_stage(1, breg1, areg1);
+        load_stage(s_begin, breg0, areg0);
+        if (n > 1) load_stage(s_begin + 1, breg1, areg1);
         store_stage(0, breg0, areg0);
         __syncthreads();
-        for (int st = 0; st < n; st += 2) {
-            // even stage: set 0 is free, set 1 holds stage st+1
-            if (st + 2 < n) load_stage(st + 2, breg0, areg0);
+        for (int j = 0; j < n; j += 2) {
+            // even stage: set 0 is free, set 1 holds stage j+1
+            if (j + 2 < n) load_stage(s_begin + j + 2, breg0, areg0);
             compute(0);
-            if (st + 1 < n) store_stage(1, breg1, areg1);
+            if (j + 1 < n) store_stage(1, breg1, areg1);
             __syncthreads();
-            if (st + 1 >= n) break;
-            // odd stage: set 1 is free, set 0 holds stage st+2
-            if (st + 3 < n) load_stage(st + 3, breg1, areg1);
+            if (j + 1 >= n) break;
+            // odd stage: set 1 is free, set 0 holds stage j+2
+            if (j + 3 < n) load_stage(s_begin + j + 3, breg1, areg1);
             compute(1);
-            if (st + 2 < n) store_stage(0, breg0, areg0);
+            if (j + 2 < n) store_stage(0, breg0, areg0);
             __syncthreads();
         }
     }
 
-    store_tile<TM, TN, EPI, TOut>(A, acc, gi, m0 + wm0, p0 + wn0, lrow, lcol);
+    store_tile<TM, TN, EPI, TOut>(A, acc, gi, sp, m0 + wm0, p0 + wn0, lrow, lcol);
 }
 
 // ============================================================================ bf16
@@ -345,7 +357,12 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs A) {
     const int t = threadIdx.x;
     const int lane = t & 63;
     const int wave = t >> 6;
-    const int gi = blockIdx.z;
+    const int ksplit = A.ksplit > 1 ? A.ksplit : 1;
+    const int gi = blockIdx.z / ksplit;
+    const int sp = blockIdx.z - gi * ksplit;
+    // this block's stages [s_begin, s_end)
+    const int s_begin = ksplit > 1 ? sp * A.split_stages : 0;
+    const int s_end = ksplit > 1 ? min(s_begin + A.split_stages, A.nstages) : A.nstages;
 
     const int tile = xcd_remap(blockIdx.x, gridDim.x);
     const int tile_p = tile / A.grid_m;
@@ -376,6 +393,13 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs A) {
     u32x4 breg[BUNITS];
     u32x4 areg[AUNITS];
     int cur_c0 = 0, cur_r = 0, cur_s = 0;  // tap-major cursor of the next stage
+    if constexpr (BSRC == BSRC_IMPLICIT_TAP || BSRC == BSRC_NHWC_TAP) {
+        const int cblocks = A.Cg / BK;
+        const int tap = s_begin / cblocks;
+        cur_c0 = (s_begin - tap * cblocks) * BK;
+        cur_r = tap / A.S;
+        cur_s = tap - cur_r * A.S;
+    }
 
     auto load_weights_tap = [&]() {
         // weights in tap-major order [K][R*S][C/g]: 8 consecutive channels per 16-byte load
@@ -500,12 +524,12 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs A) {
     const int lrow = lane >> 5;
     const int lcol = lane & 31;
 
-    load_stage(0);
+    load_stage(s_begin);
     store_stage(0);
     __syncthreads();
-    for (int st = 0; st < A.nstages; ++st) {
-        const int buf = st & 1;
-        const bool more = st + 1 < A.nstages;
+    for (int st = s_begin; st < s_end; ++st) {
+        const int buf = (st - s_begin) & 1;
+        const bool more = st + 1 < s_end;
         if (more) load_stage(st + 1);
 #pragma unroll
         for (int ks = 0; ks < BK / 16; ++ks) {
@@ -526,18 +550,21 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs A) {
         __syncthreads();
     }
 
-    store_tile<TM, TN, EPI, TOut>(A, acc, gi, m0 + wm0, p0 + wn0, lrow, lcol);
+    store_tile<TM, TN, EPI, TOut>(A, acc, gi, sp, m0 + wm0, p0 + wn0, lrow, lcol);
 }
 
 // ============================================================================ dispatch
 template <int BM, int BN, int WM, int WN, int BK, int PF>
 static hipError_t launch_f32(const GemmArgs& a, int bsrc, int epi, int groups, hipStream_t stream) {
-    dim3 grid((unsigned)(a.grid_p * a.grid_m), 1, (unsigned)groups);
+    dim3 grid((unsigned)(a.grid_p * a.grid_m), 1, (unsigned)(groups * (a.ksplit > 1 ? a.ksplit : 1)));
 #define CV_F32(BS, EP) \
     hipLaunchKernelGGL((gemm_f32_kernel<BM, BN, WM, WN, BK, PF, BS, EP, float>), grid, dim3(256), 0, stream, a)
     if (bsrc == BSRC_IMPLICIT_NCHW && epi == EPI_NCHW) CV_F32(BSRC_IMPLICIT_NCHW, EPI_NCHW);
     else if (bsrc == BSRC_IMPLICIT_TAP && epi == EPI_NCHW) CV_F32(BSRC_IMPLICIT_TAP, EPI_NCHW);
     else if (bsrc == BSRC_DENSE && epi == EPI_DENSE) CV_F32(BSRC_DENSE, EPI_DENSE);
+    // partial sums of a split reduction
+    else if (bsrc == BSRC_IMPLICIT_NCHW && epi == EPI_DENSE) CV_F32(BSRC_IMPLICIT_NCHW, EPI_DENSE);
+    else if (bsrc == BSRC_IMPLICIT_TAP && epi == EPI_DENSE) CV_F32(BSRC_IMPLICIT_TAP, EPI_DENSE);
     else return hipErrorInvalidValue;
 #undef CV_F32
     return hipGetLastError();
@@ -545,12 +572,14 @@ static hipError_t launch_f32(const GemmArgs& a, int bsrc, int epi, int groups, h
 
 template <int BM, int BN, int WM, int WN, int BK>
 static hipError_t launch_bf16(const GemmArgs& a, int bsrc, int epi, int ydt, int groups, hipStream_t stream) {
-    dim3 grid((unsigned)(a.grid_p * a.grid_m), 1, (unsigned)groups);
+    dim3 grid((unsigned)(a.grid_p * a.grid_m), 1, (unsigned)(groups * (a.ksplit > 1 ? a.ksplit : 1)));
 #define CV_BF(BS, EP, TO) \
     hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, BK, BS, EP, TO>), grid, dim3(256), 0, stream, a)
     if (bsrc == BSRC_NHWC_TAP && epi == EPI_NCHW) {
         if (ydt == CONV2D_BF16) CV_BF(BSRC_NHWC_TAP, EPI_NCHW, uint16_t);
         else CV_BF(BSRC_NHWC_TAP, EPI_NCHW, float);
+    } else if (bsrc == BSRC_NHWC_TAP && epi == EPI_DENSE) {
+        CV_BF(BSRC_NHWC_TAP, EPI_DENSE, float);  // partial sums of a split reduction
     } else if (BK != 32) {
         return hipErrorInvalidValue;  // the NCHW gathers and the dense source use 32-row stages
     } else if (bsrc == BSRC_IMPLICIT_NCHW && epi == EPI_NCHW) {
@@ -561,6 +590,10 @@ static hipError_t launch_bf16(const GemmArgs& a, int bsrc, int epi, int ydt, int
         else CV_BF(BSRC_IMPLICIT_TAP, EPI_NCHW, float);
     } else if (bsrc == BSRC_DENSE && epi == EPI_DENSE) {
         CV_BF(BSRC_DENSE, EPI_DENSE, float);
+    } else if (bsrc == BSRC_IMPLICIT_NCHW && epi == EPI_DENSE) {
+        CV_BF(BSRC_IMPLICIT_NCHW, EPI_DENSE, float);  // partial sums of a split reduction
+    } else if (bsrc == BSRC_IMPLICIT_TAP && epi == EPI_DENSE) {
+        CV_BF(BSRC_IMPLICIT_TAP, EPI_DENSE, float);
     } else {
         return hipErrorInvalidValue;
     }

@@ -129,6 +129,7 @@ hipError_t launch_im2col(const Im2colArgs& a, int xdt, int groups, hipStream_t s
 // 16-byte load and one 16-byte (fp32) or 8-byte (bf16) store.
 template <bool BF16OUT>
 __global__ __launch_bounds__(256) void unpack_kernel(UnpackArgs A) {
+    typedef float f32x4 __attribute__((ext_vector_type(4)));
     const int pl0 = (blockIdx.x * 256 + threadIdx.x) * 4;
     const int m = blockIdx.y;
     const int gi = blockIdx.z;
@@ -136,15 +137,17 @@ __global__ __launch_bounds__(256) void unpack_kernel(UnpackArgs A) {
     const int ch = gi * A.Kg + m;
     const float bias = A.bias ? A.bias[ch] : 0.0f;
     const float* crow = A.c + ((int64_t)gi * A.Kg + m) * A.pc;
+    const int splits = A.splits > 1 ? A.splits : 1;
     const __amdgpu_buffer_rsrc_t ry = pk_rsrc(A.y, A.y_bytes);
     const int64_t p = A.p_begin + pl0;
     const int64_t n = p / A.HoWo;
     const int64_t hw = p - n * A.HoWo;
     const int64_t off = n * A.y_nstride + (int64_t)ch * A.HoWo + hw;
-    const bool vec = ((A.HoWo & 3) == 0) & ((A.pc & 3) == 0) & ((A.p_begin & 3) == 0) & (pl0 + 4 <= A.pc);
+    const bool vec = ((A.HoWo & 3) == 0) & ((A.pc & 3) == 0) & ((A.p_begin & 3) == 0) & (pl0 + 4 <= A.pc) &
+                     ((A.split_stride & 3) == 0);
     if (vec) {
-        typedef float f32x4 __attribute__((ext_vector_type(4)));
-        const f32x4 c = *reinterpret_cast<const f32x4*>(crow + pl0);
+        f32x4 c = *reinterpret_cast<const f32x4*>(crow + pl0);
+        for (int sp = 1; sp < splits; ++sp) c += *reinterpret_cast<const f32x4*>(crow + sp * A.split_stride + pl0);
         if (BF16OUT) {
             typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
             const u32x2 q = {(uint32_t)pk_f32_to_bf16(c[0] + bias) | ((uint32_t)pk_f32_to_bf16(c[1] + bias) << 16),
@@ -162,7 +165,9 @@ __global__ __launch_bounds__(256) void unpack_kernel(UnpackArgs A) {
         const int64_t pj = p + j;
         const int64_t nj = pj / A.HoWo;
         const int64_t o = nj * A.y_nstride + (int64_t)ch * A.HoWo + (pj - nj * A.HoWo);
-        const float v = crow[pl0 + j] + bias;
+        float c = crow[pl0 + j];
+        for (int sp = 1; sp < splits; ++sp) c += crow[sp * A.split_stride + pl0 + j];
+        const float v = c + bias;
         if (BF16OUT)
             __builtin_amdgcn_raw_buffer_store_b16(pk_f32_to_bf16(v), ry, (uint32_t)(o * 2), 0, 0);
         else

@@ -155,6 +155,23 @@ def test_implicit_microkernel_choice(monkeypatch):
     B.conv2d_desc_destroy(d)
 
 
+def test_split_reduction_plan(monkeypatch):
+    """Few output tiles and a long reduction: the implicit path splits the reduction."""
+    monkeypatch.delenv("CONV2D_KSPLIT", raising=False)
+    def plan(cs):
+        d = B.conv2d_desc_create(params_for(cs))
+        try:
+            return B.conv2d_plan_query(d, B.CONV2D_ALGO_IMPLICIT_GEMM)
+        finally:
+            B.conv2d_desc_destroy(d)
+    small = datagen.CONFIGS["cfg2"].with_(n=1, c=512, h=7, w=7, k=256)   # 4 tiles, 4608-long reduction
+    info = plan(small)
+    assert info.ksplit > 1 and info.workspace_bytes == info.ksplit * 256 * 49 * 4
+    assert plan(datagen.CONFIGS["cfg2"]).ksplit == 1                    # 1568 tiles
+    monkeypatch.setenv("CONV2D_KSPLIT", "3")
+    assert plan(datagen.CONFIGS["cfg2"]).ksplit == 3
+
+
 def test_explicit_workspace_chunking(monkeypatch):
     cs = datagen.CONFIGS["cfg4"]
     d = B.conv2d_desc_create(params_for(cs))

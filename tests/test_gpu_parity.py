@@ -208,6 +208,45 @@ def test_bf16_nhwc_gather(idx, layout):
     _check(cs.with_(y_dtype="f32"), IMPLICIT, "integer", "nhwc")
 
 
+# split reductions: layers with few output tiles and long reductions (the planner splits
+# them), and forced splits through every gather; partial sums are added in split order
+SPLIT = [
+    (_shape(1, 512, 7, 7, 256, 3, 3, pd=(1, 1), seed=230), None),
+    (_shape(2, 96, 5, 6, 40, 3, 3, pd=(1, 1), seed=231), "5"),
+    (_shape(1, 37, 9, 9, 33, 5, 3, st=(2, 1), pd=(2, 1), seed=232), "3"),
+    (_shape(1, 64, 12, 12, 70, 3, 3, pd=(2, 2), dl=(2, 2), g=2, seed=233), "4"),
+]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16", "bf16-nhwc"])
+@pytest.mark.parametrize("idx", range(len(SPLIT)))
+def test_split_reduction(idx, dt):
+    base, force = SPLIT[idx]
+    cs = base.with_(x_dtype="f32" if dt == "f32" else "bf16", y_dtype="f32" if dt == "f32" else "bf16")
+    env = {"CONV2D_KSPLIT": force} if force else {}
+    kernel = "nhwc" if dt == "bf16-nhwc" else "0"
+    old = {k: os.environ.get(k) for k in env}
+    os.environ.update(env)
+    try:
+        with _Kernel(kernel):
+            dc = DeviceConv(cs, "random")
+        try:
+            plan = dc.plan(IMPLICIT)
+        finally:
+            dc.close()
+        if dt == "bf16-nhwc" and (cs.c // cs.groups) % 32:
+            pytest.skip("the NHWC gather needs C/g a multiple of 32")
+        assert plan.ksplit > 1, plan.ksplit
+        _check(cs, IMPLICIT, "random", kernel)
+        _check(cs.with_(y_dtype="f32"), IMPLICIT, "integer", kernel)
+    finally:
+        for k, v in old.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+
+
 EDGE_ALGOS = [("implicit", IMPLICIT, None, None), ("implicit-gemm", IMPLICIT, "0", None),
               ("implicit-slice4", IMPLICIT, "1", "4"), ("implicit-slice8", IMPLICIT, "1", "8"),
               ("implicit-nhwc", IMPLICIT, "nhwc", None),
