@@ -137,12 +137,18 @@ struct DwPlan {
 // One block per work item (a group of PB planes x a band of TH output rows).  The input
 // tile lives in dynamic LDS sized to the item, so many blocks fit on a CU and their tile
 // loads overlap (the kernel is bound by HBM bandwidth, which needs many bytes in flight).
-constexpr int DWP_TILE = 4096;                           // max floats of one tile (16 KiB)
-constexpr int DWP_VMAX = DWP_TILE / 4 / DIRECT_THREADS;  // 16-byte loads per thread
-constexpr int DWP_SMAX = DWP_TILE / DIRECT_THREADS;      // 4-byte loads per thread
+// TILEF is the tile capacity in floats: 4096 (16 KiB) when a plane fits, 8192 (32 KiB) for
+// tall planes cut into bands, where a larger band re-reads fewer halo rows.
+constexpr int DWP_TILE_SMALL = 4096;
+constexpr int DWP_TILE_LARGE = 8192;
 
-template <int R, int S, int ST, int DL, typename TX, typename TY>
+template <int R, int S, int ST, int DL, int TILEF, typename TX, typename TY>
 __global__ __launch_bounds__(DIRECT_THREADS) void dw_kernel(DirectArgs A, DwPlan P) {
+    constexpr int DWP_VMAX = TILEF / 4 / DIRECT_THREADS;  // 16-byte loads per thread
+    constexpr int DWP_SMAX = TILEF / DIRECT_THREADS;      // 4-byte loads per thread
+    // With stride 2 and an even dilation (or a 1x1 filter) every window reads only the even
+    // rows of the tile; the odd ones are neither loaded nor read.
+    constexpr bool EVEN_ROWS = ST == 2 && (DL % 2 == 0 || R == 1);
     extern __shared__ __attribute__((aligned(16))) float tile[];  // PB * IR * LDW floats
     __shared__ float wsh[DW_MAX_PLANES * R * S];
     __shared__ float bsh[DW_MAX_PLANES];
@@ -205,7 +211,8 @@ __global__ __launch_bounds__(DIRECT_THREADS) void dw_kernel(DirectArgs A, DwPlan
                 const int e = t + u * DIRECT_THREADS;
                 const int hi = hi_base + tr;
                 const int w0 = 4 * cg - P.LPAD;
-                const bool ok = (e < total) & ((unsigned)hi < (unsigned)A.H) & ((unsigned)w0 < (unsigned)A.W);
+                const bool ok = (e < total) & ((unsigned)hi < (unsigned)A.H) & ((unsigned)w0 < (unsigned)A.W) &
+                                !(EVEN_ROWS && (tr & 1));
                 const int32_t idx = ok ? pbase[lp] + hi * A.W + w0 : 0;
                 if constexpr (sizeof(TX) == 4) {
                     vreg[u] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
@@ -231,7 +238,8 @@ __global__ __launch_bounds__(DIRECT_THREADS) void dw_kernel(DirectArgs A, DwPlan
                 const int e = t + u * DIRECT_THREADS;
                 const int hi = hi_base + tr;
                 const int w = cg - P.LPAD;
-                const bool ok = (e < total) & ((unsigned)hi < (unsigned)A.H) & ((unsigned)w < (unsigned)A.W);
+                const bool ok = (e < total) & ((unsigned)hi < (unsigned)A.H) & ((unsigned)w < (unsigned)A.W) &
+                                !(EVEN_ROWS && (tr & 1));
                 sreg[u] = dk_load(rx, ok, ok ? pbase[lp] + hi * A.W + w : 0, (TX*)nullptr);
                 step();
             }
@@ -244,67 +252,97 @@ __global__ __launch_bounds__(DIRECT_THREADS) void dw_kernel(DirectArgs A, DwPlan
     }
     __syncthreads();
 
-    // outputs: each thread computes a vertical strip of VR outputs of one column (consecutive
-    // lanes on consecutive columns, so LDS reads hit consecutive banks); the NR x S input
-    // values under the strip are read once and shared by its VR outputs.
-    constexpr int VR = 4;
+    // outputs: each thread computes a block of VR rows x HC columns.  It walks the NR input
+    // rows under the block once; each row's RB values are read from LDS once and feed every
+    // output row whose window contains it (which rows those are is known at compile time),
+    // so a 3x3 stride-1 block reads 2.25 LDS values per output instead of 9.  Consecutive
+    // lanes take consecutive column blocks; with Wo % 4 == 0 a row of the block is stored
+    // with one 16-byte (fp32) or 8-byte (bf16) store.
+    // HC shrinks for large filters, whose NR x RB input window would not fit the registers
+    constexpr int VR = 4, HC = R <= 3 ? 4 : (R == 5 ? 2 : 1);
     constexpr int NR = (VR - 1) * ST + (R - 1) * DL + 1;
+    constexpr int RB = (HC - 1) * ST + (S - 1) * DL + 1;
     auto compute = [&](auto uniform_w) {
         constexpr bool UW = decltype(uniform_w)::value;
         const int nrb = (nrows + VR - 1) / VR;
-        const int per_plane = nrb * A.Wo;
-        const int strips = npl * per_plane;
-        const int st_a = DIRECT_THREADS / per_plane;
-        const int st_r = DIRECT_THREADS - st_a * per_plane;
-        const int st_b = st_r / A.Wo, st_c = st_r - st_b * A.Wo;
-        int lp = t / per_plane;
-        int rb = (t - lp * per_plane) / A.Wo;
-        int ow = t - lp * per_plane - rb * A.Wo;
+        const int ncb = (A.Wo + HC - 1) / HC;
+        const int per_plane = nrb * ncb;
+        const int items = npl * per_plane;
+        const bool vec = HC == 4 && (A.Wo & 3) == 0;
         float wreg[R * S];
         if constexpr (UW) {
 #pragma unroll
             for (int i = 0; i < R * S; ++i) wreg[i] = wsh[i];
         }
-        for (int q = t; q < strips; q += DIRECT_THREADS) {
+        for (int q = t; q < items; q += DIRECT_THREADS) {
+            const int lp = q / per_plane;
+            const int rem = q - lp * per_plane;
+            const int rb = rem / ncb;
+            const int cb = rem - rb * ncb;
             if constexpr (!UW) {
 #pragma unroll
                 for (int i = 0; i < R * S; ++i) wreg[i] = wsh[lp * R * S + i];
             }
             const float bias = bsh[lp];
             const int orow0 = rb * VR;
-            const float* rp = &tile[(lp * P.IR + orow0 * ST) * P.LDW + P.LPAD - A.pw + ow * ST];
-            float xv[NR][S];
+            const int ow0 = cb * HC;
+            const float* rp = &tile[(lp * P.IR + orow0 * ST) * P.LDW + P.LPAD - A.pw + ow0 * ST];
+            float acc[VR][HC];
 #pragma unroll
-            for (int rr = 0; rr < NR; ++rr)
+            for (int v = 0; v < VR; ++v)
 #pragma unroll
-                for (int sx = 0; sx < S; ++sx) xv[rr][sx] = rp[rr * P.LDW + sx * DL];
-            const int64_t o0 = ((int64_t)(pl0 + lp) * A.Ho + oh0 + orow0) * A.Wo + ow;
+                for (int h = 0; h < HC; ++h) acc[v][h] = bias;
+#pragma unroll
+            for (int rr = 0; rr < NR; ++rr) {
+                float xrow[RB];
+#pragma unroll
+                for (int c = 0; c < RB; ++c) xrow[c] = rp[rr * P.LDW + c];
+#pragma unroll
+                for (int v = 0; v < VR; ++v) {
+                    // input row rr is filter row r of output row v when rr = v*ST + r*DL
+                    const int d = rr - v * ST;
+                    if (d < 0 || d % DL != 0 || d / DL >= R) continue;  // resolved at compile time
+                    const int r = d / DL;
+#pragma unroll
+                    for (int h = 0; h < HC; ++h)
+#pragma unroll
+                        for (int sx = 0; sx < S; ++sx)
+                            acc[v][h] = __builtin_fmaf(xrow[h * ST + sx * DL], wreg[r * S + sx], acc[v][h]);
+                }
+            }
+            const int64_t o0 = ((int64_t)(pl0 + lp) * A.Ho + oh0 + orow0) * A.Wo + ow0;
 #pragma unroll
             for (int v = 0; v < VR; ++v) {
-                float acc = bias;
-#pragma unroll
-                for (int r = 0; r < R; ++r)
-#pragma unroll
-                    for (int sx = 0; sx < S; ++sx) acc = __builtin_fmaf(xv[v * ST + r * DL][sx], wreg[r * S + sx], acc);
-                const bool ok = orow0 + v < nrows;
+                const bool rok = orow0 + v < nrows;
                 const int64_t o = o0 + (int64_t)v * A.Wo;
-                if constexpr (sizeof(TY) == 4)
-                    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, acc), ry,
-                                                          ok ? (uint32_t)(o * 4) : OOB_OFF, 0, 0);
-                else
-                    __builtin_amdgcn_raw_buffer_store_b16(dk_f32_to_bf16(acc), ry, ok ? (uint32_t)(o * 2) : OOB_OFF,
-                                                          0, 0);
-            }
-            ow += st_c;
-            rb += st_b;
-            lp += st_a;
-            if (ow >= A.Wo) {
-                ow -= A.Wo;
-                ++rb;
-            }
-            if (rb >= nrb) {
-                rb -= nrb;
-                ++lp;
+                bool done = false;
+                if constexpr (HC == 4) {
+                    if (vec) {
+                        if constexpr (sizeof(TY) == 4) {
+                            const u32x4_t val = {__builtin_bit_cast(uint32_t, acc[v][0]), __builtin_bit_cast(uint32_t, acc[v][1]),
+                                                 __builtin_bit_cast(uint32_t, acc[v][2]), __builtin_bit_cast(uint32_t, acc[v][3])};
+                            __builtin_amdgcn_raw_buffer_store_b128(val, ry, rok ? (uint32_t)(o * 4) : OOB_OFF, 0, 0);
+                        } else {
+                            typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+                            const u32x2 val = {(uint32_t)dk_f32_to_bf16(acc[v][0]) | ((uint32_t)dk_f32_to_bf16(acc[v][1]) << 16),
+                                               (uint32_t)dk_f32_to_bf16(acc[v][2]) | ((uint32_t)dk_f32_to_bf16(acc[v][3]) << 16)};
+                            __builtin_amdgcn_raw_buffer_store_b64(val, ry, rok ? (uint32_t)(o * 2) : OOB_OFF, 0, 0);
+                        }
+                        done = true;
+                    }
+                }
+                if (!done) {
+#pragma unroll
+                    for (int h = 0; h < HC; ++h) {
+                        const bool ok = rok & (ow0 + h < A.Wo);
+                        if constexpr (sizeof(TY) == 4)
+                            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, acc[v][h]), ry,
+                                                                  ok ? (uint32_t)((o + h) * 4) : OOB_OFF, 0, 0);
+                        else
+                            __builtin_amdgcn_raw_buffer_store_b16(dk_f32_to_bf16(acc[v][h]), ry,
+                                                                  ok ? (uint32_t)((o + h) * 2) : OOB_OFF, 0, 0);
+                    }
+                }
             }
         }
     };
@@ -313,10 +351,11 @@ __global__ __launch_bounds__(DIRECT_THREADS) void dw_kernel(DirectArgs A, DwPlan
 }
 
 // Host plan of the depthwise kernel; returns false when the shape needs the generic kernel.
-static bool dw_plan(const DirectArgs& a, int sw_t, int dw_t, DwPlan* p) {
+static bool dw_plan(const DirectArgs& a, int sw_t, int dw_t, int tilef, DwPlan* p) {
     const int WS = (a.Wo + 3) / 4;
     const int LPAD = (a.pw + 3) / 4 * 4;
-    const int maxcol = LPAD - a.pw + (a.Wo - 1) * sw_t + (a.S - 1) * dw_t;
+    // columns read by the last block of 4 outputs (ragged blocks read past Wo - 1)
+    const int maxcol = LPAD - a.pw + (WS * 4 - 1) * sw_t + (a.S - 1) * dw_t;
     int LDW = (maxcol + 1 + 3) / 4 * 4;
     if (LDW < LPAD + a.W) LDW = (LPAD + a.W + 3) / 4 * 4;
     // rows of the tile: TH output rows rounded up to whole strips of 4
@@ -327,15 +366,15 @@ static bool dw_plan(const DirectArgs& a, int sw_t, int dw_t, DwPlan* p) {
         PB = 1024 / (a.Ho * WS);
         if (PB < 1) PB = 1;
         if (PB > DW_MAX_PLANES) PB = DW_MAX_PLANES;
-        while (PB > 1 && PB * ir(TH) * LDW > DWP_TILE) --PB;
+        while (PB > 1 && PB * ir(TH) * LDW > tilef) --PB;
     } else {
         PB = 1;
         TH = 1024 / WS;
         if (TH < 1) TH = 1;
         if (TH > a.Ho) TH = a.Ho;
     }
-    while (TH > 1 && PB * ir(TH) * LDW > DWP_TILE) --TH;
-    if (PB * ir(TH) * LDW > DWP_TILE) return false;
+    while (TH > 1 && PB * ir(TH) * LDW > tilef) --TH;
+    if (PB * ir(TH) * LDW > tilef) return false;
     p->PB = PB;
     p->TH = TH;
     p->IR = ir(TH);
@@ -346,7 +385,7 @@ static bool dw_plan(const DirectArgs& a, int sw_t, int dw_t, DwPlan* p) {
     return true;
 }
 
-template <int R, int S, int ST, int DL>
+template <int R, int S, int ST, int DL, int TILEF>
 static hipError_t launch_dw_t(const DirectArgs& a, const DwPlan& p, int xdt, int ydt, hipStream_t stream) {
     const int64_t planes = (int64_t)a.N * a.K;
     const int64_t nblocks = (planes + p.PB - 1) / p.PB * p.nbands;
@@ -354,11 +393,14 @@ static hipError_t launch_dw_t(const DirectArgs& a, const DwPlan& p, int xdt, int
     dim3 grid((unsigned)nblocks);
     const size_t lds = (size_t)p.PB * p.IR * p.LDW * sizeof(float);
     if (xdt == CONV2D_F32)
-        hipLaunchKernelGGL((dw_kernel<R, S, ST, DL, float, float>), grid, dim3(DIRECT_THREADS), lds, stream, a, p);
+        hipLaunchKernelGGL((dw_kernel<R, S, ST, DL, TILEF, float, float>), grid, dim3(DIRECT_THREADS), lds, stream,
+                           a, p);
     else if (ydt == CONV2D_BF16)
-        hipLaunchKernelGGL((dw_kernel<R, S, ST, DL, uint16_t, uint16_t>), grid, dim3(DIRECT_THREADS), lds, stream, a, p);
+        hipLaunchKernelGGL((dw_kernel<R, S, ST, DL, TILEF, uint16_t, uint16_t>), grid, dim3(DIRECT_THREADS), lds,
+                           stream, a, p);
     else
-        hipLaunchKernelGGL((dw_kernel<R, S, ST, DL, uint16_t, float>), grid, dim3(DIRECT_THREADS), lds, stream, a, p);
+        hipLaunchKernelGGL((dw_kernel<R, S, ST, DL, TILEF, uint16_t, float>), grid, dim3(DIRECT_THREADS), lds,
+                           stream, a, p);
     return hipGetLastError();
 }
 
@@ -368,11 +410,20 @@ static hipError_t try_launch_dw(const DirectArgs& a, int xdt, int ydt, hipStream
     if (a.Cg != 1 || a.R != a.S || (a.sw != 1 && a.sw != 2) || (a.dw != 1 && a.dw != 2)) return hipSuccess;
     if (a.sh != a.sw || a.dh != a.dw) return hipSuccess;
     if (a.R != 1 && a.R != 3 && a.R != 5 && a.R != 7) return hipSuccess;
-    DwPlan p;
-    if (!dw_plan(a, a.sw, a.dw, &p)) return hipSuccess;
+    DwPlan p, pl;
+    bool large = false;
+    if (!dw_plan(a, a.sw, a.dw, DWP_TILE_SMALL, &p)) {
+        if (!dw_plan(a, a.sw, a.dw, DWP_TILE_LARGE, &p)) return hipSuccess;
+        large = true;
+    } else if (p.nbands > 1 && dw_plan(a, a.sw, a.dw, DWP_TILE_LARGE, &pl) && pl.nbands < p.nbands) {
+        p = pl;
+        large = true;
+    }
     *launched = true;
-#define CV_DW(RV, SWV, DWV) \
-    if (a.R == RV && a.sw == SWV && a.dw == DWV) return launch_dw_t<RV, RV, SWV, DWV>(a, p, xdt, ydt, stream);
+#define CV_DW(RV, SWV, DWV)                                                                   \
+    if (a.R == RV && a.sw == SWV && a.dw == DWV)                                              \
+        return large ? launch_dw_t<RV, RV, SWV, DWV, DWP_TILE_LARGE>(a, p, xdt, ydt, stream) \
+                     : launch_dw_t<RV, RV, SWV, DWV, DWP_TILE_SMALL>(a, p, xdt, ydt, stream);
 #define CV_DW4(RV) CV_DW(RV, 1, 1) CV_DW(RV, 1, 2) CV_DW(RV, 2, 1) CV_DW(RV, 2, 2)
     CV_DW4(1) CV_DW4(3) CV_DW4(5) CV_DW4(7)
 #undef CV_DW4
