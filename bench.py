@@ -25,6 +25,9 @@ sys.path.insert(0, ROOT)
 METRIC = "conv2d TFLOP/s and % of MFMA/HBM roofline per shape; pack-phase time share"
 PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}   # dense MFMA
 PEAK_HBM_GBS = 8000.0
+# fp32 FMA on the vector ALU without packed instructions (the build disables them):
+# 256 CUs x 4 SIMDs x 16 lanes x 2 flops x 2.4 GHz
+PEAK_VALU_TFLOPS = 78.6
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 KERNEL_SOURCES = {
     "implicit_gemm": ["paper_2407_10730_amd/csrc/gemm_mfma.hip", "paper_2407_10730_amd/csrc/pack_kernels.hip",
@@ -282,13 +285,18 @@ def run_sweep(report_path, B, torch):
         ridge = peak * 1e12 / (PEAK_HBM_GBS * 1e9)
         tf = flops / sec / 1e12
         gbs = nbytes / sec / 1e9
-        bound = "mfma" if ai >= ridge else "hbm"
-        frac = tf / peak if bound == "mfma" else gbs / PEAK_HBM_GBS
+        if ai >= ridge:
+            bound, frac, t_roof = "mfma", tf / peak, flops / (peak * 1e12)
+        elif cs.groups > 1 and ai * PEAK_HBM_GBS * 1e9 > PEAK_VALU_TFLOPS * 1e12:
+            # the direct kernel computes on the vector ALU: large filters in bf16 outrun it
+            bound, frac, t_roof = "alu", tf / PEAK_VALU_TFLOPS, flops / (PEAK_VALU_TFLOPS * 1e12)
+        else:
+            bound, frac, t_roof = "hbm", gbs / PEAK_HBM_GBS, nbytes / (PEAK_HBM_GBS * 1e9)
         algo = B.ALGO_NAMES[dc.plan(B.CONV2D_ALGO_AUTO).algo]
         rows.append({"name": cs.name, "dtype": cs.x_dtype, "n": cs.n, "c": cs.c, "hw": cs.h, "k": cs.k,
                      "r": cs.r, "stride": cs.stride[0], "dil": cs.dil[0], "groups": cs.groups,
                      "algo": algo, "us": sec * 1e6, "tflops": tf, "gbs": gbs, "ai": ai, "bound": bound,
-                     "frac": frac, "depthwise": cs.groups > 1})
+                     "frac": frac, "roofline_us": t_roof * 1e6, "depthwise": cs.groups > 1})
         dc.close()
         del x, w, b
     def summary(sel):
@@ -296,13 +304,21 @@ def run_sweep(report_path, B, torch):
             return None
         fr = sorted(r["frac"] for r in sel)
         return {"count": len(sel), "median_frac": fr[len(fr) // 2], "min_frac": fr[0], "max_frac": fr[-1]}
+    # a convolution whose roofline time is a few microseconds is bound by the launch and the
+    # kernel's fixed start-up; the "large" summaries keep those with >= 20 us of roofline time
+    big = [r for r in rows if r["roofline_us"] >= 20.0]
     out = {
         "rejected_draws": rejected,
         "contraction_bound_f32": summary([r for r in rows if r["bound"] == "mfma" and r["dtype"] == "f32"]),
         "contraction_bound_bf16": summary([r for r in rows if r["bound"] == "mfma" and r["dtype"] == "bf16"]),
         "depthwise": summary([r for r in rows if r["depthwise"]]),
+        "depthwise_alu_bound": summary([r for r in rows if r["depthwise"] and r["bound"] == "alu"]),
         "hbm_bound_other": summary([r for r in rows if r["bound"] == "hbm" and not r["depthwise"]]),
-        "depthwise_at_70pct_hbm": sum(1 for r in rows if r["depthwise"] and r["frac"] >= 0.7),
+        "large_contraction_bound_f32": summary([r for r in big if r["bound"] == "mfma" and r["dtype"] == "f32"]),
+        "large_contraction_bound_bf16": summary([r for r in big if r["bound"] == "mfma" and r["dtype"] == "bf16"]),
+        "large_depthwise": summary([r for r in big if r["depthwise"]]),
+        "large_hbm_bound_other": summary([r for r in big if r["bound"] == "hbm" and not r["depthwise"]]),
+        "depthwise_at_70pct_hbm": sum(1 for r in rows if r["depthwise"] and r["bound"] == "hbm" and r["frac"] >= 0.7),
         "contraction_at_60pct_mfma": sum(1 for r in rows if r["bound"] == "mfma" and r["frac"] >= 0.6),
         "total_seconds_one_pass": sum(r["us"] for r in rows) * 1e-6,
     }
@@ -400,6 +416,10 @@ def main():
         achieved = flops / (kern_ms * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": achieved, "peak": PEAK_TFLOPS[xdt], "unit": "TFLOP/s",
                 "frac": achieved / PEAK_TFLOPS[xdt]}
+    elif cs.groups > 1 and ai * PEAK_HBM_GBS * 1e9 > PEAK_VALU_TFLOPS * 1e12:
+        achieved = flops / (kern_ms * 1e-3) / 1e12
+        roof = {"bound": "alu", "achieved": achieved, "peak": PEAK_VALU_TFLOPS, "unit": "TFLOP/s",
+                "frac": achieved / PEAK_VALU_TFLOPS}
     else:
         achieved = alg_bytes / (kern_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
