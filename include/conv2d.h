@@ -128,13 +128,18 @@ typedef struct {
     int32_t tile_m, tile_n;   /* GEMM block tile (output channels x output pixels); 0 for DIRECT */
     int32_t kred, kred_pad;   /* reduction length (C/g)*R*S and its padded length */
     int64_t workspace_bytes;  /* device workspace this algorithm uses per chunk (explicit) or for the
-                                 split reduction's partial sums (implicit) */
+                                 partial sums of the split reduction or the tail split (implicit) */
     int64_t chunks;           /* explicit path: number of pack/GEMM/unpack chunks */
     int32_t needs_reorder;    /* 1 when pre/post layout reorders run (NHWC through an NCHW kernel) */
     int32_t op_class;         /* bit 0 pointwise, 1 grouped, 2 depthwise, 3 dilated, 4 rectangular, 5 strided */
     int32_t kernel;           /* microkernel that runs: CONV2D_KERNEL_* */
     int32_t ksplit;           /* implicit GEMM: reduction split into this many parts (1 = none);
                                  the parts' fp32 partial sums are added by the unpack phase */
+    int32_t tail_tiles;       /* implicit GEMM: output tiles computed in tail_pieces parts by extra
+                                 blocks of the same launch, so that every CU gets the same share
+                                 of tile work (0 = none); the last part of a tile to finish adds
+                                 the parts in order (fp32 partials in the workspace) */
+    int32_t tail_pieces;
 } conv2d_plan_info;
 
 /* Validate params, compute the output size, classify the operation and plan

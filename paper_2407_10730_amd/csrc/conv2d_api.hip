@@ -52,6 +52,9 @@ struct GemmPlan {
     int nstages = 0;
     int ksplit = 1;        // split reduction (implicit path): partial sums reduced by the unpack kernel
     int split_stages = 0;  // stages per split
+    int tail_tiles = 0;    // tail split (implicit path): tiles computed in pieces, see plan_tail
+    int tail_pieces = 0;
+    int tail_stages = 0;
 };
 
 struct ExplicitPlan {
@@ -171,6 +174,9 @@ struct conv2d_desc {
     int64_t wr_bytes = 0;
     void* sk = nullptr;  // partial sums of the split reduction
     int64_t sk_bytes = 0;
+    void* tp = nullptr;  // partial tiles of the tail split
+    int64_t tp_bytes = 0;
+    uint32_t* tc = nullptr;  // arrival counters of the tail split (zeroed once, reset by the kernel)
 
     int timing = CONV2D_TIMING_PHASES;
     double analysis_ms = 0.0;
@@ -262,6 +268,45 @@ void plan_split(conv2d_desc* d) {
     const int64_t per = ceil_div(gp.nstages, S);
     gp.ksplit = (int)ceil_div(gp.nstages, per);  // every split non-empty
     gp.split_stages = (int)per;
+}
+
+// Tail split.  With one tile per block and every tile resident at once, the CUs that hold
+// one tile more than the others set the time: 1568 tiles on 256 CUs run as 7 rounds of
+// tile work although the average is 6.1.  When the tiles past the last multiple of the CU
+// count are at most half the CUs, each of them is computed instead by q blocks of
+// consecutive stages (about one extra block per CU, q <= 16, at least 2 stages each); the
+// last piece of a tile to finish adds the q partials in piece order and stores the tile.
+// One group and no split reduction.  CONV2D_TAIL=0 switches it off; CONV2D_TAIL=q forces q
+// pieces (at least one stage each) on the tiles past the last multiple of the CU count, or on
+// every tile when that count divides the tiles.
+void plan_tail(conv2d_desc* d) {
+    const Geometry& g = d->g;
+    GemmPlan& gp = d->implicit;
+    gp.tail_tiles = gp.tail_pieces = gp.tail_stages = 0;
+    if (gp.ksplit > 1 || g.G != 1) return;
+    const int64_t cus = 256;
+    const int64_t tiles = ceil_div(g.Kg, gp.bm) * ceil_div(g.P, gp.bn);
+    const int64_t full = tiles / cus;
+    int64_t rem = tiles % cus;
+    const int64_t force = env_int64("CONV2D_TAIL", -1);
+    int64_t q = 0;
+    if (force > 0) {
+        if (rem == 0) rem = tiles;
+        q = std::min<int64_t>(force, gp.nstages);
+    } else if (force < 0 && full >= 1 && rem > 0 && rem <= cus / 2) {
+        q = std::min<int64_t>(std::min<int64_t>(cus / rem, 16), gp.nstages / 2);
+    }
+    if (q < 2 || tiles + rem * (q - 1) > 0x7fffffffLL) return;
+    const int64_t per = ceil_div(gp.nstages, q);
+    const int64_t pieces = ceil_div(gp.nstages, per);  // every piece non-empty
+    if (pieces < 2 || rem * pieces * gp.bm * gp.bn * 4 >= ((int64_t)1 << 31)) return;
+    gp.tail_tiles = (int)rem;
+    gp.tail_pieces = (int)pieces;
+    gp.tail_stages = (int)per;
+}
+
+int64_t tail_part_bytes(const GemmPlan& gp) {
+    return (int64_t)gp.tail_tiles * gp.tail_pieces * gp.bm * gp.bn * 4;
 }
 
 void plan_explicit(conv2d_desc* d) {
@@ -480,6 +525,22 @@ int run_implicit(conv2d_desc* d, const void* x, const void* w, const float* bias
     a.HoWo = (int32_t)(g.Ho * g.Wo);
     const int bsrc = d->implicit_nhwc ? BSRC_NHWC_TAP : d->implicit_tap ? BSRC_IMPLICIT_TAP : BSRC_IMPLICIT_NCHW;
     if (gp.ksplit <= 1) {
+        if (gp.tail_tiles > 0) {
+            CV_TRY(ensure_buffer(&d->tp, &d->tp_bytes, tail_part_bytes(gp)));
+            if (!d->tc) {
+                const size_t cb = (size_t)gp.tail_tiles * sizeof(uint32_t);
+                if (hipMalloc(&d->tc, cb) != hipSuccess) {
+                    d->tc = nullptr;
+                    return CONV2D_E_ALLOC;
+                }
+                CV_HIP(hipMemsetAsync(d->tc, 0, cb, s));
+            }
+            a.tail_tiles = gp.tail_tiles;
+            a.tail_pieces = gp.tail_pieces;
+            a.tail_stages = gp.tail_stages;
+            a.tail_part = static_cast<float*>(d->tp);
+            a.tail_count = d->tc;
+        }
         Scope sc(d, CONV2D_ALGO_IMPLICIT_GEMM, CONV2D_PH_IN_MICROKERNEL, s, ph);
         CV_TRY(sc.begin());
         CV_HIP(dispatch_gemm(gp, a, bsrc, EPI_NCHW, g.xdt, g.ydt, (int)g.G, s));
@@ -661,6 +722,7 @@ int conv2d_desc_create(const conv2d_params* params, conv2d_desc** out) {
     d->implicit = choose_tile(g.Kg, g.P, g.G, g.Kred, g.xdt, g.Cg, d->implicit_nhwc);
     d->implicit_tap = g.Cg % d->implicit.bk == 0;
     plan_split(d);
+    plan_tail(d);
     {
         // 8 waves (256-pixel tiles) unless an image has at most 128 output pixels;
         // CONV2D_SLICE_WAVES = 4 or 8 overrides for tests and tuning
@@ -705,6 +767,8 @@ int conv2d_desc_destroy(conv2d_desc* d) {
     if (d->ws) hipFree(d->ws);
     if (d->xr) hipFree(d->xr);
     if (d->sk) hipFree(d->sk);
+    if (d->tp) hipFree(d->tp);
+    if (d->tc) hipFree(d->tc);
     if (d->yr) hipFree(d->yr);
     if (d->wr) hipFree(d->wr);
     delete d;
@@ -858,12 +922,16 @@ int conv2d_plan_query(const conv2d_desc* d, int algo, conv2d_plan_info* out) {
         out->kernel = CONV2D_KERNEL_GEMM;
         out->ksplit = d->implicit.ksplit;
         if (d->implicit.ksplit > 1) out->workspace_bytes = d->implicit.ksplit * g.G * g.Kg * g.P * 4;
+        out->tail_tiles = d->implicit.tail_tiles;
+        out->tail_pieces = d->implicit.tail_pieces;
+        if (d->implicit.tail_tiles > 0) out->workspace_bytes = tail_part_bytes(d->implicit);
         if (d->implicit_slice) {
             out->tile_m = 64;
             out->tile_n = 32 * d->slice.nw;
             out->kred_pad = 2 * d->slice.kh;
             out->kernel = CONV2D_KERNEL_SLICE;
             out->ksplit = 1;
+            out->tail_tiles = out->tail_pieces = 0;
             out->workspace_bytes = 0;
         }
         if (!d->implicit_ok) return CONV2D_E_UNSUPPORTED;

@@ -77,6 +77,14 @@ struct GemmArgs {
     // epilogue) at offset s*c_sstride.  ksplit 0 or 1: no split.
     int32_t ksplit, split_stages;
     int64_t c_sstride;
+    // tail split (ksplit 1, one group): the last tail_tiles output tiles are each computed by
+    // tail_pieces blocks of tail_stages consecutive stages, placed after the other blocks of the
+    // grid.  Each piece writes its fp32 partial tile to tail_part; the last piece of a tile to
+    // arrive (counted in tail_count, zero before a launch and reset to zero by that piece) adds
+    // the partials in piece order and stores the tile.  tail_tiles 0: no tail split.
+    int32_t tail_tiles, tail_pieces, tail_stages;
+    float* tail_part;      // [tail_tiles][tail_pieces][BM*BN]
+    uint32_t* tail_count;  // [tail_tiles]
 };
 
 // 32x32-MFMA kernels.  fp32: stage depth bk in {16, 32}, register prefetch distance pf in {1, 2};

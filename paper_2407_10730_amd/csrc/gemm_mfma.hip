@@ -67,6 +67,98 @@ __device__ __forceinline__ void store_tile(const GemmArgs& A, f32x16 (&acc)[TM][
     }
 }
 
+// Work of one block: its output tile and its stages [s_begin, s_end).  The blocks past
+// the whole tiles of the grid are the pieces of the tail split (tail_tile >= 0).
+struct BlockWork {
+    int tile, s_begin, s_end, tail_tile, piece;
+};
+
+__device__ __forceinline__ BlockWork block_work(const GemmArgs& A, int ksplit, int sp) {
+    BlockWork w;
+    const int ndp = (int)gridDim.x - A.tail_tiles * A.tail_pieces;
+    const int q = (int)blockIdx.x - ndp;
+    if (q < 0) {
+        w.tile = xcd_remap(blockIdx.x, ndp);
+        w.s_begin = ksplit > 1 ? sp * A.split_stages : 0;
+        w.s_end = ksplit > 1 ? min(w.s_begin + A.split_stages, A.nstages) : A.nstages;
+        w.tail_tile = -1;
+        w.piece = 0;
+    } else {
+        w.tail_tile = q / A.tail_pieces;
+        w.piece = q - w.tail_tile * A.tail_pieces;
+        w.tile = ndp + w.tail_tile;
+        w.s_begin = w.piece * A.tail_stages;
+        w.s_end = min(w.s_begin + A.tail_stages, A.nstages);
+    }
+    return w;
+}
+
+// Tail split: store this piece's partial tile, count its arrival, and in the piece that
+// arrives last replace acc by the sum of all pieces of the tile in piece order (the same
+// result whatever the arrival order).  Returns false in the other pieces, which are done.
+// The pieces of a tile may run on different XCDs, whose L2 caches are not coherent with
+// each other.  The partials are therefore stored and loaded with the device-scope cache
+// policy (sc1: written through to, and read from, the point where all XCDs agree), and each
+// piece waits for its stores to complete before it counts itself; no fence is used, since
+// a device-scope fence writes back and invalidates the whole L2 of the XCD and costs every
+// other block on it its cached input.  The counter is an atomic, coherent device-wide.
+// Partial layout: 16-byte unit ((i*TN + j)*4 + q)*256 + t of the piece's BM x BN tile, through
+// buffer operations with a wave-uniform base (no per-lane address kept alive).
+template <int TM, int TN>
+__device__ __forceinline__ bool tail_reduce(const GemmArgs& A, f32x16 (&acc)[TM][TN], const BlockWork& w,
+                                            int t) {
+    constexpr uint32_t PIECE = TM * TN * 4 * 256 * 16;  // bytes of one partial tile
+    constexpr int SC1 = 1 << 4;                         // buffer cache policy bit: device scope
+    __shared__ int s_last;
+    const __amdgpu_buffer_rsrc_t rp =
+        make_rsrc(A.tail_part, (uint32_t)A.tail_tiles * (uint32_t)A.tail_pieces * PIECE);
+    const uint32_t tile_base = (uint32_t)w.tail_tile * (uint32_t)A.tail_pieces * PIECE;
+    const uint32_t lane_off = (uint32_t)t * 16u;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const f32x4 v{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+                __builtin_amdgcn_raw_buffer_store_b128(
+                    __builtin_bit_cast(u32x4, v), rp, lane_off,
+                    (int)(tile_base + (uint32_t)w.piece * PIECE + (uint32_t)((i * TN + j) * 4 + q) * 4096u), SC1);
+            }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the partial is complete device-wide
+    __syncthreads();
+    if (t == 0)
+        s_last = __hip_atomic_fetch_add(A.tail_count + w.tail_tile, 1u, __ATOMIC_RELAXED,
+                                        __HIP_MEMORY_SCOPE_AGENT) == (unsigned)(A.tail_pieces - 1);
+    __syncthreads();
+    if (!s_last) return false;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+#pragma unroll 1
+    for (int pc = 0; pc < A.tail_pieces; ++pc) {
+        const uint32_t base = tile_base + (uint32_t)pc * PIECE;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const f32x4 v = __builtin_bit_cast(
+                        f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                   rp, lane_off, (int)(base + (uint32_t)((i * TN + j) * 4 + q) * 4096u), SC1));
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) acc[i][j][4 * q + e] += v[e];
+                }
+    }
+    // ready for the next launch
+    if (t == 0) __hip_atomic_store(A.tail_count + w.tail_tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return true;
+}
+
 // ============================================================================ fp32
 // Block: 256 threads = 4 waves arranged WM x WN over a BM x BN tile; each wave
 // owns (BM/WM) x (BN/WN) = TM x TN MFMA 32x32x2 tiles.  BK reduction rows per
@@ -79,8 +171,10 @@ __device__ __forceinline__ void store_tile(const GemmArgs& A, f32x16 (&acc)[TM][
 // PF = 1: the global loads of stage s+1 are issued before the MFMAs of stage s;
 // PF = 2: two register sets, the loads of stage s+2 are issued before the
 // MFMAs of stage s, so a load has two stages of MFMA work to land.
+// 64x64 tiles with 16-row stages fit seven blocks per CU (LDS 20 KiB each); the bound keeps
+// the register budget at seven blocks with the tail-split epilogue compiled in.
 template <int BM, int BN, int WM, int WN, int BK, int PF, int BSRC, int EPI, typename TOut>
-__global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs A) {
+__global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 16 ? 7 : 1)) void gemm_f32_kernel(GemmArgs A) {
     constexpr int WTM = BM / WM, WTN = BN / WN;
     constexpr int TM = WTM / 32, TN = WTN / 32;
     static_assert(WM * WN == 4 && TM >= 1 && TN >= 1, "bad wave layout");
@@ -105,11 +199,10 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs A) {
     const int ksplit = A.ksplit > 1 ? A.ksplit : 1;
     const int gi = blockIdx.z / ksplit;
     const int sp = blockIdx.z - gi * ksplit;
-    // this block's stages [s_begin, s_end)
-    const int s_begin = ksplit > 1 ? sp * A.split_stages : 0;
-    const int s_end = ksplit > 1 ? min(s_begin + A.split_stages, A.nstages) : A.nstages;
-
-    const int tile = xcd_remap(blockIdx.x, gridDim.x);
+    // this block's tile and stages [s_begin, s_end)
+    const BlockWork wk = block_work(A, ksplit, sp);
+    const int s_begin = wk.s_begin, s_end = wk.s_end;
+    const int tile = wk.tile;
     const int tile_p = tile / A.grid_m;
     const int tile_m = tile - tile_p * A.grid_m;
     const int p0 = tile_p * BN;
@@ -303,6 +396,9 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs A) {
         }
     }
 
+    if constexpr (EPI == EPI_NCHW) {
+        if (wk.tail_tile >= 0 && !tail_reduce<TM, TN>(A, acc, wk, t)) return;
+    }
     store_tile<TM, TN, EPI, TOut>(A, acc, gi, sp, m0 + wm0, p0 + wn0, lrow, lcol);
 }
 
@@ -339,7 +435,7 @@ __device__ __forceinline__ ColState col_state_nhwc(const GemmArgs& A, int p, int
 }
 
 template <int BM, int BN, int WM, int WN, int BK, int BSRC, int EPI, typename TOut>
-__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs A) {
+__global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void gemm_bf16_kernel(GemmArgs A) {
     constexpr int LDK = BK + 8;
     constexpr int WTM = BM / WM, WTN = BN / WN;
     constexpr int TM = WTM / 32, TN = WTN / 32;
@@ -360,11 +456,10 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs A) {
     const int ksplit = A.ksplit > 1 ? A.ksplit : 1;
     const int gi = blockIdx.z / ksplit;
     const int sp = blockIdx.z - gi * ksplit;
-    // this block's stages [s_begin, s_end)
-    const int s_begin = ksplit > 1 ? sp * A.split_stages : 0;
-    const int s_end = ksplit > 1 ? min(s_begin + A.split_stages, A.nstages) : A.nstages;
-
-    const int tile = xcd_remap(blockIdx.x, gridDim.x);
+    // this block's tile and stages [s_begin, s_end)
+    const BlockWork wk = block_work(A, ksplit, sp);
+    const int s_begin = wk.s_begin, s_end = wk.s_end;
+    const int tile = wk.tile;
     const int tile_p = tile / A.grid_m;
     const int tile_m = tile - tile_p * A.grid_m;
     const int p0 = tile_p * BN;
@@ -550,13 +645,17 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs A) {
         __syncthreads();
     }
 
+    if constexpr (EPI == EPI_NCHW) {
+        if (wk.tail_tile >= 0 && !tail_reduce<TM, TN>(A, acc, wk, t)) return;
+    }
     store_tile<TM, TN, EPI, TOut>(A, acc, gi, sp, m0 + wm0, p0 + wn0, lrow, lcol);
 }
 
 // ============================================================================ dispatch
 template <int BM, int BN, int WM, int WN, int BK, int PF>
 static hipError_t launch_f32(const GemmArgs& a, int bsrc, int epi, int groups, hipStream_t stream) {
-    dim3 grid((unsigned)(a.grid_p * a.grid_m), 1, (unsigned)(groups * (a.ksplit > 1 ? a.ksplit : 1)));
+    dim3 grid((unsigned)(a.grid_p * a.grid_m + a.tail_tiles * (a.tail_pieces - 1)), 1,
+              (unsigned)(groups * (a.ksplit > 1 ? a.ksplit : 1)));
 #define CV_F32(BS, EP) \
     hipLaunchKernelGGL((gemm_f32_kernel<BM, BN, WM, WN, BK, PF, BS, EP, float>), grid, dim3(256), 0, stream, a)
     if (bsrc == BSRC_IMPLICIT_NCHW && epi == EPI_NCHW) CV_F32(BSRC_IMPLICIT_NCHW, EPI_NCHW);
@@ -572,7 +671,8 @@ static hipError_t launch_f32(const GemmArgs& a, int bsrc, int epi, int groups, h
 
 template <int BM, int BN, int WM, int WN, int BK>
 static hipError_t launch_bf16(const GemmArgs& a, int bsrc, int epi, int ydt, int groups, hipStream_t stream) {
-    dim3 grid((unsigned)(a.grid_p * a.grid_m), 1, (unsigned)(groups * (a.ksplit > 1 ? a.ksplit : 1)));
+    dim3 grid((unsigned)(a.grid_p * a.grid_m + a.tail_tiles * (a.tail_pieces - 1)), 1,
+              (unsigned)(groups * (a.ksplit > 1 ? a.ksplit : 1)));
 #define CV_BF(BS, EP, TO) \
     hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, BK, BS, EP, TO>), grid, dim3(256), 0, stream, a)
     if (bsrc == BSRC_NHWC_TAP && epi == EPI_NCHW) {
@@ -609,6 +709,16 @@ bool gemm32_f32_supported(int tile, int bk, int pf) {
 
 hipError_t launch_gemm(const GemmArgs& a, int tile, int bk, int pf, int bsrc, int epi, int xdt, int ydt,
                        int groups, hipStream_t stream) {
+    if (a.tail_tiles != 0) {
+        // the tail split covers whole tiles of one group, every piece non-empty
+        const int64_t tiles = (int64_t)a.grid_p * a.grid_m;
+        if (a.tail_tiles < 0 || a.tail_tiles > tiles || a.tail_pieces < 2 || a.tail_stages < 1 ||
+            groups != 1 || a.ksplit > 1 || !a.tail_part || !a.tail_count ||
+            (int64_t)a.tail_pieces * a.tail_stages < a.nstages ||
+            (int64_t)(a.tail_pieces - 1) * a.tail_stages >= a.nstages ||
+            tiles + (int64_t)a.tail_tiles * (a.tail_pieces - 1) > 0x7fffffffLL)
+            return hipErrorInvalidValue;
+    }
     if (xdt == CONV2D_BF16) {
         if (bk != 32 && bk != 64) return hipErrorInvalidValue;
 #define CV_TB(BMV, BNV, WMV, WNV) \

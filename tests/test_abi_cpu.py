@@ -172,6 +172,39 @@ def test_split_reduction_plan(monkeypatch):
     assert plan(datagen.CONFIGS["cfg2"]).ksplit == 3
 
 
+def test_tail_split_plan(monkeypatch):
+    """Tile counts a little above a multiple of the 256 CUs: the tiles past it are computed
+    in pieces of consecutive stages, so every CU gets the same share of tile work."""
+    monkeypatch.delenv("CONV2D_TAIL", raising=False)
+    monkeypatch.delenv("CONV2D_KSPLIT", raising=False)
+
+    def plan(cs):
+        d = B.conv2d_desc_create(params_for(cs))
+        try:
+            return B.conv2d_plan_query(d, B.CONV2D_ALGO_IMPLICIT_GEMM)
+        finally:
+            B.conv2d_desc_destroy(d)
+    cfg2 = datagen.CONFIGS["cfg2"]
+    info = plan(cfg2)                        # 1568 = 6 * 256 + 32 tiles of 64 x 64, 36 stages
+    assert (info.tail_tiles, info.tail_pieces) == (32, 8)
+    assert info.workspace_bytes == 32 * 8 * 64 * 64 * 4
+    info = plan(cfg2.with_(n=31))            # 1519 tiles: 239 past 5 * 256, more than half the CUs
+    assert info.tail_tiles == 0
+    info = plan(cfg2.with_(n=2))             # 98 tiles: fewer than the CUs, no tail
+    assert info.tail_tiles == 0
+    assert plan(datagen.CONFIGS["cfg3a"]).tail_pieces == 8      # 16 stages: pieces of 2
+    assert plan(cfg2.with_(groups=2)).tail_tiles == 0           # one group only
+    monkeypatch.setenv("CONV2D_TAIL", "0")
+    assert plan(cfg2).tail_tiles == 0
+    monkeypatch.setenv("CONV2D_TAIL", "5")
+    small = cfg2.with_(n=1, h=13, w=11, k=70)    # 2 x 3 tiles, all computed in 5 pieces
+    assert plan(small).ksplit > 1                # (the split reduction comes first)
+    monkeypatch.setenv("CONV2D_KSPLIT", "1")
+    info = plan(small)
+    assert (info.tail_tiles, info.tail_pieces) == (6, 5)
+    assert plan(cfg2).tail_pieces == 5
+
+
 def test_explicit_workspace_chunking(monkeypatch):
     cs = datagen.CONFIGS["cfg4"]
     d = B.conv2d_desc_create(params_for(cs))

@@ -247,6 +247,88 @@ def test_split_reduction(idx, dt):
                 os.environ[k] = v
 
 
+# tail split: the tiles past the last multiple of the CU count are computed in pieces of
+# consecutive stages by extra blocks of the launch, and the last piece of a tile to finish adds
+# the partials in piece order.  Forced here on small shapes (every tile in pieces) through
+# every gather, with ragged channel and pixel tiles; each descriptor runs twice, since the
+# arrival counters must be back at zero after a call, and both results must be identical.
+TAIL = [
+    (_shape(2, 32, 13, 11, 70, 3, 3, pd=(1, 1), seed=240), "3"),
+    (_shape(1, 37, 9, 9, 33, 5, 3, st=(2, 1), pd=(2, 1), seed=241), "4"),
+    (_shape(3, 128, 10, 10, 64, 1, 1, seed=242), "2"),
+    (_shape(1, 96, 17, 15, 130, 3, 3, pd=(2, 2), dl=(2, 2), seed=243), "7"),
+]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16", "bf16-nhwc"])
+@pytest.mark.parametrize("idx", range(len(TAIL)))
+def test_tail_split(idx, dt):
+    import torch
+    base, force = TAIL[idx]
+    cs = base.with_(x_dtype="f32" if dt == "f32" else "bf16", y_dtype="f32" if dt == "f32" else "bf16")
+    kernel = "nhwc" if dt == "bf16-nhwc" else "0"
+    if dt == "bf16-nhwc" and (cs.c // cs.groups) % 32:
+        pytest.skip("the NHWC gather needs C/g a multiple of 32")
+    env = {"CONV2D_TAIL": force, "CONV2D_KSPLIT": "1"}
+    old = {k: os.environ.get(k) for k in env}
+    os.environ.update(env)
+    try:
+        for mode, c in (("random", cs), ("integer", cs.with_(y_dtype="f32"))):
+            print(f"\n[case] tail {c} kernel={kernel} mode={mode}", flush=True)
+            with _Kernel(kernel):
+                dc = DeviceConv(c, mode)
+            try:
+                plan = dc.plan(IMPLICIT)
+                assert plan.kernel == B.CONV2D_KERNEL_GEMM and plan.ksplit == 1
+                assert plan.tail_tiles > 0 and plan.tail_pieces == int(force), (plan.tail_tiles, plan.tail_pieces)
+                ys = []
+                for _ in range(2):
+                    dc.run(IMPLICIT)
+                    torch.cuda.synchronize()
+                    ys.append(dc.y_nchw())
+                inputs = (dc.x_host, dc.w_host, dc.b_host)
+            finally:
+                dc.close()
+            assert np.array_equal(ys[0], ys[1])
+            y_ref, a_ref = _reference(c, mode, inputs)
+            if mode == "integer":
+                bad = np.argwhere(ys[0] != y_ref)
+                assert bad.size == 0, f"{len(bad)} mismatches, first at {bad[0]}"
+            else:
+                _, pt = oracle.normalised_errors(ys[0], y_ref, a_ref)
+                gate = GATE[c.x_dtype] if c.y_dtype == "f32" else max(GATE[c.x_dtype], 2.0 ** -8)
+                assert pt <= gate, f"per-point error {pt:.3e} > {gate}"
+    finally:
+        for k, v in old.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+
+
+def test_tail_split_planned_cfg2_repeat():
+    """cfg2 as planned (1568 tiles: 32 in 8 pieces) run three times on one descriptor, each
+    result identical and on the oracle's sampled outputs."""
+    import torch
+    cs = datagen.CONFIGS["cfg2"]
+    dc = DeviceConv(cs, "random")
+    try:
+        plan = dc.plan(IMPLICIT)
+        assert plan.tail_tiles == 32 and plan.tail_pieces == 8
+        ys = []
+        for _ in range(3):
+            dc.run(IMPLICIT)
+            torch.cuda.synchronize()
+            ys.append(dc.y_nchw())
+        inputs = (dc.x_host, dc.w_host, dc.b_host)
+    finally:
+        dc.close()
+    assert np.array_equal(ys[0], ys[1]) and np.array_equal(ys[0], ys[2])
+    y_ref, a_ref = _reference(cs, "random", inputs)
+    _, pt = oracle.normalised_errors(ys[0], y_ref, a_ref)
+    assert pt <= GATE["f32"]
+
+
 EDGE_ALGOS = [("implicit", IMPLICIT, None, None), ("implicit-gemm", IMPLICIT, "0", None),
               ("implicit-slice4", IMPLICIT, "1", "4"), ("implicit-slice8", IMPLICIT, "1", "8"),
               ("implicit-nhwc", IMPLICIT, "nhwc", None),
