@@ -148,15 +148,15 @@ def time_algo(dc, algo, steps, warmup, B, torch, timing):
 
 
 def cold_median(dc, algo, runs, B, torch):
-    """Median of single calls with the 256 MB last-level cache flushed before each
-    (flush outside the timed events)."""
+    """Median of single calls with the 256 MB last-level cache flushed before each (the
+    library's copy probe moves 512 MiB through it, outside the timed events)."""
     stream = torch.cuda.current_stream()
     flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
     B.conv2d_set_timing(dc.desc, B.CONV2D_TIMING_TOTAL)
     B.conv2d_breakdown_reset(dc.desc)
     times = []
     for _ in range(runs):
-        flush.fill_(1)
+        B.conv2d_probe_copy(flush[256 << 20:], flush[:256 << 20], 256 << 20, stream)
         torch.cuda.synchronize()
         before = dc.breakdown(algo)["total_ms"] if times else 0.0
         dc.run(algo, stream)
@@ -166,6 +166,44 @@ def cold_median(dc, algo, runs, B, torch):
     del flush
     times.sort()
     return times[len(times) // 2]
+
+
+def time_launches(launch, reps, torch):
+    """Average duration of `launch()` (one kernel on the current stream) over `reps`
+    back-to-back launches, from an event pair on that stream."""
+    stream = torch.cuda.current_stream()
+    for _ in range(3):
+        launch()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(reps):
+        launch()
+    b.record(stream)
+    b.synchronize()
+    return a.elapsed_time(b) / reps
+
+
+def measured_peaks(B, torch):
+    """The roofline probes: MFMA issue rate (fp32, bf16) on register operands and the
+    device copy rate (read + write bytes), next to the published peaks."""
+    stream = torch.cuda.current_stream()
+    sink = torch.empty(1 << 20, dtype=torch.float32, device="cuda")
+    out = {}
+    for name, dt, iters in (("mfma_f32_tflops", B.CONV2D_F32, 20000), ("mfma_bf16_tflops", B.CONV2D_BF16, 40000)):
+        flops = [0.0]
+
+        def run(dt=dt, iters=iters):
+            flops[0] = B.conv2d_probe_mfma(dt, iters, sink, stream)
+        ms = time_launches(run, 5, torch)
+        out[name] = flops[0] / (ms * 1e-3) / 1e12
+    buf = torch.empty(2 << 30, dtype=torch.uint8, device="cuda")
+    src, dst = buf[: 1 << 30], buf[1 << 30:]
+    ms = time_launches(lambda: B.conv2d_probe_copy(dst, src, 1 << 30, stream), 5, torch)
+    out["copy_gbs"] = 2 * (1 << 30) / (ms * 1e-3) / 1e9
+    del buf, sink
+    out["published"] = {"mfma_f32_tflops": PEAK_TFLOPS["f32"], "mfma_bf16_tflops": PEAK_TFLOPS["bf16"],
+                        "hbm_gbs": PEAK_HBM_GBS}
+    return out
 
 
 PROFILE_COMMANDS = {
@@ -446,6 +484,18 @@ def main():
         "t_explicit_over_t_implicit": ms_e / ms_per_step,
     }
     cold = cold_median(dc, algo, args.cold_runs, B, torch)
+    # pack probe: the implicit microkernel's loader alone (gather into LDS, no MFMA, no
+    # output) against the full microkernel -- an estimate of the fused packing share
+    probe = None
+    if algo == B.CONV2D_ALGO_IMPLICIT_GEMM:
+        stream = torch.cuda.current_stream()
+        B.conv2d_set_timing(dc.desc, B.CONV2D_TIMING_OFF)
+        dc.run(algo, stream)
+        probe_ms = time_launches(lambda: B.conv2d_pack_probe(dc.desc, dc.x, dc.w, stream), 20, torch)
+        probe = {"kind": "estimate (loader-only microkernel / microkernel)",
+                 "loader_only_us": probe_ms * 1e3, "microkernel_us": kern_launch_ms * 1e3,
+                 "share_estimate": probe_ms / kern_launch_ms}
+    peaks = measured_peaks(B, torch)
 
     out = {
         "metric": METRIC,
@@ -471,6 +521,8 @@ def main():
         "explicit_im2col": explicit,
         "cold_cache_ms_median": cold,
         "cold_cache_tflops": flops / (cold * 1e-3) / 1e12,
+        "implicit_pack_probe": probe,
+        "measured_peaks": peaks,
     }
     if not args.no_cpu:
         x = dc.x_host

@@ -40,7 +40,7 @@ enum {
     CONV2D_E_NULL = -4,        /* a required pointer is NULL */
     CONV2D_E_ALLOC = -5,       /* workspace could not be allocated within the limit */
     CONV2D_E_HIP = -6,         /* a HIP runtime call or kernel launch failed */
-    CONV2D_E_NO_DATA = -7      /* breakdown requested before any timed call */
+    CONV2D_E_NO_DATA = -7      /* breakdown (or pack probe) requested before any call that feeds it */
 };
 
 /* Layout of x and y.  w is always K x C/g x R x S (row-major). */
@@ -169,6 +169,34 @@ int conv2d_output_shape(const conv2d_desc* desc, int64_t out_nkhw[4]);
  * synchronisation.  Results are bitwise reproducible for a fixed algo. */
 int conv2d_fwd(conv2d_desc* desc, const void* x, const void* w, const float* bias, void* y,
                int algo, void* stream);
+
+/* Pack probe (measurement of the fused packing, Sec. III-C breakdown): queue the
+ * implicit algorithm's microkernel on `stream` with its loader only -- the im2col
+ * gather into LDS with stride, padding and dilation resolved, the filter loads
+ * and the barriers, but no MFMA and no output.  Its duration (timed by the
+ * caller's events around the call, one kernel launch) over the full
+ * microkernel's estimates the share of the packing fused into the implicit
+ * algorithm.  x and w: the device pointers of a conv2d_fwd call; y and bias are
+ * neither read nor written.  The probe reads the internal copies the last
+ * implicit conv2d_fwd on this descriptor made (tap-major weights, a reordered
+ * x), so it needs one such call first: E_NO_DATA otherwise.  E_NULL, E_UNSUPPORTED
+ * (no implicit algorithm for this shape, or another device), E_HIP. */
+int conv2d_pack_probe(conv2d_desc* desc, const void* x, const void* w, void* stream);
+
+/* Roofline probes (measurement; no descriptor).  Each queues one kernel on
+ * `stream` and returns at once; the caller times it with its own events.
+ * conv2d_probe_mfma: an MFMA issue loop on register operands over every CU (two
+ * blocks of four waves per CU, four independent accumulators per wave, `iters`
+ * iterations); dtype CONV2D_F32 runs the 32x32x2 fp32 MFMA, CONV2D_BF16 the
+ * 32x32x16 bf16 one.  *flops receives the floating-point operations the launch
+ * performs.  sink: device buffer of at least 2 * CUs * 256 * 4 bytes that
+ * receives one float per thread (their values carry no meaning).
+ * conv2d_probe_copy: dst[0:bytes] = src[0:bytes] with 16-byte accesses (bytes a
+ * positive multiple of 16, below 2^43; the buffers must not overlap): the device
+ * copy rate, and the cache flush before a cold-cache run.
+ * Errors: E_NULL, E_INVALID (dtype, iters < 1, sink too small, bytes), E_HIP. */
+int conv2d_probe_mfma(int dtype, int64_t iters, void* sink, int64_t sink_bytes, void* stream, double* flops);
+int conv2d_probe_copy(void* dst, const void* src, int64_t bytes, void* stream);
 
 /* Synchronise on the descriptor's recorded events, fold them into the
  * per-algorithm totals and copy the totals of `algo` (AUTO: the algorithm

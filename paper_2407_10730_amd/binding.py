@@ -40,7 +40,8 @@ KERNEL_NAMES = {CONV2D_KERNEL_GEMM: "gemm", CONV2D_KERNEL_SLICE: "slice", CONV2D
 # every function the header declares
 EXPORTS = ("conv2d_desc_create", "conv2d_desc_destroy", "conv2d_output_shape", "conv2d_fwd",
            "conv2d_breakdown", "conv2d_breakdown_reset", "conv2d_set_timing", "conv2d_plan_query",
-           "conv2d_status_string", "conv2d_runtime_version")
+           "conv2d_status_string", "conv2d_runtime_version", "conv2d_pack_probe", "conv2d_probe_mfma",
+           "conv2d_probe_copy")
 
 
 class Conv2dError(RuntimeError):
@@ -110,6 +111,9 @@ def load():
     lib.conv2d_desc_destroy.argtypes = [vp]
     lib.conv2d_output_shape.argtypes = [vp, i64p]
     lib.conv2d_fwd.argtypes = [vp, vp, vp, vp, vp, i32, vp]
+    lib.conv2d_pack_probe.argtypes = [vp, vp, vp, vp]
+    lib.conv2d_probe_mfma.argtypes = [i32, ctypes.c_int64, vp, ctypes.c_int64, vp, ctypes.POINTER(ctypes.c_double)]
+    lib.conv2d_probe_copy.argtypes = [vp, vp, ctypes.c_int64, vp]
     lib.conv2d_breakdown.argtypes = [vp, i32, ctypes.POINTER(conv2d_breakdown_t)]
     lib.conv2d_breakdown_reset.argtypes = [vp]
     lib.conv2d_set_timing.argtypes = [vp, i32]
@@ -168,6 +172,23 @@ def conv2d_output_shape(desc: int):
 def conv2d_fwd(desc: int, x, w, bias, y, algo: int = CONV2D_ALGO_AUTO, stream=None) -> None:
     _check(load().conv2d_fwd(desc, _ptr(x), _ptr(w), _ptr(bias), _ptr(y), int(algo), _stream(stream)),
            "conv2d_fwd")
+
+
+def conv2d_pack_probe(desc: int, x, w, stream=None) -> None:
+    _check(load().conv2d_pack_probe(desc, _ptr(x), _ptr(w), _stream(stream)), "conv2d_pack_probe")
+
+
+def conv2d_probe_mfma(dtype: int, iters: int, sink, stream=None) -> float:
+    """Queue the MFMA issue loop; returns the flops it performs."""
+    flops = ctypes.c_double()
+    nbytes = sink.numel() * sink.element_size()
+    _check(load().conv2d_probe_mfma(int(dtype), int(iters), _ptr(sink), nbytes, _stream(stream),
+                                    ctypes.byref(flops)), "conv2d_probe_mfma")
+    return flops.value
+
+
+def conv2d_probe_copy(dst, src, nbytes: int, stream=None) -> None:
+    _check(load().conv2d_probe_copy(_ptr(dst), _ptr(src), int(nbytes), _stream(stream)), "conv2d_probe_copy")
 
 
 def conv2d_breakdown(desc: int, algo: int = CONV2D_ALGO_AUTO) -> conv2d_breakdown_t:

@@ -9,7 +9,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libconv2d.so")
-SOURCES = ["conv2d_api.hip", "gemm_mfma.hip", "pack_kernels.hip", "direct_kernels.hip", "slice_conv.hip"]
+SOURCES = ["conv2d_api.hip", "gemm_mfma.hip", "pack_kernels.hip", "direct_kernels.hip", "slice_conv.hip",
+           "probes.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -447,7 +447,8 @@ int ensure_buffer(void** buf, int64_t* have, int64_t need) {
     } while (0)
 
 // ------------------------------------------------------------------ algorithms (NCHW tensors)
-int run_slice(conv2d_desc* d, const void* x, const void* w, const float* bias, void* y, hipStream_t s, bool ph) {
+int run_slice(conv2d_desc* d, const void* x, const void* w, const float* bias, void* y, hipStream_t s, bool ph,
+              bool probe) {
     const Geometry& g = d->g;
     const SlicePlan& sp = d->slice;
     SliceArgs a{};
@@ -475,18 +476,24 @@ int run_slice(conv2d_desc* d, const void* x, const void* w, const float* bias, v
     a.lds_k_off = sp.lds_k_off;
     a.lds_x_off = sp.lds_x_off;
     a.lds_bytes = sp.lds_bytes;
+    a.loader_only = probe ? 1 : 0;
     Scope sc(d, CONV2D_ALGO_IMPLICIT_GEMM, CONV2D_PH_IN_MICROKERNEL, s, ph);
     CV_TRY(sc.begin());
     CV_HIP(launch_slice(a, g.xdt, g.ydt, sp.nw, s));
     return sc.end();
 }
 
+// probe: the pack probe, which runs only the microkernel's loader on the internal copies that
+// the last call made (tap-major weights) and writes nothing.
 int run_implicit(conv2d_desc* d, const void* x, const void* w, const float* bias, void* y, hipStream_t s,
-                 bool ph) {
+                 bool ph, bool probe = false) {
     const Geometry& g = d->g;
     const GemmPlan& gp = d->implicit;
-    if (d->implicit_slice) return run_slice(d, x, w, bias, y, s, ph);
-    if ((d->implicit_tap || d->implicit_nhwc) && g.R * g.S > 1) {
+    if (d->implicit_slice) return run_slice(d, x, w, bias, y, s, ph, probe);
+    if ((d->implicit_tap || d->implicit_nhwc) && g.R * g.S > 1 && probe) {
+        if (!d->wr) return CONV2D_E_NO_DATA;
+        w = d->wr;
+    } else if ((d->implicit_tap || d->implicit_nhwc) && g.R * g.S > 1) {
         // pre-convolution reordering of the filters into the tap-major reduction order
         const int64_t wb = g.w_elems * elem_size(g.xdt);
         CV_TRY(ensure_buffer(&d->wr, &d->wr_bytes, wb));
@@ -524,6 +531,7 @@ int run_implicit(conv2d_desc* d, const void* x, const void* w, const float* bias
     a.y_nstride = g.K * g.Ho * g.Wo;
     a.HoWo = (int32_t)(g.Ho * g.Wo);
     const int bsrc = d->implicit_nhwc ? BSRC_NHWC_TAP : d->implicit_tap ? BSRC_IMPLICIT_TAP : BSRC_IMPLICIT_NCHW;
+    a.loader_only = probe ? 1 : 0;
     if (gp.ksplit <= 1) {
         if (gp.tail_tiles > 0) {
             CV_TRY(ensure_buffer(&d->tp, &d->tp_bytes, tail_part_bytes(gp)));
@@ -562,6 +570,7 @@ int run_implicit(conv2d_desc* d, const void* x, const void* w, const float* bias
         CV_HIP(dispatch_gemm(gp, a, bsrc, EPI_DENSE, g.xdt, CONV2D_F32, (int)g.G, s));
         CV_TRY(sc.end());
     }
+    if (probe) return CONV2D_OK;
     UnpackArgs u{};
     u.c = static_cast<const float*>(d->sk);
     u.y = y;
@@ -847,6 +856,21 @@ int conv2d_fwd(conv2d_desc* d, const void* x, const void* w, const float* bias, 
     d->acc[algo].used = true;
     d->last_algo = algo;
     return CONV2D_OK;
+}
+
+int conv2d_pack_probe(conv2d_desc* d, const void* x, const void* w, void* stream) {
+    if (!d || !x || !w) return CONV2D_E_NULL;
+    if (!d->implicit_ok) return CONV2D_E_UNSUPPORTED;
+    if (d->device < 0 || !d->acc[CONV2D_ALGO_IMPLICIT_GEMM].used) return CONV2D_E_NO_DATA;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return CONV2D_E_HIP;
+    if (dev != d->device) return CONV2D_E_UNSUPPORTED;
+    const Geometry& g = d->g;
+    // the x the microkernel reads: the internal copy when the layouts differ (made by the last call)
+    const bool x_nhwc = d->implicit_nhwc && !d->implicit_slice;
+    const void* xin = (g.layout == CONV2D_NHWC) != x_nhwc ? d->xr : x;
+    if (!xin) return CONV2D_E_NO_DATA;
+    return run_implicit(d, xin, w, nullptr, nullptr, static_cast<hipStream_t>(stream), false, true);
 }
 
 int conv2d_breakdown(conv2d_desc* d, int algo, conv2d_breakdown_t* out) {

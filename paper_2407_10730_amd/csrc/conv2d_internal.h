@@ -85,6 +85,8 @@ struct GemmArgs {
     int32_t tail_tiles, tail_pieces, tail_stages;
     float* tail_part;      // [tail_tiles][tail_pieces][BM*BN]
     uint32_t* tail_count;  // [tail_tiles]
+    // pack probe: 1 runs the loader only (gathers into LDS, barriers), no MFMA, no output
+    int32_t loader_only;
 };
 
 // 32x32-MFMA kernels.  fp32: stage depth bk in {16, 32}, register prefetch distance pf in {1, 2};
@@ -156,6 +158,7 @@ struct SliceArgs {
     int32_t tiles_total;  // G * grid_m * N * tiles_px
     int32_t nblocks;      // persistent grid size
     int32_t lds_k_off, lds_x_off, lds_bytes;
+    int32_t loader_only;  // pack probe: slice copies and filter loads only, no MFMA, no output
 };
 struct SlicePlan {
     bool ok;

@@ -372,7 +372,7 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 16 ? 7 : 1)) void ge
             const int buf = j & 1;
             const bool more = j + 1 < n;
             if (more) load_stage(s_begin + j + 1, breg0, areg0);
-            compute(buf);
+            if (!A.loader_only) compute(buf);
             if (more) store_stage(buf ^ 1, breg0, areg0);
             __syncthreads();
         }
@@ -384,18 +384,19 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 16 ? 7 : 1)) void ge
         for (int j = 0; j < n; j += 2) {
             // even stage: set 0 is free, set 1 holds stage j+1
             if (j + 2 < n) load_stage(s_begin + j + 2, breg0, areg0);
-            compute(0);
+            if (!A.loader_only) compute(0);
             if (j + 1 < n) store_stage(1, breg1, areg1);
             __syncthreads();
             if (j + 1 >= n) break;
             // odd stage: set 1 is free, set 0 holds stage j+2
             if (j + 3 < n) load_stage(s_begin + j + 3, breg1, areg1);
-            compute(1);
+            if (!A.loader_only) compute(1);
             if (j + 2 < n) store_stage(0, breg0, areg0);
             __syncthreads();
         }
     }
 
+    if (A.loader_only) return;
     if constexpr (EPI == EPI_NCHW) {
         if (wk.tail_tile >= 0 && !tail_reduce<TM, TN>(A, acc, wk, t)) return;
     }
@@ -626,25 +627,28 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void ge
         const int buf = (st - s_begin) & 1;
         const bool more = st + 1 < s_end;
         if (more) load_stage(st + 1);
+        if (!A.loader_only) {
 #pragma unroll
-        for (int ks = 0; ks < BK / 16; ++ks) {
-            bf16x8 a[TM], b[TN];
+            for (int ks = 0; ks < BK / 16; ++ks) {
+                bf16x8 a[TM], b[TN];
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
-                a[i] = *reinterpret_cast<const bf16x8*>(&As[buf][wm0 + i * 32 + lcol][ks * 16 + 8 * lrow]);
-#pragma unroll
-            for (int j = 0; j < TN; ++j)
-                b[j] = *reinterpret_cast<const bf16x8*>(&Bs[buf][wn0 + j * 32 + lcol][ks * 16 + 8 * lrow]);
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
+                for (int i = 0; i < TM; ++i)
+                    a[i] = *reinterpret_cast<const bf16x8*>(&As[buf][wm0 + i * 32 + lcol][ks * 16 + 8 * lrow]);
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+                    b[j] = *reinterpret_cast<const bf16x8*>(&Bs[buf][wn0 + j * 32 + lcol][ks * 16 + 8 * lrow]);
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+            }
         }
         if (more) store_stage(buf ^ 1);
         __syncthreads();
     }
 
+    if (A.loader_only) return;
     if constexpr (EPI == EPI_NCHW) {
         if (wk.tail_tile >= 0 && !tail_reduce<TM, TN>(A, acc, wk, t)) return;
     }

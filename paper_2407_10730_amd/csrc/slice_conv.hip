@@ -184,6 +184,12 @@ __global__ __launch_bounds__(64 * NW) void slice_conv_kernel(SliceArgs A) {
         __builtin_amdgcn_s_waitcnt(0);  // this wave's slice copies (and filter loads) have landed
         lds_barrier();                  // ... and every other wave's
 
+        if (A.loader_only) {
+            // pack probe: the next slice copy only
+            lds_barrier();
+            if (w + (int)gridDim.x < A.tiles_total) copy_slice(w + gridDim.x, xs);
+            continue;
+        }
         const int p = tl.p0 + wave * 32 + lcol;
         int pixbase = 0;  // pixels past the end read a valid (discarded) column
         if (p < howo) {
