@@ -9,6 +9,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libconv2d.so")
+HARNESS = os.path.join(HERE, "convbench")
 SOURCES = ["conv2d_api.hip", "gemm_mfma.hip", "pack_kernels.hip", "direct_kernels.hip", "slice_conv.hip",
            "probes.hip"]
 
@@ -49,6 +50,17 @@ def build(verbose: bool = False) -> str:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
     os.replace(tmp, LIB)
+    # the ConvBench-style harness (host code over the library's C ABI)
+    tmp = HARNESS + ".tmp"
+    cmd = [HIPCC, "-O2", "-std=c++17", "-Wall", "-I" + os.path.join(ROOT, "include"),
+           os.path.join(CSRC, "convbench.cpp"), "-o", tmp, "-L" + HERE, "-lconv2d", "-Wl,-rpath,$ORIGIN"]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        print(r.stdout + r.stderr, file=sys.stderr)
+        raise RuntimeError("hipcc failed for convbench.cpp")
+    os.replace(tmp, HARNESS)
     return LIB
 
 

@@ -1,0 +1,71 @@
+"""The ConvBench-style harness on the GPU: main, baseline and the correctness check of
+main against baseline over a small operation list, and the speedup report on the results."""
+import csv
+import os
+import subprocess
+
+import pytest
+
+from paper_2407_10730_amd import binding as B
+from paper_2407_10730_amd import convbench_report as R
+
+pytestmark = pytest.mark.gpu
+HARNESS = os.path.join(os.path.dirname(B.__file__), "convbench")
+
+OPS = [
+    # name, n, c, h, w, k, r, s, stride, pad, dil, groups, bias, dtype, layout
+    ("reg3x3", 2, 32, 17, 15, 48, 3, 3, 1, 1, 1, 1, 1, "f32", "nchw"),
+    ("dw", 2, 64, 14, 14, 64, 3, 3, 1, 1, 1, 64, 1, "f32", "nchw"),
+    ("pw_s2", 1, 64, 20, 20, 96, 1, 1, 2, 0, 1, 1, 0, "bf16", "nhwc"),
+    ("grp_dil", 1, 16, 23, 19, 24, 5, 3, 2, 2, 2, 2, 1, "f32", "nchw"),
+    ("stem", 1, 3, 64, 64, 16, 7, 7, 2, 3, 1, 1, 1, "bf16", "nchw"),
+]
+
+
+@pytest.fixture(scope="module")
+def ops_csv(tmp_path_factory):
+    import torch
+    if torch.cuda.device_count() < 1:
+        pytest.skip("no GPU")
+    p = tmp_path_factory.mktemp("cb") / "ops.csv"
+    with open(p, "w") as f:
+        f.write(",".join(R.COLUMNS) + "\n")
+        for name, n, c, h, w, k, r, s, st, pd, dl, g, b, dt, lay in OPS:
+            f.write(f"{name},{n},{c},{h},{w},{k},{r},{s},{st},{st},{pd},{pd},{dl},{dl},{g},{b},{dt},{lay}\n")
+    return p
+
+
+def _run(ops, out, *args):
+    print(f"\n[case] convbench {' '.join(args)}", flush=True)
+    r = subprocess.run([HARNESS, "--csv", str(ops), "--out", str(out), *args], capture_output=True, text=True,
+                       timeout=240)
+    with open(out) as f:
+        return r, list(csv.DictReader(f))
+
+
+def test_correctness_main_against_baseline(ops_csv, tmp_path):
+    for datagen in ("random", "constant"):
+        r, rows = _run(ops_csv, tmp_path / "c.csv", "--exec", "correctness", "--datagen", datagen)
+        assert r.returncode == 0, r.stderr
+        assert [x["name"] for x in rows] == [o[0] for o in OPS]
+        for x in rows:
+            assert x["status"] == "ok" and x["correct"] == "1", x
+
+
+def test_main_and_baseline_timings_and_speedup(ops_csv, tmp_path):
+    res = {}
+    for exe in ("main", "baseline"):
+        r, rows = _run(ops_csv, tmp_path / f"{exe}.csv", "--exec", exe, "--warmups", "2", "--runs", "5")
+        assert r.returncode == 0, r.stderr
+        for x in rows:
+            assert x["status"] == "ok", x
+            assert float(x["op_ms"]) > 0 and float(x["tflops"]) > 0
+            assert float(x["in_microkernel_ms"]) > 0 and float(x["in_microkernel_calls"]) >= 1
+            if exe == "baseline":
+                assert x["algo"] == "im2col_gemm" and float(x["in_packing_ms"]) > 0
+        res[exe] = rows
+    assert {x["algo"] for x in res["main"]} <= {"implicit_gemm", "direct"}
+    s = R.speedup(str(tmp_path / "main.csv"), str(tmp_path / "baseline.csv"), str(tmp_path / "s.csv"),
+                  str(tmp_path / "plots"))
+    assert s["ops"] == len(OPS)
+    assert os.path.exists(tmp_path / "plots" / "speedup.png")
