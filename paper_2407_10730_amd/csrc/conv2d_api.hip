@@ -749,7 +749,11 @@ int conv2d_desc_create(const conv2d_params* params, conv2d_desc** out) {
     }
     build_ktab(d);
     plan_explicit(d);
-    if (d->direct_ok && g.G > 1 && g.Cg <= 8)
+    // Grouped layers with few channels per group sum on the vector ALUs (depthwise and the
+    // grouped direct kernel): a short reduction and few output channels per group waste most of
+    // an MFMA tile.  Measured crossover on MI355X: C/g <= 16 with K/g <= 32 runs faster there in
+    // fp32 and bf16; C/g = K/g = 32 ties in fp32 and favours the bf16 MFMA path.
+    if (d->direct_ok && g.G > 1 && (g.Cg <= 8 || (g.Cg <= 16 && g.Kg <= 32)))
         d->auto_algo = CONV2D_ALGO_DIRECT;
     else if (d->implicit_ok)
         d->auto_algo = CONV2D_ALGO_IMPLICIT_GEMM;

@@ -134,6 +134,13 @@ struct DirectArgs {
     int32_t C, H, W, K, Ho, Wo, R, S, sh, sw, ph, pw, dh, dw, Cg, Kg;
     int32_t N;
 };
+// Grouped direct kernel plan: bands of TR output rows, GB groups per block, CC input
+// channels staged at a time (window in_rows x in_cols each, xfloats LDS floats for all of
+// them; CC = GB * C/g when GB > 1), kchunks chunks of output channels per group, lds_bytes
+// of dynamic LDS.
+struct GrpPlan {
+    int32_t TR, nbands, GB, CC, in_rows, in_cols, xfloats, kchunks, lds_bytes;
+};
 hipError_t launch_direct(const DirectArgs& a, int xdt, int ydt, hipStream_t stream);
 
 // Sliced direct convolution on MFMA (small C/g * R * S): per block the filters of 64 output

@@ -8,6 +8,7 @@
 // needs for one input channel are staged once in LDS with a zero halo, then
 // each thread sums R*S taps per output from LDS.  Filter taps are
 // block-uniform and come through the scalar cache.
+#include <algorithm>
 #include <cstdlib>
 #include <type_traits>
 
@@ -117,6 +118,195 @@ __global__ __launch_bounds__(DIRECT_THREADS) void direct_kernel(DirectArgs A, in
             __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, acc[q]), ry, (uint32_t)(off * 4), 0, 0);
         else
             __builtin_amdgcn_raw_buffer_store_b16(dk_f32_to_bf16(acc[q]), ry, (uint32_t)(off * 2), 0, 0);
+    }
+}
+
+// ------------------------------------------------------------------ grouped (C/g > 1 or K/g > 1)
+// One block per (image, GB consecutive groups, band of TR output rows, chunk of KG output
+// channels per group).  The input window of the band -- every input row its outputs read,
+// with a zero halo -- is staged in LDS next to the filters transposed to [c][tap][KG], so that
+// a thread reads one input value per tap and pixel and uses it for all KG output channels,
+// and reads the KG filter values of a tap as LDS broadcasts shared by its PX pixels.  Groups
+// with few channels are batched GB to a block (their channels are consecutive in x, staged
+// at once); a group with many channels is staged CC channels at a time.  Each x element is
+// read from HBM once (halo rows of neighbouring bands hit L2); each output is written once.
+constexpr int GRP_PX = 2;                 // output pixels per thread
+constexpr int GRP_XF = 8192;              // LDS floats for the input window (32 KiB)
+constexpr int GRP_WF = 2048;              // LDS floats for the filters (8 KiB)
+constexpr int GRP_UNR = 16;               // window loads in flight per thread
+
+template <int KG, typename TX, typename TY>
+__global__ __launch_bounds__(DIRECT_THREADS) void grouped_kernel(DirectArgs A, GrpPlan P) {
+    extern __shared__ __attribute__((aligned(16))) float glds[];
+    float* xs = glds;                              // [channel][in_rows][in_cols]
+    float* ws = glds + P.xfloats;                  // [channel][R*S][KG]
+    const int G = A.C / A.Cg;
+    int b = blockIdx.x;
+    const int kc = b % P.kchunks;
+    b /= P.kchunks;
+    const int band = b % P.nbands;
+    b /= P.nbands;
+    const int ngb = (G + P.GB - 1) / P.GB;
+    const int g0 = (b % ngb) * P.GB;
+    const int n = b / ngb;
+    const int gn = min(P.GB, G - g0);              // groups of this block
+    const int kq0 = kc * KG;                       // first output channel of the chunk, within a group
+    const int nk = min(KG, A.Kg - kq0);
+    const int ho0 = band * P.TR;
+    const int rows = min(P.TR, A.Ho - ho0);
+    const int npx = rows * A.Wo;
+    const int RS = A.R * A.S;
+    const int plane = P.in_rows * P.in_cols;
+    const int hi_base = ho0 * A.sh - A.ph;
+    const int t = threadIdx.x;
+    const __amdgpu_buffer_rsrc_t rx = dk_rsrc(A.x, A.x_bytes);
+    const __amdgpu_buffer_rsrc_t ry = dk_rsrc(A.y, A.y_bytes);
+    const TX* wsrc = reinterpret_cast<const TX*>(A.w);
+
+    // window offset of the thread's pixels (pixels past the band read a valid, discarded value)
+    int base[GRP_PX];
+#pragma unroll
+    for (int q = 0; q < GRP_PX; ++q) {
+        const int o = t + q * DIRECT_THREADS;
+        const int oh = o < npx ? o / A.Wo : 0;
+        const int ow = o < npx ? o - oh * A.Wo : 0;
+        base[q] = oh * A.sh * P.in_cols + ow * A.sw;
+    }
+
+    // stage channels [ch0, ch0 + nch) of x (global channel index) and, for each, the filters
+    // of the KG output channels of its group
+    auto stage = [&](int ch0, int nch) {
+        __syncthreads();  // nobody reads the previous contents any more
+        const int total = nch * plane;
+        int c = t / plane;  // incremental (channel, row, column) of element i
+        int rem = t - c * plane;
+        int rr = rem / P.in_cols;
+        int cc = rem - rr * P.in_cols;
+        const int dc = DIRECT_THREADS / plane, drem = DIRECT_THREADS - dc * plane;
+        const int drr = drem / P.in_cols, dcc = drem - drr * P.in_cols;
+        // GRP_UNR loads in flight per thread before their LDS stores
+        for (int i0 = t; i0 < total; i0 += GRP_UNR * DIRECT_THREADS) {
+            float v[GRP_UNR];
+#pragma unroll
+            for (int u = 0; u < GRP_UNR; ++u) {
+                const int hi = hi_base + rr, wi = cc - A.pw;
+                const bool ok = (i0 + u * DIRECT_THREADS < total) & ((unsigned)hi < (unsigned)A.H) &
+                                ((unsigned)wi < (unsigned)A.W);
+                const int64_t e = (((int64_t)n * A.C + ch0 + c) * A.H + hi) * A.W + wi;
+                v[u] = dk_load(rx, ok, e, (TX*)nullptr);
+                c += dc;
+                rr += drr;
+                cc += dcc;
+                if (cc >= P.in_cols) {
+                    cc -= P.in_cols;
+                    ++rr;
+                }
+                if (rr >= P.in_rows) {
+                    rr -= P.in_rows;
+                    ++c;
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < GRP_UNR; ++u)
+                if (i0 + u * DIRECT_THREADS < total) xs[i0 + u * DIRECT_THREADS] = v[u];
+        }
+        for (int c2 = 0; c2 < nch; ++c2) {
+            const int ch = ch0 + c2;
+            const int gi = ch / A.Cg;
+            const int64_t wbase = ((int64_t)gi * A.Kg + kq0) * A.Cg + (ch - gi * A.Cg);
+            for (int j = t; j < RS * KG; j += DIRECT_THREADS) {
+                const int k = j % KG;
+                const int tap = j / KG;
+                float v = 0.0f;
+                if (k < nk) {
+                    const TX raw = wsrc[(wbase + (int64_t)k * A.Cg) * RS + tap];
+                    if constexpr (sizeof(TX) == 4) v = __builtin_bit_cast(float, raw);
+                    else v = __builtin_bit_cast(float, (uint32_t)raw << 16);
+                }
+                ws[c2 * RS * KG + j] = v;
+            }
+        }
+        __syncthreads();
+    };
+
+    float acc[GRP_PX][KG];
+    // channels [c0, c0 + ccn) staged at LDS channel slot s0
+    auto accumulate = [&](int s0, int ccn) {
+        for (int c = 0; c < ccn; ++c) {
+            const float* xc = xs + (s0 + c) * plane;
+            const float* wc = ws + (s0 + c) * RS * KG;
+            for (int r = 0; r < A.R; ++r) {
+                const float* xr = xc + r * A.dh * P.in_cols;
+                const float* wr = wc + r * A.S * KG;
+                for (int sx = 0; sx < A.S; ++sx) {
+                    float wv[KG];
+                    if constexpr (KG % 4 == 0) {
+#pragma unroll
+                        for (int k4 = 0; k4 < KG / 4; ++k4) {
+                            const f32x4 v = *reinterpret_cast<const f32x4*>(wr + sx * KG + 4 * k4);
+                            wv[4 * k4] = v[0]; wv[4 * k4 + 1] = v[1]; wv[4 * k4 + 2] = v[2]; wv[4 * k4 + 3] = v[3];
+                        }
+                    } else {
+#pragma unroll
+                        for (int k = 0; k < KG; ++k) wv[k] = wr[sx * KG + k];
+                    }
+#pragma unroll
+                    for (int q = 0; q < GRP_PX; ++q) {
+                        const float xv = xr[base[q] + sx * A.dw];
+#pragma unroll
+                        for (int k = 0; k < KG; ++k) acc[q][k] = __builtin_fmaf(wv[k], xv, acc[q][k]);
+                    }
+                }
+            }
+        }
+    };
+    auto store = [&](int gi) {
+        const int kglob0 = gi * A.Kg + kq0;
+        float bv[KG];
+#pragma unroll
+        for (int k = 0; k < KG; ++k) bv[k] = (A.bias && k < nk) ? A.bias[kglob0 + k] : 0.0f;
+#pragma unroll
+        for (int q = 0; q < GRP_PX; ++q) {
+            const int o = t + q * DIRECT_THREADS;
+            if (o >= npx) continue;
+            const int oh = ho0 + o / A.Wo;
+            const int ow = o % A.Wo;
+#pragma unroll
+            for (int k = 0; k < KG; ++k) {
+                if (k >= nk) break;
+                const int64_t off = (((int64_t)n * A.K + kglob0 + k) * A.Ho + oh) * A.Wo + ow;
+                if constexpr (sizeof(TY) == 4)
+                    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, acc[q][k] + bv[k]), ry,
+                                                          (uint32_t)(off * 4), 0, 0);
+                else
+                    __builtin_amdgcn_raw_buffer_store_b16(dk_f32_to_bf16(acc[q][k] + bv[k]), ry,
+                                                          (uint32_t)(off * 2), 0, 0);
+            }
+        }
+    };
+    auto zero = [&]() {
+#pragma unroll
+        for (int q = 0; q < GRP_PX; ++q)
+#pragma unroll
+            for (int k = 0; k < KG; ++k) acc[q][k] = 0.0f;
+    };
+
+    if (P.GB > 1) {
+        // the block's groups are staged together (P.CC >= GB * Cg)
+        stage(g0 * A.Cg, gn * A.Cg);
+        for (int gg = 0; gg < gn; ++gg) {
+            zero();
+            accumulate(gg * A.Cg, A.Cg);
+            store(g0 + gg);
+        }
+    } else {
+        zero();
+        for (int c0 = 0; c0 < A.Cg; c0 += P.CC) {
+            const int ccn = min(P.CC, A.Cg - c0);
+            stage(g0 * A.Cg + c0, ccn);
+            accumulate(0, ccn);
+        }
+        store(g0);
     }
 }
 
@@ -443,10 +633,72 @@ static int direct_rows(const DirectArgs& a, int* in_rows, int* in_cols) {
     return rows;
 }
 
+// Grouped kernel plan for KG output channels per block; false when the shape does not fit.
+static bool grp_plan(const DirectArgs& a, int KG, GrpPlan* p) {
+    const int in_cols = (a.Wo - 1) * a.sw + (a.S - 1) * a.dw + 1;
+    auto in_rows = [&](int tr) { return (tr - 1) * a.sh + (a.R - 1) * a.dh + 1; };
+    const int RS = a.R * a.S;
+    if (a.Wo > GRP_PX * DIRECT_THREADS || RS * KG > GRP_WF) return false;
+    int tr = std::max(1, std::min(a.Ho, GRP_PX * DIRECT_THREADS / a.Wo));
+    while (tr > 1 && (int64_t)in_rows(tr) * in_cols > GRP_XF) --tr;
+    const int64_t window = (int64_t)in_rows(tr) * in_cols;
+    if (window > GRP_XF) return false;
+    p->TR = tr;
+    p->in_rows = in_rows(tr);
+    p->in_cols = in_cols;
+    // channels that fit: the window and the filters of each
+    const int fit = (int)std::min<int64_t>(GRP_XF / window, (int64_t)(GRP_WF / (RS * KG)));
+    if (fit < 1) return false;
+    const int G = a.C / a.Cg;
+    // groups with few channels go GB to a block, about 16 channels' worth
+    p->GB = std::max(1, std::min({G, 16 / a.Cg, fit / a.Cg}));
+    p->CC = p->GB > 1 ? p->GB * a.Cg : std::min(a.Cg, fit);
+    p->xfloats = (int)(((int64_t)p->CC * window + 3) / 4 * 4);
+    p->lds_bytes = (p->xfloats + p->CC * RS * KG) * 4;
+    p->nbands = (a.Ho + tr - 1) / tr;
+    p->kchunks = (a.Kg + KG - 1) / KG;
+    const int64_t blocks = (int64_t)a.N * ((G + p->GB - 1) / p->GB) * p->nbands * p->kchunks;
+    return blocks <= 0x7fffffffLL;
+}
+
+template <int KG>
+static hipError_t launch_grp_t(const DirectArgs& a, const GrpPlan& p, int xdt, int ydt, hipStream_t stream) {
+    const int G = a.C / a.Cg;
+    dim3 grid((unsigned)((int64_t)a.N * ((G + p.GB - 1) / p.GB) * p.nbands * p.kchunks));
+    if (xdt == CONV2D_F32)
+        hipLaunchKernelGGL((grouped_kernel<KG, float, float>), grid, dim3(DIRECT_THREADS), p.lds_bytes, stream, a, p);
+    else if (ydt == CONV2D_BF16)
+        hipLaunchKernelGGL((grouped_kernel<KG, uint16_t, uint16_t>), grid, dim3(DIRECT_THREADS), p.lds_bytes, stream,
+                           a, p);
+    else
+        hipLaunchKernelGGL((grouped_kernel<KG, uint16_t, float>), grid, dim3(DIRECT_THREADS), p.lds_bytes, stream,
+                           a, p);
+    return hipGetLastError();
+}
+
+// Grouped fast path: KG = the smallest of 1, 2, 4, 8, 16 that covers K/g (chunks of 16 beyond).
+static hipError_t try_launch_grouped(const DirectArgs& a, int xdt, int ydt, hipStream_t stream, bool* launched) {
+    *launched = false;
+    const int KG = a.Kg <= 1 ? 1 : a.Kg <= 2 ? 2 : a.Kg <= 4 ? 4 : a.Kg <= 8 ? 8 : 16;
+    GrpPlan p;
+    if (!grp_plan(a, KG, &p)) return hipSuccess;
+    *launched = true;
+    switch (KG) {
+        case 1: return launch_grp_t<1>(a, p, xdt, ydt, stream);
+        case 2: return launch_grp_t<2>(a, p, xdt, ydt, stream);
+        case 4: return launch_grp_t<4>(a, p, xdt, ydt, stream);
+        case 8: return launch_grp_t<8>(a, p, xdt, ydt, stream);
+        default: return launch_grp_t<16>(a, p, xdt, ydt, stream);
+    }
+}
+
 hipError_t launch_direct(const DirectArgs& a, int xdt, int ydt, hipStream_t stream) {
+    // CONV2D_DW_GENERIC (tests): the generic per-plane kernel for every shape
     if (!std::getenv("CONV2D_DW_GENERIC")) {
         bool launched = false;
-        const hipError_t e = try_launch_dw(a, xdt, ydt, stream, &launched);
+        hipError_t e = try_launch_dw(a, xdt, ydt, stream, &launched);
+        if (launched || e != hipSuccess) return e;
+        e = try_launch_grouped(a, xdt, ydt, stream, &launched);
         if (launched || e != hipSuccess) return e;
     }
     int in_rows = 0, in_cols = 0;

@@ -205,6 +205,26 @@ def test_tail_split_plan(monkeypatch):
     assert plan(cfg2).tail_pieces == 5
 
 
+def test_grouped_auto_choice():
+    """Grouped layers: few channels per group go to the direct (vector ALU) kernels, wider
+    groups to the MFMA implicit path."""
+    base = datagen.CONFIGS["cfg2"].with_(c=256, k=256)
+
+    def algo(**kw):
+        d = B.conv2d_desc_create(params_for(base.with_(**kw)))
+        try:
+            return B.conv2d_plan_query(d, B.CONV2D_ALGO_AUTO).algo
+        finally:
+            B.conv2d_desc_destroy(d)
+    assert algo(groups=256) == B.CONV2D_ALGO_DIRECT                  # depthwise
+    assert algo(groups=32) == B.CONV2D_ALGO_DIRECT                   # C/g = K/g = 8
+    assert algo(groups=16) == B.CONV2D_ALGO_DIRECT                   # 16, 16
+    assert algo(groups=8) == B.CONV2D_ALGO_IMPLICIT_GEMM             # 32, 32
+    assert algo(groups=16, k=1024) == B.CONV2D_ALGO_IMPLICIT_GEMM    # 16, 64
+    assert algo(groups=64, k=2048) == B.CONV2D_ALGO_DIRECT           # 4, 32
+    assert algo(groups=1) == B.CONV2D_ALGO_IMPLICIT_GEMM
+
+
 def test_explicit_workspace_chunking(monkeypatch):
     cs = datagen.CONFIGS["cfg4"]
     d = B.conv2d_desc_create(params_for(cs))

@@ -329,6 +329,33 @@ def test_tail_split_planned_cfg2_repeat():
     assert pt <= GATE["f32"]
 
 
+# grouped layers on the direct kernel (C/g > 1 or K/g > 1): per-group output channel chunks
+# of 1/2/4/8/16, input channels staged in chunks when the window and filters do not fit at
+# once, bands of output rows, strides, dilations, rectangular filters, ragged sizes
+GROUPED = [
+    _shape(2, 16, 11, 13, 16, 3, 3, pd=(1, 1), g=8, seed=250),            # C/g 2, K/g 2
+    _shape(1, 24, 9, 10, 8, 3, 3, pd=(1, 1), g=8, seed=251),              # C/g 3, K/g 1
+    _shape(2, 32, 14, 14, 32, 3, 3, pd=(1, 1), g=8, seed=252),            # 4, 4
+    _shape(1, 64, 17, 15, 64, 3, 3, st=(2, 2), pd=(1, 1), g=8, seed=253), # 8, 8, strided
+    _shape(1, 48, 12, 12, 96, 5, 3, pd=(2, 1), dl=(1, 2), g=3, seed=254), # 16, 32 (two chunks), dilated
+    _shape(1, 96, 9, 9, 120, 3, 3, pd=(2, 2), dl=(2, 2), g=3, seed=255),  # 32, 40 (three chunks)
+    _shape(1, 128, 10, 9, 48, 7, 7, pd=(3, 3), g=2, seed=256),            # 64 channels in chunks of 2
+    _shape(2, 12, 40, 33, 18, 3, 3, st=(1, 2), pd=(1, 1), g=6, seed=257), # 2, 3, bands of rows
+    _shape(1, 8, 70, 700, 16, 1, 1, g=4, seed=258),                       # rows too wide: generic kernel
+    _shape(1, 6, 5, 5, 12, 5, 5, pd=(2, 2), g=6, seed=259),               # C/g 1, K/g 2 (multiplier)
+    _shape(2, 40, 13, 11, 20, 3, 3, pd=(1, 1), g=10, seed=260),           # 4, 2: groups 4 to a block, 2 left
+    _shape(1, 24, 31, 29, 72, 3, 3, st=(2, 2), pd=(1, 1), g=12, seed=261),# 2, 6: 8 groups to a block
+]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("idx", range(len(GROUPED)))
+def test_grouped_direct(idx, dt):
+    cs = GROUPED[idx].with_(x_dtype=dt, y_dtype=dt)
+    _check(cs, DIRECT)
+    _check(cs.with_(y_dtype="f32"), DIRECT, "integer")
+
+
 EDGE_ALGOS = [("implicit", IMPLICIT, None, None), ("implicit-gemm", IMPLICIT, "0", None),
               ("implicit-slice4", IMPLICIT, "1", "4"), ("implicit-slice8", IMPLICIT, "1", "8"),
               ("implicit-nhwc", IMPLICIT, "nhwc", None),
