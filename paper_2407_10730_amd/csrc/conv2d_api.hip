@@ -753,7 +753,22 @@ int conv2d_desc_create(const conv2d_params* params, conv2d_desc** out) {
     // grouped direct kernel): a short reduction and few output channels per group waste most of
     // an MFMA tile.  Measured crossover on MI355X: C/g <= 16 with K/g <= 32 runs faster there in
     // fp32 and bf16; C/g = K/g = 32 ties in fp32 and favours the bf16 MFMA path.
-    if (d->direct_ok && g.G > 1 && (g.Cg <= 8 || (g.Cg <= 16 && g.Kg <= 32)))
+    //
+    // Ungrouped layers with very few output channels (K <= 16) waste 3/4 or more of every
+    // 64-row MFMA tile; the grouped direct kernel (one "group" of all channels) computes them on
+    // the vector ALUs instead when its grid fills the chip (its blocks walk the whole reduction,
+    // so a small grid leaves CUs idle) and the filter is not 1x1 (a pointwise layer is a plain
+    // GEMM with no gather, which the MFMA path runs well even with few rows).
+    bool direct_small_k = false;
+    if (d->direct_ok && g.G == 1 && g.K <= 16 && g.R * g.S > 1) {
+        DirectArgs da{};
+        da.C = (int32_t)g.C; da.H = (int32_t)g.H; da.W = (int32_t)g.W; da.K = (int32_t)g.K;
+        da.Ho = (int32_t)g.Ho; da.Wo = (int32_t)g.Wo; da.R = (int32_t)g.R; da.S = (int32_t)g.S;
+        da.sh = g.sh; da.sw = g.sw; da.ph = g.ph; da.pw = g.pw; da.dh = g.dh; da.dw = g.dw;
+        da.Cg = (int32_t)g.Cg; da.Kg = (int32_t)g.Kg; da.N = (int32_t)g.N;
+        direct_small_k = grouped_blocks(da) >= 384;
+    }
+    if (d->direct_ok && ((g.G > 1 && (g.Cg <= 8 || (g.Cg <= 16 && g.Kg <= 32))) || direct_small_k))
         d->auto_algo = CONV2D_ALGO_DIRECT;
     else if (d->implicit_ok)
         d->auto_algo = CONV2D_ALGO_IMPLICIT_GEMM;

@@ -142,6 +142,8 @@ struct GrpPlan {
     int32_t TR, nbands, GB, CC, in_rows, in_cols, xfloats, kchunks, lds_bytes;
 };
 hipError_t launch_direct(const DirectArgs& a, int xdt, int ydt, hipStream_t stream);
+// Blocks the grouped direct kernel launches for this shape (0: it does not take the shape).
+int64_t grouped_blocks(const DirectArgs& a);
 
 // Sliced direct convolution on MFMA (small C/g * R * S): per block the filters of 64 output
 // channels, the input rows of 256 consecutive output pixels of one image and a table of the

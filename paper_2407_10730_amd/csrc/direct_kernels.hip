@@ -692,6 +692,13 @@ static hipError_t try_launch_grouped(const DirectArgs& a, int xdt, int ydt, hipS
     }
 }
 
+int64_t grouped_blocks(const DirectArgs& a) {
+    const int KG = a.Kg <= 1 ? 1 : a.Kg <= 2 ? 2 : a.Kg <= 4 ? 4 : a.Kg <= 8 ? 8 : 16;
+    GrpPlan p;
+    if (!grp_plan(a, KG, &p)) return 0;
+    return (int64_t)a.N * ((a.C / a.Cg + p.GB - 1) / p.GB) * p.nbands * p.kchunks;
+}
+
 hipError_t launch_direct(const DirectArgs& a, int xdt, int ydt, hipStream_t stream) {
     // CONV2D_DW_GENERIC (tests): the generic per-plane kernel for every shape
     if (!std::getenv("CONV2D_DW_GENERIC")) {

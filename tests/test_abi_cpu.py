@@ -223,6 +223,12 @@ def test_grouped_auto_choice():
     assert algo(groups=16, k=1024) == B.CONV2D_ALGO_IMPLICIT_GEMM    # 16, 64
     assert algo(groups=64, k=2048) == B.CONV2D_ALGO_DIRECT           # 4, 32
     assert algo(groups=1) == B.CONV2D_ALGO_IMPLICIT_GEMM
+    # ungrouped, K <= 16: the direct kernel when its grid fills the chip and the filter is not 1x1
+    assert algo(c=512, k=3, h=112, w=112) == B.CONV2D_ALGO_DIRECT        # 32 images x 13 bands
+    assert algo(c=512, k=16, h=112, w=112) == B.CONV2D_ALGO_DIRECT
+    assert algo(c=512, k=32, h=112, w=112) == B.CONV2D_ALGO_IMPLICIT_GEMM
+    assert algo(n=2, c=512, k=3, h=112, w=112) == B.CONV2D_ALGO_IMPLICIT_GEMM   # 26 blocks
+    assert algo(c=512, k=3, h=112, w=112, r=1, s=1, pad=(0, 0)) == B.CONV2D_ALGO_IMPLICIT_GEMM
 
 
 def test_explicit_workspace_chunking(monkeypatch):
