@@ -207,13 +207,13 @@ def measured_peaks(B, torch):
 
 
 PROFILE_COMMANDS = {
-    "trace": "rocprofv3 --kernel-trace --stats -f csv -d {d}/trace -o run -- python -u bench.py --no-cpu --workload {w}",
+    "trace": "rocprofv3 --kernel-trace --stats -f csv -d {d}/trace -o run -- python -u bench.py --no-cpu --no-pack-probe --workload {w}",
     "pmc1": "rocprofv3 --pmc SQ_WAVES SQ_BUSY_CYCLES SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU SQ_INSTS_MFMA "
-            "SQ_LDS_BANK_CONFLICT GRBM_GUI_ACTIVE -f csv -d {d}/pmc1 -o run -- python -u bench.py --no-cpu "
+            "SQ_LDS_BANK_CONFLICT GRBM_GUI_ACTIVE -f csv -d {d}/pmc1 -o run -- python -u bench.py --no-cpu --no-pack-probe "
             "--steps 5 --warmup 1 --cold-runs 1 --workload {w}",
-    "pmc2": "rocprofv3 --pmc FETCH_SIZE -f csv -d {d}/pmc2 -o run -- python -u bench.py --no-cpu --steps 5 "
+    "pmc2": "rocprofv3 --pmc FETCH_SIZE -f csv -d {d}/pmc2 -o run -- python -u bench.py --no-cpu --no-pack-probe --steps 5 "
             "--warmup 1 --cold-runs 1 --calibrate-copy --workload {w}",
-    "pmc3": "rocprofv3 --pmc WRITE_SIZE -f csv -d {d}/pmc3 -o run -- python -u bench.py --no-cpu --steps 5 "
+    "pmc3": "rocprofv3 --pmc WRITE_SIZE -f csv -d {d}/pmc3 -o run -- python -u bench.py --no-cpu --no-pack-probe --steps 5 "
             "--warmup 1 --cold-runs 1 --calibrate-copy --workload {w}",
 }
 
@@ -249,11 +249,16 @@ def summarize_profiles(d, workload, algo_name="implicit_gemm"):
             counters[(r["Kernel_Name"], r["Grid_Size"])][r["Counter_Name"]].append(float(r["Counter_Value"]))
     # calibration: the 1 GiB device copy
     cal_f = cal_w = None
+    # (only the dispatches of that size: the same kernel also runs small copies)
     for (name, grid), cs in counters.items():
-        if "copyBuffer" in name and cs.get("FETCH_SIZE") and max(cs["FETCH_SIZE"]) > 400000:
-            cal_f = (1 << 20) / (sum(cs["FETCH_SIZE"]) / len(cs["FETCH_SIZE"]))
-        if "copyBuffer" in name and cs.get("WRITE_SIZE") and max(cs["WRITE_SIZE"]) > 400000:
-            cal_w = (1 << 20) / (sum(cs["WRITE_SIZE"]) / len(cs["WRITE_SIZE"]))
+        if "copyBuffer" not in name:
+            continue
+        big_f = [v for v in cs.get("FETCH_SIZE", []) if v > 400000]
+        big_w = [v for v in cs.get("WRITE_SIZE", []) if v > 400000]
+        if big_f:
+            cal_f = (1 << 20) / (sum(big_f) / len(big_f))
+        if big_w:
+            cal_w = (1 << 20) / (sum(big_w) / len(big_w))
     lines += ["", "## counters per kernel (mean per dispatch)", ""]
     for k in ("pmc1", "pmc2", "pmc3"):
         lines.append("command: `" + PROFILE_COMMANDS[k].format(d="gpurun_out/<dir>", w=workload) + "`")
@@ -373,6 +378,9 @@ def main():
                     help="untimed steps first; the GPU clocks need a few milliseconds of work to ramp up")
     ap.add_argument("--workload", default="cfg2")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-pack-probe", action="store_true",
+                    help="skip the pack probe (its loader-only launches share the microkernel's name, so "
+                         "profiling runs leave them out)")
     ap.add_argument("--cold-runs", type=int, default=20)
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (reference kernel for HBM byte counters)")
@@ -487,7 +495,7 @@ def main():
     # pack probe: the implicit microkernel's loader alone (gather into LDS, no MFMA, no
     # output) against the full microkernel -- an estimate of the fused packing share
     probe = None
-    if algo == B.CONV2D_ALGO_IMPLICIT_GEMM:
+    if algo == B.CONV2D_ALGO_IMPLICIT_GEMM and not args.no_pack_probe:
         stream = torch.cuda.current_stream()
         B.conv2d_set_timing(dc.desc, B.CONV2D_TIMING_OFF)
         dc.run(algo, stream)
