@@ -491,6 +491,22 @@ def main():
         "pack_share": bd_e["ms"]["in_packing"] / opsum if opsum > 0 else None,
         "t_explicit_over_t_implicit": ms_e / ms_per_step,
     }
+    # Winograd F(2x2, 3x3) on the same workload when it applies (3x3, stride 1, fp32)
+    wino = None
+    if algo != B.CONV2D_ALGO_WINOGRAD:
+        try:
+            dc.plan(B.CONV2D_ALGO_WINOGRAD)
+            wino_ok = True
+        except B.Conv2dError:
+            wino_ok = False
+        if wino_ok:
+            wall_w, _ = time_algo(dc, B.CONV2D_ALGO_WINOGRAD, ne, 3, B, torch, B.CONV2D_TIMING_OFF)
+            _, bd_w = time_algo(dc, B.CONV2D_ALGO_WINOGRAD, ne, 1, B, torch, B.CONV2D_TIMING_PHASES)
+            ms_w = wall_w * 1e3 / ne
+            wino = {"ms_per_step": ms_w, "tflops": flops / (ms_w * 1e-3) / 1e12,
+                    "phase_ms_per_step": {p: v / bd_w["fwd_calls"] for p, v in bd_w["ms"].items()
+                                          if p != "pre_analysis"},
+                    "t_winograd_over_t_main": ms_w / ms_per_step}
     cold = cold_median(dc, algo, args.cold_runs, B, torch)
     # pack probe: the implicit microkernel's loader alone (gather into LDS, no MFMA, no
     # output) against the full microkernel -- an estimate of the fused packing share
@@ -527,6 +543,7 @@ def main():
         "fused_phases": bd["fused"],
         "pre_analysis_ms_once": bd["ms"]["pre_analysis"],
         "explicit_im2col": explicit,
+        "winograd": wino,
         "cold_cache_ms_median": cold,
         "cold_cache_tflops": flops / (cold * 1e-3) / 1e12,
         "implicit_pack_probe": probe,

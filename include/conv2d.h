@@ -55,8 +55,15 @@ enum {
     CONV2D_ALGO_IMPLICIT_GEMM = 1, /* sliced direct convolution: im2col slices gathered into LDS, MFMA */
     CONV2D_ALGO_IM2COL_GEMM = 2,   /* explicit im2col pack, MFMA GEMM, unpack (ConvBench's default baseline) */
     CONV2D_ALGO_DIRECT = 3,        /* direct VALU kernel for depthwise / small-group convolutions */
-    CONV2D_ALGO_COUNT = 4
+    CONV2D_ALGO_WINOGRAD = 4,      /* Winograd F(2x2,3x3): 3x3, stride 1, dilation 1, one group, fp32 */
+    CONV2D_ALGO_COUNT = 5
 };
+/* Winograd's phases: PRE_REORDER the filter transform, IN_PACKING the input
+ * transform, IN_MICROKERNEL the 16 GEMMs of the transformed domain, IN_UNPACKING
+ * the output transform with the bias (Sec. I names the family; the minimal
+ * filtering algorithm is Lavin and Gray's).  Its workspace (transformed filters,
+ * then inputs and products per chunk of 2x2 output tiles) obeys
+ * CONV2D_WORKSPACE_LIMIT_BYTES like the explicit path's. */
 
 /* Processing steps of the timing tool (Sec. III-A): pre-convolution analysis and
  * reordering; in-convolution tiling, packing, microkernel and unpacking;
@@ -163,8 +170,8 @@ int conv2d_output_shape(const conv2d_desc* desc, int64_t out_nkhw[4]);
  *   y    : N x K x Ho x Wo (NCHW) or N x Ho x Wo x K (NHWC), y_dtype
  *   algo : CONV2D_ALGO_*; AUTO lets the planner choose.
  * Errors: E_NULL (x, w, y or a required bias missing), E_INVALID (bad algo),
- * E_UNSUPPORTED (algo cannot run this op), E_ALLOC (explicit path workspace
- * over CONV2D_WORKSPACE_LIMIT_BYTES, default 1 GiB, even after chunking),
+ * E_UNSUPPORTED (algo cannot run this op), E_ALLOC (explicit or Winograd
+ * workspace over CONV2D_WORKSPACE_LIMIT_BYTES, default 1 GiB, even after chunking),
  * E_HIP (a launch failed).  Faults inside kernels surface at the next
  * synchronisation.  Results are bitwise reproducible for a fixed algo. */
 int conv2d_fwd(conv2d_desc* desc, const void* x, const void* w, const float* bias, void* y,

@@ -29,7 +29,8 @@ CONV2D_E_NO_DATA = -7
 CONV2D_NCHW, CONV2D_NHWC = 0, 1
 CONV2D_F32, CONV2D_BF16 = 0, 1
 CONV2D_ALGO_AUTO, CONV2D_ALGO_IMPLICIT_GEMM, CONV2D_ALGO_IM2COL_GEMM, CONV2D_ALGO_DIRECT = 0, 1, 2, 3
-ALGO_NAMES = {0: "auto", 1: "implicit_gemm", 2: "im2col_gemm", 3: "direct"}
+CONV2D_ALGO_WINOGRAD = 4
+ALGO_NAMES = {0: "auto", 1: "implicit_gemm", 2: "im2col_gemm", 3: "direct", 4: "winograd"}
 PHASE_NAMES = ["pre_analysis", "pre_reorder", "in_tiling", "in_packing", "in_microkernel",
                "in_unpacking", "post_reorder"]
 CONV2D_PH_COUNT = 7

@@ -11,7 +11,7 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libconv2d.so")
 HARNESS = os.path.join(HERE, "convbench")
 SOURCES = ["conv2d_api.hip", "gemm_mfma.hip", "pack_kernels.hip", "direct_kernels.hip", "slice_conv.hip",
-           "probes.hip"]
+           "probes.hip", "winograd.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -66,6 +66,16 @@ struct ExplicitPlan {
     int status = CONV2D_OK;
 };
 
+// Winograd F(2x2, 3x3): transformed filters U [16][K][C] once per call, then chunks of tc
+// tiles: transformed inputs V [16][C][tc] and GEMM results M [16][K][tc] in the workspace.
+struct WinoPlan {
+    bool ok = false;
+    int status = CONV2D_E_UNSUPPORTED;
+    int64_t tiles = 0, tc = 0, chunks = 0;
+    int64_t u_bytes = 0, v_bytes = 0, m_bytes = 0;  // V and M per chunk
+    GemmPlan gemm;
+};
+
 int64_t elem_size(int dt) { return dt == CONV2D_BF16 ? 2 : 4; }
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -174,6 +184,11 @@ struct conv2d_desc {
     int64_t wr_bytes = 0;
     void* sk = nullptr;  // partial sums of the split reduction
     int64_t sk_bytes = 0;
+    WinoPlan wino;
+    void* wu = nullptr;  // Winograd transformed filters
+    int64_t wu_bytes = 0;
+    void* wvm = nullptr;  // Winograd V and M of one chunk
+    int64_t wvm_bytes = 0;
     void* tp = nullptr;  // partial tiles of the tail split
     int64_t tp_bytes = 0;
     uint32_t* tc = nullptr;  // arrival counters of the tail split (zeroed once, reset by the kernel)
@@ -307,6 +322,48 @@ void plan_tail(conv2d_desc* d) {
 
 int64_t tail_part_bytes(const GemmPlan& gp) {
     return (int64_t)gp.tail_tiles * gp.tail_pieces * gp.bm * gp.bn * 4;
+}
+
+// Winograd F(2x2, 3x3) runs 3x3 filters at stride 1 and dilation 1 with one group in fp32.
+// Tiles go in chunks whose V and M fit CONV2D_WORKSPACE_LIMIT_BYTES (default 1 GiB) and the
+// 2 GiB buffer limit.
+void plan_winograd(conv2d_desc* d) {
+    const Geometry& g = d->g;
+    WinoPlan& p = d->wino;
+    p = WinoPlan{};
+    if (g.R != 3 || g.S != 3 || g.sh != 1 || g.sw != 1 || g.dh != 1 || g.dw != 1 || g.G != 1 ||
+        g.xdt != CONV2D_F32 || g.ydt != CONV2D_F32 || g.x_elems * 4 > kBufferLimit || g.y_elems * 4 > kBufferLimit)
+        return;
+    p.u_bytes = 16 * g.K * g.C * 4;
+    if (p.u_bytes > kBufferLimit) return;
+    p.tiles = g.N * ceil_div(g.Ho, 2) * ceil_div(g.Wo, 2);
+    int64_t cap = env_int64("CONV2D_WORKSPACE_LIMIT_BYTES", (int64_t)1 << 30);
+    if (cap < 0) cap = 0;
+    int64_t tc = cap / (16 * (g.C + g.K) * 4);
+    tc = std::min<int64_t>(tc, kBufferLimit / (16 * g.C * 4));
+    tc = std::min<int64_t>(tc, kBufferLimit / (16 * g.K * 4));
+    tc = std::min<int64_t>(tc, p.tiles);
+    if (tc < 1) {
+        p.status = CONV2D_E_ALLOC;
+        return;
+    }
+    p.tc = tc;
+    p.chunks = ceil_div(p.tiles, tc);
+    p.v_bytes = 16 * g.C * tc * 4;
+    p.m_bytes = 16 * g.K * tc * 4;
+    // 64 x 128 tiles: measured fastest for these GEMMs (dense operands, reductions of a few
+    // hundred channels) on MI355X, ahead of 64 x 64, 128 x 128 and 64 x 256
+    p.gemm = choose_tile(g.K, tc, 16, g.C, CONV2D_F32, g.C);
+    if (!std::getenv("CONV2D_GEMM")) {
+        p.gemm.tile = TILE_64x128;
+        p.gemm.bm = kTileShapes[TILE_64x128].bm;
+        p.gemm.bn = kTileShapes[TILE_64x128].bn;
+        p.gemm.bk = 16;
+        p.gemm.pf = 1;
+        p.gemm.nstages = (int)ceil_div(g.C, 16);
+    }
+    p.ok = true;
+    p.status = CONV2D_OK;
 }
 
 void plan_explicit(conv2d_desc* d) {
@@ -589,6 +646,80 @@ int run_implicit(conv2d_desc* d, const void* x, const void* w, const float* bias
     return sc.end();
 }
 
+int run_winograd(conv2d_desc* d, const void* x, const void* w, const float* bias, void* y, hipStream_t s,
+                 bool ph) {
+    const Geometry& g = d->g;
+    const WinoPlan& p = d->wino;
+    if (!p.ok) return p.status;
+    CV_TRY(ensure_buffer(&d->wu, &d->wu_bytes, p.u_bytes));
+    CV_TRY(ensure_buffer(&d->wvm, &d->wvm_bytes, p.v_bytes + p.m_bytes));
+    float* u = static_cast<float*>(d->wu);
+    float* v = static_cast<float*>(d->wvm);
+    float* m = reinterpret_cast<float*>(static_cast<char*>(d->wvm) + p.v_bytes);
+    {
+        // pre-convolution reordering: the filter transform
+        Scope sc(d, CONV2D_ALGO_WINOGRAD, CONV2D_PH_PRE_REORDER, s, ph);
+        CV_TRY(sc.begin());
+        CV_HIP(launch_wino_filter(static_cast<const float*>(w), u, (int)g.K, (int)g.C, s));
+        CV_TRY(sc.end());
+    }
+    WinoArgs wa{};
+    wa.x = x;
+    wa.x_bytes = (uint32_t)(g.x_elems * 4);
+    wa.y = y;
+    wa.y_bytes = (uint32_t)(g.y_elems * 4);
+    wa.bias = g.has_bias ? bias : nullptr;
+    wa.C = (int32_t)g.C; wa.H = (int32_t)g.H; wa.W = (int32_t)g.W; wa.K = (int32_t)g.K;
+    wa.Ho = (int32_t)g.Ho; wa.Wo = (int32_t)g.Wo; wa.ph = g.ph; wa.pw = g.pw;
+    wa.th = (int32_t)ceil_div(g.Ho, 2);
+    wa.tw = (int32_t)ceil_div(g.Wo, 2);
+    for (int64_t t0 = 0; t0 < p.tiles; t0 += p.tc) {
+        wa.t0 = t0;
+        wa.tc = (int32_t)std::min<int64_t>(p.tc, p.tiles - t0);
+        {
+            Scope sc(d, CONV2D_ALGO_WINOGRAD, CONV2D_PH_IN_PACKING, s, ph);
+            CV_TRY(sc.begin());
+            CV_HIP(launch_wino_input(wa, v, s));
+            CV_TRY(sc.end());
+        }
+        {
+            // 16 GEMMs, one per transformed position: M[xi] = U[xi] (K x C) * V[xi] (C x tc)
+            const GemmPlan& gp = p.gemm;
+            GemmArgs a{};
+            a.a = u;
+            a.a_bytes = (uint32_t)p.u_bytes;
+            a.lda = (int32_t)g.C;
+            a.a_gstride = g.K * g.C;
+            a.b = v;
+            a.b_bytes = (uint32_t)(16 * g.C * wa.tc * 4);
+            a.b_gstride = g.C * wa.tc;
+            a.ldb = wa.tc;
+            a.M = (int32_t)g.K;
+            a.Kred = (int32_t)g.C;
+            a.P = wa.tc;
+            a.nstages = gp.nstages;
+            a.grid_m = (int32_t)ceil_div(g.K, gp.bm);
+            a.grid_p = (int32_t)ceil_div(wa.tc, gp.bn);
+            a.y = m;
+            a.y_bytes = (uint32_t)(16 * g.K * wa.tc * 4);
+            a.ldc = wa.tc;
+            a.c_gstride = g.K * wa.tc;
+            a.HoWo = (int32_t)(g.Ho * g.Wo);
+            Scope sc(d, CONV2D_ALGO_WINOGRAD, CONV2D_PH_IN_MICROKERNEL, s, ph);
+            CV_TRY(sc.begin());
+            CV_HIP(dispatch_gemm(gp, a, BSRC_DENSE, EPI_DENSE, CONV2D_F32, CONV2D_F32, 16, s));
+            CV_TRY(sc.end());
+        }
+        {
+            Scope sc(d, CONV2D_ALGO_WINOGRAD, CONV2D_PH_IN_UNPACKING, s, ph);
+            CV_TRY(sc.begin());
+            CV_HIP(launch_wino_output(wa, m, s));
+            CV_TRY(sc.end());
+        }
+    }
+    return CONV2D_OK;
+}
+
 int run_explicit(conv2d_desc* d, const void* x, const void* w, const float* bias, void* y, hipStream_t s,
                  bool ph) {
     const Geometry& g = d->g;
@@ -749,6 +880,7 @@ int conv2d_desc_create(const conv2d_params* params, conv2d_desc** out) {
     }
     build_ktab(d);
     plan_explicit(d);
+    plan_winograd(d);
     // Grouped layers with few channels per group sum on the vector ALUs (depthwise and the
     // grouped direct kernel): a short reduction and few output channels per group waste most of
     // an MFMA tile.  Measured crossover on MI355X: C/g <= 16 with K/g <= 32 runs faster there in
@@ -770,6 +902,11 @@ int conv2d_desc_create(const conv2d_params* params, conv2d_desc** out) {
     }
     if (d->direct_ok && ((g.G > 1 && (g.Cg <= 8 || (g.Cg <= 16 && g.Kg <= 32))) || direct_small_k))
         d->auto_algo = CONV2D_ALGO_DIRECT;
+    // 3x3 stride-1 fp32 layers with at least 128 input and output channels: Winograd F(2x2,3x3)
+    // does 2.25x fewer multiplications, which outweighs its transforms (measured faster for
+    // C, K >= 128 on MI355X except 128 -> 128 on 56x56 planes, within 6 %)
+    else if (d->wino.ok && g.C >= 128 && g.K >= 128)
+        d->auto_algo = CONV2D_ALGO_WINOGRAD;
     else if (d->implicit_ok)
         d->auto_algo = CONV2D_ALGO_IMPLICIT_GEMM;
     else if (d->expl.status == CONV2D_OK && g.y_elems * elem_size(g.ydt) <= kBufferLimit)
@@ -795,6 +932,8 @@ int conv2d_desc_destroy(conv2d_desc* d) {
     if (d->ws) hipFree(d->ws);
     if (d->xr) hipFree(d->xr);
     if (d->sk) hipFree(d->sk);
+    if (d->wu) hipFree(d->wu);
+    if (d->wvm) hipFree(d->wvm);
     if (d->tp) hipFree(d->tp);
     if (d->tc) hipFree(d->tc);
     if (d->yr) hipFree(d->yr);
@@ -821,6 +960,7 @@ int conv2d_fwd(conv2d_desc* d, const void* x, const void* w, const float* bias, 
     const Geometry& g = d->g;
     if (algo == CONV2D_ALGO_IMPLICIT_GEMM && !d->implicit_ok) return CONV2D_E_UNSUPPORTED;
     if (algo == CONV2D_ALGO_DIRECT && !d->direct_ok) return CONV2D_E_UNSUPPORTED;
+    if (algo == CONV2D_ALGO_WINOGRAD && !d->wino.ok) return d->wino.status;
     if (algo == CONV2D_ALGO_IM2COL_GEMM) {
         if (d->expl.status != CONV2D_OK) return d->expl.status;
         if (g.y_elems * elem_size(g.ydt) > kBufferLimit) return CONV2D_E_UNSUPPORTED;
@@ -861,6 +1001,7 @@ int conv2d_fwd(conv2d_desc* d, const void* x, const void* w, const float* bias, 
         case CONV2D_ALGO_IMPLICIT_GEMM: st = run_implicit(d, xin, w, bias, yout, s, ph); break;
         case CONV2D_ALGO_IM2COL_GEMM: st = run_explicit(d, xin, w, bias, yout, s, ph); break;
         case CONV2D_ALGO_DIRECT: st = run_direct(d, xin, w, bias, yout, s, ph); break;
+        case CONV2D_ALGO_WINOGRAD: st = run_winograd(d, xin, w, bias, yout, s, ph); break;
         default: st = CONV2D_E_INVALID;
     }
     if (st != CONV2D_OK) return st;
@@ -910,7 +1051,7 @@ int conv2d_breakdown(conv2d_desc* d, int algo, conv2d_breakdown_t* out) {
     if (algo == CONV2D_ALGO_IMPLICIT_GEMM)
         out->fused_mask = (1u << CONV2D_PH_IN_TILING) | (1u << CONV2D_PH_IN_PACKING) |
                           (d->implicit.ksplit > 1 && !d->implicit_slice ? 0u : (1u << CONV2D_PH_IN_UNPACKING));
-    else if (algo == CONV2D_ALGO_IM2COL_GEMM)
+    else if (algo == CONV2D_ALGO_IM2COL_GEMM || algo == CONV2D_ALGO_WINOGRAD)
         out->fused_mask = (1u << CONV2D_PH_IN_TILING);
     else
         out->fused_mask = (1u << CONV2D_PH_IN_TILING) | (1u << CONV2D_PH_IN_PACKING);
@@ -984,6 +1125,14 @@ int conv2d_plan_query(const conv2d_desc* d, int algo, conv2d_plan_info* out) {
         out->workspace_bytes = d->expl.col_bytes + d->expl.c_bytes;
         out->chunks = d->expl.chunks;
         if (d->expl.status != CONV2D_OK) return d->expl.status;
+    } else if (algo == CONV2D_ALGO_WINOGRAD) {
+        out->tile_m = d->wino.gemm.bm;
+        out->tile_n = d->wino.gemm.bn;
+        out->kred = (int32_t)g.C;  // the GEMMs reduce over the input channels
+        out->kred_pad = (int32_t)(ceil_div(g.C, d->wino.gemm.bk) * d->wino.gemm.bk);
+        out->workspace_bytes = d->wino.u_bytes + d->wino.v_bytes + d->wino.m_bytes;
+        out->chunks = d->wino.chunks;
+        if (!d->wino.ok) return d->wino.status;
     } else {
         out->kernel = CONV2D_KERNEL_DIRECT;
         if (!d->direct_ok) return CONV2D_E_UNSUPPORTED;

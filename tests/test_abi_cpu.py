@@ -222,13 +222,49 @@ def test_grouped_auto_choice():
     assert algo(groups=8) == B.CONV2D_ALGO_IMPLICIT_GEMM             # 32, 32
     assert algo(groups=16, k=1024) == B.CONV2D_ALGO_IMPLICIT_GEMM    # 16, 64
     assert algo(groups=64, k=2048) == B.CONV2D_ALGO_DIRECT           # 4, 32
-    assert algo(groups=1) == B.CONV2D_ALGO_IMPLICIT_GEMM
+    assert algo(groups=1) == B.CONV2D_ALGO_WINOGRAD                  # 256 -> 256, 3x3, stride 1
     # ungrouped, K <= 16: the direct kernel when its grid fills the chip and the filter is not 1x1
     assert algo(c=512, k=3, h=112, w=112) == B.CONV2D_ALGO_DIRECT        # 32 images x 13 bands
     assert algo(c=512, k=16, h=112, w=112) == B.CONV2D_ALGO_DIRECT
     assert algo(c=512, k=32, h=112, w=112) == B.CONV2D_ALGO_IMPLICIT_GEMM
     assert algo(n=2, c=512, k=3, h=112, w=112) == B.CONV2D_ALGO_IMPLICIT_GEMM   # 26 blocks
     assert algo(c=512, k=3, h=112, w=112, r=1, s=1, pad=(0, 0)) == B.CONV2D_ALGO_IMPLICIT_GEMM
+
+
+def test_winograd_plan(monkeypatch):
+    cfg2 = datagen.CONFIGS["cfg2"]
+
+    def plan(cs):
+        d = B.conv2d_desc_create(params_for(cs))
+        try:
+            return B.conv2d_plan_query(d, B.CONV2D_ALGO_WINOGRAD)
+        finally:
+            B.conv2d_desc_destroy(d)
+    info = plan(cfg2)
+    tiles = 32 * 28 * 28
+    assert info.algo == B.CONV2D_ALGO_WINOGRAD and info.chunks == 1 and info.kred == 64
+    assert info.workspace_bytes == 16 * 64 * 64 * 4 + 16 * (64 + 64) * tiles * 4
+    for bad in (cfg2.with_(r=5, s=5, pad=(2, 2)), cfg2.with_(stride=(2, 2)), cfg2.with_(dil=(2, 2), pad=(2, 2)),
+                cfg2.with_(groups=2), cfg2.with_(x_dtype="bf16", y_dtype="bf16")):
+        with pytest.raises(B.Conv2dError) as e:
+            plan(bad)
+        assert e.value.status == B.CONV2D_E_UNSUPPORTED
+    def auto(cs):
+        d = B.conv2d_desc_create(params_for(cs))
+        try:
+            return B.conv2d_plan_query(d, B.CONV2D_ALGO_AUTO).algo
+        finally:
+            B.conv2d_desc_destroy(d)
+    assert auto(cfg2) == B.CONV2D_ALGO_IMPLICIT_GEMM                       # 64 channels
+    assert auto(cfg2.with_(c=128, k=256)) == B.CONV2D_ALGO_WINOGRAD
+    assert auto(cfg2.with_(c=256, k=256, stride=(2, 2))) == B.CONV2D_ALGO_IMPLICIT_GEMM
+    monkeypatch.setenv("CONV2D_WORKSPACE_LIMIT_BYTES", str(64 << 20))
+    info = plan(cfg2)
+    assert info.chunks == -(-tiles // ((64 << 20) // (16 * 128 * 4)))
+    monkeypatch.setenv("CONV2D_WORKSPACE_LIMIT_BYTES", "0")
+    with pytest.raises(B.Conv2dError) as e:
+        plan(cfg2)
+    assert e.value.status == B.CONV2D_E_ALLOC
 
 
 def test_explicit_workspace_chunking(monkeypatch):

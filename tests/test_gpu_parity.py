@@ -19,7 +19,8 @@ pytestmark = pytest.mark.gpu
 
 GATE = {"f32": 1e-5, "bf16": 1e-2}
 IMPLICIT, IM2COL, DIRECT = B.CONV2D_ALGO_IMPLICIT_GEMM, B.CONV2D_ALGO_IM2COL_GEMM, B.CONV2D_ALGO_DIRECT
-ALGO_IDS = {IMPLICIT: "implicit", IM2COL: "im2col", DIRECT: "direct", B.CONV2D_ALGO_AUTO: "auto"}
+ALGO_IDS = {IMPLICIT: "implicit", IM2COL: "im2col", DIRECT: "direct", B.CONV2D_ALGO_WINOGRAD: "winograd",
+            B.CONV2D_ALGO_AUTO: "auto"}
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -354,6 +355,41 @@ def test_grouped_direct(idx, dt):
     cs = GROUPED[idx].with_(x_dtype=dt, y_dtype=dt)
     _check(cs, DIRECT)
     _check(cs.with_(y_dtype="f32"), DIRECT, "integer")
+
+
+# Winograd F(2x2, 3x3): 3x3, stride 1, dilation 1, one group, fp32; odd output sizes (clipped
+# 2x2 tiles), paddings 0/1/2, channel counts across GEMM tiles, NHWC, chunked tiles
+WINOGRAD = B.CONV2D_ALGO_WINOGRAD
+WINO = [
+    _shape(1, 3, 9, 11, 5, 3, 3, pd=(1, 1), seed=270),
+    _shape(2, 17, 13, 10, 33, 3, 3, seed=271),
+    _shape(1, 70, 15, 15, 90, 3, 3, pd=(2, 2), seed=272),
+    _shape(3, 64, 14, 14, 128, 3, 3, pd=(1, 1), seed=273),
+    _shape(2, 24, 8, 31, 16, 3, 3, pd=(1, 0), seed=274, bias=False),
+]
+
+
+@pytest.mark.parametrize("idx", range(len(WINO)))
+def test_winograd(idx):
+    cs = WINO[idx]
+    _check(cs, WINOGRAD)
+    _check(cs, WINOGRAD, "integer")
+    _check(cs.with_(layout="nhwc"), WINOGRAD)
+
+
+def test_winograd_chunks_and_configs(monkeypatch):
+    # a workspace cap that forces several chunks of tiles
+    cs = WINO[3]
+    monkeypatch.setenv("CONV2D_WORKSPACE_LIMIT_BYTES", str(16 * (64 + 128) * 4 * 100))
+    dc = DeviceConv(cs, "random")
+    try:
+        assert dc.plan(WINOGRAD).chunks > 1
+    finally:
+        dc.close()
+    _check(cs, WINOGRAD)
+    _check(cs, WINOGRAD, "integer")
+    monkeypatch.delenv("CONV2D_WORKSPACE_LIMIT_BYTES")
+    _check(datagen.CONFIGS["cfg2"], WINOGRAD)
 
 
 EDGE_ALGOS = [("implicit", IMPLICIT, None, None), ("implicit-gemm", IMPLICIT, "0", None),
