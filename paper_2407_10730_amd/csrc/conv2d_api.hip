@@ -102,7 +102,10 @@ int env_timing() {
 // than CUs the tiles are dealt out evenly, so the busiest CU sets the time.
 // CONV2D_GEMM = "k32:TILE[:BK[:PF]]" overrides the choice for tuning.
 // nhwc: bf16 with the channel-contiguous gather (BK 64 when C/g allows).
-GemmPlan choose_tile(int64_t M, int64_t P, int64_t G, int64_t kred, int xdt, int64_t cg, bool nhwc = false) {
+// dense: the B operand is a packed matrix (explicit path), where 64 x 128 tiles measured
+// 10-25 % faster than 64 x 64 on every fixed workload (fp32 and bf16).
+GemmPlan choose_tile(int64_t M, int64_t P, int64_t G, int64_t kred, int xdt, int64_t cg, bool nhwc = false,
+                     bool dense = false) {
     const int cus = 256;
     GemmPlan best;
     double best_cost = 1e300;
@@ -120,7 +123,8 @@ GemmPlan choose_tile(int64_t M, int64_t P, int64_t G, int64_t kred, int xdt, int
     for (const Cand& c : nhwc ? cands_bf16 : cands_f32) {
         const TileShape ts = kTileShapes[c.tile];
         const int64_t tiles = ceil_div(M, ts.bm) * ceil_div(P, ts.bn) * G;
-        const double cost = (double)ceil_div(tiles, per_round) * ts.bm * ts.bn / c.eff;
+        const double eff = c.eff * (dense && c.tile == TILE_64x128 ? 1.25 : 1.0);
+        const double cost = (double)ceil_div(tiles, per_round) * ts.bm * ts.bn / eff;
         if (cost < best_cost) {
             best_cost = cost;
             best.kind = 0;
@@ -390,7 +394,7 @@ void plan_explicit(conv2d_desc* d) {
     e.chunks = ceil_div(total_rows, rows);
     e.col_bytes = rows * row_col;
     e.c_bytes = rows * row_c;
-    e.gemm = choose_tile(g.Kg, rows * g.Wo, g.G, g.Kred, g.xdt, g.Cg);
+    e.gemm = choose_tile(g.Kg, rows * g.Wo, g.G, g.Kred, g.xdt, g.Cg, false, true);
 }
 
 // ------------------------------------------------------------------ events
