@@ -55,15 +55,16 @@ enum {
     CONV2D_ALGO_IMPLICIT_GEMM = 1, /* sliced direct convolution: im2col slices gathered into LDS, MFMA */
     CONV2D_ALGO_IM2COL_GEMM = 2,   /* explicit im2col pack, MFMA GEMM, unpack (ConvBench's default baseline) */
     CONV2D_ALGO_DIRECT = 3,        /* direct VALU kernel for depthwise / small-group convolutions */
-    CONV2D_ALGO_WINOGRAD = 4,      /* Winograd F(2x2,3x3): 3x3, stride 1, dilation 1, one group, fp32 */
+    CONV2D_ALGO_WINOGRAD = 4,      /* Winograd F(2x2,3x3) / F(4x4,3x3): 3x3, stride 1, dilation 1, one group, fp32 */
     CONV2D_ALGO_COUNT = 5
 };
 /* Winograd's phases: PRE_REORDER the filter transform, IN_PACKING the input
- * transform, IN_MICROKERNEL the 16 GEMMs of the transformed domain, IN_UNPACKING
- * the output transform with the bias (Sec. I names the family; the minimal
- * filtering algorithm is Lavin and Gray's).  Its workspace (transformed filters,
- * then inputs and products per chunk of 2x2 output tiles) obeys
- * CONV2D_WORKSPACE_LIMIT_BYTES like the explicit path's. */
+ * transform, IN_MICROKERNEL the (m+2)^2 GEMMs of the transformed domain (16 for
+ * m = 2, 36 for m = 4), IN_UNPACKING the output transform with the bias (Sec. I
+ * names the family; the minimal filtering algorithm is Lavin and Gray's).  The
+ * planner picks the output tile m (conv2d_plan_info.wino_tile).  Its workspace
+ * (transformed filters, then inputs and products per chunk of m x m output
+ * tiles) obeys CONV2D_WORKSPACE_LIMIT_BYTES like the explicit path's. */
 
 /* Processing steps of the timing tool (Sec. III-A): pre-convolution analysis and
  * reordering; in-convolution tiling, packing, microkernel and unpacking;
@@ -147,6 +148,7 @@ typedef struct {
                                  of tile work (0 = none); the last part of a tile to finish adds
                                  the parts in order (fp32 partials in the workspace) */
     int32_t tail_pieces;
+    int32_t wino_tile;        /* WINOGRAD: output tile edge m of F(m x m, 3x3), 2 or 4 */
 } conv2d_plan_info;
 
 /* Validate params, compute the output size, classify the operation and plan

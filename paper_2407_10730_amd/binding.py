@@ -92,7 +92,7 @@ class conv2d_plan_info(ctypes.Structure):
                 ("workspace_bytes", ctypes.c_int64), ("chunks", ctypes.c_int64),
                 ("needs_reorder", ctypes.c_int32), ("op_class", ctypes.c_int32), ("kernel", ctypes.c_int32),
                 ("ksplit", ctypes.c_int32), ("tail_tiles", ctypes.c_int32),
-                ("tail_pieces", ctypes.c_int32)]
+                ("tail_pieces", ctypes.c_int32), ("wino_tile", ctypes.c_int32)]
 
 
 _lib = None

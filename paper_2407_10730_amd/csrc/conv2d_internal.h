@@ -134,7 +134,7 @@ struct DirectArgs {
     int32_t C, H, W, K, Ho, Wo, R, S, sh, sw, ph, pw, dh, dw, Cg, Kg;
     int32_t N;
 };
-// Winograd F(2x2, 3x3): tiles t0 .. t0+tc-1 of th x tw tiles per image.
+// Winograd F(mt x mt, 3x3), mt = 2 or 4: tiles t0 .. t0+tc-1 of th x tw tiles per image.
 struct WinoArgs {
     const void* x;
     uint32_t x_bytes;
@@ -142,11 +142,12 @@ struct WinoArgs {
     uint32_t y_bytes;
     const float* bias;  // may be NULL
     int32_t C, H, W, K, Ho, Wo, ph, pw;
-    int32_t th, tw;     // tiles per image: ceil(Ho/2) x ceil(Wo/2)
+    int32_t mt;         // output tile edge (2 or 4); (mt+2)^2 transformed positions
+    int32_t th, tw;     // tiles per image: ceil(Ho/mt) x ceil(Wo/mt)
     int64_t t0;
     int32_t tc;
 };
-hipError_t launch_wino_filter(const float* w, float* u, int K, int C, hipStream_t stream);
+hipError_t launch_wino_filter(const float* w, float* u, int K, int C, int mt, hipStream_t stream);
 hipError_t launch_wino_input(const WinoArgs& a, float* v, hipStream_t stream);
 hipError_t launch_wino_output(const WinoArgs& a, const float* m, hipStream_t stream);
 

@@ -1,11 +1,11 @@
-// winograd.hip -- Winograd minimal-filtering convolution F(2x2, 3x3) (Lavin and Gray, CVPR
-// 2016), the transform-based algorithm family the paper names next to GEMM and direct methods
-// (Sec. I), for 3x3 filters, stride 1, dilation 1, one group, fp32.
+// winograd.hip -- Winograd minimal-filtering convolution F(m x m, 3x3), m = 2 or 4 (Lavin and
+// Gray, CVPR 2016), the transform-based algorithm family the paper names next to GEMM and
+// direct methods (Sec. I), for 3x3 filters, stride 1, dilation 1, one group, fp32.
 //
-// Every 2x2 block of outputs (a tile) is computed from the 4x4 input patch under it:
+// Every m x m block of outputs (a tile) is computed from the (m+2) x (m+2) input patch under it:
 //   Y = A^T [ (G g G^T) (.) (B^T d B) ] A
-// with the element-wise product (.) summed over input channels, which turns the 16 positions
-// of the 4x4 transformed domain into 16 independent GEMMs
+// with the element-wise product (.) summed over input channels, which turns the (m+2)^2
+// positions of the transformed domain into independent GEMMs
 //   M[xi][k][t] = sum_c U[xi][k][c] * V[xi][c][t]
 // (U: transformed filters, V: transformed input patches, t: tile).  The phases map onto the
 // timing tool's steps: the filter transform is a pre-convolution reordering of the weights,
@@ -14,42 +14,102 @@
 // unpacking, which also adds the bias and writes NCHW y.  Tiles are processed in chunks that
 // fit the workspace.
 //
+// F(2x2, 3x3), interpolation points 0, 1, -1 and infinity:
 //   B^T = [1 0 -1 0; 0 1 1 0; 0 -1 1 0; 0 1 0 -1]
 //   G   = [1 0 0; 1/2 1/2 1/2; 1/2 -1/2 1/2; 0 0 1]
 //   A^T = [1 1 1 0; 0 1 -1 -1]
+// F(4x4, 3x3), points 0, 1, -1, 2, -2 and infinity (2.25x fewer multiplications than F(2x2),
+// with larger transform constants and so larger rounding errors):
+//   B^T = [4 0 -5 0 1 0; 0 -4 -4 1 1 0; 0 4 -4 -1 1 0; 0 -2 -1 2 1 0; 0 2 -1 -2 1 0; 0 4 0 -5 0 1]
+//   G   = [1/4 0 0; -1/6 -1/6 -1/6; -1/6 1/6 -1/6; 1/24 1/12 1/6; 1/24 -1/12 1/6; 0 0 1]
+//   A^T = [1 1 1 1 1 0; 0 1 -1 2 -2 0; 0 1 1 4 4 0; 0 1 -1 8 -8 1]
 #include "device_common.h"
 
 namespace cv {
 
+// o = G g for one column g of the filter (length 3 -> MT+2)
+template <int MT>
+__device__ __forceinline__ void wino_g(float g0, float g1, float g2, float* o) {
+    if constexpr (MT == 2) {
+        o[0] = g0;
+        o[1] = 0.5f * (g0 + g1 + g2);
+        o[2] = 0.5f * (g0 - g1 + g2);
+        o[3] = g2;
+    } else {
+        o[0] = 0.25f * g0;
+        o[1] = (-1.0f / 6.0f) * (g0 + g1 + g2);
+        o[2] = (-1.0f / 6.0f) * (g0 - g1 + g2);
+        o[3] = (1.0f / 24.0f) * g0 + (1.0f / 12.0f) * g1 + (1.0f / 6.0f) * g2;
+        o[4] = (1.0f / 24.0f) * g0 - (1.0f / 12.0f) * g1 + (1.0f / 6.0f) * g2;
+        o[5] = g2;
+    }
+}
+
+// o = B^T d for one column d of the input patch (length MT+2)
+template <int MT>
+__device__ __forceinline__ void wino_bt(const float* d, float* o) {
+    if constexpr (MT == 2) {
+        o[0] = d[0] - d[2];
+        o[1] = d[1] + d[2];
+        o[2] = d[2] - d[1];
+        o[3] = d[1] - d[3];
+    } else {
+        o[0] = 4.0f * d[0] - 5.0f * d[2] + d[4];
+        o[1] = (d[3] + d[4]) - 4.0f * (d[1] + d[2]);
+        o[2] = (d[4] - d[3]) + 4.0f * (d[1] - d[2]);
+        o[3] = (d[4] - d[2]) + 2.0f * (d[3] - d[1]);
+        o[4] = (d[4] - d[2]) - 2.0f * (d[3] - d[1]);
+        o[5] = 4.0f * d[1] - 5.0f * d[3] + d[5];
+    }
+}
+
+// o = A^T m for one column m of the GEMM results (length MT+2 -> MT)
+template <int MT>
+__device__ __forceinline__ void wino_at(const float* m, float* o) {
+    if constexpr (MT == 2) {
+        o[0] = m[0] + m[1] + m[2];
+        o[1] = m[1] - m[2] - m[3];
+    } else {
+        const float p12 = m[1] + m[2], d12 = m[1] - m[2];
+        const float p34 = m[3] + m[4], d34 = m[3] - m[4];
+        o[0] = m[0] + p12 + p34;
+        o[1] = d12 + 2.0f * d34;
+        o[2] = p12 + 4.0f * p34;
+        o[3] = d12 + 8.0f * d34 + m[5];
+    }
+}
+
 // U[xi][k][c] = (G g_kc G^T)[xi]; one thread per (k, c), c fastest (coalesced writes).
+template <int MT>
 __global__ __launch_bounds__(256) void wino_filter_kernel(const float* __restrict__ w, float* __restrict__ u, int K,
                                                           int C) {
+    constexpr int AL = MT + 2;
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= (int64_t)K * C) return;
     const float* g = w + i * 9;  // w[k][c][3][3], i = k*C + c
-    float t[4][3];               // G g
+    float t[AL][3];              // G g
 #pragma unroll
     for (int j = 0; j < 3; ++j) {
-        const float g0 = g[j], g1 = g[3 + j], g2 = g[6 + j];
-        t[0][j] = g0;
-        t[1][j] = 0.5f * (g0 + g1 + g2);
-        t[2][j] = 0.5f * (g0 - g1 + g2);
-        t[3][j] = g2;
+        float col[AL];
+        wino_g<MT>(g[j], g[3 + j], g[6 + j], col);
+#pragma unroll
+        for (int a = 0; a < AL; ++a) t[a][j] = col[a];
     }
     const int64_t plane = (int64_t)K * C;
 #pragma unroll
-    for (int a = 0; a < 4; ++a) {  // (G g) G^T
-        const float h0 = t[a][0], h1 = t[a][1], h2 = t[a][2];
-        u[(a * 4 + 0) * plane + i] = h0;
-        u[(a * 4 + 1) * plane + i] = 0.5f * (h0 + h1 + h2);
-        u[(a * 4 + 2) * plane + i] = 0.5f * (h0 - h1 + h2);
-        u[(a * 4 + 3) * plane + i] = h2;
+    for (int a = 0; a < AL; ++a) {  // (G g) G^T
+        float row[AL];
+        wino_g<MT>(t[a][0], t[a][1], t[a][2], row);
+#pragma unroll
+        for (int b = 0; b < AL; ++b) u[(a * AL + b) * plane + i] = row[b];
     }
 }
 
 // V[xi][c][t - t0] = (B^T d B)[xi] for the tiles t0 .. t0+tc-1 (tile t = (n, th, tw) row-major);
 // one thread per (c, tile), tile fastest.
+template <int MT>
 __global__ __launch_bounds__(256) void wino_input_kernel(WinoArgs A, float* __restrict__ v) {
+    constexpr int AL = MT + 2;
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= (int64_t)A.C * A.tc) return;
     const int c = (int)(i / A.tc);
@@ -59,42 +119,46 @@ __global__ __launch_bounds__(256) void wino_input_kernel(WinoArgs A, float* __re
     const int n = (int)(t / tiles_img);
     const int r = (int)(t - (int64_t)n * tiles_img);
     const int ty = r / A.tw, tx = r - (r / A.tw) * A.tw;
-    const int hi0 = 2 * ty - A.ph, wi0 = 2 * tx - A.pw;
+    const int hi0 = MT * ty - A.ph, wi0 = MT * tx - A.pw;
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(A.x, A.x_bytes);
     const int64_t plane0 = ((int64_t)n * A.C + c) * A.H;
-    float d[4][4];
+    float d[AL][AL];
 #pragma unroll
-    for (int a = 0; a < 4; ++a) {
+    for (int a = 0; a < AL; ++a) {
         const int hi = hi0 + a;
         const bool hok = (unsigned)hi < (unsigned)A.H;
 #pragma unroll
-        for (int b = 0; b < 4; ++b) {
+        for (int b = 0; b < AL; ++b) {
             const int wi = wi0 + b;
             const bool ok = hok & ((unsigned)wi < (unsigned)A.W);
             d[a][b] = ld_f32(rx, ok ? (uint32_t)(((plane0 + hi) * A.W + wi) * 4) : OOB_OFF);
         }
     }
-    float e[4][4];  // B^T d
+    float e[AL][AL];  // B^T d
 #pragma unroll
-    for (int b = 0; b < 4; ++b) {
-        e[0][b] = d[0][b] - d[2][b];
-        e[1][b] = d[1][b] + d[2][b];
-        e[2][b] = d[2][b] - d[1][b];
-        e[3][b] = d[1][b] - d[3][b];
+    for (int b = 0; b < AL; ++b) {
+        float col[AL], o[AL];
+#pragma unroll
+        for (int a = 0; a < AL; ++a) col[a] = d[a][b];
+        wino_bt<MT>(col, o);
+#pragma unroll
+        for (int a = 0; a < AL; ++a) e[a][b] = o[a];
     }
     const int64_t plane = (int64_t)A.C * A.tc;
 #pragma unroll
-    for (int a = 0; a < 4; ++a) {  // (B^T d) B
-        v[(a * 4 + 0) * plane + i] = e[a][0] - e[a][2];
-        v[(a * 4 + 1) * plane + i] = e[a][1] + e[a][2];
-        v[(a * 4 + 2) * plane + i] = e[a][2] - e[a][1];
-        v[(a * 4 + 3) * plane + i] = e[a][1] - e[a][3];
+    for (int a = 0; a < AL; ++a) {  // (B^T d) B
+        float o[AL];
+        wino_bt<MT>(e[a], o);
+#pragma unroll
+        for (int b = 0; b < AL; ++b) v[(a * AL + b) * plane + i] = o[b];
     }
 }
 
-// y (the 2x2 block of tile t, clipped at the edges) = A^T M A + bias; one thread per
+// y (the MT x MT block of tile t, clipped at the edges) = A^T M A + bias; one thread per
 // (k, tile), tile fastest.
+template <int MT>
 __global__ __launch_bounds__(256) void wino_output_kernel(WinoArgs A, const float* __restrict__ m) {
+    constexpr int AL = MT + 2;
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= (int64_t)A.K * A.tc) return;
     const int k = (int)(i / A.tc);
@@ -105,49 +169,66 @@ __global__ __launch_bounds__(256) void wino_output_kernel(WinoArgs A, const floa
     const int r = (int)(t - (int64_t)n * tiles_img);
     const int ty = r / A.tw, tx = r - (r / A.tw) * A.tw;
     const int64_t plane = (int64_t)A.K * A.tc;
-    float q[4][4];
+    float q[AL][AL];
 #pragma unroll
-    for (int a = 0; a < 4; ++a)
+    for (int a = 0; a < AL; ++a)
 #pragma unroll
-        for (int b = 0; b < 4; ++b) q[a][b] = m[(a * 4 + b) * plane + i];
-    float s[2][4];  // A^T M
+        for (int b = 0; b < AL; ++b) q[a][b] = m[(a * AL + b) * plane + i];
+    float s[MT][AL];  // A^T M
 #pragma unroll
-    for (int b = 0; b < 4; ++b) {
-        s[0][b] = q[0][b] + q[1][b] + q[2][b];
-        s[1][b] = q[1][b] - q[2][b] - q[3][b];
+    for (int b = 0; b < AL; ++b) {
+        float col[AL], o[MT];
+#pragma unroll
+        for (int a = 0; a < AL; ++a) col[a] = q[a][b];
+        wino_at<MT>(col, o);
+#pragma unroll
+        for (int a = 0; a < MT; ++a) s[a][b] = o[a];
     }
     const float bias = A.bias ? A.bias[k] : 0.0f;
     const __amdgpu_buffer_rsrc_t ry = make_rsrc(A.y, A.y_bytes);
 #pragma unroll
-    for (int a = 0; a < 2; ++a) {
-        const float o0 = s[a][0] + s[a][1] + s[a][2] + bias;  // (A^T M) A
-        const float o1 = s[a][1] - s[a][2] - s[a][3] + bias;
-        const int ho = 2 * ty + a, wo = 2 * tx;
+    for (int a = 0; a < MT; ++a) {
+        float o[MT];
+        wino_at<MT>(s[a], o);  // (A^T M) A
+        const int ho = MT * ty + a, wo = MT * tx;
         const bool rok = ho < A.Ho;
         const int64_t e = (((int64_t)n * A.K + k) * A.Ho + ho) * A.Wo + wo;
-        st_f32(ry, rok ? (uint32_t)(e * 4) : OOB_OFF, o0);
-        st_f32(ry, rok & (wo + 1 < A.Wo) ? (uint32_t)((e + 1) * 4) : OOB_OFF, o1);
+#pragma unroll
+        for (int b = 0; b < MT; ++b)
+            st_f32(ry, rok & (wo + b < A.Wo) ? (uint32_t)((e + b) * 4) : OOB_OFF, o[b] + bias);
     }
 }
 
-hipError_t launch_wino_filter(const float* w, float* u, int K, int C, hipStream_t stream) {
+hipError_t launch_wino_filter(const float* w, float* u, int K, int C, int mt, hipStream_t stream) {
     const int64_t n = (int64_t)K * C;
-    if (n < 1 || (n + 255) / 256 > 0x7fffffffLL) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(wino_filter_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, w, u, K, C);
+    if (n < 1 || (n + 255) / 256 > 0x7fffffffLL || (mt != 2 && mt != 4)) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)((n + 255) / 256));
+    if (mt == 2)
+        hipLaunchKernelGGL(wino_filter_kernel<2>, grid, dim3(256), 0, stream, w, u, K, C);
+    else
+        hipLaunchKernelGGL(wino_filter_kernel<4>, grid, dim3(256), 0, stream, w, u, K, C);
     return hipGetLastError();
 }
 
 hipError_t launch_wino_input(const WinoArgs& a, float* v, hipStream_t stream) {
     const int64_t n = (int64_t)a.C * a.tc;
-    if (n < 1 || (n + 255) / 256 > 0x7fffffffLL) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(wino_input_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, a, v);
+    if (n < 1 || (n + 255) / 256 > 0x7fffffffLL || (a.mt != 2 && a.mt != 4)) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)((n + 255) / 256));
+    if (a.mt == 2)
+        hipLaunchKernelGGL(wino_input_kernel<2>, grid, dim3(256), 0, stream, a, v);
+    else
+        hipLaunchKernelGGL(wino_input_kernel<4>, grid, dim3(256), 0, stream, a, v);
     return hipGetLastError();
 }
 
 hipError_t launch_wino_output(const WinoArgs& a, const float* m, hipStream_t stream) {
     const int64_t n = (int64_t)a.K * a.tc;
-    if (n < 1 || (n + 255) / 256 > 0x7fffffffLL) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(wino_output_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, a, m);
+    if (n < 1 || (n + 255) / 256 > 0x7fffffffLL || (a.mt != 2 && a.mt != 4)) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)((n + 255) / 256));
+    if (a.mt == 2)
+        hipLaunchKernelGGL(wino_output_kernel<2>, grid, dim3(256), 0, stream, a, m);
+    else
+        hipLaunchKernelGGL(wino_output_kernel<4>, grid, dim3(256), 0, stream, a, m);
     return hipGetLastError();
 }
 

@@ -240,9 +240,16 @@ def test_winograd_plan(monkeypatch):
             return B.conv2d_plan_query(d, B.CONV2D_ALGO_WINOGRAD)
         finally:
             B.conv2d_desc_destroy(d)
+    monkeypatch.setenv("CONV2D_WINO_TILE", "4")
+    info = plan(cfg2)
+    tiles4 = 32 * 14 * 14
+    assert info.wino_tile == 4 and info.chunks == 1
+    assert info.workspace_bytes == 36 * 64 * 64 * 4 + 36 * (64 + 64) * tiles4 * 4
+    assert plan(cfg2.with_(h=57, w=55)).workspace_bytes == 36 * 64 * 64 * 4 + 36 * 128 * 32 * 15 * 14 * 4
+    monkeypatch.setenv("CONV2D_WINO_TILE", "2")
     info = plan(cfg2)
     tiles = 32 * 28 * 28
-    assert info.algo == B.CONV2D_ALGO_WINOGRAD and info.chunks == 1 and info.kred == 64
+    assert info.algo == B.CONV2D_ALGO_WINOGRAD and info.chunks == 1 and info.kred == 64 and info.wino_tile == 2
     assert info.workspace_bytes == 16 * 64 * 64 * 4 + 16 * (64 + 64) * tiles * 4
     for bad in (cfg2.with_(r=5, s=5, pad=(2, 2)), cfg2.with_(stride=(2, 2)), cfg2.with_(dil=(2, 2), pad=(2, 2)),
                 cfg2.with_(groups=2), cfg2.with_(x_dtype="bf16", y_dtype="bf16")):
@@ -257,6 +264,11 @@ def test_winograd_plan(monkeypatch):
             B.conv2d_desc_destroy(d)
     assert auto(cfg2) == B.CONV2D_ALGO_IMPLICIT_GEMM                       # 64 channels
     assert auto(cfg2.with_(c=128, k=256)) == B.CONV2D_ALGO_WINOGRAD
+    assert auto(cfg2.with_(c=512, k=512, h=7, w=7)) == B.CONV2D_ALGO_IMPLICIT_GEMM    # 7x7 planes
+    monkeypatch.delenv("CONV2D_WINO_TILE")
+    assert plan(cfg2).wino_tile == 4 and plan(cfg2.with_(h=14, w=14)).wino_tile == 4
+    assert plan(cfg2.with_(h=7, w=7)).wino_tile == 2 and plan(cfg2.with_(h=40, w=7)).wino_tile == 2
+    monkeypatch.setenv("CONV2D_WINO_TILE", "2")
     assert auto(cfg2.with_(c=256, k=256, stride=(2, 2))) == B.CONV2D_ALGO_IMPLICIT_GEMM
     monkeypatch.setenv("CONV2D_WORKSPACE_LIMIT_BYTES", str(64 << 20))
     info = plan(cfg2)
