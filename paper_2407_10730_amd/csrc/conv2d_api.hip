@@ -867,10 +867,11 @@ int conv2d_desc_create(const conv2d_params* params, conv2d_desc** out) {
     d->timing = env_timing();
     d->implicit_ok = implicit_supported(g);
     d->direct_ok = direct_supported(g);
-    // bf16 with C/g a multiple of 32: gather 16-byte channel runs from an NHWC copy of x.  The
-    // copy costs 2|x| of HBM traffic (nothing when x is already NHWC), so it is taken when the
-    // convolution does at least 1000 flops per input byte; CONV2D_NHWC_GATHER=0 / 1 forces it.
-    if (g.xdt == CONV2D_BF16 && g.Cg % 32 == 0) {
+    // bf16 with C/g a multiple of 32, or C/g = 8 or 16 (whole taps per 32-deep stage): gather
+    // 16-byte channel runs from an NHWC copy of x.  The copy costs 2|x| of HBM traffic (nothing
+    // when x is already NHWC), so it is taken when the convolution does at least 1000 flops per
+    // input byte; CONV2D_NHWC_GATHER=0 / 1 forces it.
+    if (g.xdt == CONV2D_BF16 && (g.Cg % 32 == 0 || g.Cg == 8 || g.Cg == 16)) {
         const double flops = 2.0 * (double)g.N * g.K * g.Cg * g.R * g.S * g.Ho * g.Wo;
         const double xbytes = (double)g.x_elems * 2;
         const int64_t force = env_int64("CONV2D_NHWC_GATHER", -1);
@@ -893,7 +894,8 @@ int conv2d_desc_create(const conv2d_params* params, conv2d_desc** out) {
     {
         const int64_t force = env_int64("CONV2D_SLICE", -1);
         const bool grid_ok = g.G * ceil_div(g.Kg, 64) * g.N * ceil_div(g.Ho * g.Wo, 128) <= 0x7fffffffLL;
-        d->implicit_slice = d->slice.ok && grid_ok && (force < 0 ? !d->implicit_tap : force != 0);
+        d->implicit_slice =
+            d->slice.ok && grid_ok && (force < 0 ? !(d->implicit_tap || d->implicit_nhwc) : force != 0);
     }
     build_ktab(d);
     plan_explicit(d);

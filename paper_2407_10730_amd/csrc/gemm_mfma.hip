@@ -490,11 +490,13 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void ge
     u32x4 areg[AUNITS];
     int cur_c0 = 0, cur_r = 0, cur_s = 0;  // tap-major cursor of the next stage
     if constexpr (BSRC == BSRC_IMPLICIT_TAP || BSRC == BSRC_NHWC_TAP) {
-        const int cblocks = A.Cg / BK;
-        const int tap = s_begin / cblocks;
-        cur_c0 = (s_begin - tap * cblocks) * BK;
-        cur_r = tap / A.S;
-        cur_s = tap - cur_r * A.S;
+        if (A.Cg >= BK) {  // (C/g < BK: the small-group NHWC gather indexes by stage)
+            const int cblocks = A.Cg / BK;
+            const int tap = s_begin / cblocks;
+            cur_c0 = (s_begin - tap * cblocks) * BK;
+            cur_r = tap / A.S;
+            cur_s = tap - cur_r * A.S;
+        }
     }
 
     auto load_weights_tap = [&]() {
@@ -523,7 +525,32 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void ge
     auto load_stage = [&](int stage) {
         const int k0 = stage * BK;
         uint16_t h[8];
-        if constexpr (NHWC) {
+        if (NHWC && A.Cg < BK) {
+            // C/g = 8 or 16: a stage holds BK / (C/g) whole taps; chunk kc of a pixel is the
+            // 8 channels (kc*8) % (C/g) .. +7 of tap k0/(C/g) + kc*8/(C/g) (zero past the last tap)
+#pragma unroll
+            for (int i = 0; i < BUNITS; ++i) {
+                const int kc = (t + i * 256) % CPR;
+                const int kr = k0 + kc * 8;
+                const int tap = kr / A.Cg;
+                const int c = kr - tap * A.Cg;
+                const int r = tap / A.S, sx = tap - (tap / A.S) * A.S;
+                const int hi = csn[i].hi0 + r * A.dh, wi = csn[i].wi0 + sx * A.dw;
+                const bool ok = (tap < A.RS) & ((unsigned)hi < (unsigned)A.H) & ((unsigned)wi < (unsigned)A.W);
+                const int64_t e = csn[i].base + ((int64_t)(r * A.dh) * A.W + sx * A.dw) * A.Cx + c;
+                breg[i] = __builtin_amdgcn_raw_buffer_load_b128(rb, ok ? (uint32_t)(e * 2) : OOB_OFF, 0, 0);
+            }
+            // weights in tap-major order [K][R*S][C/g]: row m, reduction k0 + kc*8 .. +7
+#pragma unroll
+            for (int i = 0; i < AUNITS; ++i) {
+                const int u = t + i * 256;
+                const int m = m0 + u / CPR;
+                const int kr = k0 + (u % CPR) * 8;
+                const int64_t e0 = a_base + (int64_t)m * A.lda + kr;
+                areg[i] = __builtin_amdgcn_raw_buffer_load_b128(ra, (m < A.M) & (kr < A.Kred) ? (uint32_t)(e0 * 2)
+                                                                                              : OOB_OFF, 0, 0);
+            }
+        } else if constexpr (NHWC) {
             const int roff = cur_r * A.dh, soff = cur_s * A.dw;
             const int64_t tapoff = ((int64_t)roff * A.W + soff) * A.Cx + cur_c0;
 #pragma unroll
@@ -677,6 +704,10 @@ template <int BM, int BN, int WM, int WN, int BK>
 static hipError_t launch_bf16(const GemmArgs& a, int bsrc, int epi, int ydt, int groups, hipStream_t stream) {
     dim3 grid((unsigned)(a.grid_p * a.grid_m + a.tail_tiles * (a.tail_pieces - 1)), 1,
               (unsigned)(groups * (a.ksplit > 1 ? a.ksplit : 1)));
+    // NHWC gather: 16-byte channel runs, so C and C/g multiples of 8, and C/g a multiple or a
+    // divisor of the stage depth
+    if (bsrc == BSRC_NHWC_TAP && (a.Cg % 8 != 0 || a.Cx % 8 != 0 || (a.Cg >= BK ? a.Cg % BK : BK % a.Cg) != 0))
+        return hipErrorInvalidValue;
 #define CV_BF(BS, EP, TO) \
     hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, BK, BS, EP, TO>), grid, dim3(256), 0, stream, a)
     if (bsrc == BSRC_NHWC_TAP && epi == EPI_NCHW) {

@@ -303,3 +303,26 @@ def test_status_strings():
     for code in range(-8, 1):
         assert isinstance(B.conv2d_status_string(code), str)
     assert B.conv2d_status_string(0) == "ok"
+
+
+def test_bf16_small_group_nhwc_plan(monkeypatch):
+    """bf16 with C/g = 8 or 16 gathers whole taps from the NHWC copy (16-byte runs) when the
+    layer does enough work per input byte; other small C/g keep the NCHW gathers."""
+    for k in ("CONV2D_NHWC_GATHER", "CONV2D_SLICE"):
+        monkeypatch.delenv(k, raising=False)
+    base = datagen.ConvShape(n=32, c=16, h=56, w=56, k=1024, r=5, s=5, stride=(1, 1), pad=(2, 2), dil=(1, 1),
+                             groups=1, seed=1, has_bias=True, x_dtype="bf16", y_dtype="bf16")
+
+    def plan(cs):
+        d = B.conv2d_desc_create(params_for(cs))
+        try:
+            return B.conv2d_plan_query(d, B.CONV2D_ALGO_IMPLICIT_GEMM)
+        finally:
+            B.conv2d_desc_destroy(d)
+    for cs in (base, base.with_(c=8), base.with_(c=64, groups=4)):
+        p = plan(cs)
+        assert p.kernel == B.CONV2D_KERNEL_GEMM and p.needs_reorder == 1, cs
+        assert p.kred_pad == -(-p.kred // 32) * 32
+    assert plan(base.with_(c=24)).needs_reorder == 0                  # C/g = 24: NCHW gather
+    assert plan(base.with_(x_dtype="f32", y_dtype="f32")).needs_reorder == 0
+    assert plan(base.with_(k=16, r=3, s=3, pad=(1, 1))).needs_reorder == 0   # 144 flops per byte

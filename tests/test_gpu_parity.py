@@ -74,6 +74,12 @@ class _Kernel:
                 os.environ[k] = v
 
 
+def _nhwc_ok(cs):
+    """The bf16 NHWC gather takes C/g a multiple of 32, or C/g = 8 or 16."""
+    cg = cs.c // cs.groups
+    return cs.x_dtype == "bf16" and (cg % 32 == 0 or cg in (8, 16))
+
+
 def _run(cs, algo, mode="random", kernel=None, waves=None):
     import torch
     print(f"\n[case] {cs} algo={ALGO_IDS[algo]} kernel={kernel} waves={waves} mode={mode}", flush=True)
@@ -82,8 +88,8 @@ def _run(cs, algo, mode="random", kernel=None, waves=None):
     try:
         if kernel == "1" and dc.plan(algo).kernel != B.CONV2D_KERNEL_SLICE:
             pytest.skip("the sliced kernel does not fit this shape")
-        if kernel == "nhwc" and (cs.x_dtype != "bf16" or (cs.c // cs.groups) % 32):
-            pytest.skip("the NHWC gather needs bf16 and C/g a multiple of 32")
+        if kernel == "nhwc" and not _nhwc_ok(cs):
+            pytest.skip("the NHWC gather needs bf16 and C/g a multiple of 32, or 8 or 16")
         dc.run(algo)
         torch.cuda.synchronize()
         y = dc.y_nchw()
@@ -194,6 +200,12 @@ NHWC_BF16 = [
     _shape(1, 256, 14, 14, 256, 3, 3, pd=(1, 1), g=2, seed=213),
     _shape(3, 96, 9, 9, 200, 1, 1, seed=214),
     _shape(2, 64, 23, 23, 64, 7, 7, st=(2, 2), pd=(3, 3), seed=215),
+    # C/g = 16 or 8: two or four whole taps per 32-deep stage, the last stage part empty
+    _shape(2, 16, 20, 22, 96, 3, 3, pd=(1, 1), seed=216),
+    _shape(2, 8, 19, 17, 70, 5, 5, pd=(2, 2), seed=217),
+    _shape(1, 32, 15, 15, 64, 3, 3, st=(2, 2), pd=(2, 2), dl=(2, 2), g=2, seed=218),
+    _shape(3, 16, 9, 9, 200, 1, 1, seed=219),
+    _shape(1, 64, 13, 13, 40, 3, 3, pd=(1, 1), g=8, seed=220),
 ]
 
 
@@ -218,6 +230,7 @@ SPLIT = [
     (_shape(2, 96, 5, 6, 40, 3, 3, pd=(1, 1), seed=231), "5"),
     (_shape(1, 37, 9, 9, 33, 5, 3, st=(2, 1), pd=(2, 1), seed=232), "3"),
     (_shape(1, 64, 12, 12, 70, 3, 3, pd=(2, 2), dl=(2, 2), g=2, seed=233), "4"),
+    (_shape(1, 16, 9, 9, 40, 5, 5, pd=(2, 2), seed=234), "3"),
 ]
 
 
@@ -237,7 +250,7 @@ def test_split_reduction(idx, dt):
             plan = dc.plan(IMPLICIT)
         finally:
             dc.close()
-        if dt == "bf16-nhwc" and (cs.c // cs.groups) % 32:
+        if dt == "bf16-nhwc" and not _nhwc_ok(cs):
             pytest.skip("the NHWC gather needs C/g a multiple of 32")
         assert plan.ksplit > 1, plan.ksplit
         _check(cs, IMPLICIT, "random", kernel)
@@ -260,6 +273,7 @@ TAIL = [
     (_shape(1, 37, 9, 9, 33, 5, 3, st=(2, 1), pd=(2, 1), seed=241), "4"),
     (_shape(3, 128, 10, 10, 64, 1, 1, seed=242), "2"),
     (_shape(1, 96, 17, 15, 130, 3, 3, pd=(2, 2), dl=(2, 2), seed=243), "7"),
+    (_shape(2, 16, 13, 11, 70, 3, 3, pd=(1, 1), seed=244), "3"),
 ]
 
 
@@ -270,7 +284,7 @@ def test_tail_split(idx, dt):
     base, force = TAIL[idx]
     cs = base.with_(x_dtype="f32" if dt == "f32" else "bf16", y_dtype="f32" if dt == "f32" else "bf16")
     kernel = "nhwc" if dt == "bf16-nhwc" else "0"
-    if dt == "bf16-nhwc" and (cs.c // cs.groups) % 32:
+    if dt == "bf16-nhwc" and not _nhwc_ok(cs):
         pytest.skip("the NHWC gather needs C/g a multiple of 32")
     env = {"CONV2D_TAIL": force, "CONV2D_KSPLIT": "1"}
     old = {k: os.environ.get(k) for k in env}
