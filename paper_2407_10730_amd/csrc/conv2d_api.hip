@@ -115,10 +115,15 @@ GemmPlan choose_tile(int64_t M, int64_t P, int64_t G, int64_t kred, int xdt, int
     // their wave tiles relative to 64x64 (fp32, MI355X); with the bf16 16-byte gather the
     // larger tiles reuse each LDS operand more and win.
     struct Cand { int tile; double eff; };
+    // The 32-row tiles (four 32x32 or 32x64 wave tiles side by side) are for layers with few
+    // output channels per group, where a 64-row tile would leave half or more of every MFMA
+    // idle; rated below their 64-row peers so that they win only when they save tiles.
     const Cand cands_f32[] = {{TILE_64x64, 1.0}, {TILE_64x128, 1.0}, {TILE_64x256, 0.8},
-                              {TILE_128x64, 0.9}, {TILE_128x128, 0.85}};
+                              {TILE_128x64, 0.9}, {TILE_128x128, 0.85}, {TILE_32x128, 0.9},
+                              {TILE_32x256, 0.75}};
     const Cand cands_bf16[] = {{TILE_64x64, 0.7}, {TILE_64x128, 0.8}, {TILE_64x256, 0.6},
-                               {TILE_128x64, 0.85}, {TILE_128x128, 1.0}};
+                               {TILE_128x64, 0.85}, {TILE_128x128, 1.0}, {TILE_32x128, 0.6},
+                               {TILE_32x256, 0.7}};
     // bf16 tiles need two resident blocks per CU to hide their load latency: count rounds
     // of two blocks per CU (a single block per CU measured well below its share)
     const int per_round = nhwc ? 2 * cus : cus;
@@ -126,7 +131,14 @@ GemmPlan choose_tile(int64_t M, int64_t P, int64_t G, int64_t kred, int xdt, int
         const TileShape ts = kTileShapes[c.tile];
         const int64_t tiles = ceil_div(M, ts.bm) * ceil_div(P, ts.bn) * G;
         const double eff = c.eff * (dense && c.tile == TILE_64x128 ? 1.25 : 1.0);
-        const double cost = (double)ceil_div(tiles, per_round) * ts.bm * ts.bn / eff;
+        // at most 32 output channels per group, fewer tiles than one round and a long reduction:
+        // the split reduction fills the chip, so the time follows the total tile work (a 64-row
+        // tile then does twice the work of a 32-row one) rather than whole rounds.  (Applied to
+        // larger layers this rating picked 128 x 128 tiles with split reductions, measured up to
+        // 1.8x slower than 64 x 64 without.)
+        const double rounds = M <= 32 && tiles < per_round && kred >= 512 ? (double)tiles / per_round
+                                                                          : (double)ceil_div(tiles, per_round);
+        const double cost = rounds * ts.bm * ts.bn / eff;
         if (cost < best_cost) {
             best_cost = cost;
             best.kind = 0;
@@ -135,7 +147,8 @@ GemmPlan choose_tile(int64_t M, int64_t P, int64_t G, int64_t kred, int xdt, int
             best.bn = ts.bn;
         }
     }
-    if (best.kind == 0) best.bk = xdt == CONV2D_BF16 ? (nhwc && cg % 64 == 0 ? 64 : 32) : 16;
+    // (64-deep bf16 stages only on 64-row tiles: a 32 x 256 tile with them holds 83 KiB of LDS)
+    if (best.kind == 0) best.bk = xdt == CONV2D_BF16 ? (nhwc && cg % 64 == 0 && best.bm > 32 ? 64 : 32) : 16;
     const char* ov = std::getenv("CONV2D_GEMM");
     if (ov) {
         int a = 0, b = 0, c = 16;

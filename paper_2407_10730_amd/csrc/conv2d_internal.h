@@ -25,9 +25,10 @@ struct Geometry {
 
 // Tile configurations of the MFMA GEMM kernels.
 enum TileCfg { TILE_64x64 = 0, TILE_64x128 = 1, TILE_64x256 = 2, TILE_128x128 = 3,
-               TILE_128x64 = 4, TILE_COUNT = 5 };
+               TILE_128x64 = 4, TILE_32x128 = 5, TILE_32x256 = 6, TILE_COUNT = 7 };
 struct TileShape { int bm, bn; };
-static const TileShape kTileShapes[TILE_COUNT] = {{64, 64}, {64, 128}, {64, 256}, {128, 128}, {128, 64}};
+static const TileShape kTileShapes[TILE_COUNT] = {{64, 64}, {64, 128}, {64, 256}, {128, 128}, {128, 64},
+                                                  {32, 128}, {32, 256}};
 
 // Source of the GEMM's B operand (the im2col matrix, Kred x P).
 //  IMPLICIT_NCHW : gathered from NCHW x, reduction index kr = (c, r, s) looked up in the tap table

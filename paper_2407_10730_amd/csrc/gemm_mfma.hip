@@ -186,7 +186,8 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 16 ? 7 : 1)) void ge
     constexpr int BKT = 256 / BNT;            // threads along k (each owns runs of 4 rows)
     constexpr int BCOLS = BN / BNT;           // pixel columns per thread
     constexpr int BRUNS = BK / (4 * BKT);     // runs of 4 consecutive k rows per thread
-    constexpr int ARUNS = BM * BK / 1024;     // runs of 4 consecutive k of one A row per thread
+    constexpr int AQ = BM * BK / 4;           // runs of 4 consecutive k of one A row per stage
+    constexpr int ARUNS = (AQ + 255) / 256;   // ... per thread (the last partly idle when BM = 32)
     static_assert(BNT >= 64, "B loader needs wave-uniform k rows");
     static_assert(BRUNS >= 1 && ARUNS >= 1, "loader layout");
 
@@ -263,12 +264,13 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 16 ? 7 : 1)) void ge
 #pragma unroll
             for (int g = 0; g < ARUNS; ++g) {
                 const int q = t + g * 256;
+                const bool qa = AQ % 256 == 0 || q < AQ;
                 const int m = m0 + q / (BK / 4);
                 const int64_t e = a_base + (int64_t)m * A.lda + (int64_t)tap * A.Cg + cur_c0 + 4 * (q % (BK / 4));
                 // bit-cast the whole vector: casting its elements one by one made this
                 // compiler emit a single-dword load
                 areg[g] = __builtin_bit_cast(
-                    f32x4, __builtin_amdgcn_raw_buffer_load_b128(ra, m < A.M ? (uint32_t)(e * 4) : OOB_OFF, 0, 0));
+                    f32x4, __builtin_amdgcn_raw_buffer_load_b128(ra, (m < A.M) & qa ? (uint32_t)(e * 4) : OOB_OFF, 0, 0));
             }
             if (++cur_s == A.S) {
                 cur_s = 0;
@@ -303,12 +305,13 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 16 ? 7 : 1)) void ge
 #pragma unroll
             for (int g = 0; g < ARUNS; ++g) {
                 const int q = t + g * 256;
+                const bool qa = AQ % 256 == 0 || q < AQ;
                 const int m = m0 + q / (BK / 4);
                 const int kb = k0 + 4 * (q % (BK / 4));
                 const int64_t e = a_base + (int64_t)m * A.lda + kb;
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const bool ok = (m < A.M) & (kb + i < A.Kred);
+                    const bool ok = (m < A.M) & (kb + i < A.Kred) & qa;
                     areg[g][i] = ld_f32(ra, ok ? (uint32_t)((e + i) * 4) : OOB_OFF);
                 }
             }
@@ -323,7 +326,7 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 16 ? 7 : 1)) void ge
 #pragma unroll
         for (int g = 0; g < ARUNS; ++g) {
             const int q = t + g * 256;
-            *reinterpret_cast<f32x4*>(&As[buf][q / (BK / 4)][4 * (q % (BK / 4))]) = areg[g];
+            if (AQ % 256 == 0 || q < AQ) *reinterpret_cast<f32x4*>(&As[buf][q / (BK / 4)][4 * (q % (BK / 4))]) = areg[g];
         }
     };
 
@@ -445,7 +448,8 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void ge
     static_assert(BN <= 256 && 256 % BN == 0 && BN >= 64, "B loader assumes one column per thread");
     constexpr int CPR = BK / 8;                  // 16-byte chunks per tile row
     constexpr int BUNITS = BN * CPR / 256;       // 8-element B chunks per thread
-    constexpr int AUNITS = BM * CPR / 256;       // 8-element A chunks per thread
+    constexpr int AQ = BM * CPR;                 // 8-element A chunks per stage
+    constexpr int AUNITS = (AQ + 255) / 256;     // ... per thread (the last partly idle when BM = 32)
     constexpr bool NHWC = BSRC == BSRC_NHWC_TAP;
 
     __shared__ __attribute__((aligned(16))) uint16_t As[2][BM][LDK];
@@ -505,10 +509,11 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void ge
 #pragma unroll
         for (int i = 0; i < AUNITS; ++i) {
             const int u = t + i * 256;
+            const bool qa = AQ % 256 == 0 || u < AQ;
             const int m = m0 + u / CPR;
             const int kc = u % CPR;
             const int64_t e0 = a_base + (int64_t)m * A.lda + (int64_t)tap * A.Cg + cur_c0 + kc * 8;
-            areg[i] = __builtin_amdgcn_raw_buffer_load_b128(ra, m < A.M ? (uint32_t)(e0 * 2) : OOB_OFF, 0, 0);
+            areg[i] = __builtin_amdgcn_raw_buffer_load_b128(ra, (m < A.M) & qa ? (uint32_t)(e0 * 2) : OOB_OFF, 0, 0);
         }
     };
     auto advance_tap = [&]() {
@@ -544,11 +549,12 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void ge
 #pragma unroll
             for (int i = 0; i < AUNITS; ++i) {
                 const int u = t + i * 256;
+                const bool qa = AQ % 256 == 0 || u < AQ;
                 const int m = m0 + u / CPR;
                 const int kr = k0 + (u % CPR) * 8;
                 const int64_t e0 = a_base + (int64_t)m * A.lda + kr;
-                areg[i] = __builtin_amdgcn_raw_buffer_load_b128(ra, (m < A.M) & (kr < A.Kred) ? (uint32_t)(e0 * 2)
-                                                                                              : OOB_OFF, 0, 0);
+                areg[i] = __builtin_amdgcn_raw_buffer_load_b128(
+                    ra, (m < A.M) & (kr < A.Kred) & qa ? (uint32_t)(e0 * 2) : OOB_OFF, 0, 0);
             }
         } else if constexpr (NHWC) {
             const int roff = cur_r * A.dh, soff = cur_s * A.dw;
@@ -602,12 +608,13 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void ge
 #pragma unroll
             for (int i = 0; i < AUNITS; ++i) {
                 const int u = t + i * 256;
+                const bool qa = AQ % 256 == 0 || u < AQ;
                 const int m = m0 + u / CPR;
                 const int kc = u % CPR;
 #pragma unroll
                 for (int q = 0; q < 8; ++q) {
                     const int kr = k0 + kc * 8 + q;
-                    const bool ok = (m < A.M) & (kr < A.Kred);
+                    const bool ok = (m < A.M) & (kr < A.Kred) & qa;
                     const int64_t e = a_base + (int64_t)m * A.lda + kr;
                     h[q] = ld_u16(ra, ok ? (uint32_t)(e * 2) : OOB_OFF);
                 }
@@ -630,7 +637,7 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void ge
 #pragma unroll
         for (int i = 0; i < AUNITS; ++i) {
             const int u = t + i * 256;
-            *reinterpret_cast<u32x4*>(&As[buf][u / CPR][(u % CPR) * 8]) = areg[i];
+            if (AQ % 256 == 0 || u < AQ) *reinterpret_cast<u32x4*>(&As[buf][u / CPR][(u % CPR) * 8]) = areg[i];
         }
     };
 
@@ -765,6 +772,8 @@ hipError_t launch_gemm(const GemmArgs& a, int tile, int bk, int pf, int bsrc, in
             case TILE_64x256: CV_TB(64, 256, 1, 4);
             case TILE_128x128: CV_TB(128, 128, 2, 2);
             case TILE_128x64: CV_TB(128, 64, 2, 2);
+            case TILE_32x128: CV_TB(32, 128, 1, 4);
+            case TILE_32x256: CV_TB(32, 256, 1, 4);
             default: return hipErrorInvalidValue;
         }
 #undef CV_TB
@@ -780,6 +789,8 @@ hipError_t launch_gemm(const GemmArgs& a, int tile, int bk, int pf, int bsrc, in
     CV_T(TILE_64x256, 64, 256, 1, 4)
     CV_T(TILE_128x128, 128, 128, 2, 2)
     CV_T(TILE_128x64, 128, 64, 2, 2)
+    CV_T(TILE_32x128, 32, 128, 1, 4)
+    CV_T(TILE_32x256, 32, 256, 1, 4)
 #undef CV_T
     if (tile == TILE_64x64 && bk == 32 && pf == 1) return launch_f32<64, 64, 2, 2, 32, 1>(a, bsrc, epi, groups, stream);
     if (tile == TILE_64x64 && bk == 32 && pf == 2) return launch_f32<64, 64, 2, 2, 32, 2>(a, bsrc, epi, groups, stream);

@@ -326,3 +326,26 @@ def test_bf16_small_group_nhwc_plan(monkeypatch):
     assert plan(base.with_(c=24)).needs_reorder == 0                  # C/g = 24: NCHW gather
     assert plan(base.with_(x_dtype="f32", y_dtype="f32")).needs_reorder == 0
     assert plan(base.with_(k=16, r=3, s=3, pad=(1, 1))).needs_reorder == 0   # 144 flops per byte
+
+
+def test_small_m_tile_choice(monkeypatch):
+    """Few output channels per group: the planner takes a 32-row GEMM tile instead of leaving
+    most of a 64-row tile idle; 64 or more keep the 64-row tiles."""
+    monkeypatch.delenv("CONV2D_GEMM", raising=False)
+    base = datagen.ConvShape(n=32, c=512, h=56, w=56, k=16, r=5, s=5, stride=(1, 1), pad=(4, 4), dil=(2, 2),
+                             groups=1, seed=1, has_bias=True)
+
+    def tile(cs, algo=B.CONV2D_ALGO_IMPLICIT_GEMM):
+        d = B.conv2d_desc_create(params_for(cs))
+        try:
+            p = B.conv2d_plan_query(d, algo)
+            return p.tile_m, p.tile_n
+        finally:
+            B.conv2d_desc_destroy(d)
+    assert tile(base)[0] == 32
+    assert tile(base.with_(k=32))[0] == 32
+    assert tile(base.with_(k=3))[0] == 32
+    assert tile(base, B.CONV2D_ALGO_IM2COL_GEMM)[0] == 32
+    assert tile(base.with_(x_dtype="bf16", y_dtype="bf16", k=32))[0] == 32
+    assert tile(base.with_(k=64))[0] >= 64
+    assert tile(base.with_(k=256))[0] >= 64

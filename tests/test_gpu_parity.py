@@ -420,6 +420,40 @@ def test_winograd_chunks_and_configs(mt, monkeypatch):
     _check(datagen.CONFIGS["cfg2"], WINOGRAD)
 
 
+# 32-row tiles (layers with few output channels per group): forced on ragged and tiny K,
+# grouped layers, through every gather (NCHW table and tap-major, bf16 NHWC) and the explicit
+# path's dense GEMM, fp32 (BK 16, both prefetch distances) and bf16
+SMALL_M = [
+    _shape(2, 32, 15, 13, 3, 3, 3, pd=(1, 1), seed=290),
+    _shape(1, 64, 20, 18, 16, 5, 5, pd=(2, 2), seed=291),
+    _shape(2, 48, 11, 23, 33, 3, 3, st=(2, 1), pd=(1, 1), seed=292),
+    _shape(1, 64, 14, 14, 48, 3, 3, pd=(2, 2), dl=(2, 2), g=2, seed=293),
+    _shape(3, 16, 9, 9, 20, 1, 1, seed=294),
+]
+
+
+@pytest.mark.parametrize("algo", [IMPLICIT, IM2COL], ids=lambda a: ALGO_IDS[a])
+@pytest.mark.parametrize("dt", ["f32", "f32-pf2", "bf16", "bf16-nhwc"])
+@pytest.mark.parametrize("tile", [5, 6], ids=["32x128", "32x256"])
+@pytest.mark.parametrize("idx", range(len(SMALL_M)))
+def test_small_m_tiles(idx, tile, dt, algo, monkeypatch):
+    cs = SMALL_M[idx].with_(x_dtype="f32" if dt.startswith("f32") else "bf16",
+                            y_dtype="f32" if dt.startswith("f32") else "bf16")
+    monkeypatch.setenv("CONV2D_GEMM", f"k32:{tile}:16:2" if dt == "f32-pf2" else f"k32:{tile}")
+    kernel = "nhwc" if dt == "bf16-nhwc" else "0"
+    if algo == IM2COL and dt == "bf16-nhwc":
+        pytest.skip("the NHWC gather is an implicit-path source")
+    with _Kernel(kernel):
+        dc = DeviceConv(cs, "random")
+    try:
+        p = dc.plan(algo)
+        assert (p.tile_m, p.tile_n) == (32, 128 if tile == 5 else 256), (p.tile_m, p.tile_n)
+    finally:
+        dc.close()
+    _check(cs, algo, "random", kernel)
+    _check(cs.with_(y_dtype="f32"), algo, "integer", kernel)
+
+
 EDGE_ALGOS = [("implicit", IMPLICIT, None, None), ("implicit-gemm", IMPLICIT, "0", None),
               ("implicit-slice4", IMPLICIT, "1", "4"), ("implicit-slice8", IMPLICIT, "1", "8"),
               ("implicit-nhwc", IMPLICIT, "nhwc", None),
