@@ -54,7 +54,7 @@ enum {
     CONV2D_ALGO_AUTO = 0,          /* planner's choice */
     CONV2D_ALGO_IMPLICIT_GEMM = 1, /* sliced direct convolution: im2col slices gathered into LDS, MFMA */
     CONV2D_ALGO_IM2COL_GEMM = 2,   /* explicit im2col pack, MFMA GEMM, unpack (ConvBench's default baseline) */
-    CONV2D_ALGO_DIRECT = 3,        /* direct VALU kernel for depthwise / small-group convolutions */
+    CONV2D_ALGO_DIRECT = 3,        /* direct VALU kernels: depthwise, small groups, K <= 4 */
     CONV2D_ALGO_WINOGRAD = 4,      /* Winograd F(2x2,3x3) / F(4x4,3x3): 3x3, stride 1, dilation 1, one group, fp32 */
     CONV2D_ALGO_COUNT = 5
 };
@@ -142,7 +142,9 @@ typedef struct {
     int32_t op_class;         /* bit 0 pointwise, 1 grouped, 2 depthwise, 3 dilated, 4 rectangular, 5 strided */
     int32_t kernel;           /* microkernel that runs: CONV2D_KERNEL_* */
     int32_t ksplit;           /* implicit GEMM: reduction split into this many parts (1 = none);
-                                 the parts' fp32 partial sums are added by the unpack phase */
+                                 the parts' fp32 partial sums are added by the unpack phase.
+                                 DIRECT with K <= 4 (ungrouped, square 1/3/5/7 filter): the input
+                                 channels' ranges of the few-output-channel kernel, likewise */
     int32_t tail_tiles;       /* implicit GEMM: output tiles computed in tail_pieces parts by extra
                                  blocks of the same launch, so that every CU gets the same share
                                  of tile work (0 = none); the last part of a tile to finish adds

@@ -160,6 +160,16 @@ struct GrpPlan {
     int32_t TR, nbands, GB, CC, in_rows, in_cols, xfloats, kchunks, lds_bytes;
 };
 hipError_t launch_direct(const DirectArgs& a, int xdt, int ydt, hipStream_t stream);
+// Ungrouped layers with K <= 4 and square 1/3/5/7 filters on the vector ALUs; the input
+// channels split into `ranges` ranges (fp32 partials [range][K][P] in part, added by
+// launch_unpack) or one range (y written directly, part = NULL).
+struct SmallKArgs {
+    int32_t cper;  // input channels per range
+    float* part;
+};
+bool smallk_supported(const DirectArgs& a);
+int smallk_ranges(const DirectArgs& a);
+hipError_t launch_smallk(const DirectArgs& a, float* part, int ranges, int xdt, int ydt, hipStream_t stream);
 // Blocks the grouped direct kernel launches for this shape (0: it does not take the shape).
 int64_t grouped_blocks(const DirectArgs& a);
 

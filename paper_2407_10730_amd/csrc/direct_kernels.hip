@@ -699,6 +699,136 @@ int64_t grouped_blocks(const DirectArgs& a) {
     return (int64_t)a.N * ((a.C / a.Cg + p.GB - 1) / p.GB) * p.nbands * p.kchunks;
 }
 
+// ------------------------------------------------------------------ few output channels
+// Ungrouped layers with at most 4 output channels (image-to-image heads and the like): a GEMM
+// tile of 32 rows would leave 7/8 or more of every MFMA idle, so the vector ALUs compute them.
+// A thread owns one output pixel and walks a range of input channels (the reduction is split
+// over blockIdx.y into ranges so that the grid fills the chip) and all R x S taps: it reads each
+// input value once through the caches (neighbouring pixels share their windows there) and does
+// K FMAs with it.  The weights of a chunk of SK_CW channels sit in LDS and are read at
+// wave-uniform addresses (broadcast).  With one range the thread adds the bias and writes y;
+// otherwise it writes fp32 partial sums [range][K][P] and the unpack kernel adds the ranges in
+// order, then the bias (deterministic).
+constexpr int SK_CW = 16;
+
+template <int KK, int RR, typename TX, typename TY>
+__global__ __launch_bounds__(256) void smallk_kernel(DirectArgs A, SmallKArgs S) {
+    constexpr int RS = RR * RR;
+    __shared__ float wl[KK * SK_CW * RS];
+    const int t = threadIdx.x;
+    const int HoWo = A.Ho * A.Wo;
+    const int64_t P = (int64_t)A.N * HoWo;
+    const int64_t p = (int64_t)blockIdx.x * 256 + t;
+    const bool pok = p < P;
+    const int n = pok ? (int)(p / HoWo) : 0;
+    const int hw = pok ? (int)(p - (int64_t)n * HoWo) : 0;
+    const int ho = hw / A.Wo, wo = hw - (hw / A.Wo) * A.Wo;
+    const int hi0 = ho * A.sh - A.ph, wi0 = wo * A.sw - A.pw;
+    const int c_begin = blockIdx.y * S.cper;
+    const int c_end = min(A.C, c_begin + S.cper);
+    const __amdgpu_buffer_rsrc_t rx = dk_rsrc(A.x, A.x_bytes);
+    const TX* wp = reinterpret_cast<const TX*>(A.w);
+    float acc[KK];
+#pragma unroll
+    for (int k = 0; k < KK; ++k) acc[k] = 0.0f;
+    for (int cc = c_begin; cc < c_end; cc += SK_CW) {
+        const int cn = min(SK_CW, c_end - cc);
+        __syncthreads();  // the previous chunk's weights are no longer read
+        for (int i = t; i < KK * cn * RS; i += 256) {
+            const int k = i / (cn * RS);
+            const int rem = i - k * (cn * RS);
+            const TX v = wp[((int64_t)k * A.C + cc) * RS + rem];  // w[k][c][r][s]
+            float f;
+            if constexpr (sizeof(TX) == 4) f = __builtin_bit_cast(float, v);
+            else f = __builtin_bit_cast(float, (uint32_t)v << 16);
+            wl[k * SK_CW * RS + rem] = f;
+        }
+        __syncthreads();
+        for (int c = 0; c < cn; ++c) {
+            const int64_t plane = ((int64_t)n * A.C + cc + c) * A.H;
+#pragma unroll
+            for (int r = 0; r < RR; ++r) {
+                const int hi = hi0 + r * A.dh;
+                const bool hok = pok & ((unsigned)hi < (unsigned)A.H);
+                const int64_t row = (plane + hi) * A.W;
+                float xv[RR];
+#pragma unroll
+                for (int sx = 0; sx < RR; ++sx) {
+                    const int wi = wi0 + sx * A.dw;
+                    xv[sx] = dk_load(rx, hok & ((unsigned)wi < (unsigned)A.W), row + wi, (TX*)nullptr);
+                }
+#pragma unroll
+                for (int sx = 0; sx < RR; ++sx)
+#pragma unroll
+                    for (int k = 0; k < KK; ++k)
+                        acc[k] = __builtin_fmaf(xv[sx], wl[(k * SK_CW + c) * RS + r * RR + sx], acc[k]);
+            }
+        }
+    }
+    if (!pok) return;
+    if (S.part) {
+#pragma unroll
+        for (int k = 0; k < KK; ++k) S.part[((int64_t)blockIdx.y * KK + k) * P + p] = acc[k];
+        return;
+    }
+    const __amdgpu_buffer_rsrc_t ry = dk_rsrc(A.y, A.y_bytes);
+#pragma unroll
+    for (int k = 0; k < KK; ++k) {
+        const float v = acc[k] + (A.bias ? A.bias[k] : 0.0f);
+        const int64_t o = ((int64_t)n * KK + k) * HoWo + hw;
+        if constexpr (sizeof(TY) == 4)
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), ry, (uint32_t)(o * 4), 0, 0);
+        else
+            __builtin_amdgcn_raw_buffer_store_b16(dk_f32_to_bf16(v), ry, (uint32_t)(o * 2), 0, 0);
+    }
+}
+
+bool smallk_supported(const DirectArgs& a) {
+    return a.Cg == a.C && a.Kg == a.K && a.K >= 1 && a.K <= 4 && a.R == a.S &&
+           (a.R == 1 || a.R == 3 || a.R == 5 || a.R == 7);
+}
+
+// Channel ranges for a grid of about 2048 blocks (at least SK_CW channels each); 1 = no split.
+int smallk_ranges(const DirectArgs& a) {
+    const int64_t P = (int64_t)a.N * a.Ho * a.Wo;
+    const int64_t pblocks = (P + 255) / 256;
+    int64_t ranges = (2048 + pblocks - 1) / pblocks;
+    ranges = std::min<int64_t>(ranges, (a.C + SK_CW - 1) / SK_CW);
+    while (ranges > 1 && ranges * a.K * P * 4 > ((int64_t)256 << 20)) --ranges;
+    return (int)std::max<int64_t>(ranges, 1);
+}
+
+template <int KK, int RR>
+static hipError_t launch_smallk_t(const DirectArgs& a, const SmallKArgs& sk, int ranges, int xdt, int ydt,
+                                  hipStream_t stream) {
+    const int64_t P = (int64_t)a.N * a.Ho * a.Wo;
+    const dim3 grid((unsigned)((P + 255) / 256), (unsigned)ranges);
+    if (xdt == CONV2D_F32)
+        hipLaunchKernelGGL((smallk_kernel<KK, RR, float, float>), grid, dim3(256), 0, stream, a, sk);
+    else if (ydt == CONV2D_BF16)
+        hipLaunchKernelGGL((smallk_kernel<KK, RR, uint16_t, uint16_t>), grid, dim3(256), 0, stream, a, sk);
+    else
+        hipLaunchKernelGGL((smallk_kernel<KK, RR, uint16_t, float>), grid, dim3(256), 0, stream, a, sk);
+    return hipGetLastError();
+}
+
+hipError_t launch_smallk(const DirectArgs& a, float* part, int ranges, int xdt, int ydt, hipStream_t stream) {
+    const int64_t P = (int64_t)a.N * a.Ho * a.Wo;
+    if (!smallk_supported(a) || ranges < 1 || ranges > 65535 || (ranges > 1) != (part != nullptr) ||
+        (P + 255) / 256 > 0x7fffffffLL)
+        return hipErrorInvalidValue;
+    SmallKArgs sk{};
+    sk.cper = (a.C + ranges - 1) / ranges;
+    sk.part = part;
+#define CV_SK(KV, RV) \
+    if (a.K == KV && a.R == RV) return launch_smallk_t<KV, RV>(a, sk, ranges, xdt, ydt, stream);
+#define CV_SK4(RV) CV_SK(1, RV) CV_SK(2, RV) CV_SK(3, RV) CV_SK(4, RV)
+    CV_SK4(1) CV_SK4(3) CV_SK4(5) CV_SK4(7)
+#undef CV_SK4
+#undef CV_SK
+    return hipErrorInvalidValue;
+}
+
 hipError_t launch_direct(const DirectArgs& a, int xdt, int ydt, hipStream_t stream) {
     // CONV2D_DW_GENERIC (tests): the generic per-plane kernel for every shape
     if (!std::getenv("CONV2D_DW_GENERIC")) {

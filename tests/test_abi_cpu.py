@@ -227,7 +227,9 @@ def test_grouped_auto_choice():
     assert algo(c=512, k=3, h=112, w=112) == B.CONV2D_ALGO_DIRECT        # 32 images x 13 bands
     assert algo(c=512, k=16, h=112, w=112) == B.CONV2D_ALGO_DIRECT
     assert algo(c=512, k=32, h=112, w=112) == B.CONV2D_ALGO_IMPLICIT_GEMM
-    assert algo(n=2, c=512, k=3, h=112, w=112) == B.CONV2D_ALGO_IMPLICIT_GEMM   # 26 blocks
+    # 26 grouped-kernel blocks; K <= 4: the few-output-channel kernel splits the channels instead
+    assert algo(n=2, c=512, k=3, h=112, w=112) == B.CONV2D_ALGO_DIRECT
+    assert algo(n=2, c=512, k=16, h=112, w=112) == B.CONV2D_ALGO_IMPLICIT_GEMM
     assert algo(c=512, k=3, h=112, w=112, r=1, s=1, pad=(0, 0)) == B.CONV2D_ALGO_IMPLICIT_GEMM
 
 
@@ -349,3 +351,38 @@ def test_small_m_tile_choice(monkeypatch):
     assert tile(base.with_(x_dtype="bf16", y_dtype="bf16", k=32))[0] == 32
     assert tile(base.with_(k=64))[0] >= 64
     assert tile(base.with_(k=256))[0] >= 64
+
+
+def test_smallk_direct_plan(monkeypatch):
+    """Ungrouped layers with K <= 4: DIRECT runs the few-output-channel kernel, its input
+    channels split into ranges that fill the chip (partials in the workspace)."""
+    for k in ("CONV2D_SMALLK", "CONV2D_SMALLK_RANGES", "CONV2D_DW_GENERIC"):
+        monkeypatch.delenv(k, raising=False)
+    base = datagen.ConvShape(n=8, c=2048, h=112, w=112, k=3, r=7, s=7, stride=(2, 2), pad=(3, 3), dil=(1, 1),
+                             groups=1, seed=1, has_bias=True)
+
+    def plan(cs, algo=B.CONV2D_ALGO_DIRECT):
+        d = B.conv2d_desc_create(params_for(cs))
+        try:
+            return B.conv2d_plan_query(d, algo)
+        finally:
+            B.conv2d_desc_destroy(d)
+    p = plan(base)
+    P = 8 * 56 * 56
+    pblocks = -(-P // 256)
+    ranges = min(-(-2048 // pblocks), 2048 // 16)
+    assert p.kernel == B.CONV2D_KERNEL_DIRECT and p.ksplit == ranges
+    assert p.workspace_bytes == ranges * 3 * P * 4
+    assert plan(base.with_(n=16, c=16, h=448, w=448)).ksplit <= 1          # 3136 pixel blocks
+    assert plan(base.with_(k=5)).ksplit == 0                                # K > 4: other kernels
+    assert plan(base.with_(c=32)).ksplit == 0                               # 32 x 49 < 2048: grouped
+    bf = base.with_(x_dtype="bf16", y_dtype="bf16")
+    assert plan(bf).ksplit == 0                                             # bf16: other kernels
+    assert plan(base, B.CONV2D_ALGO_AUTO).algo == B.CONV2D_ALGO_DIRECT
+    assert plan(base.with_(r=1, s=1, pad=(0, 0)), B.CONV2D_ALGO_AUTO).algo != B.CONV2D_ALGO_DIRECT
+    monkeypatch.setenv("CONV2D_SMALLK_RANGES", "5")
+    assert plan(base).ksplit == 5
+    monkeypatch.setenv("CONV2D_SMALLK", "1")
+    assert plan(bf).ksplit == 5
+    monkeypatch.setenv("CONV2D_SMALLK", "0")
+    assert plan(base).ksplit == 0

@@ -454,6 +454,42 @@ def test_small_m_tiles(idx, tile, dt, algo, monkeypatch):
     _check(cs.with_(y_dtype="f32"), algo, "integer", kernel)
 
 
+# few output channels (ungrouped, K <= 4) on the vector-ALU direct kernel: every K and filter
+# size, strides, dilations, paddings, ragged pixel blocks, one channel, channel ranges forced to
+# 1 / 3 / 7 (partials added by the unpack kernel) and the planner's count
+SMALLK = [
+    _shape(2, 40, 17, 15, 3, 3, 3, pd=(1, 1), seed=300),
+    _shape(1, 9, 23, 21, 1, 7, 7, st=(2, 2), pd=(3, 3), seed=301),
+    _shape(3, 33, 12, 14, 4, 5, 5, pd=(4, 4), dl=(2, 2), seed=302),
+    _shape(2, 64, 9, 11, 2, 1, 1, seed=303, bias=False),
+    _shape(1, 1, 10, 10, 3, 3, 3, st=(1, 2), pd=(0, 1), seed=304),
+]
+
+
+@pytest.mark.parametrize("ranges", [None, "1", "3", "7"])
+@pytest.mark.parametrize("var", [("nchw", "f32", "f32"), ("nchw", "bf16", "bf16"), ("nhwc", "bf16", "f32"),
+                                 ("nhwc", "f32", "f32")], ids=lambda v: "-".join(v))
+@pytest.mark.parametrize("idx", range(len(SMALLK)))
+def test_smallk_direct(idx, var, ranges, monkeypatch):
+    layout, xdt, ydt = var
+    cs = SMALLK[idx].with_(layout=layout, x_dtype=xdt, y_dtype=ydt)
+    monkeypatch.setenv("CONV2D_SMALLK", "1")
+    if ranges is not None:
+        monkeypatch.setenv("CONV2D_SMALLK_RANGES", ranges)
+    dc = DeviceConv(cs, "random")
+    try:
+        p = dc.plan(DIRECT)
+        assert p.kernel == B.CONV2D_KERNEL_DIRECT and p.workspace_bytes == (p.ksplit * cs.k * 4 * dc.out_nkhw[0] *
+                                                                            dc.out_nkhw[2] * dc.out_nkhw[3]
+                                                                            if p.ksplit > 1 else 0)
+        if ranges is not None:
+            assert max(p.ksplit, 1) == min(int(ranges), cs.c), (p.ksplit, ranges)
+    finally:
+        dc.close()
+    _check(cs, DIRECT, "random")
+    _check(cs.with_(y_dtype="f32"), DIRECT, "integer")
+
+
 EDGE_ALGOS = [("implicit", IMPLICIT, None, None), ("implicit-gemm", IMPLICIT, "0", None),
               ("implicit-slice4", IMPLICIT, "1", "4"), ("implicit-slice8", IMPLICIT, "1", "8"),
               ("implicit-nhwc", IMPLICIT, "nhwc", None),
