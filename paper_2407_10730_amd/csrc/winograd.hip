@@ -186,6 +186,9 @@ __global__ __launch_bounds__(256) void wino_output_kernel(WinoArgs A, const floa
     }
     const float bias = A.bias ? A.bias[k] : 0.0f;
     const __amdgpu_buffer_rsrc_t ry = make_rsrc(A.y, A.y_bytes);
+    // with Wo a multiple of MT every row of a tile starts MT-float aligned: one vector store
+    // per row when it lies inside the plane
+    const bool vec = A.Wo % MT == 0;
 #pragma unroll
     for (int a = 0; a < MT; ++a) {
         float o[MT];
@@ -193,9 +196,21 @@ __global__ __launch_bounds__(256) void wino_output_kernel(WinoArgs A, const floa
         const int ho = MT * ty + a, wo = MT * tx;
         const bool rok = ho < A.Ho;
         const int64_t e = (((int64_t)n * A.K + k) * A.Ho + ho) * A.Wo + wo;
+        if (vec) {
+            if constexpr (MT == 4) {
+                const u32x4 v = {__builtin_bit_cast(uint32_t, o[0] + bias), __builtin_bit_cast(uint32_t, o[1] + bias),
+                                 __builtin_bit_cast(uint32_t, o[2] + bias), __builtin_bit_cast(uint32_t, o[3] + bias)};
+                __builtin_amdgcn_raw_buffer_store_b128(v, ry, rok ? (uint32_t)(e * 4) : OOB_OFF, 0, 0);
+            } else {
+                typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+                const u32x2 v = {__builtin_bit_cast(uint32_t, o[0] + bias), __builtin_bit_cast(uint32_t, o[1] + bias)};
+                __builtin_amdgcn_raw_buffer_store_b64(v, ry, rok ? (uint32_t)(e * 4) : OOB_OFF, 0, 0);
+            }
+        } else {
 #pragma unroll
-        for (int b = 0; b < MT; ++b)
-            st_f32(ry, rok & (wo + b < A.Wo) ? (uint32_t)((e + b) * 4) : OOB_OFF, o[b] + bias);
+            for (int b = 0; b < MT; ++b)
+                st_f32(ry, rok & (wo + b < A.Wo) ? (uint32_t)((e + b) * 4) : OOB_OFF, o[b] + bias);
+        }
     }
 }
 
