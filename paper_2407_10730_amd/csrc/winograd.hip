@@ -106,8 +106,11 @@ __global__ __launch_bounds__(256) void wino_filter_kernel(const float* __restric
 }
 
 // V[xi][c][t - t0] = (B^T d B)[xi] for the tiles t0 .. t0+tc-1 (tile t = (n, th, tw) row-major);
-// one thread per (c, tile), tile fastest.
-template <int MT>
+// one thread per (c, tile), tile fastest.  VPW = pw (0 or 1) for F(4x4) when W is a multiple
+// of 4 and every tile's aligned columns 4*tx .. 4*tx+3 lie inside the row: the 6 columns of a
+// patch row then hold those four, read with one 16-byte load (consecutive lanes read consecutive
+// 16-byte words), and two single columns; VPW = -1 reads 6 single columns.
+template <int MT, int VPW>
 __global__ __launch_bounds__(256) void wino_input_kernel(WinoArgs A, float* __restrict__ v) {
     constexpr int AL = MT + 2;
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -127,11 +130,28 @@ __global__ __launch_bounds__(256) void wino_input_kernel(WinoArgs A, float* __re
     for (int a = 0; a < AL; ++a) {
         const int hi = hi0 + a;
         const bool hok = (unsigned)hi < (unsigned)A.H;
+        const int64_t row = (plane0 + hi) * A.W;
+        if constexpr (VPW >= 0) {
+            // the aligned columns MT*tx .. MT*tx+3 with one 16-byte load, the other two singly
+            const f32x4 q = __builtin_bit_cast(
+                f32x4, __builtin_amdgcn_raw_buffer_load_b128(rx, hok ? (uint32_t)((row + MT * tx) * 4) : OOB_OFF, 0, 0));
 #pragma unroll
-        for (int b = 0; b < AL; ++b) {
-            const int wi = wi0 + b;
-            const bool ok = hok & ((unsigned)wi < (unsigned)A.W);
-            d[a][b] = ld_f32(rx, ok ? (uint32_t)(((plane0 + hi) * A.W + wi) * 4) : OOB_OFF);
+            for (int b = 0; b < AL; ++b) {
+                if (b >= VPW && b < VPW + 4) {
+                    d[a][b] = q[b - VPW];
+                } else {
+                    const int wi = wi0 + b;
+                    const bool ok = hok & ((unsigned)wi < (unsigned)A.W);
+                    d[a][b] = ld_f32(rx, ok ? (uint32_t)((row + wi) * 4) : OOB_OFF);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int b = 0; b < AL; ++b) {
+                const int wi = wi0 + b;
+                const bool ok = hok & ((unsigned)wi < (unsigned)A.W);
+                d[a][b] = ld_f32(rx, ok ? (uint32_t)((row + wi) * 4) : OOB_OFF);
+            }
         }
     }
     float e[AL][AL];  // B^T d
@@ -229,10 +249,16 @@ hipError_t launch_wino_input(const WinoArgs& a, float* v, hipStream_t stream) {
     const int64_t n = (int64_t)a.C * a.tc;
     if (n < 1 || (n + 255) / 256 > 0x7fffffffLL || (a.mt != 2 && a.mt != 4)) return hipErrorInvalidValue;
     const dim3 grid((unsigned)((n + 255) / 256));
+    // (with W a multiple of 4 the condition holds for paddings 0 and 1, never for 2)
+    const bool vec = a.mt == 4 && a.W % 4 == 0 && (a.pw == 0 || a.pw == 1) && 4 * (a.tw - 1) + 3 < a.W;
     if (a.mt == 2)
-        hipLaunchKernelGGL(wino_input_kernel<2>, grid, dim3(256), 0, stream, a, v);
+        hipLaunchKernelGGL((wino_input_kernel<2, -1>), grid, dim3(256), 0, stream, a, v);
+    else if (!vec)
+        hipLaunchKernelGGL((wino_input_kernel<4, -1>), grid, dim3(256), 0, stream, a, v);
+    else if (a.pw == 0)
+        hipLaunchKernelGGL((wino_input_kernel<4, 0>), grid, dim3(256), 0, stream, a, v);
     else
-        hipLaunchKernelGGL(wino_input_kernel<4>, grid, dim3(256), 0, stream, a, v);
+        hipLaunchKernelGGL((wino_input_kernel<4, 1>), grid, dim3(256), 0, stream, a, v);
     return hipGetLastError();
 }
 

@@ -382,6 +382,9 @@ WINO = [
     _shape(1, 70, 15, 15, 90, 3, 3, pd=(2, 2), seed=272),
     _shape(3, 64, 14, 14, 128, 3, 3, pd=(1, 1), seed=273),
     _shape(2, 24, 8, 31, 16, 3, 3, pd=(1, 0), seed=274, bias=False),
+    # W a multiple of 4 with padding 1 or 0: the F(4x4) input transform's 16-byte row loads
+    _shape(2, 20, 13, 16, 24, 3, 3, pd=(1, 1), seed=275),
+    _shape(1, 33, 9, 20, 17, 3, 3, seed=276),
 ]
 
 
