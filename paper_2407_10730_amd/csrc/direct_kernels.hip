@@ -337,8 +337,10 @@ __global__ __launch_bounds__(DIRECT_THREADS) void dw_kernel(DirectArgs A, DwPlan
     constexpr int DWP_VMAX = TILEF / 4 / DIRECT_THREADS;  // 16-byte loads per thread
     constexpr int DWP_SMAX = TILEF / DIRECT_THREADS;      // 4-byte loads per thread
     // With stride 2 and an even dilation (or a 1x1 filter) every window reads only the even
-    // rows of the tile; the odd ones are neither loaded nor read.
+    // rows of the tile: only those are loaded and stored (tile row j holds input row
+    // hi_base + 2j), which halves the tile and the loads.
     constexpr bool EVEN_ROWS = ST == 2 && (DL % 2 == 0 || R == 1);
+    constexpr int RSTEP = EVEN_ROWS ? 2 : 1;  // input rows per tile row
     extern __shared__ __attribute__((aligned(16))) float tile[];  // PB * IR * LDW floats
     __shared__ float wsh[DW_MAX_PLANES * R * S];
     __shared__ float bsh[DW_MAX_PLANES];
@@ -399,10 +401,9 @@ __global__ __launch_bounds__(DIRECT_THREADS) void dw_kernel(DirectArgs A, DwPlan
 #pragma unroll
             for (int u = 0; u < DWP_VMAX; ++u) {
                 const int e = t + u * DIRECT_THREADS;
-                const int hi = hi_base + tr;
+                const int hi = hi_base + RSTEP * tr;
                 const int w0 = 4 * cg - P.LPAD;
-                const bool ok = (e < total) & ((unsigned)hi < (unsigned)A.H) & ((unsigned)w0 < (unsigned)A.W) &
-                                !(EVEN_ROWS && (tr & 1));
+                const bool ok = (e < total) & ((unsigned)hi < (unsigned)A.H) & ((unsigned)w0 < (unsigned)A.W);
                 const int32_t idx = ok ? pbase[lp] + hi * A.W + w0 : 0;
                 if constexpr (sizeof(TX) == 4) {
                     vreg[u] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
@@ -426,10 +427,9 @@ __global__ __launch_bounds__(DIRECT_THREADS) void dw_kernel(DirectArgs A, DwPlan
 #pragma unroll
             for (int u = 0; u < DWP_SMAX; ++u) {
                 const int e = t + u * DIRECT_THREADS;
-                const int hi = hi_base + tr;
+                const int hi = hi_base + RSTEP * tr;
                 const int w = cg - P.LPAD;
-                const bool ok = (e < total) & ((unsigned)hi < (unsigned)A.H) & ((unsigned)w < (unsigned)A.W) &
-                                !(EVEN_ROWS && (tr & 1));
+                const bool ok = (e < total) & ((unsigned)hi < (unsigned)A.H) & ((unsigned)w < (unsigned)A.W);
                 sreg[u] = dk_load(rx, ok, ok ? pbase[lp] + hi * A.W + w : 0, (TX*)nullptr);
                 step();
             }
@@ -476,7 +476,7 @@ __global__ __launch_bounds__(DIRECT_THREADS) void dw_kernel(DirectArgs A, DwPlan
             const float bias = bsh[lp];
             const int orow0 = rb * VR;
             const int ow0 = cb * HC;
-            const float* rp = &tile[(lp * P.IR + orow0 * ST) * P.LDW + P.LPAD - A.pw + ow0 * ST];
+            const float* rp = &tile[(lp * P.IR + orow0 * ST / RSTEP) * P.LDW + P.LPAD - A.pw + ow0 * ST];
             float acc[VR][HC];
 #pragma unroll
             for (int v = 0; v < VR; ++v)
@@ -486,7 +486,7 @@ __global__ __launch_bounds__(DIRECT_THREADS) void dw_kernel(DirectArgs A, DwPlan
             for (int rr = 0; rr < NR; ++rr) {
                 float xrow[RB];
 #pragma unroll
-                for (int c = 0; c < RB; ++c) xrow[c] = rp[rr * P.LDW + c];
+                for (int c = 0; c < RB; ++c) xrow[c] = rp[(rr / RSTEP) * P.LDW + c];  // (odd rows unused)
 #pragma unroll
                 for (int v = 0; v < VR; ++v) {
                     // input row rr is filter row r of output row v when rr = v*ST + r*DL
@@ -548,8 +548,13 @@ static bool dw_plan(const DirectArgs& a, int sw_t, int dw_t, int tilef, DwPlan* 
     const int maxcol = LPAD - a.pw + (WS * 4 - 1) * sw_t + (a.S - 1) * dw_t;
     int LDW = (maxcol + 1 + 3) / 4 * 4;
     if (LDW < LPAD + a.W) LDW = (LPAD + a.W + 3) / 4 * 4;
-    // rows of the tile: TH output rows rounded up to whole strips of 4
-    auto ir = [&](int th) { return (((th + 3) / 4) * 4 - 1) * a.sh + (a.R - 1) * a.dh + 1; };
+    // rows of the tile: TH output rows rounded up to whole strips of 4; with stride 2 and an
+    // even dilation or a 1x1 filter only the even input rows are kept
+    const bool even = a.sh == 2 && (a.dh % 2 == 0 || a.R == 1);
+    auto ir = [&](int th) {
+        const int rows = (((th + 3) / 4) * 4 - 1) * a.sh + (a.R - 1) * a.dh + 1;
+        return even ? (rows + 1) / 2 : rows;
+    };
     int TH, PB;
     if (a.Ho * WS <= 1024) {
         TH = a.Ho;

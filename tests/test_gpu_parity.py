@@ -185,6 +185,12 @@ EDGE = [
     _shape(2, 6, 19, 17, 6, 7, 7, st=(2, 2), pd=(3, 3), g=6),
     _shape(1, 3, 150, 124, 3, 3, 3, st=(1, 2), pd=(1, 1), g=3),
     _shape(3, 4, 7, 7, 4, 1, 1, g=4),
+    # depthwise at stride 2 with a 1x1 filter or an even dilation (only even input rows kept),
+    # one plane tall enough for several bands
+    _shape(2, 6, 15, 16, 6, 1, 1, st=(2, 2), g=6),
+    _shape(1, 4, 21, 19, 4, 3, 3, st=(2, 2), pd=(2, 2), dl=(2, 2), g=4),
+    _shape(2, 3, 40, 24, 3, 5, 5, st=(2, 2), pd=(4, 4), dl=(2, 2), g=3),
+    _shape(1, 2, 300, 40, 2, 3, 3, st=(2, 2), pd=(2, 2), dl=(2, 2), g=2),
 ]
 VARIANTS = [("nchw", "f32", "f32"), ("nhwc", "f32", "f32"), ("nchw", "bf16", "bf16"),
             ("nhwc", "bf16", "f32")]
