@@ -122,6 +122,36 @@ def cpu_baseline(cs, x, w, b, y_gpu, flops_per_image, target_s=10.0):
     return res, {"images": n_img, "err_per_point": pt, "err_literal": lit}
 
 
+def cpu_im2col_gemm(cs, x, w, b, flops_per_image, n_img=1):
+    """Context beside the oracle: the paper's baseline algorithm (explicit im2col, then one
+    GEMM) on the host in fp32 with numpy's BLAS, timed on the first images."""
+    import numpy as np
+    from numpy.lib.stride_tricks import sliding_window_view
+    n_img = max(1, min(n_img, cs.n))
+    g = cs.groups
+    sh, sw = cs.stride
+    ph, pw = cs.pad
+    dh, dw = cs.dil
+    xs = np.ascontiguousarray(x[:n_img], dtype=np.float32)
+    wf = np.ascontiguousarray(w, dtype=np.float32)
+    t0 = time.perf_counter()
+    xp = np.pad(xs, ((0, 0), (0, 0), (ph, ph), (pw, pw)))
+    eh, ew = (cs.r - 1) * dh + 1, (cs.s - 1) * dw + 1
+    win = sliding_window_view(xp, (eh, ew), axis=(2, 3))[:, :, ::sh, ::sw, ::dh, ::dw]  # N C Ho Wo R S
+    n, c, ho, wo, r, s_ = win.shape
+    cg, kg = c // g, cs.k // g
+    ys = []
+    for gi in range(g):
+        col = win[:, gi * cg:(gi + 1) * cg].transpose(1, 4, 5, 0, 2, 3).reshape(cg * r * s_, n * ho * wo)
+        ys.append(wf[gi * kg:(gi + 1) * kg].reshape(kg, cg * r * s_) @ col)
+    y = np.concatenate(ys, axis=0).reshape(cs.k, n, ho, wo).transpose(1, 0, 2, 3)
+    if cs.has_bias:
+        y = y + b.astype(np.float32)[None, :, None, None]
+    dt = time.perf_counter() - t0
+    return {"value": flops_per_image * n_img / dt / 1e12, "unit": "TFLOP/s", "kind": "numpy im2col + BLAS GEMM, fp32",
+            "sample": f"first {n_img} of {cs.n} images", "seconds": dt}, y
+
+
 def _cpu_model():
     try:
         with open("/proc/cpuinfo") as f:
@@ -560,6 +590,8 @@ def main():
         cb, parity = cpu_baseline(cs, x, dc.w_host, dc.b_host, y_gpu, flops // n)
         out["cpu_baseline"] = cb
         cb["gpu_over_oracle"] = out["value"] / cb["value"]
+        out["cpu_im2col_gemm_context"], _ = cpu_im2col_gemm(cs, x, dc.w_host, dc.b_host, flops // n,
+                                                            n_img=min(cs.n, 4))
         out["parity_on_cpu_sample"] = parity
     dc.close()
     if args.calibrate_copy:
