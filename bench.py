@@ -29,11 +29,13 @@ PEAK_HBM_GBS = 8000.0
 # 256 CUs x 4 SIMDs x 16 lanes x 2 flops x 2.4 GHz
 PEAK_VALU_TFLOPS = 78.6
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+# the kernels' sources and the planner's (which picks the instantiation, tile and launch shape)
+_PLANNER = ["paper_2407_10730_amd/csrc/conv2d_api.hip", "paper_2407_10730_amd/csrc/conv2d_internal.h"]
 KERNEL_SOURCES = {
     "implicit_gemm": ["paper_2407_10730_amd/csrc/gemm_mfma.hip", "paper_2407_10730_amd/csrc/pack_kernels.hip",
-                      "paper_2407_10730_amd/csrc/slice_conv.hip"],
-    "im2col_gemm": ["paper_2407_10730_amd/csrc/gemm_mfma.hip", "paper_2407_10730_amd/csrc/pack_kernels.hip"],
-    "direct": ["paper_2407_10730_amd/csrc/direct_kernels.hip"],
+                      "paper_2407_10730_amd/csrc/slice_conv.hip"] + _PLANNER,
+    "im2col_gemm": ["paper_2407_10730_amd/csrc/gemm_mfma.hip", "paper_2407_10730_amd/csrc/pack_kernels.hip"] + _PLANNER,
+    "direct": ["paper_2407_10730_amd/csrc/direct_kernels.hip"] + _PLANNER,
 }
 
 

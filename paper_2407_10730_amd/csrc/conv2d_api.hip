@@ -149,6 +149,13 @@ GemmPlan choose_tile(int64_t M, int64_t P, int64_t G, int64_t kred, int xdt, int
     }
     // (64-deep bf16 stages only on 64-row tiles: a 32 x 256 tile with them holds 83 KiB of LDS)
     if (best.kind == 0) best.bk = xdt == CONV2D_BF16 ? (nhwc && cg % 64 == 0 && best.bm > 32 ? 64 : 32) : 16;
+    // fp32 64x64 tiles over a long tap-major reduction: 32-deep stages with the loads two
+    // stages ahead (half the barriers per MFMA; cfg2 76 -> 72-74 us, N31 71.5 -> 69.4 us on
+    // MI355X; no gain at reductions of 256)
+    if (xdt == CONV2D_F32 && !dense && best.tile == TILE_64x64 && kred >= 512 && cg % 32 == 0) {
+        best.bk = 32;
+        best.pf = 2;
+    }
     const char* ov = std::getenv("CONV2D_GEMM");
     if (ov) {
         int a = 0, b = 0, c = 16;

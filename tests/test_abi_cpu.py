@@ -185,9 +185,10 @@ def test_tail_split_plan(monkeypatch):
         finally:
             B.conv2d_desc_destroy(d)
     cfg2 = datagen.CONFIGS["cfg2"]
-    info = plan(cfg2)                        # 1568 = 6 * 256 + 32 tiles of 64 x 64, 36 stages
-    assert (info.tail_tiles, info.tail_pieces) == (32, 8)
-    assert info.workspace_bytes == 32 * 8 * 64 * 64 * 4
+    info = plan(cfg2)                        # 1568 = 6 * 256 + 32 tiles of 64 x 64, 18 stages of 32
+    assert (info.tail_tiles, info.tail_pieces) == (32, 6)           # 8 wanted: pieces of 3 -> 6
+    assert info.workspace_bytes == 32 * 6 * 64 * 64 * 4
+    assert info.kred_pad == 576
     info = plan(cfg2.with_(n=31))            # 1519 tiles: 239 past 5 * 256, more than half the CUs
     assert info.tail_tiles == 0
     info = plan(cfg2.with_(n=2))             # 98 tiles: fewer than the CUs, no tail
