@@ -55,7 +55,8 @@ enum {
     CONV2D_ALGO_IMPLICIT_GEMM = 1, /* sliced direct convolution: im2col slices gathered into LDS, MFMA */
     CONV2D_ALGO_IM2COL_GEMM = 2,   /* explicit im2col pack, MFMA GEMM, unpack (ConvBench's default baseline) */
     CONV2D_ALGO_DIRECT = 3,        /* direct VALU kernels: depthwise, small groups, K <= 4 */
-    CONV2D_ALGO_WINOGRAD = 4,      /* Winograd F(2x2,3x3) / F(4x4,3x3): 3x3, stride 1, dilation 1, one group, fp32 */
+    CONV2D_ALGO_WINOGRAD = 4,      /* Winograd F(2x2,3x3) / F(4x4,3x3): 3x3, stride 1, dilation 1, one group;
+                                      fp32, or bf16 with F(2x2) only and C a multiple of 8 */
     CONV2D_ALGO_COUNT = 5
 };
 /* Winograd's phases: PRE_REORDER the filter transform, IN_PACKING the input

@@ -366,20 +366,27 @@ void plan_winograd(conv2d_desc* d) {
     const Geometry& g = d->g;
     WinoPlan& p = d->wino;
     p = WinoPlan{};
+    // bf16 (x and w; y bf16 or fp32): F(2x2) only, with U and V rounded to bf16 and fp32 GEMM
+    // sums (F(4x4)'s larger transform constants put bf16 rounding past the 1e-2 gate in a CPU
+    // study: 2e-2 at C = 16, against 1.8e-3 for F(2x2)); V is laid out [16][tiles][C] from the
+    // NHWC copy of x so that the GEMM reads 8 channels per 16-byte load (C a multiple of 8)
+    const bool bf = g.xdt == CONV2D_BF16;
     if (g.R != 3 || g.S != 3 || g.sh != 1 || g.sw != 1 || g.dh != 1 || g.dw != 1 || g.G != 1 ||
-        g.xdt != CONV2D_F32 || g.ydt != CONV2D_F32 || g.x_elems * 4 > kBufferLimit || g.y_elems * 4 > kBufferLimit)
+        (g.xdt == CONV2D_F32 && g.ydt != CONV2D_F32) || (bf && g.C % 8 != 0) ||
+        g.x_elems * elem_size(g.xdt) > kBufferLimit || g.y_elems * elem_size(g.ydt) > kBufferLimit)
         return;
+    const int64_t es = elem_size(g.xdt);  // bytes of U and V elements
     const int64_t force = env_int64("CONV2D_WINO_TILE", 0);
-    p.mt = force == 2 || force == 4 ? (int)force : wino_auto_tile(g);
+    p.mt = bf ? 2 : force == 2 || force == 4 ? (int)force : wino_auto_tile(g);
     p.npos = (p.mt + 2) * (p.mt + 2);
     const int64_t np = p.npos;
-    p.u_bytes = np * g.K * g.C * 4;
+    p.u_bytes = np * g.K * g.C * es;
     if (p.u_bytes > kBufferLimit) return;
     p.tiles = g.N * ceil_div(g.Ho, p.mt) * ceil_div(g.Wo, p.mt);
     int64_t cap = env_int64("CONV2D_WORKSPACE_LIMIT_BYTES", (int64_t)1 << 30);
     if (cap < 0) cap = 0;
-    int64_t tc = cap / (np * (g.C + g.K) * 4);
-    tc = std::min<int64_t>(tc, kBufferLimit / (np * g.C * 4));
+    int64_t tc = cap / (np * (g.C * es + g.K * 4));
+    tc = std::min<int64_t>(tc, kBufferLimit / (np * g.C * es));
     tc = std::min<int64_t>(tc, kBufferLimit / (np * g.K * 4));
     tc = std::min<int64_t>(tc, p.tiles);
     if (tc < 1) {
@@ -388,12 +395,13 @@ void plan_winograd(conv2d_desc* d) {
     }
     p.tc = tc;
     p.chunks = ceil_div(p.tiles, tc);
-    p.v_bytes = np * g.C * tc * 4;
+    p.v_bytes = np * g.C * tc * es;
     p.m_bytes = np * g.K * tc * 4;
     // 64 x 128 tiles: measured fastest for these GEMMs (dense operands, reductions of a few
-    // hundred channels) on MI355X, ahead of 64 x 64, 128 x 128 and 64 x 256
-    p.gemm = choose_tile(g.K, tc, np, g.C, CONV2D_F32, g.C);
-    if (!std::getenv("CONV2D_GEMM")) {
+    // hundred channels) on MI355X, ahead of 64 x 64, 128 x 128 and 64 x 256; bf16 takes the
+    // planner's bf16 choice for 16-byte operand loads
+    p.gemm = choose_tile(g.K, tc, np, g.C, g.xdt, g.C, bf);
+    if (!bf && !std::getenv("CONV2D_GEMM")) {
         p.gemm.tile = TILE_64x128;
         p.gemm.bm = kTileShapes[TILE_64x128].bm;
         p.gemm.bn = kTileShapes[TILE_64x128].bn;
@@ -692,21 +700,22 @@ int run_winograd(conv2d_desc* d, const void* x, const void* w, const float* bias
     if (!p.ok) return p.status;
     CV_TRY(ensure_buffer(&d->wu, &d->wu_bytes, p.u_bytes));
     CV_TRY(ensure_buffer(&d->wvm, &d->wvm_bytes, p.v_bytes + p.m_bytes));
-    float* u = static_cast<float*>(d->wu);
-    float* v = static_cast<float*>(d->wvm);
+    const bool bf = g.xdt == CONV2D_BF16;  // U and V bf16, V [16][tc][C] from NHWC x
+    const int64_t es = elem_size(g.xdt);
+    void* v = d->wvm;
     float* m = reinterpret_cast<float*>(static_cast<char*>(d->wvm) + p.v_bytes);
     {
         // pre-convolution reordering: the filter transform
         Scope sc(d, CONV2D_ALGO_WINOGRAD, CONV2D_PH_PRE_REORDER, s, ph);
         CV_TRY(sc.begin());
-        CV_HIP(launch_wino_filter(static_cast<const float*>(w), u, (int)g.K, (int)g.C, p.mt, s));
+        CV_HIP(launch_wino_filter(w, d->wu, (int)g.K, (int)g.C, p.mt, g.xdt, s));
         CV_TRY(sc.end());
     }
     WinoArgs wa{};
     wa.x = x;
-    wa.x_bytes = (uint32_t)(g.x_elems * 4);
+    wa.x_bytes = (uint32_t)(g.x_elems * es);
     wa.y = y;
-    wa.y_bytes = (uint32_t)(g.y_elems * 4);
+    wa.y_bytes = (uint32_t)(g.y_elems * elem_size(g.ydt));
     wa.bias = g.has_bias ? bias : nullptr;
     wa.C = (int32_t)g.C; wa.H = (int32_t)g.H; wa.W = (int32_t)g.W; wa.K = (int32_t)g.K;
     wa.Ho = (int32_t)g.Ho; wa.Wo = (int32_t)g.Wo; wa.ph = g.ph; wa.pw = g.pw;
@@ -719,21 +728,25 @@ int run_winograd(conv2d_desc* d, const void* x, const void* w, const float* bias
         {
             Scope sc(d, CONV2D_ALGO_WINOGRAD, CONV2D_PH_IN_PACKING, s, ph);
             CV_TRY(sc.begin());
-            CV_HIP(launch_wino_input(wa, v, s));
+            if (bf)
+                CV_HIP(launch_wino_input_nhwc(wa, static_cast<uint16_t*>(v), s));
+            else
+                CV_HIP(launch_wino_input(wa, static_cast<float*>(v), s));
             CV_TRY(sc.end());
         }
         {
-            // one GEMM per transformed position: M[xi] = U[xi] (K x C) * V[xi] (C x tc)
+            // one GEMM per transformed position: M[xi] = U[xi] (K x C) * V[xi] (C x tc); in bf16
+            // V[xi] is stored transposed (tc x C)
             const GemmPlan& gp = p.gemm;
             GemmArgs a{};
-            a.a = u;
+            a.a = d->wu;
             a.a_bytes = (uint32_t)p.u_bytes;
             a.lda = (int32_t)g.C;
             a.a_gstride = g.K * g.C;
             a.b = v;
-            a.b_bytes = (uint32_t)(p.npos * g.C * wa.tc * 4);
+            a.b_bytes = (uint32_t)(p.npos * g.C * wa.tc * es);
             a.b_gstride = g.C * wa.tc;
-            a.ldb = wa.tc;
+            a.ldb = bf ? (int32_t)g.C : wa.tc;
             a.M = (int32_t)g.K;
             a.Kred = (int32_t)g.C;
             a.P = wa.tc;
@@ -747,13 +760,13 @@ int run_winograd(conv2d_desc* d, const void* x, const void* w, const float* bias
             a.HoWo = (int32_t)(g.Ho * g.Wo);
             Scope sc(d, CONV2D_ALGO_WINOGRAD, CONV2D_PH_IN_MICROKERNEL, s, ph);
             CV_TRY(sc.begin());
-            CV_HIP(dispatch_gemm(gp, a, BSRC_DENSE, EPI_DENSE, CONV2D_F32, CONV2D_F32, p.npos, s));
+            CV_HIP(dispatch_gemm(gp, a, bf ? BSRC_DENSE_T : BSRC_DENSE, EPI_DENSE, g.xdt, CONV2D_F32, p.npos, s));
             CV_TRY(sc.end());
         }
         {
             Scope sc(d, CONV2D_ALGO_WINOGRAD, CONV2D_PH_IN_UNPACKING, s, ph);
             CV_TRY(sc.begin());
-            CV_HIP(launch_wino_output(wa, m, s));
+            CV_HIP(launch_wino_output(wa, m, g.ydt, s));
             CV_TRY(sc.end());
         }
     }
@@ -1006,7 +1019,7 @@ int conv2d_desc_create(const conv2d_params* params, conv2d_desc** out) {
     // transforms (measured 1.6-2.0x faster than the implicit GEMM for C, K = 128 .. 1024 on
     // 14x14 to 112x112 planes on MI355X; 64 -> 64 channels on 56x56 gain under 10 %, 7x7 planes
     // none)
-    else if (d->wino.ok && g.C >= 128 && g.K >= 128 && std::min(g.Ho, g.Wo) >= 8)
+    else if (d->wino.ok && g.xdt == CONV2D_F32 && g.C >= 128 && g.K >= 128 && std::min(g.Ho, g.Wo) >= 8)
         d->auto_algo = CONV2D_ALGO_WINOGRAD;
     else if (d->implicit_ok)
         d->auto_algo = CONV2D_ALGO_IMPLICIT_GEMM;
@@ -1078,9 +1091,10 @@ int conv2d_fwd(conv2d_desc* d, const void* x, const void* w, const float* bias, 
     const void* xin = x;
     void* yout = y;
     const bool nhwc = g.layout == CONV2D_NHWC;
-    // The bf16 NHWC gather reads x channel-contiguous: an NHWC x goes in as it is, an NCHW x is
-    // reordered.  Every other kernel reads NCHW x.
-    const bool x_nhwc = algo == CONV2D_ALGO_IMPLICIT_GEMM && d->implicit_nhwc && !d->implicit_slice;
+    // The bf16 NHWC gather and the bf16 Winograd input transform read x channel-contiguous: an
+    // NHWC x goes in as it is, an NCHW x is reordered.  Every other kernel reads NCHW x.
+    const bool x_nhwc = (algo == CONV2D_ALGO_IMPLICIT_GEMM && d->implicit_nhwc && !d->implicit_slice) ||
+                        (algo == CONV2D_ALGO_WINOGRAD && g.xdt == CONV2D_BF16);
     if (nhwc != x_nhwc) {
         const int64_t xb = g.x_elems * elem_size(g.xdt);
         CV_TRY(ensure_buffer(&d->xr, &d->xr_bytes, xb));
@@ -1201,6 +1215,7 @@ int conv2d_plan_query(const conv2d_desc* d, int algo, conv2d_plan_info* out) {
     out->kred_pad = (int32_t)(ceil_div(g.Kred, bk) * bk);
     out->needs_reorder = g.layout == CONV2D_NHWC ? 1 : 0;
     if (algo == CONV2D_ALGO_IMPLICIT_GEMM && d->implicit_nhwc && !d->implicit_slice) out->needs_reorder = 1;
+    if (algo == CONV2D_ALGO_WINOGRAD && g.xdt == CONV2D_BF16) out->needs_reorder = 1;
     out->op_class = (int32_t)d->opclass;
     out->chunks = 1;
     if (algo == CONV2D_ALGO_IMPLICIT_GEMM) {

@@ -36,7 +36,7 @@ static const TileShape kTileShapes[TILE_COUNT] = {{64, 64}, {64, 128}, {64, 256}
 //  IMPLICIT_TAP  : gathered from NCHW x in tap-major order kr' = (r, s, c); one filter tap per
 //                  stage, so needs C/g to be a multiple of the stage depth (no table)
 //  NHWC_TAP      : (bf16) the same order gathered from an NHWC copy of x, 16 bytes per load
-enum BSrc { BSRC_IMPLICIT_NCHW = 0, BSRC_DENSE = 1, BSRC_IMPLICIT_TAP = 2, BSRC_NHWC_TAP = 3 };
+enum BSrc { BSRC_IMPLICIT_NCHW = 0, BSRC_DENSE = 1, BSRC_IMPLICIT_TAP = 2, BSRC_NHWC_TAP = 3, BSRC_DENSE_T = 4 };
 // Destination of the GEMM result.
 enum Epi { EPI_NCHW = 0, EPI_DENSE = 1 };
 
@@ -148,9 +148,12 @@ struct WinoArgs {
     int64_t t0;
     int32_t tc;
 };
-hipError_t launch_wino_filter(const float* w, float* u, int K, int C, int mt, hipStream_t stream);
+// dt = CONV2D_F32 (F(2x2) or F(4x4)) or CONV2D_BF16 (F(2x2), w and U in bf16)
+hipError_t launch_wino_filter(const void* w, void* u, int K, int C, int mt, int dt, hipStream_t stream);
 hipError_t launch_wino_input(const WinoArgs& a, float* v, hipStream_t stream);
-hipError_t launch_wino_output(const WinoArgs& a, const float* m, hipStream_t stream);
+// bf16: V [16][tc][C] from the NHWC copy of x
+hipError_t launch_wino_input_nhwc(const WinoArgs& a, uint16_t* v, hipStream_t stream);
+hipError_t launch_wino_output(const WinoArgs& a, const float* m, int ydt, hipStream_t stream);
 
 // Grouped direct kernel plan: bands of TR output rows, GB groups per block, CC input
 // channels staged at a time (window in_rows x in_cols each, xfloats LDS floats for all of

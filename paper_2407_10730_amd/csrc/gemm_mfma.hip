@@ -451,6 +451,9 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void ge
     constexpr int AQ = BM * CPR;                 // 8-element A chunks per stage
     constexpr int AUNITS = (AQ + 255) / 256;     // ... per thread (the last partly idle when BM = 32)
     constexpr bool NHWC = BSRC == BSRC_NHWC_TAP;
+    // B columns whose reduction values are contiguous in memory (NHWC gather, or a dense B^T
+    // [P][ldb]): one 16-byte load moves 8 reduction values of one column
+    constexpr bool KCONT = NHWC || BSRC == BSRC_DENSE_T;
 
     __shared__ __attribute__((aligned(16))) uint16_t As[2][BM][LDK];
     __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN][LDK];
@@ -483,7 +486,7 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void ge
     if constexpr (NHWC) {
 #pragma unroll
         for (int i = 0; i < BUNITS; ++i) csn[i] = col_state_nhwc(A, p0 + (t + i * 256) / CPR, gi);
-    } else if (BSRC != BSRC_DENSE) {
+    } else if (BSRC != BSRC_DENSE && BSRC != BSRC_DENSE_T) {
         cs = col_state(A, pcol, gi);
     }
     const uint32_t dvb = pcol < A.P ? (uint32_t)(((int64_t)gi * A.b_gstride + pcol) * 2) : OOB_OFF;
@@ -530,7 +533,28 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void ge
     auto load_stage = [&](int stage) {
         const int k0 = stage * BK;
         uint16_t h[8];
-        if (NHWC && A.Cg < BK) {
+        if constexpr (BSRC == BSRC_DENSE_T) {
+            // B^T[gi][p][k] (row pitch ldb) and A[gi][m][k] (row pitch lda), 8 values per load
+#pragma unroll
+            for (int i = 0; i < BUNITS; ++i) {
+                const int u = t + i * 256;
+                const int col = p0 + u / CPR;
+                const int kr = k0 + (u % CPR) * 8;
+                const int64_t e = (int64_t)gi * A.b_gstride + (int64_t)col * A.ldb + kr;
+                breg[i] = __builtin_amdgcn_raw_buffer_load_b128(
+                    rb, (col < A.P) & (kr < A.Kred) ? (uint32_t)(e * 2) : OOB_OFF, 0, 0);
+            }
+#pragma unroll
+            for (int i = 0; i < AUNITS; ++i) {
+                const int u = t + i * 256;
+                const bool qa = AQ % 256 == 0 || u < AQ;
+                const int m = m0 + u / CPR;
+                const int kr = k0 + (u % CPR) * 8;
+                const int64_t e0 = a_base + (int64_t)m * A.lda + kr;
+                areg[i] = __builtin_amdgcn_raw_buffer_load_b128(
+                    ra, (m < A.M) & (kr < A.Kred) & qa ? (uint32_t)(e0 * 2) : OOB_OFF, 0, 0);
+            }
+        } else if (NHWC && A.Cg < BK) {
             // C/g = 8 or 16: a stage holds BK / (C/g) whole taps; chunk kc of a pixel is the
             // 8 channels (kc*8) % (C/g) .. +7 of tap k0/(C/g) + kc*8/(C/g) (zero past the last tap)
 #pragma unroll
@@ -626,7 +650,7 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void ge
     auto store_stage = [&](int buf) {
 #pragma unroll
         for (int i = 0; i < BUNITS; ++i) {
-            if constexpr (NHWC) {
+            if constexpr (KCONT) {
                 const int u = t + i * 256;
                 *reinterpret_cast<u32x4*>(&Bs[buf][u / CPR][(u % CPR) * 8]) = breg[i];
             } else {
@@ -715,6 +739,9 @@ static hipError_t launch_bf16(const GemmArgs& a, int bsrc, int epi, int ydt, int
     // divisor of the stage depth
     if (bsrc == BSRC_NHWC_TAP && (a.Cg % 8 != 0 || a.Cx % 8 != 0 || (a.Cg >= BK ? a.Cg % BK : BK % a.Cg) != 0))
         return hipErrorInvalidValue;
+    // dense B^T: 16-byte rows of 8 reduction values
+    if (bsrc == BSRC_DENSE_T && (a.Kred % 8 != 0 || a.ldb % 8 != 0 || a.lda % 8 != 0 || epi != EPI_DENSE))
+        return hipErrorInvalidValue;
 #define CV_BF(BS, EP, TO) \
     hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, BK, BS, EP, TO>), grid, dim3(256), 0, stream, a)
     if (bsrc == BSRC_NHWC_TAP && epi == EPI_NCHW) {
@@ -722,6 +749,8 @@ static hipError_t launch_bf16(const GemmArgs& a, int bsrc, int epi, int ydt, int
         else CV_BF(BSRC_NHWC_TAP, EPI_NCHW, float);
     } else if (bsrc == BSRC_NHWC_TAP && epi == EPI_DENSE) {
         CV_BF(BSRC_NHWC_TAP, EPI_DENSE, float);  // partial sums of a split reduction
+    } else if (bsrc == BSRC_DENSE_T) {
+        CV_BF(BSRC_DENSE_T, EPI_DENSE, float);
     } else if (BK != 32) {
         return hipErrorInvalidValue;  // the NCHW gathers and the dense source use 32-row stages
     } else if (bsrc == BSRC_IMPLICIT_NCHW && epi == EPI_NCHW) {

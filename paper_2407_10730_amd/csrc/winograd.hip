@@ -79,19 +79,28 @@ __device__ __forceinline__ void wino_at(const float* m, float* o) {
     }
 }
 
-// U[xi][k][c] = (G g_kc G^T)[xi]; one thread per (k, c), c fastest (coalesced writes).
-template <int MT>
-__global__ __launch_bounds__(256) void wino_filter_kernel(const float* __restrict__ w, float* __restrict__ u, int K,
-                                                          int C) {
+// element v of w (fp32, or bf16 widened) and a transformed value in the workspace's type (fp32,
+// or bf16 rounded to nearest even)
+__device__ __forceinline__ float wino_ld(const float* p, int64_t v) { return p[v]; }
+__device__ __forceinline__ float wino_ld(const uint16_t* p, int64_t v) {
+    return __builtin_bit_cast(float, (uint32_t)p[v] << 16);
+}
+__device__ __forceinline__ void wino_st(float* p, int64_t v, float f) { p[v] = f; }
+__device__ __forceinline__ void wino_st(uint16_t* p, int64_t v, float f) { p[v] = f32_to_bf16_rne(f); }
+
+// U[xi][k][c] = (G g_kc G^T)[xi]; one thread per (k, c), c fastest (coalesced writes).  The
+// transform is computed in fp32 from the (fp32 or bf16) filters; bf16 U is rounded once.
+template <int MT, typename T>
+__global__ __launch_bounds__(256) void wino_filter_kernel(const T* __restrict__ w, T* __restrict__ u, int K, int C) {
     constexpr int AL = MT + 2;
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= (int64_t)K * C) return;
-    const float* g = w + i * 9;  // w[k][c][3][3], i = k*C + c
-    float t[AL][3];              // G g
+    const T* g = w + i * 9;  // w[k][c][3][3], i = k*C + c
+    float t[AL][3];          // G g
 #pragma unroll
     for (int j = 0; j < 3; ++j) {
         float col[AL];
-        wino_g<MT>(g[j], g[3 + j], g[6 + j], col);
+        wino_g<MT>(wino_ld(g, j), wino_ld(g, 3 + j), wino_ld(g, 6 + j), col);
 #pragma unroll
         for (int a = 0; a < AL; ++a) t[a][j] = col[a];
     }
@@ -101,7 +110,58 @@ __global__ __launch_bounds__(256) void wino_filter_kernel(const float* __restric
         float row[AL];
         wino_g<MT>(t[a][0], t[a][1], t[a][2], row);
 #pragma unroll
-        for (int b = 0; b < AL; ++b) u[(a * AL + b) * plane + i] = row[b];
+        for (int b = 0; b < AL; ++b) wino_st(u, (a * AL + b) * plane + i, row[b]);
+    }
+}
+
+// bf16: V[xi][t - t0][c] = (B^T d B)[xi] from the NHWC copy of x, one thread per (tile, c), c
+// fastest: reads of x and writes of V both run along the channels (the GEMM then reads 8
+// channels of a tile with one 16-byte load).  Computed in fp32, rounded to bf16 once.
+template <int MT>
+__global__ __launch_bounds__(256) void wino_input_nhwc_kernel(WinoArgs A, uint16_t* __restrict__ v) {
+    constexpr int AL = MT + 2;
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= (int64_t)A.C * A.tc) return;
+    const int tl = (int)(i / A.C);
+    const int c = (int)(i - (int64_t)tl * A.C);
+    const int64_t t = A.t0 + tl;
+    const int tiles_img = A.th * A.tw;
+    const int n = (int)(t / tiles_img);
+    const int r = (int)(t - (int64_t)n * tiles_img);
+    const int ty = r / A.tw, tx = r - (r / A.tw) * A.tw;
+    const int hi0 = MT * ty - A.ph, wi0 = MT * tx - A.pw;
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(A.x, A.x_bytes);
+    float d[AL][AL];
+#pragma unroll
+    for (int a = 0; a < AL; ++a) {
+        const int hi = hi0 + a;
+        const bool hok = (unsigned)hi < (unsigned)A.H;
+#pragma unroll
+        for (int b = 0; b < AL; ++b) {
+            const int wi = wi0 + b;
+            const bool ok = hok & ((unsigned)wi < (unsigned)A.W);
+            const int64_t e = (((int64_t)n * A.H + hi) * A.W + wi) * A.C + c;
+            const uint32_t h = ld_u16(rx, ok ? (uint32_t)(e * 2) : OOB_OFF);
+            d[a][b] = __builtin_bit_cast(float, h << 16);
+        }
+    }
+    float e[AL][AL];  // B^T d
+#pragma unroll
+    for (int b = 0; b < AL; ++b) {
+        float col[AL], o[AL];
+#pragma unroll
+        for (int a = 0; a < AL; ++a) col[a] = d[a][b];
+        wino_bt<MT>(col, o);
+#pragma unroll
+        for (int a = 0; a < AL; ++a) e[a][b] = o[a];
+    }
+    const int64_t plane = (int64_t)A.tc * A.C;
+#pragma unroll
+    for (int a = 0; a < AL; ++a) {  // (B^T d) B
+        float o[AL];
+        wino_bt<MT>(e[a], o);
+#pragma unroll
+        for (int b = 0; b < AL; ++b) v[(a * AL + b) * plane + i] = f32_to_bf16_rne(o[b]);
     }
 }
 
@@ -176,7 +236,7 @@ __global__ __launch_bounds__(256) void wino_input_kernel(WinoArgs A, float* __re
 
 // y (the MT x MT block of tile t, clipped at the edges) = A^T M A + bias; one thread per
 // (k, tile), tile fastest.
-template <int MT>
+template <int MT, typename TY>
 __global__ __launch_bounds__(256) void wino_output_kernel(WinoArgs A, const float* __restrict__ m) {
     constexpr int AL = MT + 2;
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -208,7 +268,7 @@ __global__ __launch_bounds__(256) void wino_output_kernel(WinoArgs A, const floa
     const __amdgpu_buffer_rsrc_t ry = make_rsrc(A.y, A.y_bytes);
     // with Wo a multiple of MT every row of a tile starts MT-float aligned: one vector store
     // per row when it lies inside the plane
-    const bool vec = A.Wo % MT == 0;
+    const bool vec = sizeof(TY) == 4 && A.Wo % MT == 0;
 #pragma unroll
     for (int a = 0; a < MT; ++a) {
         float o[MT];
@@ -216,7 +276,11 @@ __global__ __launch_bounds__(256) void wino_output_kernel(WinoArgs A, const floa
         const int ho = MT * ty + a, wo = MT * tx;
         const bool rok = ho < A.Ho;
         const int64_t e = (((int64_t)n * A.K + k) * A.Ho + ho) * A.Wo + wo;
-        if (vec) {
+        if constexpr (sizeof(TY) == 2) {
+#pragma unroll
+            for (int b = 0; b < MT; ++b)
+                st_u16(ry, rok & (wo + b < A.Wo) ? (uint32_t)((e + b) * 2) : OOB_OFF, f32_to_bf16_rne(o[b] + bias));
+        } else if (vec) {
             if constexpr (MT == 4) {
                 const u32x4 v = {__builtin_bit_cast(uint32_t, o[0] + bias), __builtin_bit_cast(uint32_t, o[1] + bias),
                                  __builtin_bit_cast(uint32_t, o[2] + bias), __builtin_bit_cast(uint32_t, o[3] + bias)};
@@ -234,14 +298,27 @@ __global__ __launch_bounds__(256) void wino_output_kernel(WinoArgs A, const floa
     }
 }
 
-hipError_t launch_wino_filter(const float* w, float* u, int K, int C, int mt, hipStream_t stream) {
+hipError_t launch_wino_filter(const void* w, void* u, int K, int C, int mt, int dt, hipStream_t stream) {
     const int64_t n = (int64_t)K * C;
-    if (n < 1 || (n + 255) / 256 > 0x7fffffffLL || (mt != 2 && mt != 4)) return hipErrorInvalidValue;
+    if (n < 1 || (n + 255) / 256 > 0x7fffffffLL || (mt != 2 && mt != 4) || (dt == CONV2D_BF16 && mt != 2))
+        return hipErrorInvalidValue;
     const dim3 grid((unsigned)((n + 255) / 256));
-    if (mt == 2)
-        hipLaunchKernelGGL(wino_filter_kernel<2>, grid, dim3(256), 0, stream, w, u, K, C);
+    if (dt == CONV2D_BF16)
+        hipLaunchKernelGGL((wino_filter_kernel<2, uint16_t>), grid, dim3(256), 0, stream,
+                           static_cast<const uint16_t*>(w), static_cast<uint16_t*>(u), K, C);
+    else if (mt == 2)
+        hipLaunchKernelGGL((wino_filter_kernel<2, float>), grid, dim3(256), 0, stream, static_cast<const float*>(w),
+                           static_cast<float*>(u), K, C);
     else
-        hipLaunchKernelGGL(wino_filter_kernel<4>, grid, dim3(256), 0, stream, w, u, K, C);
+        hipLaunchKernelGGL((wino_filter_kernel<4, float>), grid, dim3(256), 0, stream, static_cast<const float*>(w),
+                           static_cast<float*>(u), K, C);
+    return hipGetLastError();
+}
+
+hipError_t launch_wino_input_nhwc(const WinoArgs& a, uint16_t* v, hipStream_t stream) {
+    const int64_t n = (int64_t)a.C * a.tc;
+    if (n < 1 || (n + 255) / 256 > 0x7fffffffLL || a.mt != 2) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((wino_input_nhwc_kernel<2>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, a, v);
     return hipGetLastError();
 }
 
@@ -262,14 +339,18 @@ hipError_t launch_wino_input(const WinoArgs& a, float* v, hipStream_t stream) {
     return hipGetLastError();
 }
 
-hipError_t launch_wino_output(const WinoArgs& a, const float* m, hipStream_t stream) {
+hipError_t launch_wino_output(const WinoArgs& a, const float* m, int ydt, hipStream_t stream) {
     const int64_t n = (int64_t)a.K * a.tc;
     if (n < 1 || (n + 255) / 256 > 0x7fffffffLL || (a.mt != 2 && a.mt != 4)) return hipErrorInvalidValue;
     const dim3 grid((unsigned)((n + 255) / 256));
-    if (a.mt == 2)
-        hipLaunchKernelGGL(wino_output_kernel<2>, grid, dim3(256), 0, stream, a, m);
-    else
-        hipLaunchKernelGGL(wino_output_kernel<4>, grid, dim3(256), 0, stream, a, m);
+    if (ydt == CONV2D_BF16) {
+        if (a.mt != 2) return hipErrorInvalidValue;
+        hipLaunchKernelGGL((wino_output_kernel<2, uint16_t>), grid, dim3(256), 0, stream, a, m);
+    } else if (a.mt == 2) {
+        hipLaunchKernelGGL((wino_output_kernel<2, float>), grid, dim3(256), 0, stream, a, m);
+    } else {
+        hipLaunchKernelGGL((wino_output_kernel<4, float>), grid, dim3(256), 0, stream, a, m);
+    }
     return hipGetLastError();
 }
 

@@ -255,7 +255,7 @@ def test_winograd_plan(monkeypatch):
     assert info.algo == B.CONV2D_ALGO_WINOGRAD and info.chunks == 1 and info.kred == 64 and info.wino_tile == 2
     assert info.workspace_bytes == 16 * 64 * 64 * 4 + 16 * (64 + 64) * tiles * 4
     for bad in (cfg2.with_(r=5, s=5, pad=(2, 2)), cfg2.with_(stride=(2, 2)), cfg2.with_(dil=(2, 2), pad=(2, 2)),
-                cfg2.with_(groups=2), cfg2.with_(x_dtype="bf16", y_dtype="bf16")):
+                cfg2.with_(groups=2), cfg2.with_(x_dtype="bf16", y_dtype="bf16", c=60)):
         with pytest.raises(B.Conv2dError) as e:
             plan(bad)
         assert e.value.status == B.CONV2D_E_UNSUPPORTED
@@ -268,6 +268,13 @@ def test_winograd_plan(monkeypatch):
     assert auto(cfg2) == B.CONV2D_ALGO_IMPLICIT_GEMM                       # 64 channels
     assert auto(cfg2.with_(c=128, k=256)) == B.CONV2D_ALGO_WINOGRAD
     assert auto(cfg2.with_(c=512, k=512, h=7, w=7)) == B.CONV2D_ALGO_IMPLICIT_GEMM    # 7x7 planes
+    # bf16: F(2x2) only, U and V in bf16, V from the NHWC copy of x; not taken by AUTO
+    bf = cfg2.with_(x_dtype="bf16", y_dtype="bf16")
+    info = plan(bf)
+    tiles2 = 32 * 28 * 28
+    assert info.wino_tile == 2 and info.needs_reorder == 1
+    assert info.workspace_bytes == 16 * 64 * 64 * 2 + 16 * (64 * 2 + 64 * 4) * tiles2
+    assert auto(bf.with_(c=256, k=256)) != B.CONV2D_ALGO_WINOGRAD
     monkeypatch.delenv("CONV2D_WINO_TILE")
     assert plan(cfg2).wino_tile == 4 and plan(cfg2.with_(h=14, w=14)).wino_tile == 4
     assert plan(cfg2.with_(h=7, w=7)).wino_tile == 2 and plan(cfg2.with_(h=40, w=7)).wino_tile == 2

@@ -411,6 +411,44 @@ def test_winograd(idx, mt, monkeypatch):
     _check(cs.with_(layout="nhwc"), WINOGRAD)
 
 
+# bf16 Winograd (F(2x2), C a multiple of 8): U and V rounded to bf16, fp32 GEMM sums; NCHW and
+# NHWC inputs, bf16 and fp32 outputs, chunked tiles; integer data stays exact (the transforms
+# only add, subtract and halve small integers)
+WINO_BF16 = [
+    _shape(3, 64, 14, 14, 128, 3, 3, pd=(1, 1), seed=277),
+    _shape(2, 24, 8, 31, 16, 3, 3, pd=(1, 0), seed=278, bias=False),
+    _shape(1, 128, 9, 13, 72, 3, 3, pd=(1, 1), seed=279),
+    _shape(2, 16, 12, 12, 40, 3, 3, seed=280),
+]
+
+
+@pytest.mark.parametrize("var", [("nchw", "bf16"), ("nhwc", "bf16"), ("nchw", "f32")], ids=lambda v: "-".join(v))
+@pytest.mark.parametrize("idx", range(len(WINO_BF16)))
+def test_winograd_bf16(idx, var):
+    layout, ydt = var
+    cs = WINO_BF16[idx].with_(layout=layout, x_dtype="bf16", y_dtype=ydt)
+    dc = DeviceConv(cs, "random")
+    try:
+        p = dc.plan(WINOGRAD)
+        assert p.wino_tile == 2 and p.needs_reorder == 1
+    finally:
+        dc.close()
+    _check(cs, WINOGRAD)
+    _check(cs.with_(y_dtype="f32"), WINOGRAD, "integer")
+
+
+def test_winograd_bf16_chunks(monkeypatch):
+    cs = WINO_BF16[0].with_(x_dtype="bf16", y_dtype="bf16")
+    monkeypatch.setenv("CONV2D_WORKSPACE_LIMIT_BYTES", str(16 * (64 * 2 + 128 * 4) * 40))
+    dc = DeviceConv(cs, "random")
+    try:
+        assert dc.plan(WINOGRAD).chunks > 1
+    finally:
+        dc.close()
+    _check(cs, WINOGRAD)
+    _check(cs.with_(y_dtype="f32"), WINOGRAD, "integer")
+
+
 @pytest.mark.parametrize("mt", [2, 4])
 def test_winograd_chunks_and_configs(mt, monkeypatch):
     # a workspace cap that forces several chunks of tiles
