@@ -126,8 +126,9 @@ GemmPlan choose_tile(int64_t M, int64_t P, int64_t G, int64_t kred, int xdt, int
                                {TILE_32x256, 0.7}};
     // bf16 tiles need two resident blocks per CU to hide their load latency: count rounds
     // of two blocks per CU (a single block per CU measured well below its share)
-    const int per_round = nhwc ? 2 * cus : cus;
-    for (const Cand& c : nhwc ? cands_bf16 : cands_f32) {
+    const bool bfc = xdt == CONV2D_BF16;
+    const int per_round = bfc && nhwc ? 2 * cus : cus;
+    for (const Cand& c : bfc && nhwc ? cands_bf16 : cands_f32) {
         const TileShape ts = kTileShapes[c.tile];
         const int64_t tiles = ceil_div(M, ts.bm) * ceil_div(P, ts.bn) * G;
         const double eff = c.eff * (dense && c.tile == TILE_64x128 ? 1.25 : 1.0);
@@ -968,6 +969,13 @@ int conv2d_desc_create(const conv2d_params* params, conv2d_desc** out) {
         const double xbytes = (double)g.x_elems * 2;
         const int64_t force = env_int64("CONV2D_NHWC_GATHER", -1);
         d->implicit_nhwc = force < 0 ? (g.layout == CONV2D_NHWC || flops >= 1000.0 * xbytes) : force != 0;
+    }
+    // fp32 NHWC x with C/g a multiple of 16: gather 4-channel runs with 16-byte loads straight
+    // from x (no reorder of x); NCHW fp32 x keeps the NCHW gathers (a copy of x would cost more
+    // than the wider loads save).  CONV2D_NHWC_GATHER=0 / 1 forces it for such shapes.
+    if (g.xdt == CONV2D_F32 && g.Cg % 16 == 0 && g.C % 4 == 0) {
+        const int64_t force = env_int64("CONV2D_NHWC_GATHER", -1);
+        d->implicit_nhwc = force < 0 ? g.layout == CONV2D_NHWC : force != 0;
     }
     d->implicit = choose_tile(g.Kg, g.P, g.G, g.Kred, g.xdt, g.Cg, d->implicit_nhwc);
     d->implicit_tap = g.Cg % d->implicit.bk == 0;

@@ -173,6 +173,26 @@ __device__ __forceinline__ bool tail_reduce(const GemmArgs& A, f32x16 (&acc)[TM]
 // MFMAs of stage s, so a load has two stages of MFMA work to land.
 // 64x64 tiles with 16-row stages fit seven blocks per CU (LDS 20 KiB each); the bound keeps
 // the register budget at seven blocks with the tail-split epilogue compiled in.
+// Window origin of output pixel p in an NHWC input: element offset of
+// x[n, hi0, wi0, gi*Cg] (negative or past the row inside the padding).
+__device__ __forceinline__ ColState col_state_nhwc(const GemmArgs& A, int p, int gi) {
+    ColState s;
+    if (p < A.P) {
+        const int n = p / A.HoWo;
+        const int hw = p - n * A.HoWo;
+        const int ho = hw / A.Wo;
+        const int wo = hw - ho * A.Wo;
+        s.hi0 = ho * A.sh - A.ph;
+        s.wi0 = wo * A.sw - A.pw;
+        s.base = (((int64_t)n * A.H + s.hi0) * A.W + s.wi0) * A.Cx + (int64_t)gi * A.Cg;
+    } else {
+        s.hi0 = KTAB_DEAD;
+        s.wi0 = 0;
+        s.base = 0;
+    }
+    return s;
+}
+
 template <int BM, int BN, int WM, int WN, int BK, int PF, int BSRC, int EPI, typename TOut>
 __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 16 ? 7 : 1)) void gemm_f32_kernel(GemmArgs A) {
     constexpr int WTM = BM / WM, WTN = BN / WN;
@@ -220,7 +240,8 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 16 ? 7 : 1)) void ge
 #pragma unroll
     for (int j = 0; j < BCOLS; ++j) {
         const int p = p0 + tn + j * BNT;
-        if (BSRC != BSRC_DENSE) cs[j] = col_state(A, p, gi);
+        if constexpr (BSRC == BSRC_NHWC_TAP) cs[j] = col_state_nhwc(A, p, gi);
+        else if constexpr (BSRC != BSRC_DENSE) cs[j] = col_state(A, p, gi);
         dvb[j] = p < A.P ? (uint32_t)(((int64_t)gi * A.b_gstride + p) * 4) : OOB_OFF;
     }
     // ---- A loader: run g of thread t is row (t + g*256) / (BK/4), k 4*((t + g*256) % (BK/4)) + i
@@ -232,7 +253,7 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 16 ? 7 : 1)) void ge
     // taps innermost: the taps of one channel block re-read the same input lines,
     // which then hit in L1.
     int cur_c0 = 0, cur_r = 0, cur_s = 0;
-    if constexpr (BSRC == BSRC_IMPLICIT_TAP) {
+    if constexpr (BSRC == BSRC_IMPLICIT_TAP || BSRC == BSRC_NHWC_TAP) {
         const int tap = s_begin % A.RS;
         cur_c0 = (s_begin / A.RS) * BK;
         cur_r = tap / A.S;
@@ -241,9 +262,11 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 16 ? 7 : 1)) void ge
 
     auto load_stage = [&](int stage, f32x4 (&breg)[BRUNS][BCOLS], f32x4 (&areg)[ARUNS]) {
         const int k0 = stage * BK;
-        if constexpr (BSRC == BSRC_IMPLICIT_TAP) {
+        if constexpr (BSRC == BSRC_IMPLICIT_TAP || BSRC == BSRC_NHWC_TAP) {
             const int roff = cur_r * A.dh, soff = cur_s * A.dw;
-            const int tapoff = roff * A.W + soff;
+            // NCHW: channels HW apart, 4 single loads per run; NHWC: the run's 4 channels are
+            // contiguous, one 16-byte load
+            const int tapoff = BSRC == BSRC_NHWC_TAP ? (roff * A.W + soff) * A.Cx + cur_c0 : roff * A.W + soff;
             uint32_t vb[BCOLS];
 #pragma unroll
             for (int j = 0; j < BCOLS; ++j) {
@@ -251,14 +274,24 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 16 ? 7 : 1)) void ge
                 const bool ok = ((unsigned)hi < (unsigned)A.H) & ((unsigned)wi < (unsigned)A.W);
                 vb[j] = ok ? (uint32_t)(((int32_t)cs[j].base + tapoff) * 4) : OOB_OFF;
             }
+            if constexpr (BSRC == BSRC_NHWC_TAP) {
 #pragma unroll
-            for (int g = 0; g < BRUNS; ++g)
+                for (int g = 0; g < BRUNS; ++g)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const uint32_t cofs = (uint32_t)((cur_c0 + 4 * (g * BKT + tk) + i) * A.HW) * 4u;
+                    for (int j = 0; j < BCOLS; ++j)
+                        breg[g][j] = __builtin_bit_cast(
+                            f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                       rb, vb[j] == OOB_OFF ? OOB_OFF : vb[j] + (uint32_t)(4 * (g * BKT + tk)) * 4u, 0, 0));
+            } else {
 #pragma unroll
-                    for (int j = 0; j < BCOLS; ++j) breg[g][j][i] = ld_f32(rb, vb[j] + cofs);
-                }
+                for (int g = 0; g < BRUNS; ++g)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const uint32_t cofs = (uint32_t)((cur_c0 + 4 * (g * BKT + tk) + i) * A.HW) * 4u;
+#pragma unroll
+                        for (int j = 0; j < BCOLS; ++j) breg[g][j][i] = ld_f32(rb, vb[j] + cofs);
+                    }
+            }
             // weights in tap-major order [K][R*S][C/g]: 4 consecutive channels per 16-byte load
             const int tap = cur_r * A.S + cur_s;
 #pragma unroll
@@ -270,7 +303,7 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 16 ? 7 : 1)) void ge
                 // bit-cast the whole vector: casting its elements one by one made this
                 // compiler emit a single-dword load
                 areg[g] = __builtin_bit_cast(
-                    f32x4, __builtin_amdgcn_raw_buffer_load_b128(ra, (m < A.M) & qa ? (uint32_t)(e * 4) : OOB_OFF, 0, 0));
+                    f32x4, __builtin_amdgcn_raw_buffer_load_b128(ra, ((m < A.M) & qa) ? (uint32_t)(e * 4) : OOB_OFF, 0, 0));
             }
             if (++cur_s == A.S) {
                 cur_s = 0;
@@ -418,25 +451,6 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 16 ? 7 : 1)) void ge
 // one pixel at one tap, a single 16-byte load, and the 4 or 8 chunks of a
 // pixel's stage row come from consecutive threads (one 64- or 128-byte run).
 
-// Window origin of output pixel p in an NHWC input: element offset of
-// x[n, hi0, wi0, gi*Cg] (negative or past the row inside the padding).
-__device__ __forceinline__ ColState col_state_nhwc(const GemmArgs& A, int p, int gi) {
-    ColState s;
-    if (p < A.P) {
-        const int n = p / A.HoWo;
-        const int hw = p - n * A.HoWo;
-        const int ho = hw / A.Wo;
-        const int wo = hw - ho * A.Wo;
-        s.hi0 = ho * A.sh - A.ph;
-        s.wi0 = wo * A.sw - A.pw;
-        s.base = (((int64_t)n * A.H + s.hi0) * A.W + s.wi0) * A.Cx + (int64_t)gi * A.Cg;
-    } else {
-        s.hi0 = KTAB_DEAD;
-        s.wi0 = 0;
-        s.base = 0;
-    }
-    return s;
-}
 
 template <int BM, int BN, int WM, int WN, int BK, int BSRC, int EPI, typename TOut>
 __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void gemm_bf16_kernel(GemmArgs A) {
@@ -516,7 +530,7 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void ge
             const int m = m0 + u / CPR;
             const int kc = u % CPR;
             const int64_t e0 = a_base + (int64_t)m * A.lda + (int64_t)tap * A.Cg + cur_c0 + kc * 8;
-            areg[i] = __builtin_amdgcn_raw_buffer_load_b128(ra, (m < A.M) & qa ? (uint32_t)(e0 * 2) : OOB_OFF, 0, 0);
+            areg[i] = __builtin_amdgcn_raw_buffer_load_b128(ra, ((m < A.M) & qa) ? (uint32_t)(e0 * 2) : OOB_OFF, 0, 0);
         }
     };
     auto advance_tap = [&]() {
@@ -726,6 +740,10 @@ static hipError_t launch_f32(const GemmArgs& a, int bsrc, int epi, int groups, h
     // partial sums of a split reduction
     else if (bsrc == BSRC_IMPLICIT_NCHW && epi == EPI_DENSE) CV_F32(BSRC_IMPLICIT_NCHW, EPI_DENSE);
     else if (bsrc == BSRC_IMPLICIT_TAP && epi == EPI_DENSE) CV_F32(BSRC_IMPLICIT_TAP, EPI_DENSE);
+    // NHWC x with channel runs of 4 (C and C/g multiples of 4, C/g of the stage depth)
+    else if (bsrc == BSRC_NHWC_TAP && (a.Cx % 4 != 0 || a.Cg % BK != 0)) return hipErrorInvalidValue;
+    else if (bsrc == BSRC_NHWC_TAP && epi == EPI_NCHW) CV_F32(BSRC_NHWC_TAP, EPI_NCHW);
+    else if (bsrc == BSRC_NHWC_TAP && epi == EPI_DENSE) CV_F32(BSRC_NHWC_TAP, EPI_DENSE);
     else return hipErrorInvalidValue;
 #undef CV_F32
     return hipGetLastError();
