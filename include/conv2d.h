@@ -139,7 +139,8 @@ typedef struct {
     int64_t workspace_bytes;  /* device workspace this algorithm uses per chunk (explicit) or for the
                                  partial sums of the split reduction or the tail split (implicit) */
     int64_t chunks;           /* explicit path: number of pack/GEMM/unpack chunks */
-    int32_t needs_reorder;    /* 1 when pre/post layout reorders run (NHWC through an NCHW kernel) */
+    int32_t needs_reorder;    /* 1 when a pre- or post-convolution layout reorder runs (x or y in the
+                                 other layout than the kernel reads or writes) */
     int32_t op_class;         /* bit 0 pointwise, 1 grouped, 2 depthwise, 3 dilated, 4 rectangular, 5 strided */
     int32_t kernel;           /* microkernel that runs: CONV2D_KERNEL_* */
     int32_t ksplit;           /* implicit GEMM: reduction split into this many parts (1 = none);

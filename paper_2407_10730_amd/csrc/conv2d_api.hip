@@ -588,6 +588,12 @@ int run_slice(conv2d_desc* d, const void* x, const void* w, const float* bias, v
     return sc.end();
 }
 
+// An NHWC y is written by the GEMM's own epilogue (no NCHW result, no post-convolution
+// reordering) when the GEMM gathers from NHWC x and the reduction is not split.
+bool implicit_writes_nhwc(const conv2d_desc* d) {
+    return d->g.layout == CONV2D_NHWC && d->implicit_nhwc && !d->implicit_slice && d->implicit.ksplit <= 1;
+}
+
 // probe: the pack probe, which runs only the microkernel's loader on the internal copies that
 // the last call made (tap-major weights) and writes nothing.
 int run_implicit(conv2d_desc* d, const void* x, const void* w, const float* bias, void* y, hipStream_t s,
@@ -654,9 +660,11 @@ int run_implicit(conv2d_desc* d, const void* x, const void* w, const float* bias
             a.tail_part = static_cast<float*>(d->tp);
             a.tail_count = d->tc;
         }
+        const bool y_nhwc = implicit_writes_nhwc(d);
+        if (y_nhwc) a.ldc = (int32_t)g.K;
         Scope sc(d, CONV2D_ALGO_IMPLICIT_GEMM, CONV2D_PH_IN_MICROKERNEL, s, ph);
         CV_TRY(sc.begin());
-        CV_HIP(dispatch_gemm(gp, a, bsrc, EPI_NCHW, g.xdt, g.ydt, (int)g.G, s));
+        CV_HIP(dispatch_gemm(gp, a, bsrc, y_nhwc ? EPI_NHWC : EPI_NCHW, g.xdt, g.ydt, (int)g.G, s));
         return sc.end();
     }
     // split reduction: partial sums [split][g][m][p] in fp32, then the unpack kernel adds them
@@ -1115,7 +1123,9 @@ int conv2d_fwd(conv2d_desc* d, const void* x, const void* w, const float* bias, 
         CV_TRY(sc.end());
         xin = d->xr;
     }
-    if (nhwc) {
+    // NCHW result reordered to NHWC afterwards, unless the kernel writes NHWC y itself
+    const bool y_reorder = nhwc && !(algo == CONV2D_ALGO_IMPLICIT_GEMM && implicit_writes_nhwc(d));
+    if (y_reorder) {
         const int64_t yb = g.y_elems * elem_size(g.ydt);
         CV_TRY(ensure_buffer(&d->yr, &d->yr_bytes, yb));
         yout = d->yr;
@@ -1129,7 +1139,7 @@ int conv2d_fwd(conv2d_desc* d, const void* x, const void* w, const float* bias, 
         default: st = CONV2D_E_INVALID;
     }
     if (st != CONV2D_OK) return st;
-    if (nhwc) {
+    if (y_reorder) {
         Scope sc(d, algo, CONV2D_PH_POST_REORDER, s, ph);
         CV_TRY(sc.begin());
         CV_HIP(launch_nchw_to_nhwc(d->yr, y, g.N, g.K, g.Ho * g.Wo, (int)elem_size(g.ydt), s));
@@ -1222,7 +1232,8 @@ int conv2d_plan_query(const conv2d_desc* d, int algo, conv2d_plan_info* out) {
     const int bk = algo == CONV2D_ALGO_IM2COL_GEMM ? d->expl.gemm.bk : d->implicit.bk;
     out->kred_pad = (int32_t)(ceil_div(g.Kred, bk) * bk);
     out->needs_reorder = g.layout == CONV2D_NHWC ? 1 : 0;
-    if (algo == CONV2D_ALGO_IMPLICIT_GEMM && d->implicit_nhwc && !d->implicit_slice) out->needs_reorder = 1;
+    if (algo == CONV2D_ALGO_IMPLICIT_GEMM && d->implicit_nhwc && !d->implicit_slice)
+        out->needs_reorder = implicit_writes_nhwc(d) ? 0 : 1;
     if (algo == CONV2D_ALGO_WINOGRAD && g.xdt == CONV2D_BF16) out->needs_reorder = 1;
     out->op_class = (int32_t)d->opclass;
     out->chunks = 1;

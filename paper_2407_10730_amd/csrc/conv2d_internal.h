@@ -37,8 +37,9 @@ static const TileShape kTileShapes[TILE_COUNT] = {{64, 64}, {64, 128}, {64, 256}
 //                  stage, so needs C/g to be a multiple of the stage depth (no table)
 //  NHWC_TAP      : (bf16) the same order gathered from an NHWC copy of x, 16 bytes per load
 enum BSrc { BSRC_IMPLICIT_NCHW = 0, BSRC_DENSE = 1, BSRC_IMPLICIT_TAP = 2, BSRC_NHWC_TAP = 3, BSRC_DENSE_T = 4 };
-// Destination of the GEMM result.
-enum Epi { EPI_NCHW = 0, EPI_DENSE = 1 };
+// Destination of the GEMM result: NCHW y, a dense fp32 matrix, or NHWC y (ldc = K channels per
+// pixel; NHWC gather source only).
+enum Epi { EPI_NCHW = 0, EPI_DENSE = 1, EPI_NHWC = 2 };
 
 // Per reduction index kr (one im2col row) of an NCHW input: the element offset
 // of tap (c, r, s) relative to the window origin, and the row / column shifts
@@ -65,7 +66,7 @@ struct GemmArgs {
     int64_t x_nstride;    // C*H*W
     int32_t M, Kred, P, nstages;
     int32_t grid_p, grid_m;   // pixel tiles x channel tiles
-    void* y;              // NCHW y, or dense C [G][M][ldc] (fp32)
+    void* y;              // NCHW y, NHWC y, or dense C [G][M][ldc] (fp32)
     uint32_t y_bytes;
     const float* bias;    // may be NULL
     int64_t y_nstride;    // K*Ho*Wo

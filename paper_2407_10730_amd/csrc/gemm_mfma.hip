@@ -24,11 +24,14 @@ namespace cv {
 // Epilogue of both kernels.  Accumulator v of lane l holds row 8*(v/4) + 4*(l/32) + v%4,
 // column l%32 of its 32x32 tile.  All bias values of the rows a lane writes are loaded
 // before its first store, so the stores leave back to back behind one wait (a load
-// between two stores would make each store wait for the previous one).
+// between two stores would make each store wait for the previous one).  NHWC y: element
+// (p, channel gi*M + m) sits at p*ldc + gi*M + m (ldc = K), so the four consecutive rows a
+// lane holds per v/4 are adjacent and go out as one 16-byte (fp32) or 8-byte (bf16) store
+// when M is a multiple of 4.
 template <int TM, int TN, int EPI, typename TOut>
 __device__ __forceinline__ void store_tile(const GemmArgs& A, f32x16 (&acc)[TM][TN], int gi, int sp, int mb, int pb,
                                            int lrow, int lcol) {
-    if (EPI == EPI_NCHW && A.bias != nullptr) {
+    if (EPI != EPI_DENSE && A.bias != nullptr) {
         const __amdgpu_buffer_rsrc_t rbias = make_rsrc(A.bias, (uint32_t)(gridDim.z * A.M * 4));
 #pragma unroll
         for (int i = 0; i < TM; ++i)
@@ -41,6 +44,36 @@ __device__ __forceinline__ void store_tile(const GemmArgs& A, f32x16 (&acc)[TM][
             }
     }
     const __amdgpu_buffer_rsrc_t ry = make_rsrc(A.y, A.y_bytes);
+    if (EPI == EPI_NHWC && A.M % 4 == 0) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int p = pb + j * 32 + lcol;
+            const int64_t ybase = (int64_t)p * A.ldc + (int64_t)gi * A.M;
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int v4 = 0; v4 < 4; ++v4) {
+                    const int m = mb + i * 32 + 8 * v4 + 4 * lrow;
+                    const bool ok = (p < A.P) & (m < A.M);
+                    const float q[4] = {acc[i][j][4 * v4], acc[i][j][4 * v4 + 1], acc[i][j][4 * v4 + 2],
+                                        acc[i][j][4 * v4 + 3]};
+                    if constexpr (sizeof(TOut) == 4) {
+                        const uint32_t off = ok ? (uint32_t)(ybase + m) * 4u : OOB_OFF;
+                        __builtin_amdgcn_raw_buffer_store_b128(
+                            u32x4{__builtin_bit_cast(uint32_t, q[0]), __builtin_bit_cast(uint32_t, q[1]),
+                                  __builtin_bit_cast(uint32_t, q[2]), __builtin_bit_cast(uint32_t, q[3])},
+                            ry, off, 0, 0);
+                    } else {
+                        const uint32_t off = ok ? (uint32_t)(ybase + m) * 2u : OOB_OFF;
+                        __builtin_amdgcn_raw_buffer_store_b64(
+                            u32x2{(uint32_t)f32_to_bf16_rne(q[0]) | ((uint32_t)f32_to_bf16_rne(q[1]) << 16),
+                                  (uint32_t)f32_to_bf16_rne(q[2]) | ((uint32_t)f32_to_bf16_rne(q[3]) << 16)},
+                            ry, off, 0, 0);
+                    }
+                }
+        }
+        return;
+    }
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
         const int p = pb + j * 32 + lcol;
@@ -50,6 +83,8 @@ __device__ __forceinline__ void store_tile(const GemmArgs& A, f32x16 (&acc)[TM][
             const int n_img = p / A.HoWo;
             const int hw = p - n_img * A.HoWo;
             ybase = (int64_t)n_img * A.y_nstride + (int64_t)gi * A.M * A.HoWo + hw;
+        } else if (EPI == EPI_NHWC) {
+            ybase = (int64_t)p * A.ldc + (int64_t)gi * A.M;
         } else {
             ybase = (int64_t)sp * A.c_sstride + (int64_t)gi * A.c_gstride + p;
         }
@@ -61,6 +96,8 @@ __device__ __forceinline__ void store_tile(const GemmArgs& A, f32x16 (&acc)[TM][
                 const bool ok = pok & (m < A.M);
                 if (EPI == EPI_NCHW)
                     store_out<TOut>(ry, (uint32_t)(ybase + (int64_t)m * A.HoWo), ok, acc[i][j][v]);
+                else if (EPI == EPI_NHWC)
+                    store_out<TOut>(ry, (uint32_t)(ybase + m), ok, acc[i][j][v]);
                 else
                     store_out<float>(ry, (uint32_t)(ybase + (int64_t)m * A.ldc), ok, acc[i][j][v]);
             }
@@ -433,7 +470,7 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 16 ? 7 : 1)) void ge
     }
 
     if (A.loader_only) return;
-    if constexpr (EPI == EPI_NCHW) {
+    if constexpr (EPI != EPI_DENSE) {
         if (wk.tail_tile >= 0 && !tail_reduce<TM, TN>(A, acc, wk, t)) return;
     }
     store_tile<TM, TN, EPI, TOut>(A, acc, gi, sp, m0 + wm0, p0 + wn0, lrow, lcol);
@@ -721,7 +758,7 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void ge
     }
 
     if (A.loader_only) return;
-    if constexpr (EPI == EPI_NCHW) {
+    if constexpr (EPI != EPI_DENSE) {
         if (wk.tail_tile >= 0 && !tail_reduce<TM, TN>(A, acc, wk, t)) return;
     }
     store_tile<TM, TN, EPI, TOut>(A, acc, gi, sp, m0 + wm0, p0 + wn0, lrow, lcol);
@@ -744,6 +781,7 @@ static hipError_t launch_f32(const GemmArgs& a, int bsrc, int epi, int groups, h
     else if (bsrc == BSRC_NHWC_TAP && (a.Cx % 4 != 0 || a.Cg % BK != 0)) return hipErrorInvalidValue;
     else if (bsrc == BSRC_NHWC_TAP && epi == EPI_NCHW) CV_F32(BSRC_NHWC_TAP, EPI_NCHW);
     else if (bsrc == BSRC_NHWC_TAP && epi == EPI_DENSE) CV_F32(BSRC_NHWC_TAP, EPI_DENSE);
+    else if (bsrc == BSRC_NHWC_TAP && epi == EPI_NHWC) CV_F32(BSRC_NHWC_TAP, EPI_NHWC);
     else return hipErrorInvalidValue;
 #undef CV_F32
     return hipGetLastError();
@@ -765,6 +803,9 @@ static hipError_t launch_bf16(const GemmArgs& a, int bsrc, int epi, int ydt, int
     if (bsrc == BSRC_NHWC_TAP && epi == EPI_NCHW) {
         if (ydt == CONV2D_BF16) CV_BF(BSRC_NHWC_TAP, EPI_NCHW, uint16_t);
         else CV_BF(BSRC_NHWC_TAP, EPI_NCHW, float);
+    } else if (bsrc == BSRC_NHWC_TAP && epi == EPI_NHWC) {
+        if (ydt == CONV2D_BF16) CV_BF(BSRC_NHWC_TAP, EPI_NHWC, uint16_t);
+        else CV_BF(BSRC_NHWC_TAP, EPI_NHWC, float);
     } else if (bsrc == BSRC_NHWC_TAP && epi == EPI_DENSE) {
         CV_BF(BSRC_NHWC_TAP, EPI_DENSE, float);  // partial sums of a split reduction
     } else if (bsrc == BSRC_DENSE_T) {

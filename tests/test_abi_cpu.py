@@ -336,6 +336,12 @@ def test_bf16_small_group_nhwc_plan(monkeypatch):
     assert plan(base.with_(c=24)).needs_reorder == 0                  # C/g = 24: NCHW gather
     assert plan(base.with_(x_dtype="f32", y_dtype="f32")).needs_reorder == 0
     assert plan(base.with_(k=16, r=3, s=3, pad=(1, 1))).needs_reorder == 0   # 144 flops per byte
+    # NHWC x and y: the gather reads x as it is and the GEMM's epilogue writes NHWC y (bf16, and
+    # fp32 with C/g a multiple of 16); fp32 with C/g = 24 reads an NCHW copy and reorders y
+    for dt in ("bf16", "f32"):
+        p = plan(base.with_(layout="nhwc", x_dtype=dt, y_dtype=dt))
+        assert p.kernel == B.CONV2D_KERNEL_GEMM and p.ksplit <= 1 and p.needs_reorder == 0, dt
+    assert plan(base.with_(layout="nhwc", c=24, x_dtype="f32", y_dtype="f32")).needs_reorder == 1
 
 
 def test_small_m_tile_choice(monkeypatch):

@@ -283,15 +283,20 @@ TAIL = [
 ]
 
 
-@pytest.mark.parametrize("dt", ["f32", "bf16", "bf16-nhwc"])
+# "-io": NHWC x and y, so the tail tiles go out through the NHWC epilogue
+@pytest.mark.parametrize("dt", ["f32", "bf16", "bf16-nhwc", "f32-nhwc-io", "bf16-nhwc-io"])
 @pytest.mark.parametrize("idx", range(len(TAIL)))
 def test_tail_split(idx, dt):
     import torch
     base, force = TAIL[idx]
-    cs = base.with_(x_dtype="f32" if dt == "f32" else "bf16", y_dtype="f32" if dt == "f32" else "bf16")
-    kernel = "nhwc" if dt == "bf16-nhwc" else "0"
-    if dt == "bf16-nhwc" and not _nhwc_ok(cs):
+    f32 = dt.startswith("f32")
+    cs = base.with_(x_dtype="f32" if f32 else "bf16", y_dtype="f32" if f32 else "bf16",
+                    layout="nhwc" if dt.endswith("-io") else "nchw")
+    kernel = "nhwc" if "nhwc" in dt else "0"
+    if dt.startswith("bf16-nhwc") and not _nhwc_ok(cs):
         pytest.skip("the NHWC gather needs C/g a multiple of 32")
+    if dt == "f32-nhwc-io" and (cs.c // cs.groups) % 16 != 0:
+        pytest.skip("the fp32 NHWC gather needs C/g a multiple of 16")
     env = {"CONV2D_TAIL": force, "CONV2D_KSPLIT": "1"}
     old = {k: os.environ.get(k) for k in env}
     os.environ.update(env)
@@ -304,6 +309,7 @@ def test_tail_split(idx, dt):
                 plan = dc.plan(IMPLICIT)
                 assert plan.kernel == B.CONV2D_KERNEL_GEMM and plan.ksplit == 1
                 assert plan.tail_tiles > 0 and plan.tail_pieces == int(force), (plan.tail_tiles, plan.tail_pieces)
+                assert plan.needs_reorder == (0 if dt.endswith("-io") else plan.needs_reorder)
                 ys = []
                 for _ in range(2):
                     dc.run(IMPLICIT)
@@ -511,6 +517,44 @@ SMALLK = [
     _shape(2, 64, 9, 11, 2, 1, 1, seed=303, bias=False),
     _shape(1, 1, 10, 10, 3, 3, 3, st=(1, 2), pd=(0, 1), seed=304),
 ]
+
+
+# NHWC x and y through the NHWC gather: the GEMM's epilogue writes NHWC y itself (four adjacent
+# channels per 16-byte fp32 or 8-byte bf16 store when K/g is a multiple of 4, one element per
+# store otherwise), so neither x nor y is reordered.  Groups, bias, ragged
+# pixel and channel tiles, K/g = 30 and 33, strides, padding and dilation.
+NHWC_EPI = [
+    _shape(2, 64, 15, 17, 96, 3, 3, pd=(1, 1), seed=230),
+    _shape(1, 128, 14, 14, 64, 3, 3, pd=(1, 1), g=2, seed=231),
+    _shape(3, 32, 11, 9, 30, 3, 3, st=(2, 2), pd=(1, 1), seed=232),
+    _shape(2, 64, 12, 12, 66, 1, 1, g=2, seed=233),
+    _shape(1, 32, 9, 13, 40, 5, 5, pd=(4, 4), dl=(2, 2), seed=234, bias=False),
+    _shape(2, 96, 7, 7, 200, 3, 3, pd=(1, 1), seed=235),
+]
+
+
+@pytest.mark.parametrize("dt", [("f32", "f32"), ("bf16", "bf16"), ("bf16", "f32")], ids=lambda d: "-".join(d))
+@pytest.mark.parametrize("idx", range(len(NHWC_EPI)))
+def test_nhwc_epilogue(idx, dt):
+    import torch
+    cs = NHWC_EPI[idx].with_(layout="nhwc", x_dtype=dt[0], y_dtype=dt[1])
+    with _Kernel("nhwc"):
+        dc = DeviceConv(cs, "random")
+    try:
+        p = dc.plan(IMPLICIT)
+        assert p.kernel == B.CONV2D_KERNEL_GEMM
+        split = p.ksplit > 1   # a split reduction's partials go through the NCHW unpack
+        assert p.needs_reorder == (1 if split else 0)
+        dc.run(IMPLICIT)
+        torch.cuda.synchronize()
+        calls = dc.breakdown(IMPLICIT)["calls"]
+        # pre-convolution reordering: only the filters' tap-major repack (R*S > 1), never x
+        assert calls["pre_reorder"] == (1 if cs.r * cs.s > 1 else 0), calls
+        assert calls["post_reorder"] == (1 if split else 0), calls
+    finally:
+        dc.close()
+    _check(cs, IMPLICIT, "random", "nhwc")
+    _check(cs.with_(y_dtype="f32"), IMPLICIT, "integer", "nhwc")
 
 
 @pytest.mark.parametrize("ranges", [None, "1", "3", "7"])
