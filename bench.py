@@ -105,6 +105,15 @@ def cpu_baseline(cs, x, w, b, y_gpu, flops_per_image, target_s=10.0):
     y_ref, a_ref = oracle.conv2d(x[:n_img], w, bias, cs.stride, cs.pad, cs.dil, cs.groups, nthreads=threads)
     dt = time.perf_counter() - t0
     lit, pt = oracle.normalised_errors(y_gpu[:n_img], y_ref, a_ref)
+    # a whole batch that takes well under the target is timed over repeated passes
+    passes = 1
+    if n_img == cs.n and dt < 0.5 * target_s:
+        passes = int(min(100, max(2, round(target_s / max(dt, 1e-6)))))
+        t0 = time.perf_counter()
+        for _ in range(passes):
+            oracle.conv2d(x[:n_img], w, bias, cs.stride, cs.pad, cs.dil, cs.groups, nthreads=threads,
+                          want_abs=False)
+        dt = (time.perf_counter() - t0) / passes
     # one image on one thread as well, as the paper's single-thread protocol times the CPU
     t0 = time.perf_counter()
     oracle.conv2d(x[:1], w, bias, cs.stride, cs.pad, cs.dil, cs.groups, nthreads=1, want_abs=False)
@@ -114,9 +123,10 @@ def cpu_baseline(cs, x, w, b, y_gpu, flops_per_image, target_s=10.0):
         "unit": "TFLOP/s",
         "cores": threads,
         "kind": "oracle",
-        "sample": f"fp64 seven-loop oracle over the first {n_img} of {cs.n} images (all outputs), "
-                  f"{dt:.2f} s wall",
-        "seconds": dt,
+        "sample": f"fp64 seven-loop oracle over the first {n_img} of {cs.n} images (all outputs)"
+                  + (f", {passes} passes" if passes > 1 else "") + f", {dt * passes:.2f} s wall",
+        "seconds": dt * passes,
+        "passes": passes,
         "cpu_model": _cpu_model(),
         "single_thread": {"value": flops_per_image / dt1 / 1e12, "unit": "TFLOP/s", "cores": 1,
                           "sample": "first image", "seconds": dt1},
