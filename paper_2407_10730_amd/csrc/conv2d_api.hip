@@ -588,10 +588,10 @@ int run_slice(conv2d_desc* d, const void* x, const void* w, const float* bias, v
     return sc.end();
 }
 
-// An NHWC y is written by the GEMM's own epilogue (no NCHW result, no post-convolution
-// reordering) when the GEMM gathers from NHWC x and the reduction is not split.
+// An NHWC y is written by the GEMM's own epilogue, or by the unpack of a split reduction's
+// partials (no NCHW result, no post-convolution reordering), when the GEMM gathers from NHWC x.
 bool implicit_writes_nhwc(const conv2d_desc* d) {
-    return d->g.layout == CONV2D_NHWC && d->implicit_nhwc && !d->implicit_slice && d->implicit.ksplit <= 1;
+    return d->g.layout == CONV2D_NHWC && d->implicit_nhwc && !d->implicit_slice;
 }
 
 // probe: the pack probe, which runs only the microkernel's loader on the internal copies that
@@ -696,6 +696,7 @@ int run_implicit(conv2d_desc* d, const void* x, const void* w, const float* bias
     u.y_nstride = g.K * g.Ho * g.Wo;
     u.splits = gp.ksplit;
     u.split_stride = slice;
+    u.nhwc = implicit_writes_nhwc(d) ? 1 : 0;
     Scope sc(d, CONV2D_ALGO_IMPLICIT_GEMM, CONV2D_PH_IN_UNPACKING, s, ph);
     CV_TRY(sc.begin());
     CV_HIP(launch_unpack(u, g.ydt, (int)g.G, s));

@@ -111,8 +111,9 @@ struct Im2colArgs {
 };
 hipError_t launch_im2col(const Im2colArgs& a, int xdt, int groups, hipStream_t stream);
 
-// unpack C[g][m][pl] (fp32) to NCHW y (+bias, cast).  With splits > 1 the value is the sum,
-// in split order, of C + s*split_stride over s < splits (a split reduction's partials).
+// unpack C[g][m][pl] (fp32) to NCHW y, or NHWC y with nhwc = 1 (+bias, cast).  With splits > 1
+// the value is the sum, in split order, of C + s*split_stride over s < splits (a split
+// reduction's partials).
 struct UnpackArgs {
     const float* c;
     void* y;
@@ -123,6 +124,7 @@ struct UnpackArgs {
     int64_t y_nstride;
     int32_t splits;
     int64_t split_stride;
+    int32_t nhwc;
 };
 hipError_t launch_unpack(const UnpackArgs& a, int ydt, int groups, hipStream_t stream);
 

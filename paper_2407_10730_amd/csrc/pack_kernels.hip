@@ -175,7 +175,61 @@ __global__ __launch_bounds__(256) void unpack_kernel(UnpackArgs A) {
     }
 }
 
+// NHWC y: grid (ceil(pc / 256), ceil(Kg / 4), G).  A thread takes one pixel and 4 consecutive
+// channels: 4 loads, each coalesced over the wave's consecutive pixels, and one 16-byte (fp32)
+// or 8-byte (bf16) store of y[p][g*Kg + m .. +3] when Kg % 4 == 0, element stores otherwise.
+template <bool BF16OUT>
+__global__ __launch_bounds__(256) void unpack_nhwc_kernel(UnpackArgs A) {
+    const int pl = blockIdx.x * 256 + threadIdx.x;
+    const int m0 = blockIdx.y * 4;
+    const int gi = blockIdx.z;
+    if (pl >= A.pc) return;
+    const int splits = A.splits > 1 ? A.splits : 1;
+    const int kall = A.Kg * gridDim.z;
+    float v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int m = m0 + j < A.Kg ? m0 + j : A.Kg - 1;  // rows past Kg are computed but not stored
+        const float* crow = A.c + ((int64_t)gi * A.Kg + m) * A.pc + pl;
+        float c = crow[0];
+        for (int sp = 1; sp < splits; ++sp) c += crow[sp * A.split_stride];
+        v[j] = c + (A.bias ? A.bias[gi * A.Kg + m] : 0.0f);
+    }
+    const __amdgpu_buffer_rsrc_t ry = pk_rsrc(A.y, A.y_bytes);
+    const int64_t o = (A.p_begin + pl) * kall + (int64_t)gi * A.Kg + m0;
+    if ((A.Kg & 3) == 0) {
+        if (BF16OUT) {
+            typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+            const u32x2 q = {(uint32_t)pk_f32_to_bf16(v[0]) | ((uint32_t)pk_f32_to_bf16(v[1]) << 16),
+                             (uint32_t)pk_f32_to_bf16(v[2]) | ((uint32_t)pk_f32_to_bf16(v[3]) << 16)};
+            __builtin_amdgcn_raw_buffer_store_b64(q, ry, (uint32_t)(o * 2), 0, 0);
+        } else {
+            typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+            const u32x4 q = {__builtin_bit_cast(uint32_t, v[0]), __builtin_bit_cast(uint32_t, v[1]),
+                             __builtin_bit_cast(uint32_t, v[2]), __builtin_bit_cast(uint32_t, v[3])};
+            __builtin_amdgcn_raw_buffer_store_b128(q, ry, (uint32_t)(o * 4), 0, 0);
+        }
+        return;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        if (m0 + j >= A.Kg) break;
+        if (BF16OUT)
+            __builtin_amdgcn_raw_buffer_store_b16(pk_f32_to_bf16(v[j]), ry, (uint32_t)((o + j) * 2), 0, 0);
+        else
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v[j]), ry, (uint32_t)((o + j) * 4), 0, 0);
+    }
+}
+
 hipError_t launch_unpack(const UnpackArgs& a, int ydt, int groups, hipStream_t stream) {
+    if (a.nhwc) {
+        dim3 grid((unsigned)((a.pc + 255) / 256), (unsigned)((a.Kg + 3) / 4), (unsigned)groups);
+        if (ydt == CONV2D_BF16)
+            hipLaunchKernelGGL(unpack_nhwc_kernel<true>, grid, dim3(256), 0, stream, a);
+        else
+            hipLaunchKernelGGL(unpack_nhwc_kernel<false>, grid, dim3(256), 0, stream, a);
+        return hipGetLastError();
+    }
     dim3 grid((unsigned)((a.pc + 1023) / 1024), (unsigned)a.Kg, (unsigned)groups);
     if (ydt == CONV2D_BF16)
         hipLaunchKernelGGL(unpack_kernel<true>, grid, dim3(256), 0, stream, a);

@@ -543,14 +543,40 @@ def test_nhwc_epilogue(idx, dt):
     try:
         p = dc.plan(IMPLICIT)
         assert p.kernel == B.CONV2D_KERNEL_GEMM
-        split = p.ksplit > 1   # a split reduction's partials go through the NCHW unpack
-        assert p.needs_reorder == (1 if split else 0)
+        assert p.needs_reorder == 0
         dc.run(IMPLICIT)
         torch.cuda.synchronize()
         calls = dc.breakdown(IMPLICIT)["calls"]
         # pre-convolution reordering: only the filters' tap-major repack (R*S > 1), never x
         assert calls["pre_reorder"] == (1 if cs.r * cs.s > 1 else 0), calls
-        assert calls["post_reorder"] == (1 if split else 0), calls
+        assert calls["post_reorder"] == 0, calls
+    finally:
+        dc.close()
+    _check(cs, IMPLICIT, "random", "nhwc")
+    _check(cs.with_(y_dtype="f32"), IMPLICIT, "integer", "nhwc")
+
+
+# split reductions with NHWC x and y: the unpack adds the partials and writes NHWC y (16- or
+# 8-byte stores of 4 channels when K/g is a multiple of 4), forced to 2, 3 and 5 splits
+@pytest.mark.parametrize("ksplit", ["2", "3", "5"])
+@pytest.mark.parametrize("dt", [("f32", "f32"), ("bf16", "bf16")], ids=lambda d: "-".join(d))
+@pytest.mark.parametrize("idx", range(len(NHWC_EPI)))
+def test_nhwc_split_unpack(idx, dt, ksplit, monkeypatch):
+    import torch
+    cs = NHWC_EPI[idx].with_(layout="nhwc", x_dtype=dt[0], y_dtype=dt[1])
+    monkeypatch.setenv("CONV2D_KSPLIT", ksplit)
+    monkeypatch.setenv("CONV2D_TAIL", "0")
+    with _Kernel("nhwc"):
+        dc = DeviceConv(cs, "random")
+    try:
+        p = dc.plan(IMPLICIT)
+        assert p.kernel == B.CONV2D_KERNEL_GEMM and p.needs_reorder == 0
+        if p.ksplit <= 1:
+            pytest.skip("reduction too short for the forced split")
+        dc.run(IMPLICIT)
+        torch.cuda.synchronize()
+        calls = dc.breakdown(IMPLICIT)["calls"]
+        assert calls["in_unpacking"] == 1 and calls["post_reorder"] == 0, calls
     finally:
         dc.close()
     _check(cs, IMPLICIT, "random", "nhwc")
