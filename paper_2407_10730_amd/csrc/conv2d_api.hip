@@ -582,16 +582,18 @@ int run_slice(conv2d_desc* d, const void* x, const void* w, const float* bias, v
     a.lds_x_off = sp.lds_x_off;
     a.lds_bytes = sp.lds_bytes;
     a.loader_only = probe ? 1 : 0;
+    a.y_nhwc = g.layout == CONV2D_NHWC ? 1 : 0;
     Scope sc(d, CONV2D_ALGO_IMPLICIT_GEMM, CONV2D_PH_IN_MICROKERNEL, s, ph);
     CV_TRY(sc.begin());
     CV_HIP(launch_slice(a, g.xdt, g.ydt, sp.nw, s));
     return sc.end();
 }
 
-// An NHWC y is written by the GEMM's own epilogue, or by the unpack of a split reduction's
-// partials (no NCHW result, no post-convolution reordering), when the GEMM gathers from NHWC x.
+// An NHWC y is written by the sliced kernel, or by the GEMM's own epilogue or the unpack of a
+// split reduction's partials when the GEMM gathers from NHWC x: no NCHW result, no
+// post-convolution reordering.
 bool implicit_writes_nhwc(const conv2d_desc* d) {
-    return d->g.layout == CONV2D_NHWC && d->implicit_nhwc && !d->implicit_slice;
+    return d->g.layout == CONV2D_NHWC && (d->implicit_slice || d->implicit_nhwc);
 }
 
 // probe: the pack probe, which runs only the microkernel's loader on the internal copies that

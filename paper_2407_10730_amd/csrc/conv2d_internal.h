@@ -183,7 +183,7 @@ int64_t grouped_blocks(const DirectArgs& a);
 // channels, the input rows of 256 consecutive output pixels of one image and a table of the
 // slice offset of every reduction index sit in LDS (weights at byte 0, then the table at
 // lds_k_off, then the slice at lds_x_off).  Persistent blocks walk the tiles
-// (group x channel tile, image, pixel tile).  NCHW x and y.
+// (group x channel tile, image, pixel tile).  NCHW x; NCHW or NHWC y.
 constexpr int64_t SLICE_MAX_KRED = 1024;
 constexpr int64_t SLICE_MAX_LDS = 80 * 1024;  // two blocks per CU
 struct SliceArgs {
@@ -202,6 +202,7 @@ struct SliceArgs {
     int32_t nblocks;      // persistent grid size
     int32_t lds_k_off, lds_x_off, lds_bytes;
     int32_t loader_only;  // pack probe: slice copies and filter loads only, no MFMA, no output
+    int32_t y_nhwc;       // 1: y is NHWC (x stays NCHW)
 };
 struct SlicePlan {
     bool ok;

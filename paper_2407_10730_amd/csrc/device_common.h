@@ -51,6 +51,27 @@ __device__ __forceinline__ void store_out<uint16_t>(__amdgpu_buffer_rsrc_t r, ui
     st_u16(r, ok ? e * 2u : OOB_OFF, f32_to_bf16_rne(v));
 }
 
+// Four consecutive output elements starting at element e (e a multiple of 4): one 16-byte
+// (fp32) or 8-byte (bf16, round to nearest even) store.
+template <typename TOut>
+__device__ __forceinline__ void store_out4(__amdgpu_buffer_rsrc_t r, uint32_t e, bool ok, float a, float b, float c,
+                                           float d);
+template <>
+__device__ __forceinline__ void store_out4<float>(__amdgpu_buffer_rsrc_t r, uint32_t e, bool ok, float a, float b,
+                                                  float c, float d) {
+    __builtin_amdgcn_raw_buffer_store_b128(u32x4{__builtin_bit_cast(uint32_t, a), __builtin_bit_cast(uint32_t, b),
+                                                 __builtin_bit_cast(uint32_t, c), __builtin_bit_cast(uint32_t, d)},
+                                           r, ok ? e * 4u : OOB_OFF, 0, 0);
+}
+template <>
+__device__ __forceinline__ void store_out4<uint16_t>(__amdgpu_buffer_rsrc_t r, uint32_t e, bool ok, float a, float b,
+                                                     float c, float d) {
+    __builtin_amdgcn_raw_buffer_store_b64(
+        u32x2{(uint32_t)f32_to_bf16_rne(a) | ((uint32_t)f32_to_bf16_rne(b) << 16),
+              (uint32_t)f32_to_bf16_rne(c) | ((uint32_t)f32_to_bf16_rne(d) << 16)},
+        r, ok ? e * 2u : OOB_OFF, 0, 0);
+}
+
 // Linear block id -> tile id such that consecutive tile ids land on the same
 // XCD (workgroups are handed to the 8 XCDs round-robin), so the M tiles of one
 // pixel tile and neighbouring pixel tiles share an L2.

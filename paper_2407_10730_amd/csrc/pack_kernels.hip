@@ -8,6 +8,7 @@
 //            bias, cast to the output type.
 //  nhwc<->nchw : pre- and post-convolution reordering of x and y.
 #include "conv2d_internal.h"
+#include <algorithm>
 
 namespace cv {
 
@@ -291,8 +292,47 @@ __global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ in
     }
 }
 
+// The same transform when one side has at most NARROW_MAX entries (an image with few channels):
+// the 32x32 tiles would stay mostly empty, so a thread takes one index j of the long side and
+// moves its short row (reads or writes of consecutive threads are adjacent for every short
+// index).  grid (ceil(long / 256), n).
+constexpr int64_t NARROW_MAX = 8;
+template <typename T, bool NARROW_COLS>
+__global__ __launch_bounds__(256) void narrow_transpose_kernel(const T* __restrict__ in, T* __restrict__ out,
+                                                               int64_t rows, int64_t cols) {
+    const int64_t img = blockIdx.y;
+    const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const T* src = in + img * rows * cols;
+    T* dst = out + img * rows * cols;
+    if (NARROW_COLS) {
+        if (j >= rows) return;
+        for (int64_t c = 0; c < cols; ++c) dst[c * rows + j] = src[j * cols + c];
+    } else {
+        if (j >= cols) return;
+        for (int64_t r = 0; r < rows; ++r) dst[j * rows + r] = src[r * cols + j];
+    }
+}
+
+template <typename T>
+static void launch_narrow(const void* src, void* dst, int64_t n, int64_t rows, int64_t cols, hipStream_t stream) {
+    const bool ncols = cols <= NARROW_MAX;
+    dim3 grid((unsigned)(((ncols ? rows : cols) + 255) / 256), (unsigned)n);
+    if (ncols)
+        hipLaunchKernelGGL((narrow_transpose_kernel<T, true>), grid, dim3(256), 0, stream, (const T*)src, (T*)dst,
+                           rows, cols);
+    else
+        hipLaunchKernelGGL((narrow_transpose_kernel<T, false>), grid, dim3(256), 0, stream, (const T*)src, (T*)dst,
+                           rows, cols);
+}
+
 static hipError_t launch_transpose(const void* src, void* dst, int64_t n, int64_t rows, int64_t cols,
                                    int elem_bytes, hipStream_t stream) {
+    if (n > 65535) return hipErrorInvalidValue;
+    if (std::min(rows, cols) <= NARROW_MAX) {
+        if (elem_bytes == 4) launch_narrow<uint32_t>(src, dst, n, rows, cols, stream);
+        else launch_narrow<uint16_t>(src, dst, n, rows, cols, stream);
+        return hipGetLastError();
+    }
     dim3 grid((unsigned)((cols + 31) / 32), (unsigned)((rows + 31) / 32), (unsigned)n);
     if (elem_bytes == 4)
         hipLaunchKernelGGL(transpose_kernel<uint32_t>, grid, dim3(256), 0, stream,

@@ -281,15 +281,40 @@ __global__ __launch_bounds__(64 * NW) void slice_conv_kernel(SliceArgs A) {
 
         // ---- epilogue: accumulator v of lane l holds channel 8*(v/4) + 4*(l/32) + v%4 (+32
         // for acc1) and pixel l%32; the bias sits in registers since the filters were loaded
+        // NHWC y: channel gi*Kg + m of pixel p at (n*howo + p)*K + gi*Kg + m, the 4 channels
+        // of each v/4 group adjacent (one 16- or 8-byte store when Kg % 4 == 0)
         const bool pok = p < howo;
         const __amdgpu_buffer_rsrc_t ry = make_rsrc(A.y, A.y_bytes);
-        const uint32_t ybase = (uint32_t)(tl.n * A.K + gi * A.Kg) * (uint32_t)howo + (uint32_t)p;
+        if (A.y_nhwc) {
+            const uint32_t pbase = ((uint32_t)tl.n * (uint32_t)howo + (uint32_t)p) * (uint32_t)A.K +
+                                   (uint32_t)(gi * A.Kg);
+            if ((A.Kg & 3) == 0) {
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            const int m = m0 + 8 * (v >> 2) + 4 * lrow + (v & 3);
-            store_out<TOut>(ry, ybase + (uint32_t)m * (uint32_t)howo, pok & (m < A.Kg), acc0[v] + bv0[v]);
-            store_out<TOut>(ry, ybase + (uint32_t)(m + 32) * (uint32_t)howo, pok & (m + 32 < A.Kg),
-                            acc1[v] + bv1[v]);
+                for (int v4 = 0; v4 < 4; ++v4) {
+                    const int m = m0 + 8 * v4 + 4 * lrow;
+                    const int v = 4 * v4;
+                    store_out4<TOut>(ry, pbase + (uint32_t)m, pok & (m < A.Kg), acc0[v] + bv0[v],
+                                     acc0[v + 1] + bv0[v + 1], acc0[v + 2] + bv0[v + 2], acc0[v + 3] + bv0[v + 3]);
+                    store_out4<TOut>(ry, pbase + (uint32_t)(m + 32), pok & (m + 32 < A.Kg), acc1[v] + bv1[v],
+                                     acc1[v + 1] + bv1[v + 1], acc1[v + 2] + bv1[v + 2], acc1[v + 3] + bv1[v + 3]);
+                }
+            } else {
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int m = m0 + 8 * (v >> 2) + 4 * lrow + (v & 3);
+                    store_out<TOut>(ry, pbase + (uint32_t)m, pok & (m < A.Kg), acc0[v] + bv0[v]);
+                    store_out<TOut>(ry, pbase + (uint32_t)(m + 32), pok & (m + 32 < A.Kg), acc1[v] + bv1[v]);
+                }
+            }
+        } else {
+            const uint32_t ybase = (uint32_t)(tl.n * A.K + gi * A.Kg) * (uint32_t)howo + (uint32_t)p;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int m = m0 + 8 * (v >> 2) + 4 * lrow + (v & 3);
+                store_out<TOut>(ry, ybase + (uint32_t)m * (uint32_t)howo, pok & (m < A.Kg), acc0[v] + bv0[v]);
+                store_out<TOut>(ry, ybase + (uint32_t)(m + 32) * (uint32_t)howo, pok & (m + 32 < A.Kg),
+                                acc1[v] + bv1[v]);
+            }
         }
         lds_barrier();  // every wave is done with the slice before it is overwritten
         if (w + (int)gridDim.x < A.tiles_total) copy_slice(w + gridDim.x, xs);

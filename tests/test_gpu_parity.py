@@ -556,6 +556,36 @@ def test_nhwc_epilogue(idx, dt):
     _check(cs.with_(y_dtype="f32"), IMPLICIT, "integer", "nhwc")
 
 
+# the sliced kernel with NHWC x and y: x is reordered to NCHW first, y written NHWC by the
+# kernel (4 adjacent channels per store when K/g is a multiple of 4, element stores otherwise),
+# so no post-convolution reorder; 7x7 stride-2 stem (Wo = 125), K/g = 30, groups, two channel tiles
+SLICE_NHWC = [
+    _shape(1, 3, 22, 250, 64, 7, 7, st=(2, 2), pd=(3, 3), seed=250),
+    _shape(1, 3, 30, 30, 30, 3, 3, pd=(1, 1), seed=251),
+    _shape(2, 8, 20, 21, 48, 3, 3, pd=(1, 1), g=2, seed=252),
+    _shape(1, 4, 17, 19, 100, 3, 3, pd=(1, 1), seed=253, bias=False),
+]
+
+
+@pytest.mark.parametrize("dt", [("f32", "f32"), ("bf16", "bf16"), ("bf16", "f32")], ids=lambda d: "-".join(d))
+@pytest.mark.parametrize("idx", range(len(SLICE_NHWC)))
+def test_slice_nhwc_output(idx, dt):
+    import torch
+    cs = SLICE_NHWC[idx].with_(layout="nhwc", x_dtype=dt[0], y_dtype=dt[1])
+    with _Kernel("1"):
+        dc = DeviceConv(cs, "random")
+    try:
+        assert dc.plan(IMPLICIT).kernel == B.CONV2D_KERNEL_SLICE
+        dc.run(IMPLICIT)
+        torch.cuda.synchronize()
+        calls = dc.breakdown(IMPLICIT)["calls"]
+        assert calls["pre_reorder"] == 1 and calls["post_reorder"] == 0, calls
+    finally:
+        dc.close()
+    _check(cs, IMPLICIT, "random", "1")
+    _check(cs.with_(y_dtype="f32"), IMPLICIT, "integer", "1")
+
+
 # split reductions with NHWC x and y: the unpack adds the partials and writes NHWC y (16- or
 # 8-byte stores of 4 channels when K/g is a multiple of 4), forced to 2, 3 and 5 splits
 @pytest.mark.parametrize("ksplit", ["2", "3", "5"])
@@ -693,7 +723,9 @@ def test_breakdown_phases_and_invariants():
             ms, calls = bd["ms"], bd["calls"]
             assert bd["fwd_calls"] == 3 and calls["pre_analysis"] == 1
             assert calls["in_microkernel"] == 3
-            assert calls["pre_reorder"] == 3 and calls["post_reorder"] == 3
+            # the sliced kernel (cfg1's implicit path) writes NHWC y itself
+            post = 0 if dc.plan(algo).kernel == B.CONV2D_KERNEL_SLICE else 3
+            assert calls["pre_reorder"] == 3 and calls["post_reorder"] == post
             assert all(v >= 0 for v in ms.values())
             assert bd["operation_ms"] == pytest.approx(sum(ms.values()))
             assert bd["convolution_ms"] == pytest.approx(
