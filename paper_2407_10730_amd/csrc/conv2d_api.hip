@@ -192,6 +192,9 @@ struct conv2d_desc {
     bool implicit_ok = false, direct_ok = false;
     bool implicit_tap = false;  // tap-major gather (C/g a multiple of the stage depth)
     int smallk_ranges = 0;      // > 0: DIRECT runs the few-output-channel kernel with this many channel ranges
+    bool direct_nhwc = false;   // DIRECT runs the NHWC depthwise kernel on NHWC x and y
+    void* wd = nullptr;         // its filters as [R*S][C]
+    int64_t wd_bytes = 0;
     bool implicit_slice = false;  // sliced direct MFMA kernel instead of the GEMM
     bool implicit_nhwc = false;   // bf16 GEMM gathering from an NHWC copy of x (16-byte loads)
     GemmPlan implicit;
@@ -874,6 +877,20 @@ int run_direct(conv2d_desc* d, const void* x, const void* w, const float* bias, 
     a.Ho = (int32_t)g.Ho; a.Wo = (int32_t)g.Wo; a.R = (int32_t)g.R; a.S = (int32_t)g.S;
     a.sh = g.sh; a.sw = g.sw; a.ph = g.ph; a.pw = g.pw; a.dh = g.dh; a.dw = g.dw;
     a.Cg = (int32_t)g.Cg; a.Kg = (int32_t)g.Kg; a.N = (int32_t)g.N;
+    if (d->direct_nhwc) {
+        // pre-convolution reordering of the filters [C][R*S] -> [R*S][C] (4 channels per load)
+        CV_TRY(ensure_buffer(&d->wd, &d->wd_bytes, g.w_elems * elem_size(g.xdt)));
+        {
+            Scope sc(d, CONV2D_ALGO_DIRECT, CONV2D_PH_PRE_REORDER, s, ph);
+            CV_TRY(sc.begin());
+            CV_HIP(launch_nchw_to_nhwc(w, d->wd, 1, g.C, g.R * g.S, (int)elem_size(g.xdt), s));
+            CV_TRY(sc.end());
+        }
+        Scope sc(d, CONV2D_ALGO_DIRECT, CONV2D_PH_IN_MICROKERNEL, s, ph);
+        CV_TRY(sc.begin());
+        CV_HIP(launch_dw_nhwc(a, d->wd, g.xdt, g.ydt, s));
+        return sc.end();
+    }
     if (d->smallk_ranges > 0) {
         // few output channels: channel ranges summed in fp32 partials, then the unpack kernel
         const int ranges = d->smallk_ranges;
@@ -968,6 +985,13 @@ int conv2d_desc_create(const conv2d_params* params, conv2d_desc** out) {
             const int64_t force = env_int64("CONV2D_SMALLK_RANGES", 0);
             d->smallk_ranges = force > 0 ? (int)std::min<int64_t>(force, std::min<int64_t>(g.C, 65535))
                                          : smallk_ranges(da);
+            d->direct_ok = true;
+        }
+        // depthwise layers with NHWC x and y: the NHWC depthwise kernel reads x and writes y as
+        // they are (no layout reorders; CONV2D_DW_GENERIC keeps the NCHW kernels)
+        if (fits && g.layout == CONV2D_NHWC && d->smallk_ranges == 0 && dw_nhwc_supported(da) &&
+            !std::getenv("CONV2D_DW_GENERIC")) {
+            d->direct_nhwc = true;
             d->direct_ok = true;
         }
     }
@@ -1066,6 +1090,7 @@ int conv2d_desc_destroy(conv2d_desc* d) {
     if (d->xr) hipFree(d->xr);
     if (d->sk) hipFree(d->sk);
     if (d->dk) hipFree(d->dk);
+    if (d->wd) hipFree(d->wd);
     if (d->wu) hipFree(d->wu);
     if (d->wvm) hipFree(d->wvm);
     if (d->tp) hipFree(d->tp);
@@ -1113,7 +1138,8 @@ int conv2d_fwd(conv2d_desc* d, const void* x, const void* w, const float* bias, 
     // The bf16 NHWC gather and the bf16 Winograd input transform read x channel-contiguous: an
     // NHWC x goes in as it is, an NCHW x is reordered.  Every other kernel reads NCHW x.
     const bool x_nhwc = (algo == CONV2D_ALGO_IMPLICIT_GEMM && d->implicit_nhwc && !d->implicit_slice) ||
-                        (algo == CONV2D_ALGO_WINOGRAD && g.xdt == CONV2D_BF16);
+                        (algo == CONV2D_ALGO_WINOGRAD && g.xdt == CONV2D_BF16) ||
+                        (algo == CONV2D_ALGO_DIRECT && d->direct_nhwc);
     if (nhwc != x_nhwc) {
         const int64_t xb = g.x_elems * elem_size(g.xdt);
         CV_TRY(ensure_buffer(&d->xr, &d->xr_bytes, xb));
@@ -1127,7 +1153,8 @@ int conv2d_fwd(conv2d_desc* d, const void* x, const void* w, const float* bias, 
         xin = d->xr;
     }
     // NCHW result reordered to NHWC afterwards, unless the kernel writes NHWC y itself
-    const bool y_reorder = nhwc && !(algo == CONV2D_ALGO_IMPLICIT_GEMM && implicit_writes_nhwc(d));
+    const bool y_reorder = nhwc && !(algo == CONV2D_ALGO_IMPLICIT_GEMM && implicit_writes_nhwc(d)) &&
+                           !(algo == CONV2D_ALGO_DIRECT && d->direct_nhwc);
     if (y_reorder) {
         const int64_t yb = g.y_elems * elem_size(g.ydt);
         CV_TRY(ensure_buffer(&d->yr, &d->yr_bytes, yb));
@@ -1238,6 +1265,7 @@ int conv2d_plan_query(const conv2d_desc* d, int algo, conv2d_plan_info* out) {
     if (algo == CONV2D_ALGO_IMPLICIT_GEMM && d->implicit_nhwc && !d->implicit_slice)
         out->needs_reorder = implicit_writes_nhwc(d) ? 0 : 1;
     if (algo == CONV2D_ALGO_WINOGRAD && g.xdt == CONV2D_BF16) out->needs_reorder = 1;
+    if (algo == CONV2D_ALGO_DIRECT && d->direct_nhwc) out->needs_reorder = 0;
     out->op_class = (int32_t)d->opclass;
     out->chunks = 1;
     if (algo == CONV2D_ALGO_IMPLICIT_GEMM) {

@@ -176,6 +176,10 @@ struct SmallKArgs {
 bool smallk_supported(const DirectArgs& a);
 int smallk_ranges(const DirectArgs& a);
 hipError_t launch_smallk(const DirectArgs& a, float* part, int ranges, int xdt, int ydt, hipStream_t stream);
+// Depthwise layers (C/g = K/g = 1, C a multiple of 4) with NHWC x and y; wt = the filters
+// as [R*S][C] (x dtype).
+bool dw_nhwc_supported(const DirectArgs& a);
+hipError_t launch_dw_nhwc(const DirectArgs& a, const void* wt, int xdt, int ydt, hipStream_t stream);
 // Blocks the grouped direct kernel launches for this shape (0: it does not take the shape).
 int64_t grouped_blocks(const DirectArgs& a);
 

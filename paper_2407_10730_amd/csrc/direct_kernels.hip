@@ -834,6 +834,150 @@ hipError_t launch_smallk(const DirectArgs& a, float* part, int ranges, int xdt, 
     return hipErrorInvalidValue;
 }
 
+// ------------------------------------------------------------------ NHWC depthwise
+// Depthwise layers (one input and one output channel per group, C a multiple of 4) with NHWC x
+// and y: a thread takes 4 adjacent channels of DWN_PX (DWN_PX1) consecutive output pixels of one
+// row.
+// Per filter tap it loads the 4 channels' weights from the [R*S][C] copy once and one x run
+// per pixel (16 bytes fp32, 8 bytes bf16); a tap in the padding reads zero through the buffer
+// bounds.  Consecutive threads take consecutive channel quads, so each load and store of a
+// wave covers a contiguous channel run.
+// Stride 1, dilation 1 and S <= DWN_SMAX (the common depthwise layers): DWN_PX1 pixels per thread,
+// and per filter row the DWN_PX1 + S - 1 input columns they share are loaded once and reused
+// for every tap of the row.
+constexpr int DWN_PX = 4;
+constexpr int DWN_PX1 = 8;
+constexpr int DWN_SMAX = 7;
+
+template <typename T>
+__device__ __forceinline__ f32x4 dwn_load4(__amdgpu_buffer_rsrc_t r, bool ok, int64_t e) {
+    if constexpr (sizeof(T) == 4) {
+        return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, ok ? (uint32_t)(e * 4) : OOB_OFF,
+                                                                               0, 0));
+    } else {
+        typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+        const u32x2 h = __builtin_bit_cast(
+            u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, ok ? (uint32_t)(e * 2) : OOB_OFF, 0, 0));
+        return f32x4{__builtin_bit_cast(float, h[0] << 16), __builtin_bit_cast(float, h[0] & 0xFFFF0000u),
+                     __builtin_bit_cast(float, h[1] << 16), __builtin_bit_cast(float, h[1] & 0xFFFF0000u)};
+    }
+}
+
+// Workgroups go to the 8 XCDs round-robin and each XCD has its own L2: block b computes the
+// work item range of logical block dwn_remap(b), so that each XCD takes one contiguous eighth of
+// the output rows and the input rows that neighbouring output rows share stay in one L2
+// (without it each input row was fetched from HBM by up to three XCDs).
+__device__ __forceinline__ int64_t dwn_remap(int64_t bid, int64_t nb) {
+    const int64_t per = nb >> 3, rem = nb & 7;
+    const int64_t xcd = bid & 7, slot = bid >> 3;
+    return xcd < rem ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
+}
+
+template <typename TX, typename TY, bool S1>
+__global__ __launch_bounds__(256) void dw_nhwc_kernel(DirectArgs A, const TX* __restrict__ wt, int64_t total) {
+    constexpr int PX = S1 ? DWN_PX1 : DWN_PX;
+    const int64_t idx = dwn_remap(blockIdx.x, gridDim.x) * 256 + threadIdx.x;
+    if (idx >= total) return;
+    const int cq = A.C >> 2;
+    const int wgroups = (A.Wo + PX - 1) / PX;
+    const int q = (int)(idx % cq);
+    int64_t t = idx / cq;
+    const int wg = (int)(t % wgroups);
+    t /= wgroups;
+    const int ho = (int)(t % A.Ho);
+    const int n = (int)(t / A.Ho);
+    const int c0 = 4 * q;
+    const int wo0 = wg * PX;
+    f32x4 acc[PX];
+    const f32x4 b = A.bias ? f32x4{A.bias[c0], A.bias[c0 + 1], A.bias[c0 + 2], A.bias[c0 + 3]} : f32x4{0, 0, 0, 0};
+#pragma unroll
+    for (int p = 0; p < PX; ++p) acc[p] = b;
+    const __amdgpu_buffer_rsrc_t rx = dk_rsrc(A.x, A.x_bytes);
+    const __amdgpu_buffer_rsrc_t rw = dk_rsrc(wt, (uint32_t)(A.R * A.S * A.C * (int)sizeof(TX)));
+    for (int r = 0; r < A.R; ++r) {
+        const int hi = ho * A.sh - A.ph + r * A.dh;
+        const bool hok = (unsigned)hi < (unsigned)A.H;
+        const int64_t rowbase = ((int64_t)n * A.H + hi) * A.W;
+        if constexpr (S1) {
+            // columns wo0 - pw + j, j < PX + S - 1
+            f32x4 xc[PX + DWN_SMAX - 1];
+#pragma unroll
+            for (int j = 0; j < PX + DWN_SMAX - 1; ++j) {
+                const int wi = wo0 - A.pw + j;
+                const bool ok = hok & (j < PX + A.S - 1) & ((unsigned)wi < (unsigned)A.W);
+                xc[j] = dwn_load4<TX>(rx, ok, (rowbase + wi) * A.C + c0);
+            }
+#pragma unroll
+            for (int s = 0; s < DWN_SMAX; ++s) {
+                if (s < A.S) {
+                    const f32x4 wv = dwn_load4<TX>(rw, true, (int64_t)(r * A.S + s) * A.C + c0);
+#pragma unroll
+                    for (int p = 0; p < PX; ++p)
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) acc[p][j] = __builtin_fmaf(xc[p + s][j], wv[j], acc[p][j]);
+                }
+            }
+        } else {
+            for (int s = 0; s < A.S; ++s) {
+                const f32x4 wv = dwn_load4<TX>(rw, true, (int64_t)(r * A.S + s) * A.C + c0);
+#pragma unroll
+                for (int p = 0; p < PX; ++p) {
+                    const int wi = (wo0 + p) * A.sw - A.pw + s * A.dw;
+                    const bool ok = hok & ((unsigned)wi < (unsigned)A.W);
+                    const f32x4 xv = dwn_load4<TX>(rx, ok, (rowbase + wi) * A.C + c0);
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) acc[p][j] = __builtin_fmaf(xv[j], wv[j], acc[p][j]);
+                }
+            }
+        }
+    }
+    const int64_t ybase = (((int64_t)n * A.Ho + ho) * A.Wo + wo0) * A.K + c0;
+#pragma unroll
+    for (int p = 0; p < PX; ++p) {
+        if (wo0 + p >= A.Wo) break;
+        const int64_t e = ybase + (int64_t)p * A.K;
+        if constexpr (sizeof(TY) == 4) {
+            *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(A.y) + e) = acc[p];
+        } else {
+            typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+            const u32x2 h = {(uint32_t)dk_f32_to_bf16(acc[p][0]) | ((uint32_t)dk_f32_to_bf16(acc[p][1]) << 16),
+                             (uint32_t)dk_f32_to_bf16(acc[p][2]) | ((uint32_t)dk_f32_to_bf16(acc[p][3]) << 16)};
+            *reinterpret_cast<u32x2*>(reinterpret_cast<uint16_t*>(A.y) + e) = h;
+        }
+    }
+}
+
+bool dw_nhwc_supported(const DirectArgs& a) {
+    return a.Cg == 1 && a.Kg == 1 && a.C == a.K && a.C % 4 == 0 && a.N > 0 && a.Ho > 0 && a.Wo > 0;
+}
+
+template <bool S1>
+static void launch_dw_nhwc_cfg(const DirectArgs& a, const void* wt, int xdt, int ydt, int64_t total, dim3 grid,
+                               hipStream_t stream) {
+    if (xdt == CONV2D_F32)
+        hipLaunchKernelGGL((dw_nhwc_kernel<float, float, S1>), grid, dim3(256), 0, stream, a, (const float*)wt,
+                           total);
+    else if (ydt == CONV2D_BF16)
+        hipLaunchKernelGGL((dw_nhwc_kernel<uint16_t, uint16_t, S1>), grid, dim3(256), 0, stream, a,
+                           (const uint16_t*)wt, total);
+    else
+        hipLaunchKernelGGL((dw_nhwc_kernel<uint16_t, float, S1>), grid, dim3(256), 0, stream, a,
+                           (const uint16_t*)wt, total);
+}
+
+hipError_t launch_dw_nhwc(const DirectArgs& a, const void* wt, int xdt, int ydt, hipStream_t stream) {
+    if (!dw_nhwc_supported(a)) return hipErrorInvalidValue;
+    const bool s1 = a.sw == 1 && a.dw == 1 && a.S <= DWN_SMAX;
+    const int px = s1 ? DWN_PX1 : DWN_PX;
+    const int64_t total = (int64_t)a.N * a.Ho * ((a.Wo + px - 1) / px) * (a.C / 4);
+    const int64_t blocks = (total + 255) / 256;
+    if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
+    dim3 grid((unsigned)blocks);
+    if (s1) launch_dw_nhwc_cfg<true>(a, wt, xdt, ydt, total, grid, stream);
+    else launch_dw_nhwc_cfg<false>(a, wt, xdt, ydt, total, grid, stream);
+    return hipGetLastError();
+}
+
 hipError_t launch_direct(const DirectArgs& a, int xdt, int ydt, hipStream_t stream) {
     // CONV2D_DW_GENERIC (tests): the generic per-plane kernel for every shape
     if (!std::getenv("CONV2D_DW_GENERIC")) {

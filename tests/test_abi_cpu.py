@@ -344,6 +344,27 @@ def test_bf16_small_group_nhwc_plan(monkeypatch):
     assert plan(base.with_(layout="nhwc", c=24, x_dtype="f32", y_dtype="f32")).needs_reorder == 1
 
 
+def test_depthwise_nhwc_plan(monkeypatch):
+    """Depthwise NHWC layers (C a multiple of 4) run the NHWC depthwise kernel without layout
+    reorders; C = 6, NCHW and the forced generic kernel keep the reorders or the NCHW kernels."""
+    monkeypatch.delenv("CONV2D_DW_GENERIC", raising=False)
+    base = datagen.ConvShape(n=2, c=64, h=15, w=17, k=64, r=3, s=3, stride=(1, 1), pad=(1, 1), dil=(1, 1),
+                             groups=64, seed=1, has_bias=True, layout="nhwc")
+
+    def plan(cs):
+        d = B.conv2d_desc_create(params_for(cs))
+        try:
+            return B.conv2d_plan_query(d, B.CONV2D_ALGO_DIRECT)
+        finally:
+            B.conv2d_desc_destroy(d)
+    assert plan(base).needs_reorder == 0
+    assert plan(base.with_(x_dtype="bf16", y_dtype="bf16")).needs_reorder == 0
+    assert plan(base.with_(c=6, k=6, groups=6)).needs_reorder == 1
+    assert plan(base.with_(layout="nchw")).needs_reorder == 0
+    monkeypatch.setenv("CONV2D_DW_GENERIC", "1")
+    assert plan(base).needs_reorder == 1
+
+
 def test_small_m_tile_choice(monkeypatch):
     """Few output channels per group: the planner takes a 32-row GEMM tile instead of leaving
     most of a 64-row tile idle; 64 or more keep the 64-row tiles."""

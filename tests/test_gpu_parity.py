@@ -586,6 +586,42 @@ def test_slice_nhwc_output(idx, dt):
     _check(cs.with_(y_dtype="f32"), IMPLICIT, "integer", "1")
 
 
+# depthwise layers with NHWC x and y on the NHWC depthwise kernel (4 channels x 4 or 8 output
+# pixels per thread, filters reordered to [R*S][C]): 3x3, 5x5 at stride 2, dilation 2, 1x1,
+# rectangular, ragged rows (Wo not a multiple of 4 or 8), C = 4 and 12, no bias
+DW_NHWC = [
+    _shape(2, 64, 15, 17, 64, 3, 3, pd=(1, 1), g=64, seed=260),
+    _shape(1, 32, 23, 21, 32, 5, 5, st=(2, 2), pd=(2, 2), g=32, seed=261),
+    _shape(2, 12, 13, 14, 12, 3, 3, pd=(2, 2), dl=(2, 2), g=12, seed=262, bias=False),
+    _shape(3, 4, 9, 10, 4, 1, 1, g=4, seed=263),
+    _shape(1, 128, 7, 9, 128, 3, 5, st=(1, 2), pd=(1, 2), g=128, seed=264),
+    # stride 1, dilation 1, S <= 7: 8 pixels per thread, shared input columns loaded once per
+    # row; 7x7, 5x3 with Wo = 17, and S = 9 (beyond the shared-column path)
+    _shape(1, 16, 11, 13, 16, 7, 7, pd=(3, 3), g=16, seed=265),
+    _shape(2, 8, 6, 19, 8, 5, 3, pd=(2, 0), g=8, seed=266),
+    _shape(1, 4, 5, 20, 4, 1, 9, pd=(0, 4), g=4, seed=267),
+]
+
+
+@pytest.mark.parametrize("dt", [("f32", "f32"), ("bf16", "bf16"), ("bf16", "f32")], ids=lambda d: "-".join(d))
+@pytest.mark.parametrize("idx", range(len(DW_NHWC)))
+def test_depthwise_nhwc(idx, dt):
+    import torch
+    cs = DW_NHWC[idx].with_(layout="nhwc", x_dtype=dt[0], y_dtype=dt[1])
+    dc = DeviceConv(cs, "random")
+    try:
+        assert dc.plan(DIRECT).needs_reorder == 0
+        dc.run(DIRECT)
+        torch.cuda.synchronize()
+        calls = dc.breakdown(DIRECT)["calls"]
+        # pre-convolution reordering: the filters only
+        assert calls["pre_reorder"] == 1 and calls["post_reorder"] == 0, calls
+    finally:
+        dc.close()
+    _check(cs, DIRECT, "random")
+    _check(cs.with_(y_dtype="f32"), DIRECT, "integer")
+
+
 # split reductions with NHWC x and y: the unpack adds the partials and writes NHWC y (16- or
 # 8-byte stores of 4 channels when K/g is a multiple of 4), forced to 2, 3 and 5 splits
 @pytest.mark.parametrize("ksplit", ["2", "3", "5"])
