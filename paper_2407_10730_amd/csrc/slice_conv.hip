@@ -23,7 +23,8 @@
 // operand is one LDS read per reduction index at (pixel base + table offset).
 //
 // Blocks are persistent: each walks the tiles blockIdx.x, +gridDim.x, ... in
-// (group, channel tile, image, pixel tile) order and keeps the filters while
+// (group, channel tile, image, pixel tile) order, permuted within each round of gridDim.x
+// tiles so that the blocks of one XCD take consecutive tiles, and keeps the filters while
 // the channel tile stays the same.  The slice is copied global -> LDS by the
 // buffer unit itself (buffer loads with the LDS bit: no registers, padding
 // comes back as zero from out-of-range offsets), one 4-byte LDS word per
@@ -97,6 +98,11 @@ __global__ __launch_bounds__(64 * NW) void slice_conv_kernel(SliceArgs A) {
     // Geometry of tile w: image n, first pixel p0, first slice row hi0.
     struct Tile { int gz, n, p0, oh0, hi0; };
     auto decode = [&](int w) {
+        // XCD-contiguous order: the blocks of one XCD take consecutive tiles of each round of
+        // gridDim.x tiles, so input rows that neighbouring tiles share stay in one L2
+        const int nb = (int)gridDim.x;
+        const int round = w / nb;
+        w = round * nb + xcd_remap(w - round * nb, min(nb, A.tiles_total - round * nb));
         Tile tl;
         tl.gz = w / per_gz;
         const int rem = w - tl.gz * per_gz;
