@@ -54,7 +54,8 @@ enum {
     CONV2D_ALGO_AUTO = 0,          /* planner's choice */
     CONV2D_ALGO_IMPLICIT_GEMM = 1, /* sliced direct convolution: im2col slices gathered into LDS, MFMA */
     CONV2D_ALGO_IM2COL_GEMM = 2,   /* explicit im2col pack, MFMA GEMM, unpack (ConvBench's default baseline) */
-    CONV2D_ALGO_DIRECT = 3,        /* direct VALU kernels: depthwise, small groups, K <= 4 */
+    CONV2D_ALGO_DIRECT = 3,        /* direct VALU kernels: depthwise (NCHW, or NHWC read and written
+                                      as it is when C is a multiple of 4), small groups, K <= 4 */
     CONV2D_ALGO_WINOGRAD = 4,      /* Winograd F(2x2,3x3) / F(4x4,3x3): 3x3, stride 1, dilation 1, one group;
                                       fp32, or bf16 with F(2x2) only and C a multiple of 8 */
     CONV2D_ALGO_COUNT = 5
@@ -175,6 +176,9 @@ int conv2d_output_shape(const conv2d_desc* desc, int64_t out_nkhw[4]);
  *   bias : K floats, or NULL when has_bias == 0 (ignored then)
  *   y    : N x K x Ho x Wo (NCHW) or N x Ho x Wo x K (NHWC), y_dtype
  *   algo : CONV2D_ALGO_*; AUTO lets the planner choose.
+ * NHWC x and y go to an NCHW kernel through library-owned reordered copies (the
+ * pre- and post-convolution reordering phases) unless the kernel reads or writes
+ * NHWC itself: conv2d_plan_info.needs_reorder tells which.
  * Errors: E_NULL (x, w, y or a required bias missing), E_INVALID (bad algo),
  * E_UNSUPPORTED (algo cannot run this op), E_ALLOC (explicit or Winograd
  * workspace over CONV2D_WORKSPACE_LIMIT_BYTES, default 1 GiB, even after chunking),
