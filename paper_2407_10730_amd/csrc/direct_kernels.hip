@@ -836,8 +836,8 @@ hipError_t launch_smallk(const DirectArgs& a, float* part, int ranges, int xdt, 
 
 // ------------------------------------------------------------------ NHWC depthwise
 // Depthwise layers (one input and one output channel per group, C a multiple of 4) with NHWC x
-// and y: a thread takes 4 adjacent channels of DWN_PX (DWN_PX1) consecutive output pixels of one
-// row.
+// and y: a thread takes 4 adjacent channels (8 in bf16 when C is a multiple of 8, one 16-byte
+// load) of dwn_px() consecutive output pixels of one row.
 // Per filter tap it loads the 4 channels' weights from the [R*S][C] copy once and one x run
 // per pixel (16 bytes fp32, 8 bytes bf16); a tap in the padding reads zero through the buffer
 // bounds.  Consecutive threads take consecutive channel quads, so each load and store of a
@@ -849,17 +849,27 @@ constexpr int DWN_PX = 4;
 constexpr int DWN_PX1 = 8;
 constexpr int DWN_SMAX = 7;
 
-template <typename T>
-__device__ __forceinline__ f32x4 dwn_load4(__amdgpu_buffer_rsrc_t r, bool ok, int64_t e) {
+// CH = 4 or 8 adjacent channels as CH/4 fp32 quads: fp32 16 bytes (CH = 4), bf16 8 or 16 bytes.
+template <typename T, int CH>
+__device__ __forceinline__ void dwn_load(__amdgpu_buffer_rsrc_t r, bool ok, int64_t e, f32x4 (&v)[CH / 4]) {
     if constexpr (sizeof(T) == 4) {
-        return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, ok ? (uint32_t)(e * 4) : OOB_OFF,
+        static_assert(CH == 4, "fp32 takes 4 channels per load");
+        v[0] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, ok ? (uint32_t)(e * 4) : OOB_OFF,
                                                                                0, 0));
-    } else {
+    } else if constexpr (CH == 4) {
         typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
         const u32x2 h = __builtin_bit_cast(
             u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, ok ? (uint32_t)(e * 2) : OOB_OFF, 0, 0));
-        return f32x4{__builtin_bit_cast(float, h[0] << 16), __builtin_bit_cast(float, h[0] & 0xFFFF0000u),
+        v[0] = f32x4{__builtin_bit_cast(float, h[0] << 16), __builtin_bit_cast(float, h[0] & 0xFFFF0000u),
                      __builtin_bit_cast(float, h[1] << 16), __builtin_bit_cast(float, h[1] & 0xFFFF0000u)};
+    } else {
+        const u32x4_t h = __builtin_bit_cast(
+            u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, ok ? (uint32_t)(e * 2) : OOB_OFF, 0, 0));
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+            v[u] = f32x4{__builtin_bit_cast(float, h[2 * u] << 16), __builtin_bit_cast(float, h[2 * u] & 0xFFFF0000u),
+                         __builtin_bit_cast(float, h[2 * u + 1] << 16),
+                         __builtin_bit_cast(float, h[2 * u + 1] & 0xFFFF0000u)};
     }
 }
 
@@ -873,12 +883,18 @@ __device__ __forceinline__ int64_t dwn_remap(int64_t bid, int64_t nb) {
     return xcd < rem ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
 }
 
-template <typename TX, typename TY, bool S1>
+// Output pixels per thread: DWN_PX, or at stride 1 DWN_PX1 (4 with 8 channels, which hold
+// twice the registers per pixel).
+template <bool S1, int CH>
+constexpr int dwn_px() { return S1 ? (CH == 8 ? 4 : DWN_PX1) : DWN_PX; }
+
+template <typename TX, typename TY, bool S1, int CH>
 __global__ __launch_bounds__(256) void dw_nhwc_kernel(DirectArgs A, const TX* __restrict__ wt, int64_t total) {
-    constexpr int PX = S1 ? DWN_PX1 : DWN_PX;
+    constexpr int PX = dwn_px<S1, CH>();
+    constexpr int NQ = CH / 4;
     const int64_t idx = dwn_remap(blockIdx.x, gridDim.x) * 256 + threadIdx.x;
     if (idx >= total) return;
-    const int cq = A.C >> 2;
+    const int cq = A.C / CH;
     const int wgroups = (A.Wo + PX - 1) / PX;
     const int q = (int)(idx % cq);
     int64_t t = idx / cq;
@@ -886,12 +902,16 @@ __global__ __launch_bounds__(256) void dw_nhwc_kernel(DirectArgs A, const TX* __
     t /= wgroups;
     const int ho = (int)(t % A.Ho);
     const int n = (int)(t / A.Ho);
-    const int c0 = 4 * q;
+    const int c0 = CH * q;
     const int wo0 = wg * PX;
-    f32x4 acc[PX];
-    const f32x4 b = A.bias ? f32x4{A.bias[c0], A.bias[c0 + 1], A.bias[c0 + 2], A.bias[c0 + 3]} : f32x4{0, 0, 0, 0};
+    f32x4 acc[PX][NQ];
 #pragma unroll
-    for (int p = 0; p < PX; ++p) acc[p] = b;
+    for (int u = 0; u < NQ; ++u) {
+        const int c = c0 + 4 * u;
+        const f32x4 b = A.bias ? f32x4{A.bias[c], A.bias[c + 1], A.bias[c + 2], A.bias[c + 3]} : f32x4{0, 0, 0, 0};
+#pragma unroll
+        for (int p = 0; p < PX; ++p) acc[p][u] = b;
+    }
     const __amdgpu_buffer_rsrc_t rx = dk_rsrc(A.x, A.x_bytes);
     const __amdgpu_buffer_rsrc_t rw = dk_rsrc(wt, (uint32_t)(A.R * A.S * A.C * (int)sizeof(TX)));
     for (int r = 0; r < A.R; ++r) {
@@ -900,33 +920,41 @@ __global__ __launch_bounds__(256) void dw_nhwc_kernel(DirectArgs A, const TX* __
         const int64_t rowbase = ((int64_t)n * A.H + hi) * A.W;
         if constexpr (S1) {
             // columns wo0 - pw + j, j < PX + S - 1
-            f32x4 xc[PX + DWN_SMAX - 1];
+            f32x4 xc[PX + DWN_SMAX - 1][NQ];
 #pragma unroll
             for (int j = 0; j < PX + DWN_SMAX - 1; ++j) {
                 const int wi = wo0 - A.pw + j;
                 const bool ok = hok & (j < PX + A.S - 1) & ((unsigned)wi < (unsigned)A.W);
-                xc[j] = dwn_load4<TX>(rx, ok, (rowbase + wi) * A.C + c0);
+                dwn_load<TX, CH>(rx, ok, (rowbase + wi) * A.C + c0, xc[j]);
             }
 #pragma unroll
             for (int s = 0; s < DWN_SMAX; ++s) {
                 if (s < A.S) {
-                    const f32x4 wv = dwn_load4<TX>(rw, true, (int64_t)(r * A.S + s) * A.C + c0);
+                    f32x4 wv[NQ];
+                    dwn_load<TX, CH>(rw, true, (int64_t)(r * A.S + s) * A.C + c0, wv);
 #pragma unroll
                     for (int p = 0; p < PX; ++p)
 #pragma unroll
-                        for (int j = 0; j < 4; ++j) acc[p][j] = __builtin_fmaf(xc[p + s][j], wv[j], acc[p][j]);
+                        for (int u = 0; u < NQ; ++u)
+#pragma unroll
+                            for (int j = 0; j < 4; ++j)
+                                acc[p][u][j] = __builtin_fmaf(xc[p + s][u][j], wv[u][j], acc[p][u][j]);
                 }
             }
         } else {
             for (int s = 0; s < A.S; ++s) {
-                const f32x4 wv = dwn_load4<TX>(rw, true, (int64_t)(r * A.S + s) * A.C + c0);
+                f32x4 wv[NQ];
+                dwn_load<TX, CH>(rw, true, (int64_t)(r * A.S + s) * A.C + c0, wv);
 #pragma unroll
                 for (int p = 0; p < PX; ++p) {
                     const int wi = (wo0 + p) * A.sw - A.pw + s * A.dw;
                     const bool ok = hok & ((unsigned)wi < (unsigned)A.W);
-                    const f32x4 xv = dwn_load4<TX>(rx, ok, (rowbase + wi) * A.C + c0);
+                    f32x4 xv[NQ];
+                    dwn_load<TX, CH>(rx, ok, (rowbase + wi) * A.C + c0, xv);
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) acc[p][j] = __builtin_fmaf(xv[j], wv[j], acc[p][j]);
+                    for (int u = 0; u < NQ; ++u)
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) acc[p][u][j] = __builtin_fmaf(xv[u][j], wv[u][j], acc[p][u][j]);
                 }
             }
         }
@@ -936,13 +964,17 @@ __global__ __launch_bounds__(256) void dw_nhwc_kernel(DirectArgs A, const TX* __
     for (int p = 0; p < PX; ++p) {
         if (wo0 + p >= A.Wo) break;
         const int64_t e = ybase + (int64_t)p * A.K;
-        if constexpr (sizeof(TY) == 4) {
-            *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(A.y) + e) = acc[p];
-        } else {
-            typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-            const u32x2 h = {(uint32_t)dk_f32_to_bf16(acc[p][0]) | ((uint32_t)dk_f32_to_bf16(acc[p][1]) << 16),
-                             (uint32_t)dk_f32_to_bf16(acc[p][2]) | ((uint32_t)dk_f32_to_bf16(acc[p][3]) << 16)};
-            *reinterpret_cast<u32x2*>(reinterpret_cast<uint16_t*>(A.y) + e) = h;
+#pragma unroll
+        for (int u = 0; u < NQ; ++u) {
+            if constexpr (sizeof(TY) == 4) {
+                *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(A.y) + e + 4 * u) = acc[p][u];
+            } else {
+                typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+                const u32x2 h = {
+                    (uint32_t)dk_f32_to_bf16(acc[p][u][0]) | ((uint32_t)dk_f32_to_bf16(acc[p][u][1]) << 16),
+                    (uint32_t)dk_f32_to_bf16(acc[p][u][2]) | ((uint32_t)dk_f32_to_bf16(acc[p][u][3]) << 16)};
+                *reinterpret_cast<u32x2*>(reinterpret_cast<uint16_t*>(A.y) + e + 4 * u) = h;
+            }
         }
     }
 }
@@ -951,30 +983,38 @@ bool dw_nhwc_supported(const DirectArgs& a) {
     return a.Cg == 1 && a.Kg == 1 && a.C == a.K && a.C % 4 == 0 && a.N > 0 && a.Ho > 0 && a.Wo > 0;
 }
 
-template <bool S1>
-static void launch_dw_nhwc_cfg(const DirectArgs& a, const void* wt, int xdt, int ydt, int64_t total, dim3 grid,
-                               hipStream_t stream) {
-    if (xdt == CONV2D_F32)
-        hipLaunchKernelGGL((dw_nhwc_kernel<float, float, S1>), grid, dim3(256), 0, stream, a, (const float*)wt,
-                           total);
-    else if (ydt == CONV2D_BF16)
-        hipLaunchKernelGGL((dw_nhwc_kernel<uint16_t, uint16_t, S1>), grid, dim3(256), 0, stream, a,
+template <bool S1, int CH>
+static void launch_dw_nhwc_cfg(const DirectArgs& a, const void* wt, int xdt, int ydt, hipStream_t stream) {
+    constexpr int PX = dwn_px<S1, CH>();
+    const int64_t total = (int64_t)a.N * a.Ho * ((a.Wo + PX - 1) / PX) * (a.C / CH);
+    dim3 grid((unsigned)((total + 255) / 256));
+    if constexpr (CH == 4) {
+        if (xdt == CONV2D_F32) {
+            hipLaunchKernelGGL((dw_nhwc_kernel<float, float, S1, 4>), grid, dim3(256), 0, stream, a,
+                               (const float*)wt, total);
+            return;
+        }
+    }
+    if (ydt == CONV2D_BF16)
+        hipLaunchKernelGGL((dw_nhwc_kernel<uint16_t, uint16_t, S1, CH>), grid, dim3(256), 0, stream, a,
                            (const uint16_t*)wt, total);
     else
-        hipLaunchKernelGGL((dw_nhwc_kernel<uint16_t, float, S1>), grid, dim3(256), 0, stream, a,
+        hipLaunchKernelGGL((dw_nhwc_kernel<uint16_t, float, S1, CH>), grid, dim3(256), 0, stream, a,
                            (const uint16_t*)wt, total);
 }
 
 hipError_t launch_dw_nhwc(const DirectArgs& a, const void* wt, int xdt, int ydt, hipStream_t stream) {
     if (!dw_nhwc_supported(a)) return hipErrorInvalidValue;
+    // upper bound of the work items of every configuration (4 channels, 4 pixels per thread)
+    if ((int64_t)a.N * a.Ho * ((a.Wo + DWN_PX - 1) / DWN_PX) * (a.C / 4) > 0x7fffff00LL * 256)
+        return hipErrorInvalidConfiguration;
     const bool s1 = a.sw == 1 && a.dw == 1 && a.S <= DWN_SMAX;
-    const int px = s1 ? DWN_PX1 : DWN_PX;
-    const int64_t total = (int64_t)a.N * a.Ho * ((a.Wo + px - 1) / px) * (a.C / 4);
-    const int64_t blocks = (total + 255) / 256;
-    if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
-    dim3 grid((unsigned)blocks);
-    if (s1) launch_dw_nhwc_cfg<true>(a, wt, xdt, ydt, total, grid, stream);
-    else launch_dw_nhwc_cfg<false>(a, wt, xdt, ydt, total, grid, stream);
+    // bf16 with C a multiple of 8: 8 channels per thread, 16-byte loads
+    const bool ch8 = xdt == CONV2D_BF16 && a.C % 8 == 0;
+    if (s1 && ch8) launch_dw_nhwc_cfg<true, 8>(a, wt, xdt, ydt, stream);
+    else if (s1) launch_dw_nhwc_cfg<true, 4>(a, wt, xdt, ydt, stream);
+    else if (ch8) launch_dw_nhwc_cfg<false, 8>(a, wt, xdt, ydt, stream);
+    else launch_dw_nhwc_cfg<false, 4>(a, wt, xdt, ydt, stream);
     return hipGetLastError();
 }
 
