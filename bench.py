@@ -176,9 +176,11 @@ def _cpu_model():
 
 
 def time_algo(dc, algo, steps, warmup, B, torch, timing):
-    """Warm up, then time exactly `steps` calls bracketed by device synchronisation.
-    timing = CONV2D_TIMING_OFF for the headline loop (no events between kernels), or
-    CONV2D_TIMING_PHASES for the breakdown loop (an event pair around every phase launch)."""
+    """Warm up, then time exactly `steps` calls bracketed by device synchronisation, with an
+    event pair on the launch stream around the timed calls.  timing = CONV2D_TIMING_OFF for
+    the timed loops (no events between kernels), or CONV2D_TIMING_PHASES for the breakdown
+    loop (an event pair around every phase launch).  Returns (wall seconds, event ms per
+    step, breakdown or None)."""
     stream = torch.cuda.current_stream()
     B.conv2d_set_timing(dc.desc, timing)
     for _ in range(warmup):
@@ -186,13 +188,61 @@ def time_algo(dc, algo, steps, warmup, B, torch, timing):
     torch.cuda.synchronize()
     B.conv2d_breakdown_reset(dc.desc)
     torch.cuda.synchronize()
+    ea, eb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
+    ea.record(stream)
     for _ in range(steps):
         dc.run(algo, stream)
+    eb.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     bd = dc.breakdown(algo) if timing == B.CONV2D_TIMING_PHASES else None
-    return wall, bd
+    B.conv2d_set_timing(dc.desc, B.CONV2D_TIMING_OFF)
+    return wall, ea.elapsed_time(eb) / steps, bd
+
+
+def clock_ramp(dc, algo, seconds, torch):
+    """Run the workload back to back for a fixed time before anything is counted: the GPU's
+    clocks take a few milliseconds of load to come up, more than a handful of warm-up calls."""
+    stream = torch.cuda.current_stream()
+    calls = 0
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(10):
+            dc.run(algo, stream)
+        calls += 10
+        torch.cuda.synchronize()
+    return {"seconds": time.perf_counter() - t0, "calls": calls}
+
+
+def launches_per_step(dc, algo, B, torch):
+    """Kernel launches of one call (every phase launch once), from one PHASES-mode call."""
+    B.conv2d_set_timing(dc.desc, B.CONV2D_TIMING_PHASES)
+    B.conv2d_breakdown_reset(dc.desc)
+    dc.run(algo)
+    torch.cuda.synchronize()
+    bd = dc.breakdown(algo)
+    B.conv2d_set_timing(dc.desc, B.CONV2D_TIMING_OFF)
+    B.conv2d_breakdown_reset(dc.desc)
+    return sum(v for p, v in bd["calls"].items() if p != "pre_analysis"), bd
+
+
+def kernel_duration(dc, algo, event_ms_per_step, B, torch):
+    """Average duration of the step's dominant kernel from an event pair on its stream around
+    back-to-back launches of that kernel alone: the timed loop's own events when a step is that
+    one launch, else the kernel probe (the implicit microkernel without the launches around
+    it).  Returns (ms, source) or (None, reason)."""
+    launches, bd = launches_per_step(dc, algo, B, torch)
+    if launches == 1:
+        return event_ms_per_step, "timed loop (one launch per step)"
+    if algo == B.CONV2D_ALGO_IMPLICIT_GEMM and bd["calls"]["in_microkernel"] == 1:
+        stream = torch.cuda.current_stream()
+        ms = time_launches(lambda: B.conv2d_kernel_probe(dc.desc, dc.x, dc.w, dc.b, dc.y, stream), 50, torch)
+        # restore y: the probe may leave split partials only
+        dc.run(algo, stream)
+        torch.cuda.synchronize()
+        return ms, "kernel probe (microkernel alone, back to back)"
+    return None, f"{launches} launches per step and no single-kernel probe for this algorithm"
 
 
 def cold_median(dc, algo, runs, B, torch):
@@ -212,6 +262,7 @@ def cold_median(dc, algo, runs, B, torch):
         after = dc.breakdown(algo)["total_ms"]
         times.append(after - before)
     del flush
+    B.conv2d_set_timing(dc.desc, B.CONV2D_TIMING_OFF)
     times.sort()
     return times[len(times) // 2]
 
@@ -229,6 +280,33 @@ def time_launches(launch, reps, torch):
     b.record(stream)
     b.synchronize()
     return a.elapsed_time(b) / reps
+
+
+def roofline(cs, nkhw, flops, kern_ms):
+    """Which roofline bounds the operation (MFMA when the arithmetic intensity on algorithmic
+    bytes reaches the dtype's ridge point; the vector ALU for direct grouped kernels whose
+    intensity outruns it; HBM otherwise) and the kernel's fraction of it."""
+    xdt = cs.x_dtype
+    alg_bytes = algorithmic_bytes(cs, nkhw)
+    ai = flops / alg_bytes
+    ridge = PEAK_TFLOPS[xdt] * 1e12 / (PEAK_HBM_GBS * 1e9)
+    out = {"algorithmic_bytes": alg_bytes, "algorithmic_flops": flops, "arith_intensity": ai}
+    if kern_ms is None:
+        out.update({"bound": None, "achieved": None, "peak": None, "unit": None, "frac": None})
+        return out
+    if ai >= ridge:
+        achieved = flops / (kern_ms * 1e-3) / 1e12
+        out.update({"bound": "mfma", "achieved": achieved, "peak": PEAK_TFLOPS[xdt], "unit": "TFLOP/s",
+                    "frac": achieved / PEAK_TFLOPS[xdt]})
+    elif cs.groups > 1 and ai * PEAK_HBM_GBS * 1e9 > PEAK_VALU_TFLOPS * 1e12:
+        achieved = flops / (kern_ms * 1e-3) / 1e12
+        out.update({"bound": "alu", "achieved": achieved, "peak": PEAK_VALU_TFLOPS, "unit": "TFLOP/s",
+                    "frac": achieved / PEAK_VALU_TFLOPS})
+    else:
+        achieved = alg_bytes / (kern_ms * 1e-3) / 1e9
+        out.update({"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                    "frac": achieved / PEAK_HBM_GBS})
+    return out
 
 
 def measured_peaks(B, torch):
@@ -255,14 +333,15 @@ def measured_peaks(B, torch):
 
 
 PROFILE_COMMANDS = {
-    "trace": "rocprofv3 --kernel-trace --stats -f csv -d {d}/trace -o run -- python -u bench.py --no-cpu --no-pack-probe --workload {w}",
+    "trace": "rocprofv3 --kernel-trace --stats -f csv -d {d}/trace -o run -- python -u bench.py --no-cpu --no-pack-probe "
+             "--no-per-config --workload {w}",
     "pmc1": "rocprofv3 --pmc SQ_WAVES SQ_BUSY_CYCLES SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU SQ_INSTS_MFMA "
             "SQ_LDS_BANK_CONFLICT GRBM_GUI_ACTIVE -f csv -d {d}/pmc1 -o run -- python -u bench.py --no-cpu --no-pack-probe "
-            "--steps 5 --warmup 1 --cold-runs 1 --workload {w}",
-    "pmc2": "rocprofv3 --pmc FETCH_SIZE -f csv -d {d}/pmc2 -o run -- python -u bench.py --no-cpu --no-pack-probe --steps 5 "
-            "--warmup 1 --cold-runs 1 --calibrate-copy --workload {w}",
-    "pmc3": "rocprofv3 --pmc WRITE_SIZE -f csv -d {d}/pmc3 -o run -- python -u bench.py --no-cpu --no-pack-probe --steps 5 "
-            "--warmup 1 --cold-runs 1 --calibrate-copy --workload {w}",
+            "--no-per-config --ramp-seconds 0.2 --steps 5 --warmup 1 --cold-runs 1 --workload {w}",
+    "pmc2": "rocprofv3 --pmc FETCH_SIZE -f csv -d {d}/pmc2 -o run -- python -u bench.py --no-cpu --no-pack-probe "
+            "--no-per-config --ramp-seconds 0.2 --steps 5 --warmup 1 --cold-runs 1 --calibrate-copy --workload {w}",
+    "pmc3": "rocprofv3 --pmc WRITE_SIZE -f csv -d {d}/pmc3 -o run -- python -u bench.py --no-cpu --no-pack-probe "
+            "--no-per-config --ramp-seconds 0.2 --steps 5 --warmup 1 --cold-runs 1 --calibrate-copy --workload {w}",
 }
 
 
@@ -418,14 +497,111 @@ def run_sweep(report_path, B, torch):
     return out
 
 
+PER_CONFIG = ["cfg1", "cfg2", "cfg3a", "cfg3b", "cfg4", "cfg4_bf16", "dw", "grp_g64", "grp_g32", "bf16_3x3"]
+# the oracle evaluated on every output (the other rows: sampled outputs), and single-threaded
+ORACLE_FULL = {"cfg1", "cfg2", "cfg3a", "cfg3b", "cfg4", "cfg4_bf16"}
+ORACLE_SINGLE_THREAD = {"cfg1", "cfg2"}
+
+
+def config_gpu(name, args, B, torch):
+    """GPU half of one per-shape row: step time, kernel time, roofline position, the explicit
+    path's pack share; the output is kept on the host for the oracle half."""
+    import datagen
+    from paper_2407_10730_amd.runner import DeviceConv
+    cs = datagen.CONFIGS[name]
+    print(f"[bench] per-config {name}: {describe(cs)}", file=sys.stderr, flush=True)
+    dc = DeviceConv(cs)
+    try:
+        n, k, ho, wo = dc.out_nkhw
+        flops = 2 * n * k * (cs.c // cs.groups) * cs.r * cs.s * ho * wo
+        algo = dc.plan(B.CONV2D_ALGO_AUTO).algo
+        plan = dc.plan(algo)
+        clock_ramp(dc, algo, 0.15, torch)
+        wall, _, _ = time_algo(dc, algo, 3, 0, B, torch, B.CONV2D_TIMING_OFF)
+        steps = int(max(args.steps, min(2000, 0.03 / max(wall / 3, 1e-7))))
+        wall, ev_ms, _ = time_algo(dc, algo, steps, args.warmup, B, torch, B.CONV2D_TIMING_OFF)
+        ms = wall * 1e3 / steps
+        kern_ms, src = kernel_duration(dc, algo, ev_ms, B, torch)
+        roof = roofline(cs, dc.out_nkhw, flops, kern_ms)
+        roof["kernel_us"] = None if kern_ms is None else kern_ms * 1e3
+        roof["kernel_source"] = src
+        _, _, bd = time_algo(dc, algo, 5, 1, B, torch, B.CONV2D_TIMING_PHASES)
+        row = {"workload": describe(cs), "algo": B.ALGO_NAMES[algo],
+               "kernel": f"{B.KERNEL_NAMES[plan.kernel]} {plan.tile_m}x{plan.tile_n}",
+               "steps": steps, "ms_per_step": ms, "event_ms_per_step": ev_ms,
+               "tflops": flops / (ms * 1e-3) / 1e12, "roofline": roof,
+               "kernel_le_step": None if kern_ms is None else kern_ms <= max(ms, ev_ms) * 1.02,
+               "breakdown_ms_per_call": {p: v / 5 for p, v in bd["ms"].items() if p != "pre_analysis"}}
+        # the explicit im2col path on the same operation: its packing share of the time
+        try:
+            dc.plan(B.CONV2D_ALGO_IM2COL_GEMM)
+            ok = True
+        except B.Conv2dError:
+            ok = False
+        if ok:
+            wall_e, _, _ = time_algo(dc, B.CONV2D_ALGO_IM2COL_GEMM, 5, 2, B, torch, B.CONV2D_TIMING_OFF)
+            _, _, bd_e = time_algo(dc, B.CONV2D_ALGO_IM2COL_GEMM, 5, 1, B, torch, B.CONV2D_TIMING_PHASES)
+            opsum = sum(v for p, v in bd_e["ms"].items() if p != "pre_analysis")
+            row["explicit_im2col"] = {"ms_per_step": wall_e * 1e3 / 5,
+                                      "pack_share": bd_e["ms"]["in_packing"] / opsum if opsum > 0 else None,
+                                      "t_explicit_over_t_main": wall_e * 1e3 / 5 / ms}
+            dc.run(algo)   # y back to the main algorithm's result
+            torch.cuda.synchronize()
+        y = dc.y_nchw()
+        host = (dc.x_host, dc.w_host, dc.b_host)
+    finally:
+        dc.close()
+    return row, (cs, y, host, flops)
+
+
+def config_oracle(name, cs, y, host, flops, threads):
+    """CPU half of one row: the fp64 oracle on all host cores (full evaluation, timed) or on
+    sampled outputs, the GPU result's normalised errors against it, and the single-threaded
+    full evaluation for the smallest workloads."""
+    import numpy as np
+    import oracle
+    x, w, b = host
+    bias = b if cs.has_bias else None
+    out = {}
+    if name in ORACLE_FULL:
+        t0 = time.perf_counter()
+        y_ref, a_ref = oracle.conv2d(x, w, bias, cs.stride, cs.pad, cs.dil, cs.groups, nthreads=threads)
+        dt = time.perf_counter() - t0
+        lit, pt = oracle.normalised_errors(y, y_ref, a_ref)
+        out["oracle"] = {"kind": "oracle", "sample": "every output", "cores": threads, "seconds": dt,
+                         "tflops": flops / dt / 1e12}
+        if name in ORACLE_SINGLE_THREAD:
+            t0 = time.perf_counter()
+            oracle.conv2d(x, w, bias, cs.stride, cs.pad, cs.dil, cs.groups, nthreads=1, want_abs=False)
+            dt1 = time.perf_counter() - t0
+            out["oracle_single_thread"] = {"cores": 1, "seconds": dt1, "tflops": flops / dt1 / 1e12}
+        sample = "every output"
+    else:
+        rng = np.random.default_rng(12345)
+        npts = min(65536, y.size)
+        flat = rng.choice(y.size, size=npts, replace=False)
+        idx = np.stack(np.unravel_index(flat, y.shape), axis=1).astype(np.int64)
+        y_ref, a_ref = oracle.conv2d_points(x, w, bias, idx, cs.stride, cs.pad, cs.dil, cs.groups,
+                                            nthreads=threads)
+        lit, pt = oracle.normalised_errors(y[tuple(idx.T)], y_ref, a_ref)
+        sample = f"{npts} sampled outputs"
+    gate = 1e-5 if cs.x_dtype == "f32" else 1e-2
+    out["parity"] = {"sample": sample, "err_per_point": pt, "err_literal": lit, "gate": gate, "pass": pt <= gate}
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=200,
-                    help="untimed steps first; the GPU clocks need a few milliseconds of work to ramp up")
+    ap.add_argument("--warmup", type=int, default=10,
+                    help="untimed steps before the timed ones (after the fixed-time clock ramp)")
+    ap.add_argument("--ramp-seconds", type=float, default=1.0,
+                    help="back-to-back calls for this long before the warm-up: the GPU clocks need "
+                         "sustained load to come up")
     ap.add_argument("--workload", default="cfg2")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-per-config", action="store_true", help="skip the per-shape rows")
     ap.add_argument("--no-pack-probe", action="store_true",
                     help="skip the pack probe (its loader-only launches share the microkernel's name, so "
                          "profiling runs leave them out)")
@@ -467,7 +643,6 @@ def main():
               f"(the conv2d library runs on a single MI355X)", file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
     import torch
     import datagen
     from paper_2407_10730_amd import binding as B
@@ -488,48 +663,32 @@ def main():
     flops = 2 * n * k * (cs.c // cs.groups) * cs.r * cs.s * ho * wo
     algo = dc.plan(B.CONV2D_ALGO_AUTO).algo
     algo_name = B.ALGO_NAMES[algo]
+    plan = dc.plan(algo)
 
-    # headline: no events inside the timed region
-    wall, _ = time_algo(dc, algo, args.steps, args.warmup, B, torch, B.CONV2D_TIMING_OFF)
+    # headline: the clock ramp, the warm-up, then exactly `steps` calls with no events between
+    # kernels (an event pair on the stream around all of them)
+    ramp = clock_ramp(dc, algo, args.ramp_seconds, torch)
+    wall, ev_ms, _ = time_algo(dc, algo, args.steps, args.warmup, B, torch, B.CONV2D_TIMING_OFF)
     ms_per_step = wall * 1e3 / args.steps
     tflops = flops / (ms_per_step * 1e-3) / 1e12
-    # the same loop again with an event pair around every phase launch: kernel durations
-    wall_ph, bd = time_algo(dc, algo, args.steps, 2, B, torch, B.CONV2D_TIMING_PHASES)
-    mk_calls = bd["calls"]["in_microkernel"]
-    kern_ms = bd["ms"]["in_microkernel"] / max(mk_calls, 1) * (mk_calls / args.steps)
-    kern_launch_ms = bd["ms"]["in_microkernel"] / max(mk_calls, 1)
-    print(f"[bench] {algo_name}: {ms_per_step*1e3:.1f} us/step, {tflops:.1f} TFLOP/s, kernel "
-          f"{kern_launch_ms*1e3:.1f} us/launch", file=sys.stderr, flush=True)
+    kern_ms, kern_src = kernel_duration(dc, algo, ev_ms, B, torch)
+    # the breakdown: the same loop with an event pair around every phase launch
+    wall_ph, _, bd = time_algo(dc, algo, args.steps, 2, B, torch, B.CONV2D_TIMING_PHASES)
+    print(f"[bench] {algo_name}: {ms_per_step*1e3:.1f} us/step (events {ev_ms*1e3:.1f}), {tflops:.1f} TFLOP/s, "
+          f"kernel {kern_ms*1e3 if kern_ms else float('nan'):.1f} us ({kern_src})", file=sys.stderr, flush=True)
     y_gpu = dc.y_nchw()
 
     xdt = cs.x_dtype
-    alg_bytes = algorithmic_bytes(cs, nkhw)
-    ai = flops / alg_bytes
-    ridge = PEAK_TFLOPS[xdt] * 1e12 / (PEAK_HBM_GBS * 1e9)
-    if ai >= ridge:
-        achieved = flops / (kern_ms * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": achieved, "peak": PEAK_TFLOPS[xdt], "unit": "TFLOP/s",
-                "frac": achieved / PEAK_TFLOPS[xdt]}
-    elif cs.groups > 1 and ai * PEAK_HBM_GBS * 1e9 > PEAK_VALU_TFLOPS * 1e12:
-        achieved = flops / (kern_ms * 1e-3) / 1e12
-        roof = {"bound": "alu", "achieved": achieved, "peak": PEAK_VALU_TFLOPS, "unit": "TFLOP/s",
-                "frac": achieved / PEAK_VALU_TFLOPS}
-    else:
-        achieved = alg_bytes / (kern_ms * 1e-3) / 1e9
-        roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": achieved / PEAK_HBM_GBS}
-    plan = dc.plan(algo)
+    roof = roofline(cs, nkhw, flops, kern_ms)
     roof["kernel"] = f"{algo_name} microkernel ({B.KERNEL_NAMES[plan.kernel]}, tile {plan.tile_m}x{plan.tile_n})"
-    roof["kernel_us_per_launch"] = kern_launch_ms * 1e3
-    roof["launches_per_step"] = mk_calls / args.steps
-    roof["algorithmic_bytes"] = alg_bytes
-    roof["algorithmic_flops"] = flops
+    roof["kernel_us_per_launch"] = None if kern_ms is None else kern_ms * 1e3
+    roof["kernel_source"] = kern_src
     roof["traffic"] = load_traffic(args.workload, algo_name)
 
     # explicit im2col baseline on the same workload: pack-phase share
     ne = max(5, args.steps // 5)
-    wall_e, _ = time_algo(dc, B.CONV2D_ALGO_IM2COL_GEMM, ne, 3, B, torch, B.CONV2D_TIMING_OFF)
-    _, bd_e = time_algo(dc, B.CONV2D_ALGO_IM2COL_GEMM, ne, 1, B, torch, B.CONV2D_TIMING_PHASES)
+    wall_e, _, _ = time_algo(dc, B.CONV2D_ALGO_IM2COL_GEMM, ne, 3, B, torch, B.CONV2D_TIMING_OFF)
+    _, _, bd_e = time_algo(dc, B.CONV2D_ALGO_IM2COL_GEMM, ne, 1, B, torch, B.CONV2D_TIMING_PHASES)
     ms_e = wall_e * 1e3 / ne
     opsum = bd_e["ms"]["in_packing"] + bd_e["ms"]["in_microkernel"] + bd_e["ms"]["in_unpacking"]
     explicit = {
@@ -539,7 +698,7 @@ def main():
         "pack_share": bd_e["ms"]["in_packing"] / opsum if opsum > 0 else None,
         "t_explicit_over_t_implicit": ms_e / ms_per_step,
     }
-    # Winograd F(2x2, 3x3) on the same workload when it applies (3x3, stride 1, fp32)
+    # Winograd on the same workload when it applies (3x3, stride 1)
     wino = None
     if algo != B.CONV2D_ALGO_WINOGRAD:
         try:
@@ -548,8 +707,8 @@ def main():
         except B.Conv2dError:
             wino_ok = False
         if wino_ok:
-            wall_w, _ = time_algo(dc, B.CONV2D_ALGO_WINOGRAD, ne, 3, B, torch, B.CONV2D_TIMING_OFF)
-            _, bd_w = time_algo(dc, B.CONV2D_ALGO_WINOGRAD, ne, 1, B, torch, B.CONV2D_TIMING_PHASES)
+            wall_w, _, _ = time_algo(dc, B.CONV2D_ALGO_WINOGRAD, ne, 3, B, torch, B.CONV2D_TIMING_OFF)
+            _, _, bd_w = time_algo(dc, B.CONV2D_ALGO_WINOGRAD, ne, 1, B, torch, B.CONV2D_TIMING_PHASES)
             ms_w = wall_w * 1e3 / ne
             wino = {"ms_per_step": ms_w, "tflops": flops / (ms_w * 1e-3) / 1e12,
                     "phase_ms_per_step": {p: v / bd_w["fwd_calls"] for p, v in bd_w["ms"].items()
@@ -559,14 +718,13 @@ def main():
     # pack probe: the implicit microkernel's loader alone (gather into LDS, no MFMA, no
     # output) against the full microkernel -- an estimate of the fused packing share
     probe = None
-    if algo == B.CONV2D_ALGO_IMPLICIT_GEMM and not args.no_pack_probe:
+    if algo == B.CONV2D_ALGO_IMPLICIT_GEMM and not args.no_pack_probe and kern_ms:
         stream = torch.cuda.current_stream()
-        B.conv2d_set_timing(dc.desc, B.CONV2D_TIMING_OFF)
         dc.run(algo, stream)
         probe_ms = time_launches(lambda: B.conv2d_pack_probe(dc.desc, dc.x, dc.w, stream), 20, torch)
         probe = {"kind": "estimate (loader-only microkernel / microkernel)",
-                 "loader_only_us": probe_ms * 1e3, "microkernel_us": kern_launch_ms * 1e3,
-                 "share_estimate": probe_ms / kern_launch_ms}
+                 "loader_only_us": probe_ms * 1e3, "microkernel_us": kern_ms * 1e3,
+                 "share_estimate": probe_ms / kern_ms}
     peaks = measured_peaks(B, torch)
 
     out = {
@@ -583,8 +741,11 @@ def main():
         "dtype": {"f32": "f32", "bf16": "bf16"}[xdt],
         "data": "synthetic (seeded U[-1,1])",
         "config": {"workload": f"{args.workload}: {describe(cs)}", "algo": algo_name,
-                   "flops": flops, "arith_intensity": ai},
+                   "flops": flops, "arith_intensity": roof["arith_intensity"]},
         "roofline": roof,
+        "kernel_le_step": None if kern_ms is None else kern_ms <= max(ms_per_step, ev_ms) * 1.02,
+        "event_ms_per_step": ev_ms,
+        "clock_ramp": ramp,
         "breakdown_ms_per_step": {p: v / bd["fwd_calls"] for p, v in bd["ms"].items()
                                   if p != "pre_analysis"},
         "phase_events_overhead_ms_per_step": (wall_ph - wall) * 1e3 / args.steps,
@@ -597,15 +758,46 @@ def main():
         "implicit_pack_probe": probe,
         "measured_peaks": peaks,
     }
+    if out["kernel_le_step"] is False:
+        print("[bench] WARNING: kernel duration exceeds the step time", file=sys.stderr, flush=True)
+    host = (dc.x_host, dc.w_host, dc.b_host)
+    dc.close()
+
+    # per-shape rows: every GPU measurement first (the host work in between would let the
+    # clocks drop), then the oracle on the host cores
+    per_gpu = []
+    if not args.no_per_config:
+        for name in PER_CONFIG:
+            if name == args.workload:
+                continue
+            per_gpu.append((name,) + config_gpu(name, args, B, torch))
+
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or len(os.sched_getaffinity(0))
+    threads = max(1, min(threads, len(os.sched_getaffinity(0))))
     if not args.no_cpu:
-        x = dc.x_host
-        cb, parity = cpu_baseline(cs, x, dc.w_host, dc.b_host, y_gpu, flops // n)
+        cb, parity = cpu_baseline(cs, host[0], host[1], host[2], y_gpu, flops // n)
         out["cpu_baseline"] = cb
         cb["gpu_over_oracle"] = out["value"] / cb["value"]
-        out["cpu_im2col_gemm_context"], _ = cpu_im2col_gemm(cs, x, dc.w_host, dc.b_host, flops // n,
+        out["cpu_im2col_gemm_context"], _ = cpu_im2col_gemm(cs, host[0], host[1], host[2], flops // n,
                                                             n_img=min(cs.n, 4))
         out["parity_on_cpu_sample"] = parity
-    dc.close()
+    if per_gpu:
+        per = {}
+        head_row = {"workload": describe(cs), "algo": algo_name, "steps": args.steps, "ms_per_step": ms_per_step,
+                    "event_ms_per_step": ev_ms, "tflops": tflops,
+                    "roofline": {kk: roof[kk] for kk in ("bound", "achieved", "peak", "unit", "frac")}
+                    | {"kernel_us": roof["kernel_us_per_launch"], "kernel_source": kern_src},
+                    "kernel_le_step": out["kernel_le_step"],
+                    "explicit_im2col": {"ms_per_step": ms_e, "pack_share": explicit["pack_share"],
+                                        "t_explicit_over_t_main": ms_e / ms_per_step}}
+        if not args.no_cpu:
+            head_row.update(config_oracle(args.workload, cs, y_gpu, host, flops, threads))
+        per[args.workload] = head_row
+        for name, row, (ccs, y, chost, cflops) in per_gpu:
+            if not args.no_cpu:
+                row.update(config_oracle(name, ccs, y, chost, cflops, threads))
+            per[name] = row
+        out["per_config"] = {kk: per[kk] for kk in PER_CONFIG if kk in per}
     if args.calibrate_copy:
         src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)

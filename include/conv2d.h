@@ -21,6 +21,10 @@
  *   - `stream` is a hipStream_t passed as void*; NULL means the null stream.
  *   - A descriptor must not be used by two host threads at once; distinct
  *     descriptors are independent.
+ *   - Calls on one descriptor are ordered: a conv2d_fwd (or pack probe) queued
+ *     on another stream than the previous conv2d_fwd on that descriptor first
+ *     waits (hipStreamWaitEvent) for that call, since both use the
+ *     descriptor's workspaces.  The same stream every time costs nothing extra.
  */
 #ifndef CONV2D_H
 #define CONV2D_H
@@ -82,10 +86,11 @@ enum {
     CONV2D_PH_COUNT = 7
 };
 
-/* Timing modes of a descriptor.  OFF records nothing; TOTAL records one
- * event pair around each conv2d_fwd (Operation Time only); PHASES records one
- * event pair around every phase launch.  The initial mode comes from the
- * environment variable CONV2D_TIMING = off | total | phases (default: phases). */
+/* Timing modes of a descriptor (the timing tool of Sec. III-A).  OFF records
+ * nothing; TOTAL records one event pair around each conv2d_fwd (Operation Time
+ * only); PHASES records one event pair around every phase launch, which costs a
+ * few microseconds per phase on the GPU.  The initial mode comes from the
+ * environment variable CONV2D_TIMING = off | total | phases (default: off). */
 enum { CONV2D_TIMING_OFF = 0, CONV2D_TIMING_TOTAL = 1, CONV2D_TIMING_PHASES = 2 };
 
 typedef struct conv2d_desc conv2d_desc; /* opaque, owned by the library */
@@ -166,11 +171,16 @@ int conv2d_desc_create(const conv2d_params* params, conv2d_desc** out);
  * the caller must make sure no work using it is still queued.  NULL is OK. */
 int conv2d_desc_destroy(conv2d_desc* desc);
 
-/* out_nkhw = {N, K, Ho, Wo} (logical dims; the memory layout is the
- * descriptor's layout). */
+/* Output dimensions of the operation: out_nkhw = {N, K, Ho, Wo} with
+ * Ho = floor((H + 2*pad_h - dil_h*(R-1) - 1)/stride_h) + 1, likewise Wo (the
+ * Conv2d layers of Sec. III-B; logical dims, the memory layout is the
+ * descriptor's layout).  E_NULL only. */
 int conv2d_output_shape(const conv2d_desc* desc, int64_t out_nkhw[4]);
 
-/* Queue one forward convolution on `stream` and return without waiting.
+/* Queue one forward convolution (the operation ConvBench times, Sec. III-B / III-C:
+ * convolution() and convolution_baseline() of the harness are this call with an
+ * implicit/direct algo and with CONV2D_ALGO_IM2COL_GEMM) on `stream` and return
+ * without waiting.
  *   x    : N x C x H x W (NCHW) or N x H x W x C (NHWC), x_dtype
  *   w    : K x C/g x R x S, x_dtype
  *   bias : K floats, or NULL when has_bias == 0 (ignored then)
@@ -200,6 +210,19 @@ int conv2d_fwd(conv2d_desc* desc, const void* x, const void* w, const float* bia
  * (no implicit algorithm for this shape, or another device), E_HIP. */
 int conv2d_pack_probe(conv2d_desc* desc, const void* x, const void* w, void* stream);
 
+/* Kernel probe (measurement of the microkernel's own duration, Sec. III-A's
+ * microkernel step): queue only the implicit algorithm's microkernel launch --
+ * the tiled MFMA GEMM with its fused gather and epilogue, or the sliced kernel --
+ * on `stream`, without the steps around it (filter repack, layout reorders, the
+ * split reduction's unpack).  Back-to-back calls timed by the caller's events
+ * give the kernel's average duration with no other launch in between.  x, w,
+ * bias, y: the pointers of a conv2d_fwd call; y (or the internal NCHW result of
+ * an NHWC operation, or the split partial sums) is written as that call's
+ * microkernel writes it.  Reads the internal copies the last implicit conv2d_fwd
+ * on this descriptor made: E_NO_DATA before such a call.  E_NULL, E_UNSUPPORTED
+ * (no implicit algorithm, or another device), E_HIP. */
+int conv2d_kernel_probe(conv2d_desc* desc, const void* x, const void* w, const float* bias, void* y, void* stream);
+
 /* Roofline probes (measurement; no descriptor).  Each queues one kernel on
  * `stream` and returns at once; the caller times it with its own events.
  * conv2d_probe_mfma: an MFMA issue loop on register operands over every CU (two
@@ -215,10 +238,13 @@ int conv2d_pack_probe(conv2d_desc* desc, const void* x, const void* w, void* str
 int conv2d_probe_mfma(int dtype, int64_t iters, void* sink, int64_t sink_bytes, void* stream, double* flops);
 int conv2d_probe_copy(void* dst, const void* src, int64_t bytes, void* stream);
 
-/* Synchronise on the descriptor's recorded events, fold them into the
- * per-algorithm totals and copy the totals of `algo` (AUTO: the algorithm
- * of the last conv2d_fwd) into *out.  E_NO_DATA when that algorithm has never
- * been run. */
+/* The timing tool's breakdown (Sec. III-A, Fig. 1: elapsed time and call count
+ * per processing step; Operation Time = all steps, Convolution Time = the
+ * in-convolution steps).  Synchronises on the descriptor's recorded events,
+ * folds them into the per-algorithm totals and copies the totals of `algo`
+ * (AUTO: the algorithm of the last conv2d_fwd) into *out.  With timing OFF the
+ * times stay zero and only fwd_calls counts.  E_NULL, E_INVALID (algo),
+ * E_NO_DATA when that algorithm has never been run, E_HIP. */
 int conv2d_breakdown(conv2d_desc* desc, int algo, conv2d_breakdown_t* out);
 
 /* Discard all accumulated phase times (PRE_ANALYSIS is kept). */

@@ -42,7 +42,7 @@ KERNEL_NAMES = {CONV2D_KERNEL_GEMM: "gemm", CONV2D_KERNEL_SLICE: "slice", CONV2D
 EXPORTS = ("conv2d_desc_create", "conv2d_desc_destroy", "conv2d_output_shape", "conv2d_fwd",
            "conv2d_breakdown", "conv2d_breakdown_reset", "conv2d_set_timing", "conv2d_plan_query",
            "conv2d_status_string", "conv2d_runtime_version", "conv2d_pack_probe", "conv2d_probe_mfma",
-           "conv2d_probe_copy")
+           "conv2d_probe_copy", "conv2d_kernel_probe")
 
 
 class Conv2dError(RuntimeError):
@@ -113,6 +113,7 @@ def load():
     lib.conv2d_output_shape.argtypes = [vp, i64p]
     lib.conv2d_fwd.argtypes = [vp, vp, vp, vp, vp, i32, vp]
     lib.conv2d_pack_probe.argtypes = [vp, vp, vp, vp]
+    lib.conv2d_kernel_probe.argtypes = [vp, vp, vp, vp, vp, vp]
     lib.conv2d_probe_mfma.argtypes = [i32, ctypes.c_int64, vp, ctypes.c_int64, vp, ctypes.POINTER(ctypes.c_double)]
     lib.conv2d_probe_copy.argtypes = [vp, vp, ctypes.c_int64, vp]
     lib.conv2d_breakdown.argtypes = [vp, i32, ctypes.POINTER(conv2d_breakdown_t)]
@@ -177,6 +178,11 @@ def conv2d_fwd(desc: int, x, w, bias, y, algo: int = CONV2D_ALGO_AUTO, stream=No
 
 def conv2d_pack_probe(desc: int, x, w, stream=None) -> None:
     _check(load().conv2d_pack_probe(desc, _ptr(x), _ptr(w), _stream(stream)), "conv2d_pack_probe")
+
+
+def conv2d_kernel_probe(desc: int, x, w, bias, y, stream=None) -> None:
+    _check(load().conv2d_kernel_probe(desc, _ptr(x), _ptr(w), _ptr(bias), _ptr(y), _stream(stream)),
+           "conv2d_kernel_probe")
 
 
 def conv2d_probe_mfma(dtype: int, iters: int, sink, stream=None) -> float:

@@ -91,12 +91,14 @@ int64_t env_int64(const char* name, int64_t dflt) {
     return (int64_t)v;
 }
 
+// Initial timing mode: OFF unless CONV2D_TIMING = total | phases (events cost every caller
+// time between kernels; the benchmark harness and the breakdown reports switch them on).
 int env_timing() {
     const char* s = std::getenv("CONV2D_TIMING");
-    if (!s) return CONV2D_TIMING_PHASES;
-    if (!std::strcmp(s, "off")) return CONV2D_TIMING_OFF;
+    if (!s) return CONV2D_TIMING_OFF;
     if (!std::strcmp(s, "total")) return CONV2D_TIMING_TOTAL;
-    return CONV2D_TIMING_PHASES;
+    if (!std::strcmp(s, "phases")) return CONV2D_TIMING_PHASES;
+    return CONV2D_TIMING_OFF;
 }
 
 // Choose the GEMM kernel and block tile.  Cost = (most tiles any CU runs) x
@@ -182,6 +184,21 @@ hipError_t dispatch_gemm(const GemmPlan& gp, const GemmArgs& a_in, int bsrc, int
     return launch_gemm(a, gp.tile, gp.bk, gp.pf, bsrc, epi, xdt, ydt, groups, s);
 }
 
+// Workspace slots of a descriptor (one use each).
+enum BufSlot {
+    BUF_WS,    // explicit path: col [g][Kred][P_chunk] then the GEMM result [g][Kg][P_chunk]
+    BUF_XR,    // NCHW copy of an NHWC input, or NHWC copy of an NCHW one (channel-contiguous gathers)
+    BUF_YR,    // NCHW result before the NHWC reorder
+    BUF_WR,    // weights in tap-major order for the implicit GEMM
+    BUF_SK,    // partial sums of the split reduction
+    BUF_DK,    // partial sums of the few-output-channel direct kernel's channel ranges
+    BUF_WD,    // depthwise filters as [R*S][C] for the NHWC depthwise kernel
+    BUF_WU,    // Winograd transformed filters
+    BUF_WVM,   // Winograd V and M of one chunk
+    BUF_TP,    // partial tiles of the tail split
+    BUF_COUNT
+};
+
 }  // namespace
 
 struct conv2d_desc {
@@ -202,31 +219,25 @@ struct conv2d_desc {
     ExplicitPlan expl;
     std::vector<KTabEntry> ktab_host;
 
+    WinoPlan wino;
+
     int device = -1;
     int cus = 256;  // compute units of that device
     KTabEntry* ktab_dev = nullptr;
-    void* ws = nullptr;
-    int64_t ws_bytes = 0;
-    void* xr = nullptr;  // NCHW copy of an NHWC input, or NHWC copy of an NCHW one (bf16 NHWC gather)
-    int64_t xr_bytes = 0;
-    void* yr = nullptr;  // NCHW result before the NHWC reorder
-    int64_t yr_bytes = 0;
-    void* wr = nullptr;  // weights in tap-major order for the implicit GEMM
-    int64_t wr_bytes = 0;
-    void* sk = nullptr;  // partial sums of the split reduction
-    int64_t sk_bytes = 0;
-    void* dk = nullptr;  // partial sums of the few-output-channel direct kernel's channel ranges
-    int64_t dk_bytes = 0;
-    WinoPlan wino;
-    void* wu = nullptr;  // Winograd transformed filters
-    int64_t wu_bytes = 0;
-    void* wvm = nullptr;  // Winograd V and M of one chunk
-    int64_t wvm_bytes = 0;
-    void* tp = nullptr;  // partial tiles of the tail split
-    int64_t tp_bytes = 0;
+    // Workspaces (BufSlot), allocated on first use.  Each slot has one size per descriptor,
+    // fixed by the plan, so a slot is allocated once and never resized.
+    void* buf[BUF_COUNT] = {};
+    int64_t buf_bytes[BUF_COUNT] = {};
     uint32_t* tc = nullptr;  // arrival counters of the tail split (zeroed once, reset by the kernel)
+    // Ordering between calls: `done` is recorded at the end of every conv2d_fwd on the stream it
+    // used; a call on another stream first waits for it, so calls that share the workspaces
+    // above never overlap.
+    hipEvent_t done = nullptr;
+    hipStream_t last_stream = nullptr;
+    bool has_last = false;
+    bool implicit_ran = false;  // an implicit conv2d_fwd made the internal copies the probes read
 
-    int timing = CONV2D_TIMING_PHASES;
+    int timing = CONV2D_TIMING_OFF;
     double analysis_ms = 0.0;
     PhaseAcc acc[CONV2D_ALGO_COUNT];
     int last_algo = -1;
@@ -454,9 +465,20 @@ hipError_t get_event(conv2d_desc* d, hipEvent_t* ev) {
     return hipEventCreate(ev);
 }
 
-int harvest(conv2d_desc* d) {
+// Fold the recorded event pairs into the per-algorithm totals.  block = false folds only the
+// pairs whose end event has completed (hipEventQuery) and keeps the rest pending, so a call
+// never waits for the GPU; block = true waits for every pair.
+int harvest(conv2d_desc* d, bool block = true) {
     int st = CONV2D_OK;
+    std::vector<EvRec> keep;
     for (const EvRec& r : d->pending) {
+        if (!block) {
+            const hipError_t q = hipEventQuery(r.b);
+            if (q == hipErrorNotReady) {
+                keep.push_back(r);
+                continue;
+            }
+        }
         float ms = 0.0f;
         if (hipEventSynchronize(r.b) != hipSuccess || hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) {
             st = CONV2D_E_HIP;
@@ -473,7 +495,7 @@ int harvest(conv2d_desc* d) {
         d->free_events.push_back(r.a);
         d->free_events.push_back(r.b);
     }
-    d->pending.clear();
+    d->pending.swap(keep);
     return st;
 }
 
@@ -510,38 +532,65 @@ int ensure_device(conv2d_desc* d, hipStream_t s) {
     if (hipGetDevice(&dev) != hipSuccess) return CONV2D_E_HIP;
     if (d->device >= 0 && d->device != dev) return CONV2D_E_UNSUPPORTED;
     if (d->device < 0) {
-        d->device = dev;
         int cus = 0;
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cus > 0)
             d->cus = cus;
+        if (!d->done && hipEventCreateWithFlags(&d->done, hipEventDisableTiming) != hipSuccess) {
+            d->done = nullptr;
+            return CONV2D_E_HIP;
+        }
         const size_t bytes = d->ktab_host.size() * sizeof(KTabEntry);
         if (hipMalloc(&d->ktab_dev, bytes) != hipSuccess) {
             d->ktab_dev = nullptr;
-            d->device = -1;
             return CONV2D_E_ALLOC;
         }
         if (hipMemcpyAsync(d->ktab_dev, d->ktab_host.data(), bytes, hipMemcpyHostToDevice, s) != hipSuccess)
             return CONV2D_E_HIP;
+        d->device = dev;
     }
     return CONV2D_OK;
 }
 
-int ensure_buffer(void** buf, int64_t* have, int64_t need) {
-    if (*have >= need) return CONV2D_OK;
-    if (*buf) {
-        // the old buffer may still be read by queued work
-        if (hipDeviceSynchronize() != hipSuccess) return CONV2D_E_HIP;
-        hipFree(*buf);
-        *buf = nullptr;
-        *have = 0;
+// Where one call's workspaces come from: the descriptor's own buffers, allocated on first
+// use; a slot that ever needed more would first wait for the descriptor's previous call (its
+// `done` event: the buffer may still be read by it), never for the whole device.
+struct Ws {
+    conv2d_desc* d;
+    int cus = 256;  // compute units of the device the call runs on
+
+    int get(int slot, int64_t need, void** out) {
+        if (need <= 0) need = 1;
+        if (d->buf[slot] && d->buf_bytes[slot] >= need) {
+            *out = d->buf[slot];
+            return CONV2D_OK;
+        }
+        if (d->buf[slot]) {
+            if (d->done && hipEventSynchronize(d->done) != hipSuccess) return CONV2D_E_HIP;
+            hipFree(d->buf[slot]);
+            d->buf[slot] = nullptr;
+            d->buf_bytes[slot] = 0;
+        }
+        if (hipMalloc(&d->buf[slot], (size_t)need) != hipSuccess) {
+            d->buf[slot] = nullptr;
+            return CONV2D_E_ALLOC;
+        }
+        d->buf_bytes[slot] = need;
+        *out = d->buf[slot];
+        return CONV2D_OK;
     }
-    if (hipMalloc(buf, (size_t)need) != hipSuccess) {
-        *buf = nullptr;
-        return CONV2D_E_ALLOC;
+    // arrival counters of the tail split, zero at every launch start
+    int tail_counters(int64_t n, hipStream_t s, uint32_t** out) {
+        if (!d->tc) {
+            if (hipMalloc(&d->tc, (size_t)n * sizeof(uint32_t)) != hipSuccess) {
+                d->tc = nullptr;
+                return CONV2D_E_ALLOC;
+            }
+            if (launch_fill_u32(d->tc, n, 0u, s) != hipSuccess) return CONV2D_E_HIP;
+        }
+        *out = d->tc;
+        return CONV2D_OK;
     }
-    *have = need;
-    return CONV2D_OK;
-}
+};
 
 #define CV_TRY(expr)                 \
     do {                             \
@@ -555,8 +604,8 @@ int ensure_buffer(void** buf, int64_t* have, int64_t need) {
     } while (0)
 
 // ------------------------------------------------------------------ algorithms (NCHW tensors)
-int run_slice(conv2d_desc* d, const void* x, const void* w, const float* bias, void* y, hipStream_t s, bool ph,
-              bool probe) {
+int run_slice(conv2d_desc* d, const Ws& ws, const void* x, const void* w, const float* bias, void* y, hipStream_t s,
+              bool ph, bool probe) {
     const Geometry& g = d->g;
     const SlicePlan& sp = d->slice;
     SliceArgs a{};
@@ -580,7 +629,7 @@ int run_slice(conv2d_desc* d, const void* x, const void* w, const float* bias, v
     a.grid_m = (int32_t)ceil_div(g.Kg, 64);
     a.tiles_total = (int32_t)(g.G * a.grid_m * g.N * a.tiles_px);
     const int per_cu = std::max(1, std::min(16 / sp.nw, (int)((160 << 10) / sp.lds_bytes)));
-    a.nblocks = std::min(a.tiles_total, d->cus * per_cu);
+    a.nblocks = std::min(a.tiles_total, ws.cus * per_cu);
     a.lds_k_off = sp.lds_k_off;
     a.lds_x_off = sp.lds_x_off;
     a.lds_bytes = sp.lds_bytes;
@@ -599,25 +648,28 @@ bool implicit_writes_nhwc(const conv2d_desc* d) {
     return d->g.layout == CONV2D_NHWC && (d->implicit_slice || d->implicit_nhwc);
 }
 
-// probe: the pack probe, which runs only the microkernel's loader on the internal copies that
-// the last call made (tap-major weights) and writes nothing.
-int run_implicit(conv2d_desc* d, const void* x, const void* w, const float* bias, void* y, hipStream_t s,
-                 bool ph, bool probe = false) {
+// probe: PROBE_LOADER runs only the microkernel's loader (the pack probe) and writes nothing;
+// PROBE_KERNEL runs only the microkernel launch (no filter repack, no split-reduction unpack).
+// Both read the internal copies that the last call made (tap-major weights).
+enum { PROBE_NONE = 0, PROBE_LOADER = 1, PROBE_KERNEL = 2 };
+int run_implicit(conv2d_desc* d, Ws& ws, const void* x, const void* w, const float* bias, void* y, hipStream_t s,
+                 bool ph, int probe = PROBE_NONE) {
     const Geometry& g = d->g;
     const GemmPlan& gp = d->implicit;
-    if (d->implicit_slice) return run_slice(d, x, w, bias, y, s, ph, probe);
+    if (d->implicit_slice) return run_slice(d, ws, x, w, bias, y, s, ph, probe == PROBE_LOADER);
     if ((d->implicit_tap || d->implicit_nhwc) && g.R * g.S > 1 && probe) {
-        if (!d->wr) return CONV2D_E_NO_DATA;
-        w = d->wr;
+        if (!d->buf[BUF_WR]) return CONV2D_E_NO_DATA;
+        w = d->buf[BUF_WR];
     } else if ((d->implicit_tap || d->implicit_nhwc) && g.R * g.S > 1) {
         // pre-convolution reordering of the filters into the tap-major reduction order
         const int64_t wb = g.w_elems * elem_size(g.xdt);
-        CV_TRY(ensure_buffer(&d->wr, &d->wr_bytes, wb));
+        void* wr = nullptr;
+        CV_TRY(ws.get(BUF_WR, wb, &wr));
         Scope sc(d, CONV2D_ALGO_IMPLICIT_GEMM, CONV2D_PH_PRE_REORDER, s, ph);
         CV_TRY(sc.begin());
-        CV_HIP(launch_repack_tap_major(w, d->wr, g.K, g.Cg, g.R * g.S, (int)elem_size(g.xdt), s));
+        CV_HIP(launch_repack_tap_major(w, wr, g.K, g.Cg, g.R * g.S, (int)elem_size(g.xdt), s));
         CV_TRY(sc.end());
-        w = d->wr;
+        w = wr;
     }
     GemmArgs a{};
     a.a = w;
@@ -627,7 +679,8 @@ int run_implicit(conv2d_desc* d, const void* x, const void* w, const float* bias
     a.b = x;
     a.b_bytes = (uint32_t)(g.x_elems * elem_size(g.xdt));
     a.b_gstride = g.Cg * g.H * g.W;
-    a.ktab = d->ktab_dev;
+    a.ktab = nullptr;
+    if (!(d->implicit_tap || d->implicit_nhwc)) a.ktab = d->ktab_dev;
     a.H = (int32_t)g.H; a.W = (int32_t)g.W; a.Ho = (int32_t)g.Ho; a.Wo = (int32_t)g.Wo;
     a.sh = g.sh; a.sw = g.sw; a.ph = g.ph; a.pw = g.pw;
     a.dh = g.dh; a.dw = g.dw; a.R = (int32_t)g.R; a.S = (int32_t)g.S; a.RS = (int32_t)(g.R * g.S);
@@ -647,23 +700,16 @@ int run_implicit(conv2d_desc* d, const void* x, const void* w, const float* bias
     a.y_nstride = g.K * g.Ho * g.Wo;
     a.HoWo = (int32_t)(g.Ho * g.Wo);
     const int bsrc = d->implicit_nhwc ? BSRC_NHWC_TAP : d->implicit_tap ? BSRC_IMPLICIT_TAP : BSRC_IMPLICIT_NCHW;
-    a.loader_only = probe ? 1 : 0;
+    a.loader_only = probe == PROBE_LOADER ? 1 : 0;
     if (gp.ksplit <= 1) {
         if (gp.tail_tiles > 0) {
-            CV_TRY(ensure_buffer(&d->tp, &d->tp_bytes, tail_part_bytes(gp)));
-            if (!d->tc) {
-                const size_t cb = (size_t)gp.tail_tiles * sizeof(uint32_t);
-                if (hipMalloc(&d->tc, cb) != hipSuccess) {
-                    d->tc = nullptr;
-                    return CONV2D_E_ALLOC;
-                }
-                CV_HIP(hipMemsetAsync(d->tc, 0, cb, s));
-            }
+            void* tp = nullptr;
+            CV_TRY(ws.get(BUF_TP, tail_part_bytes(gp), &tp));
+            CV_TRY(ws.tail_counters(gp.tail_tiles, s, &a.tail_count));
             a.tail_tiles = gp.tail_tiles;
             a.tail_pieces = gp.tail_pieces;
             a.tail_stages = gp.tail_stages;
-            a.tail_part = static_cast<float*>(d->tp);
-            a.tail_count = d->tc;
+            a.tail_part = static_cast<float*>(tp);
         }
         const bool y_nhwc = implicit_writes_nhwc(d);
         if (y_nhwc) a.ldc = (int32_t)g.K;
@@ -674,8 +720,9 @@ int run_implicit(conv2d_desc* d, const void* x, const void* w, const float* bias
     }
     // split reduction: partial sums [split][g][m][p] in fp32, then the unpack kernel adds them
     const int64_t slice = g.G * g.Kg * g.P;  // elements of one split's partials
-    CV_TRY(ensure_buffer(&d->sk, &d->sk_bytes, gp.ksplit * slice * 4));
-    a.y = d->sk;
+    void* sk = nullptr;
+    CV_TRY(ws.get(BUF_SK, gp.ksplit * slice * 4, &sk));
+    a.y = sk;
     a.y_bytes = (uint32_t)(gp.ksplit * slice * 4);
     a.ldc = (int32_t)g.P;
     a.c_gstride = g.Kg * g.P;
@@ -690,7 +737,7 @@ int run_implicit(conv2d_desc* d, const void* x, const void* w, const float* bias
     }
     if (probe) return CONV2D_OK;
     UnpackArgs u{};
-    u.c = static_cast<const float*>(d->sk);
+    u.c = static_cast<const float*>(sk);
     u.y = y;
     u.y_bytes = (uint32_t)(g.y_elems * elem_size(g.ydt));
     u.bias = g.has_bias ? bias : nullptr;
@@ -708,22 +755,24 @@ int run_implicit(conv2d_desc* d, const void* x, const void* w, const float* bias
     return sc.end();
 }
 
-int run_winograd(conv2d_desc* d, const void* x, const void* w, const float* bias, void* y, hipStream_t s,
+int run_winograd(conv2d_desc* d, Ws& ws, const void* x, const void* w, const float* bias, void* y, hipStream_t s,
                  bool ph) {
     const Geometry& g = d->g;
     const WinoPlan& p = d->wino;
     if (!p.ok) return p.status;
-    CV_TRY(ensure_buffer(&d->wu, &d->wu_bytes, p.u_bytes));
-    CV_TRY(ensure_buffer(&d->wvm, &d->wvm_bytes, p.v_bytes + p.m_bytes));
+    void* wu = nullptr;
+    void* wvm = nullptr;
+    CV_TRY(ws.get(BUF_WU, p.u_bytes, &wu));
+    CV_TRY(ws.get(BUF_WVM, p.v_bytes + p.m_bytes, &wvm));
     const bool bf = g.xdt == CONV2D_BF16;  // U and V bf16, V [16][tc][C] from NHWC x
     const int64_t es = elem_size(g.xdt);
-    void* v = d->wvm;
-    float* m = reinterpret_cast<float*>(static_cast<char*>(d->wvm) + p.v_bytes);
+    void* v = wvm;
+    float* m = reinterpret_cast<float*>(static_cast<char*>(wvm) + p.v_bytes);
     {
         // pre-convolution reordering: the filter transform
         Scope sc(d, CONV2D_ALGO_WINOGRAD, CONV2D_PH_PRE_REORDER, s, ph);
         CV_TRY(sc.begin());
-        CV_HIP(launch_wino_filter(w, d->wu, (int)g.K, (int)g.C, p.mt, g.xdt, s));
+        CV_HIP(launch_wino_filter(w, wu, (int)g.K, (int)g.C, p.mt, g.xdt, s));
         CV_TRY(sc.end());
     }
     WinoArgs wa{};
@@ -754,7 +803,7 @@ int run_winograd(conv2d_desc* d, const void* x, const void* w, const float* bias
             // V[xi] is stored transposed (tc x C)
             const GemmPlan& gp = p.gemm;
             GemmArgs a{};
-            a.a = d->wu;
+            a.a = wu;
             a.a_bytes = (uint32_t)p.u_bytes;
             a.lda = (int32_t)g.C;
             a.a_gstride = g.K * g.C;
@@ -788,13 +837,15 @@ int run_winograd(conv2d_desc* d, const void* x, const void* w, const float* bias
     return CONV2D_OK;
 }
 
-int run_explicit(conv2d_desc* d, const void* x, const void* w, const float* bias, void* y, hipStream_t s,
+int run_explicit(conv2d_desc* d, Ws& ws, const void* x, const void* w, const float* bias, void* y, hipStream_t s,
                  bool ph) {
     const Geometry& g = d->g;
     const ExplicitPlan& e = d->expl;
     if (e.status != CONV2D_OK) return e.status;
-    CV_TRY(ensure_buffer(&d->ws, &d->ws_bytes, e.col_bytes + e.c_bytes));
-    char* col = static_cast<char*>(d->ws);
+    void* wsb = nullptr;
+    CV_TRY(ws.get(BUF_WS, e.col_bytes + e.c_bytes, &wsb));
+    const KTabEntry* ktab = d->ktab_dev;
+    char* col = static_cast<char*>(wsb);
     float* cbuf = reinterpret_cast<float*>(col + e.col_bytes);
     const int64_t total_rows = g.N * g.Ho;
     for (int64_t r0 = 0; r0 < total_rows; r0 += e.rows_per_chunk) {
@@ -806,7 +857,7 @@ int run_explicit(conv2d_desc* d, const void* x, const void* w, const float* bias
             a.x = x;
             a.col = col;
             a.col_bytes = (uint32_t)(g.G * g.Kred * pc * elem_size(g.xdt));
-            a.ktab = d->ktab_dev;
+            a.ktab = ktab;
             a.H = (int32_t)g.H; a.W = (int32_t)g.W; a.Ho = (int32_t)g.Ho; a.Wo = (int32_t)g.Wo;
             a.sh = g.sh; a.sw = g.sw; a.ph = g.ph; a.pw = g.pw;
             a.x_nstride = g.C * g.H * g.W;
@@ -866,7 +917,7 @@ int run_explicit(conv2d_desc* d, const void* x, const void* w, const float* bias
     return CONV2D_OK;
 }
 
-int run_direct(conv2d_desc* d, const void* x, const void* w, const float* bias, void* y, hipStream_t s,
+int run_direct(conv2d_desc* d, Ws& ws, const void* x, const void* w, const float* bias, void* y, hipStream_t s,
                bool ph) {
     const Geometry& g = d->g;
     DirectArgs a{};
@@ -879,16 +930,17 @@ int run_direct(conv2d_desc* d, const void* x, const void* w, const float* bias, 
     a.Cg = (int32_t)g.Cg; a.Kg = (int32_t)g.Kg; a.N = (int32_t)g.N;
     if (d->direct_nhwc) {
         // pre-convolution reordering of the filters [C][R*S] -> [R*S][C] (4 channels per load)
-        CV_TRY(ensure_buffer(&d->wd, &d->wd_bytes, g.w_elems * elem_size(g.xdt)));
+        void* wd = nullptr;
+        CV_TRY(ws.get(BUF_WD, g.w_elems * elem_size(g.xdt), &wd));
         {
             Scope sc(d, CONV2D_ALGO_DIRECT, CONV2D_PH_PRE_REORDER, s, ph);
             CV_TRY(sc.begin());
-            CV_HIP(launch_nchw_to_nhwc(w, d->wd, 1, g.C, g.R * g.S, (int)elem_size(g.xdt), s));
+            CV_HIP(launch_nchw_to_nhwc(w, wd, 1, g.C, g.R * g.S, (int)elem_size(g.xdt), s));
             CV_TRY(sc.end());
         }
         Scope sc(d, CONV2D_ALGO_DIRECT, CONV2D_PH_IN_MICROKERNEL, s, ph);
         CV_TRY(sc.begin());
-        CV_HIP(launch_dw_nhwc(a, d->wd, g.xdt, g.ydt, s));
+        CV_HIP(launch_dw_nhwc(a, wd, g.xdt, g.ydt, s));
         return sc.end();
     }
     if (d->smallk_ranges > 0) {
@@ -896,8 +948,9 @@ int run_direct(conv2d_desc* d, const void* x, const void* w, const float* bias, 
         const int ranges = d->smallk_ranges;
         float* part = nullptr;
         if (ranges > 1) {
-            CV_TRY(ensure_buffer(&d->dk, &d->dk_bytes, (int64_t)ranges * g.K * g.P * 4));
-            part = static_cast<float*>(d->dk);
+            void* dk = nullptr;
+            CV_TRY(ws.get(BUF_DK, (int64_t)ranges * g.K * g.P * 4, &dk));
+            part = static_cast<float*>(dk);
         }
         {
             Scope sc(d, CONV2D_ALGO_DIRECT, CONV2D_PH_IN_MICROKERNEL, s, ph);
@@ -941,6 +994,74 @@ bool direct_supported(const Geometry& g) {
 bool implicit_supported(const Geometry& g) {
     return g.x_elems * elem_size(g.xdt) <= kBufferLimit && g.y_elems * elem_size(g.ydt) <= kBufferLimit &&
            g.w_elems * elem_size(g.xdt) <= kBufferLimit && g.P <= 0x7fffffffLL && g.Kred <= 0x7fffffffLL;
+}
+
+// Argument and algorithm checks shared by both forward entry points; resolves AUTO.
+int check_call(const conv2d_desc* d, const void* x, const void* w, const float* bias, const void* y, int* algo) {
+    if (!d || !x || !w || !y) return CONV2D_E_NULL;
+    if (d->g.has_bias && !bias) return CONV2D_E_NULL;
+    if (*algo < 0 || *algo >= CONV2D_ALGO_COUNT) return CONV2D_E_INVALID;
+    if (*algo == CONV2D_ALGO_AUTO) *algo = d->auto_algo;
+    const Geometry& g = d->g;
+    if (*algo == CONV2D_ALGO_IMPLICIT_GEMM && !d->implicit_ok) return CONV2D_E_UNSUPPORTED;
+    if (*algo == CONV2D_ALGO_DIRECT && !d->direct_ok) return CONV2D_E_UNSUPPORTED;
+    if (*algo == CONV2D_ALGO_WINOGRAD && !d->wino.ok) return d->wino.status;
+    if (*algo == CONV2D_ALGO_IM2COL_GEMM) {
+        if (d->expl.status != CONV2D_OK) return d->expl.status;
+        if (g.y_elems * elem_size(g.ydt) > kBufferLimit) return CONV2D_E_UNSUPPORTED;
+    }
+    return CONV2D_OK;
+}
+
+// One forward convolution: the layout reorders around the algorithm's kernels, with the
+// workspaces from ws.  ph: an event pair around every phase launch.
+int fwd_core(conv2d_desc* d, Ws& ws, const void* x, const void* w, const float* bias, void* y, int algo,
+             hipStream_t s, bool ph) {
+    const Geometry& g = d->g;
+    const void* xin = x;
+    void* yout = y;
+    const bool nhwc = g.layout == CONV2D_NHWC;
+    // The bf16 NHWC gather and the bf16 Winograd input transform read x channel-contiguous: an
+    // NHWC x goes in as it is, an NCHW x is reordered.  Every other kernel reads NCHW x.
+    const bool x_nhwc = (algo == CONV2D_ALGO_IMPLICIT_GEMM && d->implicit_nhwc && !d->implicit_slice) ||
+                        (algo == CONV2D_ALGO_WINOGRAD && g.xdt == CONV2D_BF16) ||
+                        (algo == CONV2D_ALGO_DIRECT && d->direct_nhwc);
+    if (nhwc != x_nhwc) {
+        const int64_t xb = g.x_elems * elem_size(g.xdt);
+        void* xr = nullptr;
+        CV_TRY(ws.get(BUF_XR, xb, &xr));
+        Scope sc(d, algo, CONV2D_PH_PRE_REORDER, s, ph);
+        CV_TRY(sc.begin());
+        if (nhwc)
+            CV_HIP(launch_nhwc_to_nchw(x, xr, g.N, g.C, g.H * g.W, (int)elem_size(g.xdt), s));
+        else
+            CV_HIP(launch_nchw_to_nhwc(x, xr, g.N, g.C, g.H * g.W, (int)elem_size(g.xdt), s));
+        CV_TRY(sc.end());
+        xin = xr;
+    }
+    // NCHW result reordered to NHWC afterwards, unless the kernel writes NHWC y itself
+    const bool y_reorder = nhwc && !(algo == CONV2D_ALGO_IMPLICIT_GEMM && implicit_writes_nhwc(d)) &&
+                           !(algo == CONV2D_ALGO_DIRECT && d->direct_nhwc);
+    if (y_reorder) {
+        const int64_t yb = g.y_elems * elem_size(g.ydt);
+        CV_TRY(ws.get(BUF_YR, yb, &yout));
+    }
+    int st = CONV2D_OK;
+    switch (algo) {
+        case CONV2D_ALGO_IMPLICIT_GEMM: st = run_implicit(d, ws, xin, w, bias, yout, s, ph); break;
+        case CONV2D_ALGO_IM2COL_GEMM: st = run_explicit(d, ws, xin, w, bias, yout, s, ph); break;
+        case CONV2D_ALGO_DIRECT: st = run_direct(d, ws, xin, w, bias, yout, s, ph); break;
+        case CONV2D_ALGO_WINOGRAD: st = run_winograd(d, ws, xin, w, bias, yout, s, ph); break;
+        default: st = CONV2D_E_INVALID;
+    }
+    if (st != CONV2D_OK) return st;
+    if (y_reorder) {
+        Scope sc(d, algo, CONV2D_PH_POST_REORDER, s, ph);
+        CV_TRY(sc.begin());
+        CV_HIP(launch_nchw_to_nhwc(yout, y, g.N, g.K, g.Ho * g.Wo, (int)elem_size(g.ydt), s));
+        CV_TRY(sc.end());
+    }
+    return CONV2D_OK;
 }
 
 }  // namespace
@@ -1086,17 +1207,10 @@ int conv2d_desc_destroy(conv2d_desc* d) {
     }
     for (hipEvent_t e : d->free_events) hipEventDestroy(e);
     if (d->ktab_dev) hipFree(d->ktab_dev);
-    if (d->ws) hipFree(d->ws);
-    if (d->xr) hipFree(d->xr);
-    if (d->sk) hipFree(d->sk);
-    if (d->dk) hipFree(d->dk);
-    if (d->wd) hipFree(d->wd);
-    if (d->wu) hipFree(d->wu);
-    if (d->wvm) hipFree(d->wvm);
-    if (d->tp) hipFree(d->tp);
+    for (int i = 0; i < BUF_COUNT; ++i)
+        if (d->buf[i]) hipFree(d->buf[i]);
     if (d->tc) hipFree(d->tc);
-    if (d->yr) hipFree(d->yr);
-    if (d->wr) hipFree(d->wr);
+    if (d->done) hipEventDestroy(d->done);
     delete d;
     return CONV2D_OK;
 }
@@ -1112,89 +1226,69 @@ int conv2d_output_shape(const conv2d_desc* d, int64_t out_nkhw[4]) {
 
 int conv2d_fwd(conv2d_desc* d, const void* x, const void* w, const float* bias, void* y, int algo,
                void* stream) {
-    if (!d || !x || !w || !y) return CONV2D_E_NULL;
-    if (d->g.has_bias && !bias) return CONV2D_E_NULL;
-    if (algo < 0 || algo >= CONV2D_ALGO_COUNT) return CONV2D_E_INVALID;
-    if (algo == CONV2D_ALGO_AUTO) algo = d->auto_algo;
-    const Geometry& g = d->g;
-    if (algo == CONV2D_ALGO_IMPLICIT_GEMM && !d->implicit_ok) return CONV2D_E_UNSUPPORTED;
-    if (algo == CONV2D_ALGO_DIRECT && !d->direct_ok) return CONV2D_E_UNSUPPORTED;
-    if (algo == CONV2D_ALGO_WINOGRAD && !d->wino.ok) return d->wino.status;
-    if (algo == CONV2D_ALGO_IM2COL_GEMM) {
-        if (d->expl.status != CONV2D_OK) return d->expl.status;
-        if (g.y_elems * elem_size(g.ydt) > kBufferLimit) return CONV2D_E_UNSUPPORTED;
-    }
+    CV_TRY(check_call(d, x, w, bias, y, &algo));
     hipStream_t s = static_cast<hipStream_t>(stream);
     CV_TRY(ensure_device(d, s));
-    if (d->pending.size() > 8192) CV_TRY(harvest(d));
+    // a call on another stream than the previous one waits for that call first (the two share
+    // this descriptor's workspaces and counters)
+    if (d->has_last && s != d->last_stream) CV_HIP(hipStreamWaitEvent(s, d->done, 0));
+    if (d->pending.size() > 8192) CV_TRY(harvest(d, false));
+    if (d->pending.size() > 65536) CV_TRY(harvest(d, true));
 
-    const bool ph = d->timing == CONV2D_TIMING_PHASES;
     Scope total(d, algo, -1, s, d->timing == CONV2D_TIMING_TOTAL);
     CV_TRY(total.begin());
-
-    const void* xin = x;
-    void* yout = y;
-    const bool nhwc = g.layout == CONV2D_NHWC;
-    // The bf16 NHWC gather and the bf16 Winograd input transform read x channel-contiguous: an
-    // NHWC x goes in as it is, an NCHW x is reordered.  Every other kernel reads NCHW x.
-    const bool x_nhwc = (algo == CONV2D_ALGO_IMPLICIT_GEMM && d->implicit_nhwc && !d->implicit_slice) ||
-                        (algo == CONV2D_ALGO_WINOGRAD && g.xdt == CONV2D_BF16) ||
-                        (algo == CONV2D_ALGO_DIRECT && d->direct_nhwc);
-    if (nhwc != x_nhwc) {
-        const int64_t xb = g.x_elems * elem_size(g.xdt);
-        CV_TRY(ensure_buffer(&d->xr, &d->xr_bytes, xb));
-        Scope sc(d, algo, CONV2D_PH_PRE_REORDER, s, ph);
-        CV_TRY(sc.begin());
-        if (nhwc)
-            CV_HIP(launch_nhwc_to_nchw(x, d->xr, g.N, g.C, g.H * g.W, (int)elem_size(g.xdt), s));
-        else
-            CV_HIP(launch_nchw_to_nhwc(x, d->xr, g.N, g.C, g.H * g.W, (int)elem_size(g.xdt), s));
-        CV_TRY(sc.end());
-        xin = d->xr;
-    }
-    // NCHW result reordered to NHWC afterwards, unless the kernel writes NHWC y itself
-    const bool y_reorder = nhwc && !(algo == CONV2D_ALGO_IMPLICIT_GEMM && implicit_writes_nhwc(d)) &&
-                           !(algo == CONV2D_ALGO_DIRECT && d->direct_nhwc);
-    if (y_reorder) {
-        const int64_t yb = g.y_elems * elem_size(g.ydt);
-        CV_TRY(ensure_buffer(&d->yr, &d->yr_bytes, yb));
-        yout = d->yr;
-    }
-    int st = CONV2D_OK;
-    switch (algo) {
-        case CONV2D_ALGO_IMPLICIT_GEMM: st = run_implicit(d, xin, w, bias, yout, s, ph); break;
-        case CONV2D_ALGO_IM2COL_GEMM: st = run_explicit(d, xin, w, bias, yout, s, ph); break;
-        case CONV2D_ALGO_DIRECT: st = run_direct(d, xin, w, bias, yout, s, ph); break;
-        case CONV2D_ALGO_WINOGRAD: st = run_winograd(d, xin, w, bias, yout, s, ph); break;
-        default: st = CONV2D_E_INVALID;
-    }
-    if (st != CONV2D_OK) return st;
-    if (y_reorder) {
-        Scope sc(d, algo, CONV2D_PH_POST_REORDER, s, ph);
-        CV_TRY(sc.begin());
-        CV_HIP(launch_nchw_to_nhwc(d->yr, y, g.N, g.K, g.Ho * g.Wo, (int)elem_size(g.ydt), s));
-        CV_TRY(sc.end());
-    }
+    Ws ws{d};
+    ws.cus = d->cus;
+    CV_TRY(fwd_core(d, ws, x, w, bias, y, algo, s, d->timing == CONV2D_TIMING_PHASES));
     CV_TRY(total.end());
+    CV_HIP(hipEventRecord(d->done, s));
+    d->last_stream = s;
+    d->has_last = true;
     d->acc[algo].fwd_calls += 1;
     d->acc[algo].used = true;
     d->last_algo = algo;
+    if (algo == CONV2D_ALGO_IMPLICIT_GEMM) d->implicit_ran = true;
     return CONV2D_OK;
 }
 
 int conv2d_pack_probe(conv2d_desc* d, const void* x, const void* w, void* stream) {
     if (!d || !x || !w) return CONV2D_E_NULL;
     if (!d->implicit_ok) return CONV2D_E_UNSUPPORTED;
-    if (d->device < 0 || !d->acc[CONV2D_ALGO_IMPLICIT_GEMM].used) return CONV2D_E_NO_DATA;
+    if (d->device < 0 || !d->implicit_ran) return CONV2D_E_NO_DATA;
     int dev = -1;
     if (hipGetDevice(&dev) != hipSuccess) return CONV2D_E_HIP;
     if (dev != d->device) return CONV2D_E_UNSUPPORTED;
     const Geometry& g = d->g;
     // the x the microkernel reads: the internal copy when the layouts differ (made by the last call)
     const bool x_nhwc = d->implicit_nhwc && !d->implicit_slice;
-    const void* xin = (g.layout == CONV2D_NHWC) != x_nhwc ? d->xr : x;
+    const void* xin = (g.layout == CONV2D_NHWC) != x_nhwc ? d->buf[BUF_XR] : x;
     if (!xin) return CONV2D_E_NO_DATA;
-    return run_implicit(d, xin, w, nullptr, nullptr, static_cast<hipStream_t>(stream), false, true);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (d->has_last && s != d->last_stream) CV_HIP(hipStreamWaitEvent(s, d->done, 0));
+    Ws ws{d};
+    ws.cus = d->cus;
+    return run_implicit(d, ws, xin, w, nullptr, nullptr, s, false, PROBE_LOADER);
+}
+
+int conv2d_kernel_probe(conv2d_desc* d, const void* x, const void* w, const float* bias, void* y, void* stream) {
+    if (!d || !x || !w || !y) return CONV2D_E_NULL;
+    if (d->g.has_bias && !bias) return CONV2D_E_NULL;
+    if (!d->implicit_ok) return CONV2D_E_UNSUPPORTED;
+    if (d->device < 0 || !d->implicit_ran) return CONV2D_E_NO_DATA;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return CONV2D_E_HIP;
+    if (dev != d->device) return CONV2D_E_UNSUPPORTED;
+    const Geometry& g = d->g;
+    // the x and y the microkernel reads and writes: the internal copies when the layouts differ
+    const bool x_nhwc = d->implicit_nhwc && !d->implicit_slice;
+    const void* xin = (g.layout == CONV2D_NHWC) != x_nhwc ? d->buf[BUF_XR] : x;
+    void* yout = g.layout == CONV2D_NHWC && !implicit_writes_nhwc(d) ? d->buf[BUF_YR] : y;
+    if (!xin || !yout) return CONV2D_E_NO_DATA;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (d->has_last && s != d->last_stream) CV_HIP(hipStreamWaitEvent(s, d->done, 0));
+    Ws ws{d};
+    ws.cus = d->cus;
+    return run_implicit(d, ws, xin, w, bias, yout, s, false, PROBE_KERNEL);
 }
 
 int conv2d_breakdown(conv2d_desc* d, int algo, conv2d_breakdown_t* out) {

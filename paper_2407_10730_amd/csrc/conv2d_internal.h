@@ -221,6 +221,9 @@ hipError_t launch_slice(const SliceArgs& a, int xdt, int ydt, int nw, hipStream_
 hipError_t launch_repack_tap_major(const void* w, void* wr, int64_t k, int64_t cg, int64_t rs, int elem_bytes,
                                    hipStream_t stream);
 
+// dst[0:n] = value (counters that a launch expects at zero).
+hipError_t launch_fill_u32(uint32_t* dst, int64_t n, uint32_t value, hipStream_t stream);
+
 // layout transforms between NHWC and NCHW (one image = a [HW x C] <-> [C x HW] transpose).
 hipError_t launch_nhwc_to_nchw(const void* src, void* dst, int64_t n, int64_t c, int64_t hw,
                                int elem_bytes, hipStream_t stream);

@@ -269,6 +269,21 @@ hipError_t launch_repack_tap_major(const void* w, void* wr, int64_t k, int64_t c
     return hipGetLastError();
 }
 
+// ------------------------------------------------------------------ fills
+// dst[0:n] = value.  Clears counters with a kernel rather than hipMemsetAsync, so that a
+// caller may record the call into a HIP graph.
+__global__ __launch_bounds__(256) void fill_u32_kernel(uint32_t* __restrict__ dst, uint32_t n, uint32_t value) {
+    const uint32_t i = blockIdx.x * 256u + threadIdx.x;
+    if (i < n) dst[i] = value;
+}
+
+hipError_t launch_fill_u32(uint32_t* dst, int64_t n, uint32_t value, hipStream_t stream) {
+    if (n <= 0 || n >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(fill_u32_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, dst, (uint32_t)n,
+                       value);
+    return hipGetLastError();
+}
+
 // ------------------------------------------------------------------ layout transforms
 // One image is a rows x cols matrix; out[c][r] = in[r][c].  32x32 tiles through LDS,
 // block 32 x 8.  grid (ceil(cols/32), ceil(rows/32), n).

@@ -63,9 +63,11 @@ def from_device(t) -> np.ndarray:
 class DeviceConv:
     """One operation on one device: inputs, descriptor, output."""
 
-    def __init__(self, cs, mode: str = "random", device: str = "cuda:0", inputs=None, device_inputs=None):
+    def __init__(self, cs, mode: str = "random", device: str = "cuda:0", inputs=None, device_inputs=None,
+                 timing=None):
         """inputs: host float32 (x NCHW, w, b) to upload; device_inputs: tensors already on the
-        device in the layout and dtype of `cs` (then x_host etc. are not kept)."""
+        device in the layout and dtype of `cs` (then x_host etc. are not kept); timing: a
+        CONV2D_TIMING_* mode for the descriptor (None keeps the library's default, OFF)."""
         import torch
         self.cs = cs
         self.device = torch.device(device)
@@ -83,6 +85,8 @@ class DeviceConv:
             self.w = to_device(self.w_host, cs.x_dtype, self.device)
             self.b = torch.from_numpy(self.b_host).to(self.device) if cs.has_bias else None
         self.desc = B.conv2d_desc_create(params_for(cs))
+        if timing is not None:
+            B.conv2d_set_timing(self.desc, timing)
         n, k, ho, wo = B.conv2d_output_shape(self.desc)
         self.out_nkhw = (n, k, ho, wo)
         shape = (n, ho, wo, k) if cs.layout == "nhwc" else (n, k, ho, wo)

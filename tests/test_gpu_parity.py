@@ -358,6 +358,31 @@ def test_tail_split_planned_cfg2_repeat():
     assert pt <= GATE["f32"]
 
 
+def test_descriptor_shared_across_streams():
+    """One descriptor (cfg2 as planned: tail-split partials and arrival counters and the
+    tap-major filter copy in its workspaces) called on two streams in turn without any
+    synchronisation between the calls: each call on the other stream waits for the previous
+    one, so every result equals the one of a call on the current stream alone."""
+    import torch
+    cs = datagen.CONFIGS["cfg2"]
+    dc = DeviceConv(cs, "random")
+    try:
+        assert dc.plan(IMPLICIT).tail_tiles > 0
+        dc.run(IMPLICIT)
+        torch.cuda.synchronize()
+        ref = dc.y.clone()
+        streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+        outs = [torch.empty_like(dc.y) for _ in range(24)]
+        torch.cuda.synchronize()
+        for i, y in enumerate(outs):
+            B.conv2d_fwd(dc.desc, dc.x, dc.w, dc.b, y, IMPLICIT, streams[i % 2])
+        torch.cuda.synchronize()
+        bad = [i for i, y in enumerate(outs) if not torch.equal(y, ref)]
+        assert not bad, f"calls {bad} differ from the single-stream result"
+    finally:
+        dc.close()
+
+
 # grouped layers on the direct kernel (C/g > 1 or K/g > 1): per-group output channel chunks
 # of 1/2/4/8/16, input channels staged in chunks when the window and filters do not fit at
 # once, bands of output rows, strides, dilations, rectangular filters, ragged sizes
@@ -539,7 +564,7 @@ def test_nhwc_epilogue(idx, dt):
     import torch
     cs = NHWC_EPI[idx].with_(layout="nhwc", x_dtype=dt[0], y_dtype=dt[1])
     with _Kernel("nhwc"):
-        dc = DeviceConv(cs, "random")
+        dc = DeviceConv(cs, "random", timing=B.CONV2D_TIMING_PHASES)
     try:
         p = dc.plan(IMPLICIT)
         assert p.kernel == B.CONV2D_KERNEL_GEMM
@@ -573,7 +598,7 @@ def test_slice_nhwc_output(idx, dt):
     import torch
     cs = SLICE_NHWC[idx].with_(layout="nhwc", x_dtype=dt[0], y_dtype=dt[1])
     with _Kernel("1"):
-        dc = DeviceConv(cs, "random")
+        dc = DeviceConv(cs, "random", timing=B.CONV2D_TIMING_PHASES)
     try:
         assert dc.plan(IMPLICIT).kernel == B.CONV2D_KERNEL_SLICE
         dc.run(IMPLICIT)
@@ -608,7 +633,7 @@ DW_NHWC = [
 def test_depthwise_nhwc(idx, dt):
     import torch
     cs = DW_NHWC[idx].with_(layout="nhwc", x_dtype=dt[0], y_dtype=dt[1])
-    dc = DeviceConv(cs, "random")
+    dc = DeviceConv(cs, "random", timing=B.CONV2D_TIMING_PHASES)
     try:
         assert dc.plan(DIRECT).needs_reorder == 0
         dc.run(DIRECT)
@@ -633,7 +658,7 @@ def test_nhwc_split_unpack(idx, dt, ksplit, monkeypatch):
     monkeypatch.setenv("CONV2D_KSPLIT", ksplit)
     monkeypatch.setenv("CONV2D_TAIL", "0")
     with _Kernel("nhwc"):
-        dc = DeviceConv(cs, "random")
+        dc = DeviceConv(cs, "random", timing=B.CONV2D_TIMING_PHASES)
     try:
         p = dc.plan(IMPLICIT)
         assert p.kernel == B.CONV2D_KERNEL_GEMM and p.needs_reorder == 0
@@ -731,7 +756,7 @@ def test_chunked_explicit_path(monkeypatch):
     monkeypatch.setenv("CONV2D_WORKSPACE_LIMIT_BYTES", "200000")
     cs = _shape(3, 16, 33, 31, 24, 3, 3, st=(1, 2), pd=(1, 1), seed=9)
     import torch
-    dc = DeviceConv(cs)
+    dc = DeviceConv(cs, timing=B.CONV2D_TIMING_PHASES)
     try:
         assert dc.plan(IM2COL).chunks > 2
         dc.run(IM2COL)
@@ -748,7 +773,7 @@ def test_chunked_explicit_path(monkeypatch):
 def test_breakdown_phases_and_invariants():
     import torch
     cs = datagen.CONFIGS["cfg1"].with_(layout="nhwc")
-    dc = DeviceConv(cs)
+    dc = DeviceConv(cs, timing=B.CONV2D_TIMING_PHASES)
     try:
         for algo in (IMPLICIT, IM2COL, DIRECT):
             for _ in range(3):

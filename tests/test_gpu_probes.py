@@ -1,5 +1,6 @@
 """The measurement entry points on the GPU: the pack probe (the implicit microkernel's
-loader alone) and the roofline probes (MFMA issue loop, device copy)."""
+loader alone), the kernel probe (the microkernel alone) and the roofline probes (MFMA
+issue loop, device copy)."""
 import os
 
 import numpy as np
@@ -81,6 +82,40 @@ def test_pack_probe_needs_a_call_and_writes_nothing(idx):
         dc.run(B.CONV2D_ALGO_IMPLICIT_GEMM)
         torch.cuda.synchronize()
         assert np.array_equal(dc.y_nchw(), y0)
+    finally:
+        dc.close()
+
+
+@pytest.mark.parametrize("idx", range(len(PROBE_CASES)))
+def test_kernel_probe_reproduces_the_microkernel(idx):
+    """The kernel probe needs a call first; then, run alone, its microkernel writes the same y
+    as the whole call (split-reduction cases: the partials only, y untouched), and calls
+    after it still give that result."""
+    import torch
+    cs, env, kernel = PROBE_CASES[idx]
+    print(f"\n[case] kernel probe {cs} env={env}", flush=True)
+    with _Env(env):
+        dc = DeviceConv(cs, "random")
+    try:
+        plan = dc.plan(B.CONV2D_ALGO_IMPLICIT_GEMM)
+        with pytest.raises(B.Conv2dError) as e:
+            B.conv2d_kernel_probe(dc.desc, dc.x, dc.w, dc.b, dc.y)
+        assert e.value.status == B.CONV2D_E_NO_DATA
+        dc.run(B.CONV2D_ALGO_IMPLICIT_GEMM)
+        torch.cuda.synchronize()
+        y0 = dc.y.clone()
+        dc.y.zero_()
+        for _ in range(2):
+            B.conv2d_kernel_probe(dc.desc, dc.x, dc.w, dc.b, dc.y)
+        torch.cuda.synchronize()
+        if plan.ksplit > 1:
+            assert not dc.y.any()
+        else:
+            assert torch.equal(dc.y, y0)
+        dc.y.zero_()
+        dc.run(B.CONV2D_ALGO_IMPLICIT_GEMM)
+        torch.cuda.synchronize()
+        assert torch.equal(dc.y, y0)
     finally:
         dc.close()
 
