@@ -44,7 +44,9 @@ enum {
     CONV2D_E_NULL = -4,        /* a required pointer is NULL */
     CONV2D_E_ALLOC = -5,       /* workspace could not be allocated within the limit */
     CONV2D_E_HIP = -6,         /* a HIP runtime call or kernel launch failed */
-    CONV2D_E_NO_DATA = -7      /* breakdown (or pack probe) requested before any call that feeds it */
+    CONV2D_E_NO_DATA = -7,     /* breakdown (or pack probe) requested before any call that feeds it */
+    CONV2D_E_SCRATCH = -8      /* conv2d_fwd_noalloc: the call needs more workspace than its static
+                                  scratch array holds (CONV2D_NOALLOC_SCRATCH_BYTES) */
 };
 
 /* Layout of x and y.  w is always K x C/g x R x S (row-major). */
@@ -196,6 +198,27 @@ int conv2d_output_shape(const conv2d_desc* desc, int64_t out_nkhw[4]);
  * synchronisation.  Results are bitwise reproducible for a fixed algo. */
 int conv2d_fwd(conv2d_desc* desc, const void* x, const void* w, const float* bias, void* y,
                int algo, void* stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): conv2d_fwd without any
+ * allocation.  Same arguments, layouts, algorithms and results (bit for bit) as
+ * conv2d_fwd; the workspaces (reordered copies, tap-major filters, split and
+ * tail-split partial sums and counters, the tap table, the explicit path's
+ * columns) come from one static device array of CONV2D_NOALLOC_SCRATCH_BYTES
+ * per GPU, which the library holds from its first use on that GPU until the
+ * process ends.  The first call on a device looks the array up and clears its
+ * counter region (queued on `stream`).  No events are recorded (the
+ * descriptor's timing mode is ignored) and the descriptor is not modified.
+ * Every call on a GPU shares that GPU's array and overwrites what the previous
+ * call left there: calls that can overlap on one GPU (other streams, other host
+ * threads) race and must be serialised by the caller; conv2d_fwd calls on the
+ * same descriptor are independent of it.  Errors as conv2d_fwd, plus
+ * E_SCRATCH when the call needs more than the array holds (kernels of the call
+ * that came before the workspace that did not fit may already be queued; y is
+ * then undefined). */
+#define CONV2D_NOALLOC_SCRATCH_BYTES (64LL << 20)
+int conv2d_fwd_noalloc(const conv2d_desc* desc, const void* x, const void* w, const float* bias, void* y,
+                       int algo, void* stream);
 
 /* Pack probe (measurement of the fused packing, Sec. III-C breakdown): queue the
  * implicit algorithm's microkernel on `stream` with its loader only -- the im2col

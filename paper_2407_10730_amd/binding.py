@@ -25,6 +25,8 @@ CONV2D_E_NULL = -4
 CONV2D_E_ALLOC = -5
 CONV2D_E_HIP = -6
 CONV2D_E_NO_DATA = -7
+CONV2D_E_SCRATCH = -8
+CONV2D_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 CONV2D_NCHW, CONV2D_NHWC = 0, 1
 CONV2D_F32, CONV2D_BF16 = 0, 1
@@ -42,7 +44,7 @@ KERNEL_NAMES = {CONV2D_KERNEL_GEMM: "gemm", CONV2D_KERNEL_SLICE: "slice", CONV2D
 EXPORTS = ("conv2d_desc_create", "conv2d_desc_destroy", "conv2d_output_shape", "conv2d_fwd",
            "conv2d_breakdown", "conv2d_breakdown_reset", "conv2d_set_timing", "conv2d_plan_query",
            "conv2d_status_string", "conv2d_runtime_version", "conv2d_pack_probe", "conv2d_probe_mfma",
-           "conv2d_probe_copy", "conv2d_kernel_probe")
+           "conv2d_probe_copy", "conv2d_fwd_noalloc", "conv2d_kernel_probe")
 
 
 class Conv2dError(RuntimeError):
@@ -112,6 +114,7 @@ def load():
     lib.conv2d_desc_destroy.argtypes = [vp]
     lib.conv2d_output_shape.argtypes = [vp, i64p]
     lib.conv2d_fwd.argtypes = [vp, vp, vp, vp, vp, i32, vp]
+    lib.conv2d_fwd_noalloc.argtypes = [vp, vp, vp, vp, vp, i32, vp]
     lib.conv2d_pack_probe.argtypes = [vp, vp, vp, vp]
     lib.conv2d_kernel_probe.argtypes = [vp, vp, vp, vp, vp, vp]
     lib.conv2d_probe_mfma.argtypes = [i32, ctypes.c_int64, vp, ctypes.c_int64, vp, ctypes.POINTER(ctypes.c_double)]
@@ -174,6 +177,11 @@ def conv2d_output_shape(desc: int):
 def conv2d_fwd(desc: int, x, w, bias, y, algo: int = CONV2D_ALGO_AUTO, stream=None) -> None:
     _check(load().conv2d_fwd(desc, _ptr(x), _ptr(w), _ptr(bias), _ptr(y), int(algo), _stream(stream)),
            "conv2d_fwd")
+
+
+def conv2d_fwd_noalloc(desc: int, x, w, bias, y, algo: int = CONV2D_ALGO_AUTO, stream=None) -> None:
+    _check(load().conv2d_fwd_noalloc(desc, _ptr(x), _ptr(w), _ptr(bias), _ptr(y), int(algo), _stream(stream)),
+           "conv2d_fwd_noalloc")
 
 
 def conv2d_pack_probe(desc: int, x, w, stream=None) -> None:

@@ -17,6 +17,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -196,6 +197,7 @@ enum BufSlot {
     BUF_WU,    // Winograd transformed filters
     BUF_WVM,   // Winograd V and M of one chunk
     BUF_TP,    // partial tiles of the tail split
+    BUF_KTAB,  // the tap table, written on the device (no-allocation entry point only)
     BUF_COUNT
 };
 
@@ -551,15 +553,28 @@ int ensure_device(conv2d_desc* d, hipStream_t s) {
     return CONV2D_OK;
 }
 
-// Where one call's workspaces come from: the descriptor's own buffers, allocated on first
-// use; a slot that ever needed more would first wait for the descriptor's previous call (its
-// `done` event: the buffer may still be read by it), never for the whole device.
+// Where one call's workspaces come from.  Normally the descriptor's own buffers, allocated
+// on first use; a slot that ever needed more would first wait for the descriptor's previous
+// call (its `done` event: the buffer may still be read by it), never for the whole device.
+// For the no-allocation entry point, consecutive 256-byte aligned pieces of the static scratch
+// array (the tail split's counters sit in its own fixed region, see there).
 struct Ws {
     conv2d_desc* d;
+    char* scratch = nullptr;  // non-null: carve from here
+    int64_t cap = 0, used = 0;
+    uint32_t* counters = nullptr;  // scratch mode: tail-split counters (kept at zero between launches)
+    int64_t counter_cap = 0;
     int cus = 256;  // compute units of the device the call runs on
 
     int get(int slot, int64_t need, void** out) {
         if (need <= 0) need = 1;
+        if (scratch) {
+            const int64_t at = (used + 255) / 256 * 256;
+            if (at + need > cap) return CONV2D_E_SCRATCH;
+            *out = scratch + at;
+            used = at + need;
+            return CONV2D_OK;
+        }
         if (d->buf[slot] && d->buf_bytes[slot] >= need) {
             *out = d->buf[slot];
             return CONV2D_OK;
@@ -580,6 +595,11 @@ struct Ws {
     }
     // arrival counters of the tail split, zero at every launch start
     int tail_counters(int64_t n, hipStream_t s, uint32_t** out) {
+        if (scratch) {
+            if (n > counter_cap) return CONV2D_E_SCRATCH;
+            *out = counters;
+            return CONV2D_OK;
+        }
         if (!d->tc) {
             if (hipMalloc(&d->tc, (size_t)n * sizeof(uint32_t)) != hipSuccess) {
                 d->tc = nullptr;
@@ -588,6 +608,23 @@ struct Ws {
             if (launch_fill_u32(d->tc, n, 0u, s) != hipSuccess) return CONV2D_E_HIP;
         }
         *out = d->tc;
+        return CONV2D_OK;
+    }
+    // the tap table: uploaded once by ensure_device, or written into the scratch by a kernel
+    int table(hipStream_t s, const KTabEntry** out) {
+        if (!scratch) {
+            *out = d->ktab_dev;
+            return CONV2D_OK;
+        }
+        const int64_t len = (int64_t)d->ktab_host.size();
+        void* p = nullptr;
+        const int st = get(BUF_KTAB, len * (int64_t)sizeof(KTabEntry), &p);
+        if (st != CONV2D_OK) return st;
+        const Geometry& g = d->g;
+        if (launch_ktab_fill(static_cast<KTabEntry*>(p), len, g.Kred, g.Cg, g.R, g.S, g.H, g.W, g.dh, g.dw, s) !=
+            hipSuccess)
+            return CONV2D_E_HIP;
+        *out = static_cast<const KTabEntry*>(p);
         return CONV2D_OK;
     }
 };
@@ -680,7 +717,7 @@ int run_implicit(conv2d_desc* d, Ws& ws, const void* x, const void* w, const flo
     a.b_bytes = (uint32_t)(g.x_elems * elem_size(g.xdt));
     a.b_gstride = g.Cg * g.H * g.W;
     a.ktab = nullptr;
-    if (!(d->implicit_tap || d->implicit_nhwc)) a.ktab = d->ktab_dev;
+    if (!(d->implicit_tap || d->implicit_nhwc)) CV_TRY(ws.table(s, &a.ktab));
     a.H = (int32_t)g.H; a.W = (int32_t)g.W; a.Ho = (int32_t)g.Ho; a.Wo = (int32_t)g.Wo;
     a.sh = g.sh; a.sw = g.sw; a.ph = g.ph; a.pw = g.pw;
     a.dh = g.dh; a.dw = g.dw; a.R = (int32_t)g.R; a.S = (int32_t)g.S; a.RS = (int32_t)(g.R * g.S);
@@ -844,7 +881,8 @@ int run_explicit(conv2d_desc* d, Ws& ws, const void* x, const void* w, const flo
     if (e.status != CONV2D_OK) return e.status;
     void* wsb = nullptr;
     CV_TRY(ws.get(BUF_WS, e.col_bytes + e.c_bytes, &wsb));
-    const KTabEntry* ktab = d->ktab_dev;
+    const KTabEntry* ktab = nullptr;
+    CV_TRY(ws.table(s, &ktab));
     char* col = static_cast<char*>(wsb);
     float* cbuf = reinterpret_cast<float*>(col + e.col_bytes);
     const int64_t total_rows = g.N * g.Ho;
@@ -1064,6 +1102,46 @@ int fwd_core(conv2d_desc* d, Ws& ws, const void* x, const void* w, const float* 
     return CONV2D_OK;
 }
 
+// ------------------------------------------------------------------ no-allocation scratch
+// The workspaces of conv2d_fwd_noalloc live in this array: one copy per device, at a
+// different address on each, held until the process ends.  Host code never passes the
+// array's name to a kernel or a copy (on the host it is a stand-in symbol, not a device
+// address): it uses the address hipGetSymbolAddress returned on that device.
+// Bytes [0, kScratchCounterBytes) hold the tail split's arrival counters and nothing else:
+// they are cleared once per device here, and the tail-split kernel returns every counter it
+// uses to zero before it exits, so they are zero at the start of every launch.  The rest is
+// carved into the call's workspaces; each call overwrites what the previous one left there.
+constexpr int64_t kScratchCounterBytes = 4096;
+static __device__ __align__(256) char scratch[CONV2D_NOALLOC_SCRATCH_BYTES];
+
+struct ScratchDev {
+    char* base;
+    int cus;
+};
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+ScratchDev g_scratch[kMaxDevices] = {};
+
+int scratch_for(int dev, hipStream_t s, ScratchDev* out) {
+    if (dev < 0 || dev >= kMaxDevices) return CONV2D_E_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    ScratchDev& e = g_scratch[dev];
+    if (!e.base) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return CONV2D_E_HIP;
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+            return CONV2D_E_HIP;
+        if (launch_fill_u32(static_cast<uint32_t*>(p), kScratchCounterBytes / (int64_t)sizeof(uint32_t), 0u, s) !=
+            hipSuccess)
+            return CONV2D_E_HIP;
+        e.base = static_cast<char*>(p);
+        e.cus = cus;
+    }
+    *out = e;
+    return CONV2D_OK;
+}
+
 }  // namespace
 
 // ====================================================================== C ABI
@@ -1251,6 +1329,26 @@ int conv2d_fwd(conv2d_desc* d, const void* x, const void* w, const float* bias, 
     return CONV2D_OK;
 }
 
+int conv2d_fwd_noalloc(const conv2d_desc* dc, const void* x, const void* w, const float* bias, void* y, int algo,
+                       void* stream) {
+    // Nothing below writes the descriptor: no events (timing is off for this entry point), no
+    // device buffers (every workspace is carved from the scratch array), no uploaded table.
+    conv2d_desc* d = const_cast<conv2d_desc*>(dc);
+    CV_TRY(check_call(d, x, w, bias, y, &algo));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return CONV2D_E_HIP;
+    ScratchDev sd{};
+    CV_TRY(scratch_for(dev, s, &sd));
+    Ws ws{d};
+    ws.scratch = sd.base + kScratchCounterBytes;
+    ws.cap = CONV2D_NOALLOC_SCRATCH_BYTES - kScratchCounterBytes;
+    ws.counters = reinterpret_cast<uint32_t*>(sd.base);
+    ws.counter_cap = kScratchCounterBytes / (int64_t)sizeof(uint32_t);
+    ws.cus = sd.cus;
+    return fwd_core(d, ws, x, w, bias, y, algo, s, false);
+}
+
 int conv2d_pack_probe(conv2d_desc* d, const void* x, const void* w, void* stream) {
     if (!d || !x || !w) return CONV2D_E_NULL;
     if (!d->implicit_ok) return CONV2D_E_UNSUPPORTED;
@@ -1417,6 +1515,7 @@ const char* conv2d_status_string(int status) {
         case CONV2D_E_ALLOC: return "workspace allocation failed or exceeds the limit";
         case CONV2D_E_HIP: return "HIP runtime error";
         case CONV2D_E_NO_DATA: return "no timing data recorded";
+        case CONV2D_E_SCRATCH: return "workspace exceeds the no-allocation scratch array";
         default: return "unknown status";
     }
 }

@@ -223,6 +223,10 @@ hipError_t launch_repack_tap_major(const void* w, void* wr, int64_t k, int64_t c
 
 // dst[0:n] = value (counters that a launch expects at zero).
 hipError_t launch_fill_u32(uint32_t* dst, int64_t n, uint32_t value, hipStream_t stream);
+// The tap table (len entries, Kred live ones) written by a kernel: the same entries the
+// planner computes on the host, for the entry point that uploads nothing.
+hipError_t launch_ktab_fill(KTabEntry* t, int64_t len, int64_t kred, int64_t cg, int64_t r, int64_t s, int64_t h,
+                            int64_t w, int dh, int dw, hipStream_t stream);
 
 // layout transforms between NHWC and NCHW (one image = a [HW x C] <-> [C x HW] transpose).
 hipError_t launch_nhwc_to_nchw(const void* src, void* dst, int64_t n, int64_t c, int64_t hw,

@@ -284,6 +284,37 @@ hipError_t launch_fill_u32(uint32_t* dst, int64_t n, uint32_t value, hipStream_t
     return hipGetLastError();
 }
 
+// Tap table on the device: entry kr = (c, r, s) of the natural reduction order holds the
+// element offset c*H*W + r*dh*W + s*dw of the tap from the window origin and the row / column
+// shifts r*dh, s*dw; entries past Kred get the dead row shift, so every bounds test fails.
+// The same table the planner builds on the host, for callers that cannot upload it.
+__global__ __launch_bounds__(256) void ktab_fill_kernel(KTabEntry* __restrict__ t, int32_t len, int32_t kred,
+                                                        int32_t rs, int32_t S, int32_t hw, int32_t W, int32_t dh,
+                                                        int32_t dw) {
+    const int32_t kr = (int32_t)(blockIdx.x * 256u + threadIdx.x);
+    if (kr >= len) return;
+    KTabEntry e{0, KTAB_DEAD, 0, 0};
+    if (kr < kred) {
+        const int32_t c = kr / rs;
+        const int32_t q = kr - c * rs;
+        const int32_t r = q / S;
+        const int32_t s = q - r * S;
+        e.roff = r * dh;
+        e.soff = s * dw;
+        e.coff = c * hw + e.roff * W + e.soff;
+    }
+    t[kr] = e;
+}
+
+hipError_t launch_ktab_fill(KTabEntry* t, int64_t len, int64_t kred, int64_t cg, int64_t r, int64_t s, int64_t h,
+                            int64_t w, int dh, int dw, hipStream_t stream) {
+    if (len <= 0 || len >= ((int64_t)1 << 31) || kred > len || cg * h * w >= ((int64_t)1 << 31))
+        return hipErrorInvalidValue;
+    hipLaunchKernelGGL(ktab_fill_kernel, dim3((unsigned)((len + 255) / 256)), dim3(256), 0, stream, t, (int32_t)len,
+                       (int32_t)kred, (int32_t)(r * s), (int32_t)s, (int32_t)(h * w), (int32_t)w, dh, dw);
+    return hipGetLastError();
+}
+
 // ------------------------------------------------------------------ layout transforms
 // One image is a rows x cols matrix; out[c][r] = in[r][c].  32x32 tiles through LDS,
 // block 32 x 8.  grid (ceil(cols/32), ceil(rows/32), n).

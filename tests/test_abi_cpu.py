@@ -64,6 +64,11 @@ def test_null_pointers_rejected():
         assert lib.conv2d_fwd(d, None, None, None, None, 0, None) == B.CONV2D_E_NULL
         assert lib.conv2d_fwd(d, 1, 1, None, 1, 0, None) == B.CONV2D_E_NULL  # bias missing
         assert lib.conv2d_fwd(d, 1, 1, 1, 1, 9, None) == B.CONV2D_E_INVALID
+        # the no-allocation entry point checks its arguments the same way, before any HIP call
+        assert lib.conv2d_fwd_noalloc(d, None, None, None, None, 0, None) == B.CONV2D_E_NULL
+        assert lib.conv2d_fwd_noalloc(d, 1, 1, None, 1, 0, None) == B.CONV2D_E_NULL
+        assert lib.conv2d_fwd_noalloc(d, 1, 1, 1, 1, 9, None) == B.CONV2D_E_INVALID
+        assert lib.conv2d_fwd_noalloc(None, 1, 1, 1, 1, 0, None) == B.CONV2D_E_NULL
     finally:
         B.conv2d_desc_destroy(d)
     assert lib.conv2d_desc_destroy(None) == 0
@@ -310,9 +315,10 @@ def test_explicit_workspace_chunking(monkeypatch):
 
 
 def test_status_strings():
-    for code in range(-7, 1):
+    for code in range(-8, 1):
         assert isinstance(B.conv2d_status_string(code), str)
         assert B.conv2d_status_string(code) != "unknown status"
+    assert "scratch" in B.conv2d_status_string(B.CONV2D_E_SCRATCH)
     assert B.conv2d_status_string(0) == "ok"
 
 
