@@ -21,10 +21,13 @@
  *   - `stream` is a hipStream_t passed as void*; NULL means the null stream.
  *   - A descriptor must not be used by two host threads at once; distinct
  *     descriptors are independent.
- *   - Calls on one descriptor are ordered: a conv2d_fwd (or pack probe) queued
- *     on another stream than the previous conv2d_fwd on that descriptor first
- *     waits (hipStreamWaitEvent) for that call, since both use the
- *     descriptor's workspaces.  The same stream every time costs nothing extra.
+ *   - Calls on one descriptor are ordered: a conv2d_fwd (or probe) queued on
+ *     another stream than the previous call on that descriptor first makes its
+ *     stream wait (hipStreamWaitEvent) for an event recorded on that previous
+ *     stream, behind the previous call, since both use the descriptor's
+ *     workspaces.  The previous call's stream must therefore still exist when
+ *     the next call names another one.  Calls on the same stream every time
+ *     record no event and cost nothing extra.
  */
 #ifndef CONV2D_H
 #define CONV2D_H

@@ -231,9 +231,10 @@ struct conv2d_desc {
     void* buf[BUF_COUNT] = {};
     int64_t buf_bytes[BUF_COUNT] = {};
     uint32_t* tc = nullptr;  // arrival counters of the tail split (zeroed once, reset by the kernel)
-    // Ordering between calls: `done` is recorded at the end of every conv2d_fwd on the stream it
-    // used; a call on another stream first waits for it, so calls that share the workspaces
-    // above never overlap.
+    // Ordering between calls: a call on another stream than the previous call's records `done`
+    // on that previous stream (behind everything queued there, the previous call included) and
+    // makes its own stream wait for it, so calls that share the workspaces above never overlap.
+    // Calls on the same stream are ordered by the stream and record nothing.
     hipEvent_t done = nullptr;
     hipStream_t last_stream = nullptr;
     bool has_last = false;
@@ -528,6 +529,18 @@ struct Scope {
     }
 };
 
+// A call on stream s waits for the previous call on this descriptor when that one went to
+// another stream (see conv2d_desc::done).  last_stream must still exist.
+int order_after_last(conv2d_desc* d, hipStream_t s) {
+    if (d->has_last && s != d->last_stream) {
+        if (hipEventRecord(d->done, d->last_stream) != hipSuccess || hipStreamWaitEvent(s, d->done, 0) != hipSuccess)
+            return CONV2D_E_HIP;
+    }
+    d->last_stream = s;
+    d->has_last = true;
+    return CONV2D_OK;
+}
+
 // ------------------------------------------------------------------ device resources
 int ensure_device(conv2d_desc* d, hipStream_t s) {
     int dev = -1;
@@ -580,7 +593,11 @@ struct Ws {
             return CONV2D_OK;
         }
         if (d->buf[slot]) {
-            if (d->done && hipEventSynchronize(d->done) != hipSuccess) return CONV2D_E_HIP;
+            // the buffer may still be read by queued work of this descriptor, all of which sits
+            // on last_stream
+            if (d->has_last && (hipEventRecord(d->done, d->last_stream) != hipSuccess ||
+                                hipEventSynchronize(d->done) != hipSuccess))
+                return CONV2D_E_HIP;
             hipFree(d->buf[slot]);
             d->buf[slot] = nullptr;
             d->buf_bytes[slot] = 0;
@@ -1309,7 +1326,7 @@ int conv2d_fwd(conv2d_desc* d, const void* x, const void* w, const float* bias, 
     CV_TRY(ensure_device(d, s));
     // a call on another stream than the previous one waits for that call first (the two share
     // this descriptor's workspaces and counters)
-    if (d->has_last && s != d->last_stream) CV_HIP(hipStreamWaitEvent(s, d->done, 0));
+    CV_TRY(order_after_last(d, s));
     if (d->pending.size() > 8192) CV_TRY(harvest(d, false));
     if (d->pending.size() > 65536) CV_TRY(harvest(d, true));
 
@@ -1319,9 +1336,6 @@ int conv2d_fwd(conv2d_desc* d, const void* x, const void* w, const float* bias, 
     ws.cus = d->cus;
     CV_TRY(fwd_core(d, ws, x, w, bias, y, algo, s, d->timing == CONV2D_TIMING_PHASES));
     CV_TRY(total.end());
-    CV_HIP(hipEventRecord(d->done, s));
-    d->last_stream = s;
-    d->has_last = true;
     d->acc[algo].fwd_calls += 1;
     d->acc[algo].used = true;
     d->last_algo = algo;
@@ -1362,7 +1376,7 @@ int conv2d_pack_probe(conv2d_desc* d, const void* x, const void* w, void* stream
     const void* xin = (g.layout == CONV2D_NHWC) != x_nhwc ? d->buf[BUF_XR] : x;
     if (!xin) return CONV2D_E_NO_DATA;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if (d->has_last && s != d->last_stream) CV_HIP(hipStreamWaitEvent(s, d->done, 0));
+    CV_TRY(order_after_last(d, s));
     Ws ws{d};
     ws.cus = d->cus;
     return run_implicit(d, ws, xin, w, nullptr, nullptr, s, false, PROBE_LOADER);
@@ -1383,7 +1397,7 @@ int conv2d_kernel_probe(conv2d_desc* d, const void* x, const void* w, const floa
     void* yout = g.layout == CONV2D_NHWC && !implicit_writes_nhwc(d) ? d->buf[BUF_YR] : y;
     if (!xin || !yout) return CONV2D_E_NO_DATA;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if (d->has_last && s != d->last_stream) CV_HIP(hipStreamWaitEvent(s, d->done, 0));
+    CV_TRY(order_after_last(d, s));
     Ws ws{d};
     ws.cus = d->cus;
     return run_implicit(d, ws, xin, w, bias, yout, s, false, PROBE_KERNEL);

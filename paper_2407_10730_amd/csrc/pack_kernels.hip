@@ -242,30 +242,43 @@ hipError_t launch_unpack(const UnpackArgs& a, int ydt, int groups, hipStream_t s
 // ------------------------------------------------------------------ weight repack
 // w [K][C/g][R*S] -> wr [K][R*S][C/g]: the tap-major order of the implicit GEMM's
 // reduction, so one stage's weights (one tap, consecutive channels) are contiguous.
+// Block (x, k) moves channels [x*cc, x*cc + cc) of filter k: it reads their cc*R*S
+// contiguous elements into LDS (one word each) with consecutive threads on consecutive
+// elements, then writes every tap's run of channels, again consecutive threads on
+// consecutive elements (the LDS reads of one tap are R*S words apart).
 template <typename T>
 __global__ __launch_bounds__(256) void repack_tap_major_kernel(const T* __restrict__ w, T* __restrict__ wr,
-                                                              uint32_t total, uint32_t cg, uint32_t rs) {
-    // 32-bit index arithmetic: the host guarantees total < 2^31
-    const uint32_t o = blockIdx.x * 256u + threadIdx.x;
-    if (o >= total) return;
-    const uint32_t c = o % cg;
-    const uint32_t kt = o / cg;
-    const uint32_t tap = kt % rs;
-    const uint32_t k = kt / rs;
-    wr[o] = w[(k * cg + c) * rs + tap];
+                                                              uint32_t cg, uint32_t rs, uint32_t cc) {
+    extern __shared__ uint32_t rtile[];
+    const uint32_t k = blockIdx.y;
+    const uint32_t c0 = blockIdx.x * cc;
+    const uint32_t nc = min(cc, cg - c0);
+    const uint32_t n = nc * rs;
+    const T* src = w + ((size_t)k * cg + c0) * rs;
+    for (uint32_t i = threadIdx.x; i < n; i += 256) rtile[i] = (uint32_t)src[i];
+    __syncthreads();
+    T* dst = wr + (size_t)k * rs * cg + c0;
+    for (uint32_t i = threadIdx.x; i < n; i += 256) {
+        const uint32_t tap = i / nc;
+        const uint32_t c = i - tap * nc;
+        dst[(size_t)tap * cg + c] = (T)rtile[c * rs + tap];
+    }
 }
 
 hipError_t launch_repack_tap_major(const void* w, void* wr, int64_t k, int64_t cg, int64_t rs, int elem_bytes,
                                    hipStream_t stream) {
     const int64_t total = k * cg * rs;
-    if (total <= 0 || total >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
-    dim3 grid((unsigned)((total + 255) / 256));
+    if (total <= 0 || total >= ((int64_t)1 << 31) || k > 65535 || rs > 4096) return hipErrorInvalidValue;
+    // channels per block: at most 4096 elements (16 KiB of LDS)
+    const int64_t cc = std::max<int64_t>(1, std::min<int64_t>(cg, 4096 / rs));
+    dim3 grid((unsigned)((cg + cc - 1) / cc), (unsigned)k);
+    const size_t lds = (size_t)(cc * rs) * 4;
     if (elem_bytes == 4)
-        hipLaunchKernelGGL(repack_tap_major_kernel<uint32_t>, grid, dim3(256), 0, stream, (const uint32_t*)w,
-                           (uint32_t*)wr, (uint32_t)total, (uint32_t)cg, (uint32_t)rs);
+        hipLaunchKernelGGL(repack_tap_major_kernel<uint32_t>, grid, dim3(256), lds, stream, (const uint32_t*)w,
+                           (uint32_t*)wr, (uint32_t)cg, (uint32_t)rs, (uint32_t)cc);
     else
-        hipLaunchKernelGGL(repack_tap_major_kernel<uint16_t>, grid, dim3(256), 0, stream, (const uint16_t*)w,
-                           (uint16_t*)wr, (uint32_t)total, (uint32_t)cg, (uint32_t)rs);
+        hipLaunchKernelGGL(repack_tap_major_kernel<uint16_t>, grid, dim3(256), lds, stream, (const uint16_t*)w,
+                           (uint16_t*)wr, (uint32_t)cg, (uint32_t)rs, (uint32_t)cc);
     return hipGetLastError();
 }
 
