@@ -19,8 +19,24 @@
 //
 // Usage: convbench --csv OPS.csv --out RESULTS.csv [--datagen random|constant]
 //                  [--exec main|baseline|correctness] [--warmups W] [--runs R]
-//                  [--seed S] [--dry-run]
+//                  [--seed S] [--dry-run] [--dump DIR]
 // --dry-run plans every operation (no GPU needed) and writes the planner's choices.
+// --dump DIR writes, per operation i, the inputs the GPU reads as raw little-endian fp32
+// (DIR/i.x, i.w, i.b; x in the operation's layout, bf16 operations' values after rounding)
+// and, in correctness mode, both results (i.y_main, i.y_base, fp32, in the layout), so that
+// an independent checker can compare them with its own reference.
+//
+// Data: operation i uses seed S + i.  "random" draws x, w and bias from the SplitMix64
+// streams (seed, tensor 0 / 1 / 2): stream start mix64((seed << 8) | tensor), element j =
+// mix64(start + (j + 1) * 0x9E3779B97F4A7C15), value 2 * ((z >> 40) * 2^-24) - 1, exact in
+// fp32 (Steele, Lea and Flood, OOPSLA 2014; Vigna's splitmix64 finaliser); "constant" sets
+// x = 0.5, w = 0.25, bias = 1.
+//
+// Correctness mode runs main and baseline on the same data and reports the largest per-output
+// difference normalised by A_o = |b_k| + sum |x * w| over the window, which the library
+// itself computes as the baseline convolution of |x|, |w| and |b|.  Both results carry their
+// own rounding, so the gate is twice the reference gate: 2e-5 for fp32 inputs, 2e-2 for bf16.
+// A non-finite output, or a difference where A_o = 0, fails the operation.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -138,13 +154,29 @@ float from_bf16(uint16_t h) {
     return f;
 }
 
-// SplitMix64 (Steele, Lea and Flood, OOPSLA 2014): value i of stream `seed`, mapped to [-1, 1).
-float uniform_pm1(uint64_t seed, uint64_t i) {
-    uint64_t z = seed * 0x9E3779B97F4A7C15ull + i + 1;
+// SplitMix64's output finaliser (Vigna, splitmix64.c).
+uint64_t mix64(uint64_t z) {
     z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
     z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
-    z ^= z >> 31;
-    return (float)((double)(z >> 11) * (1.0 / 9007199254740992.0)) * 2.0f - 1.0f;
+    return z ^ (z >> 31);
+}
+
+// Element j of the (seed, tensor) stream mapped to [-1, 1) on a 2^-23 grid.
+struct Stream {
+    uint64_t start;
+    Stream(uint64_t seed, uint64_t tensor) : start(mix64((seed << 8) | tensor)) {}
+    float at(uint64_t j) const {
+        const uint64_t z = mix64(start + (j + 1) * 0x9E3779B97F4A7C15ull);
+        const double u = (double)(z >> 40) * (1.0 / 16777216.0);
+        return (float)(2.0 * u - 1.0);
+    }
+};
+
+bool write_raw(const std::string& path, const void* data, size_t bytes) {
+    FILE* f = std::fopen(path.c_str(), "wb");
+    if (!f) return false;
+    const bool ok = std::fwrite(data, 1, bytes, f) == bytes;
+    return std::fclose(f) == 0 && ok;
 }
 
 struct Result {
@@ -154,7 +186,7 @@ struct Result {
     double phase_ms[CONV2D_PH_COUNT] = {};
     double phase_calls[CONV2D_PH_COUNT] = {};
     double tflops = 0.0;
-    double max_abs_diff = -1.0, rel_diff = -1.0;
+    double max_abs_diff = -1.0, rel_diff = -1.0, err_per_point = -1.0;
     int correct = -1;
     int64_t ho = 0, wo = 0;
     conv2d_plan_info plan{};
@@ -174,11 +206,11 @@ class ConvBench {
     virtual int main_algo() const = 0;
 
     int convset_exec(const std::vector<Op>& ops, const std::string& datagen, const std::string& exec, int warmups,
-                     int runs, uint64_t seed, bool dry, const std::string& out_path);
+                     int runs, uint64_t seed, bool dry, const std::string& out_path, const std::string& dump);
 
    private:
     Result run_one(const Op& op, size_t idx, const std::string& datagen, const std::string& exec, int warmups,
-                   int runs, uint64_t seed, bool dry);
+                   int runs, uint64_t seed, bool dry, const std::string& dump);
 };
 
 class Conv2dBench : public ConvBench {
@@ -198,8 +230,18 @@ const char* algo_name(int a) {
     }
 }
 
+// Device output (fp32 or bf16) as fp32 values; false when the copy fails.
+bool fetch_f32(const void* dev, int64_t n, size_t es, std::vector<float>* out) {
+    out->resize(n);
+    if (es == 4) return hipMemcpy(out->data(), dev, n * 4, hipMemcpyDeviceToHost) == hipSuccess;
+    std::vector<uint16_t> h(n);
+    if (hipMemcpy(h.data(), dev, n * 2, hipMemcpyDeviceToHost) != hipSuccess) return false;
+    for (int64_t i = 0; i < n; ++i) (*out)[i] = from_bf16(h[i]);
+    return true;
+}
+
 Result ConvBench::run_one(const Op& op, size_t idx, const std::string& datagen, const std::string& exec,
-                          int warmups, int runs, uint64_t seed, bool dry) {
+                          int warmups, int runs, uint64_t seed, bool dry, const std::string& dump) {
     Result r;
     conv2d_desc* d = nullptr;
     r.status = conv2d_desc_create(&op.p, &d);
@@ -212,30 +254,49 @@ Result ConvBench::run_one(const Op& op, size_t idx, const std::string& datagen, 
     const int algo = baseline ? CONV2D_ALGO_IM2COL_GEMM : main_algo();
     r.status = conv2d_plan_query(d, algo, &r.plan);
     r.algo = algo_name(r.plan.algo);
-    if (dry || r.status != CONV2D_OK) {
-        conv2d_desc_destroy(d);
-        return r;
-    }
     const conv2d_params& p = op.p;
     const int64_t xe = p.n * p.c * p.h * p.w, we = p.k * (p.c / p.groups) * p.r * p.s;
     const int64_t ye = nkhw[0] * nkhw[1] * nkhw[2] * nkhw[3];
     const size_t es = p.x_dtype == CONV2D_BF16 ? 2 : 4, ys = p.y_dtype == CONV2D_BF16 ? 2 : 4;
-    // host data: x, w, bias (random: U[-1,1) from the op's stream; constant: fixed values)
+    // host data, in the operation's layout: x, w, bias (random: the op's SplitMix64 streams;
+    // constant: fixed values).  The random streams run over x in NCHW order, so an NHWC x holds
+    // the same tensor.  bf16 operations read the values rounded to nearest even.
     std::vector<float> hx(xe), hw(we), hb(p.k);
     const uint64_t s0 = seed + idx;
-    for (int64_t i = 0; i < xe; ++i) hx[i] = datagen == "constant" ? 0.5f : uniform_pm1(3 * s0, i);
-    for (int64_t i = 0; i < we; ++i) hw[i] = datagen == "constant" ? 0.25f : uniform_pm1(3 * s0 + 1, i);
-    for (int64_t i = 0; i < p.k; ++i) hb[i] = datagen == "constant" ? 1.0f : uniform_pm1(3 * s0 + 2, i);
+    const Stream sx(s0, 0), sw(s0, 1), sb(s0, 2);
+    const bool cst = datagen == "constant";
+    const int64_t hw_ = p.h * p.w;
+    for (int64_t i = 0; i < xe; ++i) {
+        // element i in NCHW order lands at its position in the layout
+        int64_t at = i;
+        if (p.layout == CONV2D_NHWC) {
+            const int64_t n = i / (p.c * hw_), rem = i - n * p.c * hw_, c = rem / hw_, q = rem - c * hw_;
+            at = (n * hw_ + q) * p.c + c;
+        }
+        hx[at] = cst ? 0.5f : sx.at((uint64_t)i);
+    }
+    for (int64_t i = 0; i < we; ++i) hw[i] = cst ? 0.25f : sw.at((uint64_t)i);
+    for (int64_t i = 0; i < p.k; ++i) hb[i] = !p.has_bias ? 0.0f : cst ? 1.0f : sb.at((uint64_t)i);
     std::vector<uint16_t> hx16, hw16;
     const void* xsrc = hx.data();
     const void* wsrc = hw.data();
     if (es == 2) {
         hx16.resize(xe);
         hw16.resize(we);
-        for (int64_t i = 0; i < xe; ++i) hx16[i] = to_bf16(hx[i]);
-        for (int64_t i = 0; i < we; ++i) hw16[i] = to_bf16(hw[i]);
+        for (int64_t i = 0; i < xe; ++i) hx[i] = from_bf16(hx16[i] = to_bf16(hx[i]));
+        for (int64_t i = 0; i < we; ++i) hw[i] = from_bf16(hw16[i] = to_bf16(hw[i]));
         xsrc = hx16.data();
         wsrc = hw16.data();
+    }
+    const std::string stem = dump.empty() ? std::string() : dump + "/" + std::to_string(idx);
+    if (!dump.empty() && (!write_raw(stem + ".x", hx.data(), xe * 4) || !write_raw(stem + ".w", hw.data(), we * 4) ||
+                          !write_raw(stem + ".b", hb.data(), p.k * 4))) {
+        std::fprintf(stderr, "convbench: cannot write %s.*\n", stem.c_str());
+        r.status = CONV2D_E_INVALID;
+    }
+    if (dry || r.status != CONV2D_OK) {
+        conv2d_desc_destroy(d);
+        return r;
     }
     void *x = nullptr, *w = nullptr, *b = nullptr, *y = nullptr, *y2 = nullptr;
     hipStream_t s = nullptr;
@@ -264,30 +325,61 @@ Result ConvBench::run_one(const Op& op, size_t idx, const std::string& datagen, 
         return base ? convolution_baseline(d, x, w, bias, out, s) : convolution(d, x, w, bias, out, s);
     };
     if (exec == "correctness") {
-        // main against baseline on the same data
+        // main against baseline on the same data, then A = the baseline convolution of |x|,
+        // |w| and |b| (overwriting the device inputs) as the per-output denominator
+        std::vector<float> ya, yb, aa;
         if ((r.status = call(false, y)) == CONV2D_OK) r.status = call(true, y2);
         if (r.status == CONV2D_OK && hipStreamSynchronize(s) != hipSuccess) r.status = CONV2D_E_HIP;
+        if (r.status == CONV2D_OK && (!fetch_f32(y, ye, ys, &ya) || !fetch_f32(y2, ye, ys, &yb))) r.status = CONV2D_E_HIP;
         if (r.status == CONV2D_OK) {
-            std::vector<uint8_t> a(ye * ys), c(ye * ys);
-            (void)hipMemcpy(a.data(), y, ye * ys, hipMemcpyDeviceToHost);
-            (void)hipMemcpy(c.data(), y2, ye * ys, hipMemcpyDeviceToHost);
-            double md = 0.0, mref = 0.0;
-            for (int64_t i = 0; i < ye; ++i) {
-                float va, vc;
-                if (ys == 2) {
-                    va = from_bf16(reinterpret_cast<uint16_t*>(a.data())[i]);
-                    vc = from_bf16(reinterpret_cast<uint16_t*>(c.data())[i]);
-                } else {
-                    va = reinterpret_cast<float*>(a.data())[i];
-                    vc = reinterpret_cast<float*>(c.data())[i];
-                }
-                md = std::fmax(md, std::fabs((double)va - vc));
-                mref = std::fmax(mref, std::fabs((double)vc));
+            std::vector<float> ax(xe), aw(we), ab(p.k);
+            for (int64_t i = 0; i < xe; ++i) ax[i] = std::fabs(hx[i]);
+            for (int64_t i = 0; i < we; ++i) aw[i] = std::fabs(hw[i]);
+            for (int64_t i = 0; i < p.k; ++i) ab[i] = std::fabs(hb[i]);
+            std::vector<uint16_t> ax16, aw16;
+            const void* axs = ax.data();
+            const void* aws = aw.data();
+            if (es == 2) {
+                ax16.resize(xe);
+                aw16.resize(we);
+                for (int64_t i = 0; i < xe; ++i) ax16[i] = to_bf16(ax[i]);  // exact: |bf16| is a bf16
+                for (int64_t i = 0; i < we; ++i) aw16[i] = to_bf16(aw[i]);
+                axs = ax16.data();
+                aws = aw16.data();
             }
-            r.max_abs_diff = md;
-            r.rel_diff = mref > 0 ? md / mref : md;
-            // both run in fp32 accumulation; bf16 outputs differ by their rounding
-            r.correct = r.rel_diff <= (ys == 2 ? 2e-2 : 1e-4) ? 1 : 0;
+            if (hipMemcpy(x, axs, xe * es, hipMemcpyHostToDevice) != hipSuccess ||
+                hipMemcpy(w, aws, we * es, hipMemcpyHostToDevice) != hipSuccess ||
+                hipMemcpy(b, ab.data(), p.k * 4, hipMemcpyHostToDevice) != hipSuccess)
+                r.status = CONV2D_E_HIP;
+            if (r.status == CONV2D_OK) r.status = call(true, y2);
+            if (r.status == CONV2D_OK && (hipStreamSynchronize(s) != hipSuccess || !fetch_f32(y2, ye, ys, &aa)))
+                r.status = CONV2D_E_HIP;
+        }
+        if (r.status == CONV2D_OK) {
+            double md = 0.0, mref = 0.0, pt = 0.0;
+            bool finite = true;
+            for (int64_t i = 0; i < ye; ++i) {
+                const double va = ya[i], vb = yb[i], a = aa[i];
+                if (!std::isfinite(va) || !std::isfinite(vb) || !std::isfinite(a)) {
+                    finite = false;
+                    break;
+                }
+                const double e = std::fabs(va - vb);
+                md = std::max(md, e);
+                mref = std::max(mref, std::fabs(vb));
+                if (a > 0) pt = std::max(pt, e / a);
+                else if (e != 0) pt = HUGE_VAL;
+            }
+            r.max_abs_diff = finite ? md : NAN;
+            r.rel_diff = finite ? (mref > 0 ? md / mref : md) : NAN;
+            r.err_per_point = finite ? pt : NAN;
+            const double gate = p.x_dtype == CONV2D_BF16 ? 2e-2 : 2e-5;
+            r.correct = finite && pt <= gate ? 1 : 0;
+            if (!dump.empty() && (!write_raw(stem + ".y_main", ya.data(), ye * 4) ||
+                                  !write_raw(stem + ".y_base", yb.data(), ye * 4))) {
+                std::fprintf(stderr, "convbench: cannot write %s.y_*\n", stem.c_str());
+                r.correct = 0;
+            }
         }
         cleanup();
         return r;
@@ -322,7 +414,8 @@ Result ConvBench::run_one(const Op& op, size_t idx, const std::string& datagen, 
 }
 
 int ConvBench::convset_exec(const std::vector<Op>& ops, const std::string& datagen, const std::string& exec,
-                            int warmups, int runs, uint64_t seed, bool dry, const std::string& out_path) {
+                            int warmups, int runs, uint64_t seed, bool dry, const std::string& out_path,
+                            const std::string& dump) {
     std::ofstream out(out_path);
     if (!out) {
         std::fprintf(stderr, "convbench: cannot write %s\n", out_path.c_str());
@@ -332,11 +425,11 @@ int ConvBench::convset_exec(const std::vector<Op>& ops, const std::string& datag
            "datagen,algo,kernel,tile_m,tile_n,status,warmups,runs,op_ms,tflops";
     for (const char* ph : kPhaseNames) out << "," << ph << "_ms";
     for (const char* ph : kPhaseNames) out << "," << ph << "_calls";
-    out << ",max_abs_diff,rel_diff,correct\n";
+    out << ",max_abs_diff,rel_diff,err_per_point,correct\n";
     int failures = 0;
     for (size_t i = 0; i < ops.size(); ++i) {
         const Op& op = ops[i];
-        const Result r = run_one(op, i, datagen, exec, warmups, runs, seed, dry);
+        const Result r = run_one(op, i, datagen, exec, warmups, runs, seed, dry, dump);
         const conv2d_params& p = op.p;
         if (r.status != CONV2D_OK || r.correct == 0) ++failures;
         char buf[1024];
@@ -352,7 +445,7 @@ int ConvBench::convset_exec(const std::vector<Op>& ops, const std::string& datag
         out << buf;
         for (int ph = 0; ph < CONV2D_PH_COUNT; ++ph) out << "," << r.phase_ms[ph];
         for (int ph = 0; ph < CONV2D_PH_COUNT; ++ph) out << "," << r.phase_calls[ph];
-        out << "," << r.max_abs_diff << "," << r.rel_diff << "," << r.correct << "\n";
+        out << "," << r.max_abs_diff << "," << r.rel_diff << "," << r.err_per_point << "," << r.correct << "\n";
         out.flush();
         std::fprintf(stderr, "[convbench] %zu/%zu %s %s %s %.4f ms%s\n", i + 1, ops.size(), op.name.c_str(),
                      exec.c_str(), conv2d_status_string(r.status), r.op_ms,
@@ -365,14 +458,14 @@ int usage() {
     std::fprintf(stderr,
                  "usage: convbench --csv OPS.csv --out RESULTS.csv [--datagen random|constant]\n"
                  "                 [--exec main|baseline|correctness] [--warmups W] [--runs R] [--seed S]\n"
-                 "                 [--dry-run]\n");
+                 "                 [--dry-run] [--dump DIR]\n");
     return 2;
 }
 
 }  // namespace
 
 int main(int argc, char** argv) {
-    std::string csv, out, datagen = "random", exec = "main";
+    std::string csv, out, datagen = "random", exec = "main", dump;
     int warmups = 10, runs = 100;
     uint64_t seed = 1000;
     bool dry = false;
@@ -387,6 +480,7 @@ int main(int argc, char** argv) {
         else if (a == "--runs") runs = std::atoi(val().c_str());
         else if (a == "--seed") seed = std::strtoull(val().c_str(), nullptr, 10);
         else if (a == "--dry-run") dry = true;
+        else if (a == "--dump") dump = val();
         else return usage();
     }
     if (csv.empty() || out.empty() || (datagen != "random" && datagen != "constant") ||
@@ -399,5 +493,5 @@ int main(int argc, char** argv) {
         return 2;
     }
     Conv2dBench bench;
-    return bench.convset_exec(ops, datagen, exec, warmups, runs, seed, dry, out);
+    return bench.convset_exec(ops, datagen, exec, warmups, runs, seed, dry, out, dump);
 }

@@ -71,6 +71,47 @@ def test_harness_dry_run_plans_every_op(tmp_path):
             assert (int(x["tile_m"]), int(x["tile_n"])) == (plan.tile_m, plan.tile_n)
 
 
+# (name, n, c, h, w, k, r, s, stride, pad, dil, groups, bias, dtype, layout)
+DATA_OPS = [
+    ("f32", 2, 5, 7, 6, 4, 3, 3, 1, 1, 1, 1, 1, "f32", "nchw"),
+    ("bf16_nhwc", 1, 8, 5, 9, 6, 3, 1, 2, 1, 1, 2, 1, "bf16", "nhwc"),
+    ("nobias", 3, 4, 4, 4, 3, 1, 1, 1, 0, 1, 1, 0, "f32", "nhwc"),
+]
+
+
+def _ops_file(path, ops):
+    with open(path, "w") as f:
+        f.write(",".join(R.COLUMNS) + "\n")
+        for name, n, c, h, w, k, r, s, st, pd, dl, g, b, dt, lay in ops:
+            f.write(f"{name},{n},{c},{h},{w},{k},{r},{s},{st},{st},{pd},{pd},{dl},{dl},{g},{b},{dt},{lay}\n")
+
+
+@pytest.mark.parametrize("mode", ["random", "constant"])
+def test_harness_data_is_the_datagen_streams(tmp_path, mode):
+    """The harness draws operation i's data from the same SplitMix64 streams as datagen (seed
+    S + i, tensors x / w / bias), bit for bit, rounds bf16 operations' values the same way, and
+    lays x out in the operation's layout; the dump holds exactly what the GPU reads."""
+    import numpy as np
+    ops = tmp_path / "ops.csv"
+    _ops_file(ops, DATA_OPS)
+    dump = tmp_path / "dump"
+    dump.mkdir()
+    r = subprocess.run([HARNESS, "--csv", str(ops), "--out", str(tmp_path / "o.csv"), "--dry-run", "--seed", "4242",
+                        "--datagen", mode, "--dump", str(dump)], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0, r.stderr
+    for i, (name, n, c, h, w, k, rr, ss, st, pd, dl, g, b, dt, lay) in enumerate(DATA_OPS):
+        cs = datagen.ConvShape(n=n, c=c, h=h, w=w, k=k, r=rr, s=ss, stride=(st, st), pad=(pd, pd), dil=(dl, dl),
+                               groups=g, has_bias=bool(b), x_dtype=dt, y_dtype=dt, seed=4242 + i)
+        x, wt, bias = datagen.make_inputs(cs, mode, const=(0.5, 0.25, 1.0))
+        hx = np.fromfile(dump / f"{i}.x", dtype=np.float32)
+        if lay == "nhwc":
+            hx = hx.reshape(n, h, w, c).transpose(0, 3, 1, 2)
+        assert np.array_equal(hx.reshape(x.shape).view(np.uint32), x.view(np.uint32)), name
+        assert np.array_equal(np.fromfile(dump / f"{i}.w", dtype=np.float32).reshape(wt.shape).view(np.uint32),
+                              wt.view(np.uint32)), name
+        assert np.array_equal(np.fromfile(dump / f"{i}.b", dtype=np.float32).view(np.uint32), bias.view(np.uint32)), name
+
+
 def test_harness_rejects_bad_input(tmp_path):
     bad = tmp_path / "bad.csv"
     bad.write_text("name,n,c\nx,1,2\n")

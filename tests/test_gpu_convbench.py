@@ -1,11 +1,14 @@
 """The ConvBench-style harness on the GPU: main, baseline and the correctness check of
-main against baseline over a small operation list, and the speedup report on the results."""
+main against baseline over a small operation list, both results checked against the
+oracle through the harness's dumps, and the speedup report on the results."""
 import csv
 import os
 import subprocess
 
+import numpy as np
 import pytest
 
+import oracle
 from paper_2407_10730_amd import binding as B
 from paper_2407_10730_amd import convbench_report as R
 
@@ -43,13 +46,43 @@ def _run(ops, out, *args):
         return r, list(csv.DictReader(f))
 
 
-def test_correctness_main_against_baseline(ops_csv, tmp_path):
+GATE = {"f32": 1e-5, "bf16": 1e-2}
+
+
+def test_correctness_main_against_baseline_and_oracle(ops_csv, tmp_path):
+    """Correctness mode passes its own main-against-baseline gate, and both of its results, read
+    back from the dump with the inputs the GPU read, pass the oracle's per-output gate; the
+    harness's per-point error agrees with the one the oracle's denominator gives."""
     for datagen in ("random", "constant"):
-        r, rows = _run(ops_csv, tmp_path / "c.csv", "--exec", "correctness", "--datagen", datagen)
+        dump = tmp_path / f"dump_{datagen}"
+        dump.mkdir()
+        r, rows = _run(ops_csv, tmp_path / "c.csv", "--exec", "correctness", "--datagen", datagen,
+                       "--dump", str(dump))
         assert r.returncode == 0, r.stderr
         assert [x["name"] for x in rows] == [o[0] for o in OPS]
-        for x in rows:
+        for i, (x, op) in enumerate(zip(rows, OPS)):
             assert x["status"] == "ok" and x["correct"] == "1", x
+            name, n, c, h, w, k, rr, ss, st, pd, dl, g, b, dt, lay = op
+            ho, wo = int(x["ho"]), int(x["wo"])
+            hx = np.fromfile(dump / f"{i}.x", dtype=np.float32)
+            hx = hx.reshape(n, h, w, c).transpose(0, 3, 1, 2) if lay == "nhwc" else hx.reshape(n, c, h, w)
+            hw = np.fromfile(dump / f"{i}.w", dtype=np.float32).reshape(k, c // g, rr, ss)
+            hb = np.fromfile(dump / f"{i}.b", dtype=np.float32)
+            y_ref, a_ref = oracle.conv2d(hx, hw, hb if b else None, (st, st), (pd, pd), (dl, dl), g)
+            ys = {}
+            for which in ("y_main", "y_base"):
+                y = np.fromfile(dump / f"{i}.{which}", dtype=np.float32)
+                y = y.reshape(n, ho, wo, k).transpose(0, 3, 1, 2) if lay == "nhwc" else y.reshape(n, k, ho, wo)
+                _, pt = oracle.normalised_errors(y, y_ref, a_ref)
+                assert pt <= max(GATE[dt], 2.0 ** -8 if dt == "bf16" else 0), (name, datagen, which, pt)
+                ys[which] = y.astype(np.float64)
+            e = np.abs(ys["y_main"] - ys["y_base"])
+            pos = a_ref > 0
+            pt_py = float((e[pos] / a_ref[pos]).max()) if pos.any() else 0.0
+            pt_cb = float(x["err_per_point"])
+            # the harness's denominator is the library's own |x|*|w| convolution (rounded to the
+            # output type), so the two readings agree up to that rounding
+            assert pt_cb <= pt_py * 1.02 + 1e-12 and pt_py <= pt_cb * 1.02 + 1e-12, (name, pt_cb, pt_py)
 
 
 def test_main_and_baseline_timings_and_speedup(ops_csv, tmp_path):
