@@ -217,7 +217,8 @@ struct conv2d_desc {
     bool implicit_slice = false;  // sliced direct MFMA kernel instead of the GEMM
     bool implicit_nhwc = false;   // bf16 GEMM gathering from an NHWC copy of x (16-byte loads)
     GemmPlan implicit;
-    SlicePlan slice{};
+    SlicePlan slice{};    // the sliced kernel's plan (packed rows where they apply)
+    SlicePlan slice_u{};  // one word per element: the fallback when x is not 4-byte aligned
     ExplicitPlan expl;
     std::vector<KTabEntry> ktab_host;
 
@@ -658,10 +659,17 @@ struct Ws {
     } while (0)
 
 // ------------------------------------------------------------------ algorithms (NCHW tensors)
-int run_slice(conv2d_desc* d, const Ws& ws, const void* x, const void* w, const float* bias, void* y, hipStream_t s,
-              bool ph, bool probe) {
+// The sliced kernel's plan for this x: the packed rows copy input pairs with 4-byte loads, so
+// an x that is not 4-byte aligned takes the element-wise layout, or (when that does not fit
+// LDS) no sliced plan at all (nullptr: the tiled GEMM runs instead).
+const SlicePlan* slice_for(const conv2d_desc* d, const void* x) {
+    if (!d->slice.pk || ((uintptr_t)x & 3u) == 0) return &d->slice;
+    return d->slice_u.ok ? &d->slice_u : nullptr;
+}
+
+int run_slice(conv2d_desc* d, const SlicePlan& sp, const Ws& ws, const void* x, const void* w, const float* bias,
+              void* y, hipStream_t s, bool ph, bool probe) {
     const Geometry& g = d->g;
-    const SlicePlan& sp = d->slice;
     SliceArgs a{};
     a.x = x;
     a.x_bytes = (uint32_t)(g.x_elems * elem_size(g.xdt));
@@ -684,11 +692,34 @@ int run_slice(conv2d_desc* d, const Ws& ws, const void* x, const void* w, const 
     a.tiles_total = (int32_t)(g.G * a.grid_m * g.N * a.tiles_px);
     const int per_cu = std::max(1, std::min(16 / sp.nw, (int)((160 << 10) / sp.lds_bytes)));
     a.nblocks = std::min(a.tiles_total, ws.cus * per_cu);
+    // Persistent blocks take whole rounds of tiles; a last, partial round would leave most
+    // blocks idle while a few compute whole tiles (cfg4: 1568 tiles on 512 blocks, 3.06
+    // rounds run as 4), so its tiles are split by wave groups over the idle blocks.
+    a.tail_start = a.tiles_total;
+    a.tail_q = 0;
+    {
+        const int nb = a.nblocks, full = a.tiles_total / nb, rem = a.tiles_total % nb;
+        int q = 1;
+        while (q * 2 <= sp.nw && rem * q * 2 <= nb) q *= 2;
+        if (full >= 1 && rem > 0 && q >= 2) {
+            a.tail_start = full * nb;
+            a.tail_q = q;
+        }
+    }
     a.lds_k_off = sp.lds_k_off;
     a.lds_x_off = sp.lds_x_off;
     a.lds_bytes = sp.lds_bytes;
     a.loader_only = probe ? 1 : 0;
     a.y_nhwc = g.layout == CONV2D_NHWC ? 1 : 0;
+    a.pk = sp.pk ? 1 : 0;
+    a.pk_shift = sp.pk_shift;
+    a.nbuf = sp.nbuf;
+    a.xwords = sp.xwords;
+    a.fd_pergz = make_fastdiv((uint32_t)(a.N * a.tiles_px));
+    a.fd_tpx = make_fastdiv((uint32_t)a.tiles_px);
+    a.fd_gm = make_fastdiv((uint32_t)a.grid_m);
+    a.fd_wo = make_fastdiv((uint32_t)a.Wo);
+    a.fd_kw = make_fastdiv((uint32_t)(2 * a.kh));
     Scope sc(d, CONV2D_ALGO_IMPLICIT_GEMM, CONV2D_PH_IN_MICROKERNEL, s, ph);
     CV_TRY(sc.begin());
     CV_HIP(launch_slice(a, g.xdt, g.ydt, sp.nw, s));
@@ -710,7 +741,12 @@ int run_implicit(conv2d_desc* d, Ws& ws, const void* x, const void* w, const flo
                  bool ph, int probe = PROBE_NONE) {
     const Geometry& g = d->g;
     const GemmPlan& gp = d->implicit;
-    if (d->implicit_slice) return run_slice(d, ws, x, w, bias, y, s, ph, probe == PROBE_LOADER);
+    if (d->implicit_slice) {
+        const SlicePlan* sp = slice_for(d, x);
+        if (sp) return run_slice(d, *sp, ws, x, w, bias, y, s, ph, probe == PROBE_LOADER);
+        // misaligned x without an element-wise plan: the tiled GEMM below, with its NCHW gathers
+        if (d->implicit_nhwc) return CONV2D_E_UNSUPPORTED;
+    }
     if ((d->implicit_tap || d->implicit_nhwc) && g.R * g.S > 1 && probe) {
         if (!d->buf[BUF_WR]) return CONV2D_E_NO_DATA;
         w = d->buf[BUF_WR];
@@ -1238,7 +1274,9 @@ int conv2d_desc_create(const conv2d_params* params, conv2d_desc** out) {
         int nw = g.Ho * g.Wo <= 128 ? 4 : 8;
         const int64_t force_nw = env_int64("CONV2D_SLICE_WAVES", 0);
         if (force_nw == 4 || force_nw == 8) nw = (int)force_nw;
-        d->slice = slice_plan(g.Cg, g.R, g.S, g.Ho, g.Wo, g.sh, g.sw, g.dh, g.dw, g.xdt, nw);
+        d->slice = slice_plan(g.Cg, g.R, g.S, g.Ho, g.Wo, g.sh, g.sw, g.dh, g.dw, g.xdt, nw, g.W, g.pw,
+                              !std::getenv("CONV2D_SLICE_UNPACKED"));
+        d->slice_u = slice_plan(g.Cg, g.R, g.S, g.Ho, g.Wo, g.sh, g.sw, g.dh, g.dw, g.xdt, nw);
     }
     // The sliced kernel replaces the table-driven gather (C/g not a multiple of the stage
     // depth) when its LDS footprint fits; CONV2D_SLICE=0 / 1 forces the choice for tests.

@@ -183,6 +183,19 @@ hipError_t launch_dw_nhwc(const DirectArgs& a, const void* wt, int xdt, int ydt,
 // Blocks the grouped direct kernel launches for this shape (0: it does not take the shape).
 int64_t grouped_blocks(const DirectArgs& a);
 
+// Division by a runtime divisor d >= 1 through a multiplier and a shift (round-up method of
+// Granlund and Montgomery): n / d = (umulhi(n, m) + n) >> s for 0 <= n < 2^31, with
+// s = ceil(log2 d) and m = floor(2^32 (2^s - d) / d) + 1.
+struct FastDiv {
+    uint32_t m, s;
+};
+inline FastDiv make_fastdiv(uint32_t d) {
+    uint32_t s = 0;
+    while ((1ull << s) < d) ++s;
+    const uint64_t m = ((1ull << 32) * ((1ull << s) - d)) / d + 1;
+    return FastDiv{(uint32_t)m, s};
+}
+
 // Sliced direct convolution on MFMA (small C/g * R * S): per block the filters of 64 output
 // channels, the input rows of 256 consecutive output pixels of one image and a table of the
 // slice offset of every reduction index sit in LDS (weights at byte 0, then the table at
@@ -207,14 +220,34 @@ struct SliceArgs {
     int32_t lds_k_off, lds_x_off, lds_bytes;
     int32_t loader_only;  // pack probe: slice copies and filter loads only, no MFMA, no output
     int32_t y_nhwc;       // 1: y is NHWC (x stays NCHW)
+    // Last-round split: tiles [tail_start, tiles_total) (fewer than nblocks) are each computed
+    // by tail_q blocks (a power of two dividing the waves per block), piece j of a tile by
+    // the waves [j*nw/tail_q, (j+1)*nw/tail_q); block b takes piece b % tail_q of tile
+    // tail_start + b / tail_q.  The tiles before tail_start are whole rounds of nblocks.
+    // tail_q 0: no split (tail_start = tiles_total).
+    int32_t tail_start, tail_q;
+    // packed rows (bf16, column dilation 1, S <= 8, W even, x 4-byte aligned): the slice holds
+    // bf16 pairs (input columns wi, wi + 1 with wi even) at column j = wi + pw + pk_shift,
+    // pk_shift = pw % 2; the reduction runs over filter rows (c, r) padded to 8 taps, two rows
+    // per MFMA step (kh = 8 * steps per lane half).
+    int32_t pk, pk_shift;
+    // slice buffers (1 or 2; with 2 the next tile's copy overlaps this tile's MFMAs), words each
+    int32_t nbuf, xwords;
+    // divisions of the tile and pixel decode and the filter load: by N*tiles_px, tiles_px,
+    // grid_m, Wo and the filter row length 2*kh
+    FastDiv fd_pergz, fd_tpx, fd_gm, fd_wo, fd_kw;
 };
 struct SlicePlan {
     bool ok;
+    bool pk;              // packed-row bf16 layout (SliceArgs::pk)
     int32_t nw;           // waves per block (tile = 32*nw pixels)
     int32_t kh, ph_max, pwp, lds_k_off, lds_x_off, lds_bytes;
+    int32_t pk_shift;
+    int32_t nbuf, xwords;  // slice buffers and their size in 4-byte words
 };
+// pk: try the packed-row bf16 layout (falls back to one word per element when it does not apply)
 SlicePlan slice_plan(int64_t Cg, int64_t R, int64_t S, int64_t Ho, int64_t Wo, int sh, int sw, int dh, int dw,
-                     int xdt, int nw);
+                     int xdt, int nw, int64_t W = 0, int pw = 0, bool pk = false);
 hipError_t launch_slice(const SliceArgs& a, int xdt, int ydt, int nw, hipStream_t stream);
 
 // weight repack to tap-major order: w [K][C/g][R*S] -> wr [K][R*S][C/g].

@@ -72,6 +72,33 @@ __device__ __forceinline__ void store_out4<uint16_t>(__amdgpu_buffer_rsrc_t r, u
         r, ok ? e * 2u : OOB_OFF, 0, 0);
 }
 
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// Two consecutive output elements starting at element e (e even): one 8-byte (fp32) or
+// 4-byte (bf16: the hardware's packed conversion, round to nearest even) store.
+template <typename TOut>
+__device__ __forceinline__ void store_out2(__amdgpu_buffer_rsrc_t r, uint32_t e, bool ok, float lo, float hi);
+template <>
+__device__ __forceinline__ void store_out2<float>(__amdgpu_buffer_rsrc_t r, uint32_t e, bool ok, float lo, float hi) {
+    __builtin_amdgcn_raw_buffer_store_b64(u32x2{__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)}, r,
+                                          ok ? e * 4u : OOB_OFF, 0, 0);
+}
+template <>
+__device__ __forceinline__ void store_out2<uint16_t>(__amdgpu_buffer_rsrc_t r, uint32_t e, bool ok, float lo,
+                                                     float hi) {
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2)),
+                                          r, ok ? e * 2u : OOB_OFF, 0, 0);
+}
+
+// The value of lane l ^ 1 (a DPP quad permutation, no LDS).
+__device__ __forceinline__ float swap_adjacent_lanes(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
+}
+
+// n / d for 0 <= n < 2^31 with the divisor's multiplier and shift (FastDiv).
+__device__ __forceinline__ uint32_t fdiv(uint32_t n, FastDiv f) { return (__umulhi(n, f.m) + n) >> f.s; }
+
 // Linear block id -> tile id such that consecutive tile ids land on the same
 // XCD (workgroups are handed to the 8 XCDs round-robin), so the M tiles of one
 // pixel tile and neighbouring pixel tiles share an L2.

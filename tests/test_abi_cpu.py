@@ -141,7 +141,14 @@ def test_implicit_microkernel_choice(monkeypatch):
             B.conv2d_desc_destroy(d)
     monkeypatch.delenv("CONV2D_SLICE", raising=False)
     assert kernel(datagen.CONFIGS["cfg4"]) == (B.CONV2D_KERNEL_SLICE, 152)       # 147 -> 2 x 76
+    # bf16 packed rows: 3 x 7 filter rows padded to 8 taps, 22 rows (two per MFMA step) = 176
+    assert kernel(datagen.CONFIGS["cfg4_bf16"]) == (B.CONV2D_KERNEL_SLICE, 176)
+    monkeypatch.setenv("CONV2D_SLICE_UNPACKED", "1")
     assert kernel(datagen.CONFIGS["cfg4_bf16"]) == (B.CONV2D_KERNEL_SLICE, 160)  # 147 -> 2 x 80
+    assert kernel(datagen.CONFIGS["cfg4_bf16"].with_(w=223))[1] == 160          # odd W: element-wise
+    monkeypatch.delenv("CONV2D_SLICE_UNPACKED")
+    assert kernel(datagen.CONFIGS["cfg4_bf16"].with_(w=223))[1] == 160
+    assert kernel(datagen.CONFIGS["cfg4_bf16"].with_(dil=(1, 2)))[1] == 160      # column dilation
     assert kernel(datagen.CONFIGS["cfg1"])[0] == B.CONV2D_KERNEL_SLICE
     assert kernel(datagen.CONFIGS["cfg2"])[0] == B.CONV2D_KERNEL_GEMM
     big = datagen.CONFIGS["cfg4"].with_(c=48)                                    # 2352-long reduction

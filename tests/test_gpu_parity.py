@@ -13,7 +13,7 @@ import pytest
 import datagen
 import oracle
 from paper_2407_10730_amd import binding as B
-from paper_2407_10730_amd.runner import DeviceConv
+from paper_2407_10730_amd.runner import DeviceConv, params_for
 
 pytestmark = pytest.mark.gpu
 
@@ -381,6 +381,88 @@ def test_descriptor_shared_across_streams():
         assert not bad, f"calls {bad} differ from the single-stream result"
     finally:
         dc.close()
+
+
+# the sliced kernel's last-round split: more tiles than persistent blocks, the tiles past the
+# last whole round computed by 4 or 8 blocks each (wave groups of the tile)
+SLICE_TAIL = [
+    datagen.ConvShape(n=12, c=3, h=224, w=224, k=64, r=7, s=7, stride=(2, 2), pad=(3, 3), seed=340),   # 588 tiles
+    datagen.ConvShape(n=11, c=3, h=224, w=224, k=96, r=7, s=7, stride=(2, 2), pad=(3, 3), seed=341),   # 1078 tiles
+]
+
+
+@pytest.mark.parametrize("dt", [("f32", "f32", "nchw"), ("bf16", "bf16", "nchw"), ("f32", "f32", "nhwc")],
+                         ids=lambda d: "-".join(d))
+@pytest.mark.parametrize("idx", range(len(SLICE_TAIL)))
+def test_slice_last_round_split(idx, dt):
+    cs = SLICE_TAIL[idx].with_(x_dtype=dt[0], y_dtype=dt[1], layout=dt[2])
+    _check(cs, IMPLICIT, "random", kernel="1", waves="8")
+    _check(cs, IMPLICIT, "integer", kernel="1", waves="8")
+
+
+# the sliced kernel's packed-row bf16 layout: input pairs per LDS word, filter rows padded to 8
+# taps; odd and even padding (slice shift 1 / 0), strides 1 and 2 (window starts of both
+# parities), 1 to 8 taps per row, row dilation, rectangular filters, two channel tiles, groups
+PACKED = [
+    _shape(2, 3, 17, 20, 40, 3, 3, pd=(1, 1), seed=360),
+    _shape(1, 5, 16, 30, 70, 5, 5, st=(2, 2), pd=(2, 2), seed=361),
+    _shape(2, 2, 21, 24, 16, 7, 7, st=(2, 2), pd=(3, 3), seed=362),
+    _shape(1, 4, 12, 14, 33, 8, 8, seed=363),
+    _shape(1, 3, 9, 10, 20, 1, 1, seed=364),
+    _shape(2, 6, 15, 18, 24, 3, 2, st=(2, 1), pd=(2, 1), dl=(2, 1), seed=365),
+    _shape(1, 8, 13, 16, 48, 3, 3, st=(1, 2), pd=(1, 1), g=2, seed=366),
+    _shape(3, 1, 40, 46, 96, 7, 5, st=(2, 3), pd=(3, 2), seed=367),
+]
+
+
+@pytest.mark.parametrize("mode", ["random", "integer"])
+@pytest.mark.parametrize("ydt", ["bf16", "f32"])
+@pytest.mark.parametrize("idx", range(len(PACKED)))
+def test_slice_packed_rows(idx, ydt, mode):
+    cs = PACKED[idx].with_(x_dtype="bf16", y_dtype=ydt)
+    with _Kernel("1", "8"):
+        d = B.conv2d_desc_create(params_for(cs))
+        try:
+            plan = B.conv2d_plan_query(d, IMPLICIT)
+        finally:
+            B.conv2d_desc_destroy(d)
+    rows = (cs.c // cs.groups) * cs.r
+    assert plan.kernel == B.CONV2D_KERNEL_SLICE and plan.kred_pad == 16 * ((rows + 1) // 2)
+    _check(cs, IMPLICIT, mode, kernel="1", waves="8")
+
+
+@pytest.mark.parametrize("idx", [2, 1], ids=["elementwise-slice", "gemm"])
+def test_slice_packed_rows_unaligned_input(idx):
+    """An x that starts 2 bytes past a 4-byte boundary takes the element-wise slice layout (or,
+    when only the packed layout fits LDS, the tiled GEMM) and gives a result on the oracle's
+    gate, equal to the aligned one when the element-wise slice runs."""
+    import torch
+    cs = PACKED[idx].with_(x_dtype="bf16", y_dtype="bf16")
+    x, w, b = datagen.make_inputs(cs, "random")
+    dev = torch.device("cuda:0")
+    xb = torch.from_numpy(x).to(dev).to(torch.bfloat16)
+    store = torch.empty(x.size + 1, dtype=torch.bfloat16, device=dev)
+    xo = store[1:].view(x.shape)
+    xo.copy_(xb)
+    wb = torch.from_numpy(w).to(dev).to(torch.bfloat16)
+    bb = torch.from_numpy(b).to(dev)
+    assert xo.data_ptr() % 4 == 2
+    outs = []
+    with _Kernel("1", "8"):
+        for xx in (xb, xo):
+            dc = DeviceConv(cs, device_inputs=(xx, wb, bb))
+            try:
+                dc.run(IMPLICIT)
+                torch.cuda.synchronize()
+                outs.append(dc.y.clone())
+            finally:
+                dc.close()
+    if idx == 2:
+        assert torch.equal(outs[0], outs[1])
+    y_ref, a_ref = oracle.conv2d(x, w, b, cs.stride, cs.pad, cs.dil, cs.groups)
+    for y in outs:
+        _, pt = oracle.normalised_errors(y.float().cpu().numpy().astype(np.float64), y_ref, a_ref)
+        assert pt <= 2.0 ** -8
 
 
 # grouped layers on the direct kernel (C/g > 1 or K/g > 1): per-group output channel chunks
