@@ -497,7 +497,8 @@ def run_sweep(report_path, B, torch):
     return out
 
 
-PER_CONFIG = ["cfg1", "cfg2", "cfg3a", "cfg3b", "cfg4", "cfg4_bf16", "dw", "grp_g64", "grp_g32", "bf16_3x3"]
+PER_CONFIG = ["cfg1", "cfg2", "cfg3a", "cfg3b", "cfg4", "cfg4_bf16", "dw", "dw_bf16", "grp_g64", "grp_g32",
+              "bf16_3x3"]
 # the oracle evaluated on every output (the other rows: sampled outputs), and single-threaded
 ORACLE_FULL = {"cfg1", "cfg2", "cfg3a", "cfg3b", "cfg4", "cfg4_bf16"}
 ORACLE_SINGLE_THREAD = {"cfg1", "cfg2"}

@@ -205,6 +205,8 @@ CONFIGS = {
                       pad=(3, 3), seed=5, x_dtype="bf16", y_dtype="bf16"),
     # a depthwise layer of the sweep's kind (g = C = K), memory bound
     "dw": _cfg("dw", n=32, c=256, h=56, w=56, k=256, r=3, s=3, pad=(1, 1), groups=256, seed=6),
+    "dw_bf16": _cfg("dw_bf16", n=32, c=256, h=56, w=56, k=256, r=3, s=3, pad=(1, 1), groups=256, seed=6,
+                    x_dtype="bf16", y_dtype="bf16"),
     # grouped layers with 1 < g < C (4 and 8 channels per group), memory bound
     "grp_g64": _cfg("grp_g64", n=32, c=256, h=56, w=56, k=256, r=3, s=3, pad=(1, 1), groups=64, seed=7),
     "grp_g32": _cfg("grp_g32", n=32, c=256, h=56, w=56, k=256, r=3, s=3, pad=(1, 1), groups=32, seed=8),

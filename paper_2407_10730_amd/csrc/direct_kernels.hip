@@ -638,6 +638,268 @@ static int direct_rows(const DirectArgs& a, int* in_rows, int* in_cols) {
     return rows;
 }
 
+// ------------------------------------------------------------------ grouped, row strips
+// Grouped layers with square filters, equal strides of 1 or 2 and no dilation: each thread
+// owns a strip of GS_HC consecutive outputs of one row for KG output channels of its group.
+// Per input channel and filter row it reads the RB input values under the strip once and
+// uses every one for all the taps and pixels that need it, and it reads the KG weights of a
+// tap with one broadcast, so a 3x3 stride-1 strip does 48 FMAs per 9 LDS reads (the
+// per-pixel kernel above: 8 per 3).  A block holds GB groups x TR output rows x all column
+// strips (one item per thread) and stages their input windows (16-byte loads when the row
+// length allows) and filters; a group with more channels than fit is staged in chunks.
+constexpr int GS_HC = 4;       // outputs per strip
+constexpr int GS_XF = 8192;    // LDS floats for the windows (32 KiB)
+constexpr int GS_WF = 2048;    // LDS floats for the filters
+
+struct GsPlan {
+    int32_t TR, GB, CC, IR, LDW, LPAD, ncb, nbands, kchunks, xfloats, lds_bytes;
+};
+
+template <int R, int ST, int KG, typename TX, typename TY>
+__global__ __launch_bounds__(DIRECT_THREADS) void grouped_strip_kernel(DirectArgs A, GsPlan P) {
+    constexpr int S = R;
+    constexpr int RB = (GS_HC - 1) * ST + S;  // input columns under a strip
+    extern __shared__ __attribute__((aligned(16))) float gsl[];
+    float* xs = gsl;                // [CC][IR][LDW]
+    float* ws = gsl + P.xfloats;    // [CC][R*S][KG]
+    const int G = A.C / A.Cg;
+    int b = blockIdx.x;
+    const int kc = b % P.kchunks;
+    b /= P.kchunks;
+    const int band = b % P.nbands;
+    b /= P.nbands;
+    const int ngb = (G + P.GB - 1) / P.GB;
+    const int g0 = (b % ngb) * P.GB;
+    const int n = b / ngb;
+    const int gn = min(P.GB, G - g0);
+    const int kq0 = kc * KG;
+    const int nk = min(KG, A.Kg - kq0);
+    const int ho0 = band * P.TR;
+    const int rows = min(P.TR, A.Ho - ho0);
+    const int hi_base = ho0 * ST - A.ph;
+    const int plane = P.IR * P.LDW;
+    const int t = threadIdx.x;
+    // the thread's strip: column block cb, output row rv of the band, group gg of the block
+    const int cb = t % P.ncb;
+    const int rv = (t / P.ncb) % P.TR;
+    const int gg = t / (P.ncb * P.TR);
+    const bool act = gg < gn && rv < rows;
+    const int ow0 = cb * GS_HC;
+    const __amdgpu_buffer_rsrc_t rx = dk_rsrc(A.x, A.x_bytes);
+    const __amdgpu_buffer_rsrc_t ry = dk_rsrc(A.y, A.y_bytes);
+    const TX* wsrc = reinterpret_cast<const TX*>(A.w);
+
+    float acc[GS_HC][KG];
+#pragma unroll
+    for (int h = 0; h < GS_HC; ++h)
+#pragma unroll
+        for (int k = 0; k < KG; ++k) acc[h][k] = 0.0f;
+
+    // the block's channels: all channels of its gn groups (staged at once when GB > 1), or the
+    // Cg channels of its one group, CC at a time
+    const int cper = P.GB > 1 ? gn * A.Cg : A.Cg;
+    const int chb = g0 * A.Cg;  // first global input channel of the block
+    for (int c0 = 0; c0 < cper; c0 += P.CC) {
+        const int ccn = min(P.CC, cper - c0);
+        __syncthreads();  // nobody reads the previous chunk any more
+        // windows: line (lc, tr) holds input row hi_base + tr of channel chb + c0 + lc at
+        // columns j = wi + LPAD
+        if ((A.W & 3) == 0) {
+            const int cpl = P.LDW / 4;  // 16-byte chunks per line
+            const int total = ccn * P.IR * cpl;
+            for (int i = t; i < total; i += DIRECT_THREADS) {
+                const int line = i / cpl;
+                const int q = i - line * cpl;
+                const int lc = line / P.IR;
+                const int tr = line - lc * P.IR;
+                const int hi = hi_base + tr, w0 = 4 * q - P.LPAD;
+                const bool ok = ((unsigned)hi < (unsigned)A.H) & ((unsigned)w0 < (unsigned)A.W);
+                const int64_t e = (((int64_t)n * A.C + chb + c0 + lc) * A.H + hi) * A.W + w0;
+                f32x4 v;
+                if constexpr (sizeof(TX) == 4) {
+                    v = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                      rx, ok ? (uint32_t)(e * 4) : OOB_OFF, 0, 0));
+                } else {
+                    typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+                    const u32x2 hh = __builtin_bit_cast(
+                        u32x2, __builtin_amdgcn_raw_buffer_load_b64(rx, ok ? (uint32_t)(e * 2) : OOB_OFF, 0, 0));
+                    v = f32x4{__builtin_bit_cast(float, hh[0] << 16), __builtin_bit_cast(float, hh[0] & 0xFFFF0000u),
+                              __builtin_bit_cast(float, hh[1] << 16), __builtin_bit_cast(float, hh[1] & 0xFFFF0000u)};
+                }
+                *reinterpret_cast<f32x4*>(&xs[line * P.LDW + 4 * q]) = v;
+            }
+        } else {
+            const int total = ccn * P.IR * P.LDW;
+            for (int i = t; i < total; i += DIRECT_THREADS) {
+                const int line = i / P.LDW;
+                const int j = i - line * P.LDW;
+                const int lc = line / P.IR;
+                const int tr = line - lc * P.IR;
+                const int hi = hi_base + tr, wi = j - P.LPAD;
+                const bool ok = ((unsigned)hi < (unsigned)A.H) & ((unsigned)wi < (unsigned)A.W);
+                xs[i] = dk_load(rx, ok, (((int64_t)n * A.C + chb + c0 + lc) * A.H + hi) * A.W + wi, (TX*)nullptr);
+            }
+        }
+        // filters: ws[lc][tap][k] = w[group's output channel kq0 + k][channel within group][tap]
+        for (int i = t; i < ccn * R * S * KG; i += DIRECT_THREADS) {
+            const int k = i % KG;
+            const int tap = (i / KG) % (R * S);
+            const int lc = i / (KG * R * S);
+            const int ch = chb + c0 + lc;
+            const int gi = ch / A.Cg;
+            float v = 0.0f;
+            if (k < nk) {
+                const TX raw = wsrc[(((int64_t)gi * A.Kg + kq0 + k) * A.Cg + (ch - gi * A.Cg)) * (R * S) + tap];
+                if constexpr (sizeof(TX) == 4) v = __builtin_bit_cast(float, raw);
+                else v = __builtin_bit_cast(float, (uint32_t)raw << 16);
+            }
+            ws[i] = v;
+        }
+        __syncthreads();
+        if (act) {
+            const int lc0 = P.GB > 1 ? gg * A.Cg : 0;
+            const int lcn = P.GB > 1 ? A.Cg : ccn;
+            for (int lc = lc0; lc < lc0 + lcn; ++lc) {
+                const float* xc = xs + lc * plane + rv * ST * P.LDW + P.LPAD - A.pw + ow0 * ST;
+                const float* wc = ws + lc * (R * S * KG);
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    float xr[RB];
+#pragma unroll
+                    for (int j = 0; j < RB; ++j) xr[j] = xc[r * P.LDW + j];
+#pragma unroll
+                    for (int sx = 0; sx < S; ++sx) {
+                        float wv[KG];
+                        if constexpr (KG % 4 == 0) {
+#pragma unroll
+                            for (int k4 = 0; k4 < KG / 4; ++k4) {
+                                const f32x4 v = *reinterpret_cast<const f32x4*>(wc + (r * S + sx) * KG + 4 * k4);
+                                wv[4 * k4] = v[0]; wv[4 * k4 + 1] = v[1]; wv[4 * k4 + 2] = v[2]; wv[4 * k4 + 3] = v[3];
+                            }
+                        } else {
+#pragma unroll
+                            for (int k = 0; k < KG; ++k) wv[k] = wc[(r * S + sx) * KG + k];
+                        }
+#pragma unroll
+                        for (int h = 0; h < GS_HC; ++h)
+#pragma unroll
+                            for (int k = 0; k < KG; ++k) acc[h][k] = __builtin_fmaf(xr[h * ST + sx], wv[k], acc[h][k]);
+                    }
+                }
+            }
+        }
+    }
+    if (!act) return;
+    const int kglob0 = (g0 + gg) * A.Kg + kq0;
+    const int oh = ho0 + rv;
+    const bool vec = (A.Wo & 3) == 0;
+#pragma unroll
+    for (int k = 0; k < KG; ++k) {
+        if (k >= nk) break;
+        const float bv = A.bias ? A.bias[kglob0 + k] : 0.0f;
+        const int64_t o = (((int64_t)n * A.K + kglob0 + k) * A.Ho + oh) * A.Wo + ow0;
+        if (vec) {
+            if constexpr (sizeof(TY) == 4) {
+                const u32x4_t val = {__builtin_bit_cast(uint32_t, acc[0][k] + bv), __builtin_bit_cast(uint32_t, acc[1][k] + bv),
+                                     __builtin_bit_cast(uint32_t, acc[2][k] + bv), __builtin_bit_cast(uint32_t, acc[3][k] + bv)};
+                __builtin_amdgcn_raw_buffer_store_b128(val, ry, (uint32_t)(o * 4), 0, 0);
+            } else {
+                typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+                const u32x2 val = {(uint32_t)dk_f32_to_bf16(acc[0][k] + bv) | ((uint32_t)dk_f32_to_bf16(acc[1][k] + bv) << 16),
+                                   (uint32_t)dk_f32_to_bf16(acc[2][k] + bv) | ((uint32_t)dk_f32_to_bf16(acc[3][k] + bv) << 16)};
+                __builtin_amdgcn_raw_buffer_store_b64(val, ry, (uint32_t)(o * 2), 0, 0);
+            }
+        } else {
+#pragma unroll
+            for (int h = 0; h < GS_HC; ++h) {
+                const bool ok = ow0 + h < A.Wo;
+                if constexpr (sizeof(TY) == 4)
+                    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, acc[h][k] + bv), ry,
+                                                          ok ? (uint32_t)((o + h) * 4) : OOB_OFF, 0, 0);
+                else
+                    __builtin_amdgcn_raw_buffer_store_b16(dk_f32_to_bf16(acc[h][k] + bv), ry,
+                                                          ok ? (uint32_t)((o + h) * 2) : OOB_OFF, 0, 0);
+            }
+        }
+    }
+}
+
+// Row-strip plan: TR output rows x GB groups per block with one strip per thread; false when
+// the shape does not fit (the per-pixel grouped kernel takes it then).
+static bool gs_plan(const DirectArgs& a, int KG, GsPlan* p) {
+    if (a.R != a.S || a.sh != a.sw || (a.sh != 1 && a.sh != 2) || a.dh != 1 || a.dw != 1) return false;
+    if (a.R != 1 && a.R != 3 && a.R != 5 && a.R != 7) return false;
+    const int ncb = (a.Wo + GS_HC - 1) / GS_HC;
+    if (ncb > DIRECT_THREADS) return false;
+    const int LPAD = (a.pw + 3) / 4 * 4;
+    const int maxcol = LPAD - a.pw + (ncb * GS_HC - 1) * a.sw + a.S - 1;
+    int LDW = std::max(maxcol + 1, LPAD + a.W);
+    LDW = (LDW + 3) / 4 * 4;
+    const int RS = a.R * a.S;
+    const int G = a.C / a.Cg;
+    // rows per block: as many as the threads hold (one strip each), at most the plane
+    int tr = std::max(1, std::min(a.Ho, DIRECT_THREADS / ncb));
+    auto ir = [&](int r) { return (r - 1) * a.sh + a.R; };
+    while (tr > 1 && (int64_t)ir(tr) * LDW > GS_XF) --tr;
+    // equal bands (56 rows: 4 x 14 rather than 3 x 18 + 2)
+    tr = (a.Ho + (a.Ho + tr - 1) / tr - 1) / ((a.Ho + tr - 1) / tr);
+    const int64_t win = (int64_t)ir(tr) * LDW;
+    if (win > GS_XF || RS * KG > GS_WF) return false;
+    const int fit = (int)std::min<int64_t>(GS_XF / win, GS_WF / (RS * KG));
+    // groups per block: the threads left over by the rows, and whole groups' channels in LDS
+    int gb = std::max(1, std::min({G, DIRECT_THREADS / (ncb * tr), fit / a.Cg}));
+    p->TR = tr;
+    p->GB = gb;
+    p->CC = gb > 1 ? gb * a.Cg : std::min(a.Cg, fit);
+    p->IR = ir(tr);
+    p->LDW = LDW;
+    p->LPAD = LPAD;
+    p->ncb = ncb;
+    p->nbands = (a.Ho + tr - 1) / tr;
+    p->kchunks = (a.Kg + KG - 1) / KG;
+    p->xfloats = (int)(p->CC * win);
+    p->lds_bytes = (p->xfloats + p->CC * RS * KG) * 4;
+    const int64_t blocks = (int64_t)a.N * ((G + gb - 1) / gb) * p->nbands * p->kchunks;
+    return blocks <= 0x7fffffffLL && p->CC >= 1;
+}
+
+template <int R, int ST, int KG>
+static hipError_t launch_gs_t(const DirectArgs& a, const GsPlan& p, int xdt, int ydt, hipStream_t stream) {
+    const int G = a.C / a.Cg;
+    dim3 grid((unsigned)((int64_t)a.N * ((G + p.GB - 1) / p.GB) * p.nbands * p.kchunks));
+    if (xdt == CONV2D_F32)
+        hipLaunchKernelGGL((grouped_strip_kernel<R, ST, KG, float, float>), grid, dim3(DIRECT_THREADS), p.lds_bytes,
+                           stream, a, p);
+    else if (ydt == CONV2D_BF16)
+        hipLaunchKernelGGL((grouped_strip_kernel<R, ST, KG, uint16_t, uint16_t>), grid, dim3(DIRECT_THREADS),
+                           p.lds_bytes, stream, a, p);
+    else
+        hipLaunchKernelGGL((grouped_strip_kernel<R, ST, KG, uint16_t, float>), grid, dim3(DIRECT_THREADS),
+                           p.lds_bytes, stream, a, p);
+    return hipGetLastError();
+}
+
+// Row-strip fast path for grouped layers (G > 1, C/g > 1 or K/g > 1): KG = 1, 2, 4 or 8 output
+// channels per strip (chunks of 8 beyond).  CONV2D_GROUPED_STRIP=0 keeps the per-pixel kernel.
+static hipError_t try_launch_grouped_strip(const DirectArgs& a, int xdt, int ydt, hipStream_t stream,
+                                           bool* launched) {
+    *launched = false;
+    const char* env = std::getenv("CONV2D_GROUPED_STRIP");
+    if ((env && env[0] == '0') || a.C == a.Cg) return hipSuccess;
+    const int KG = a.Kg <= 1 ? 1 : a.Kg <= 2 ? 2 : a.Kg <= 4 ? 4 : 8;
+    GsPlan p;
+    if (!gs_plan(a, KG, &p)) return hipSuccess;
+    *launched = true;
+#define CV_GS(RV, STV, KGV) \
+    if (a.R == RV && a.sh == STV && KG == KGV) return launch_gs_t<RV, STV, KGV>(a, p, xdt, ydt, stream);
+#define CV_GS_K(RV, STV) CV_GS(RV, STV, 1) CV_GS(RV, STV, 2) CV_GS(RV, STV, 4) CV_GS(RV, STV, 8)
+    CV_GS_K(1, 1) CV_GS_K(1, 2) CV_GS_K(3, 1) CV_GS_K(3, 2) CV_GS_K(5, 1) CV_GS_K(5, 2) CV_GS_K(7, 1) CV_GS_K(7, 2)
+#undef CV_GS_K
+#undef CV_GS
+    *launched = false;
+    return hipSuccess;
+}
+
 // Grouped kernel plan for KG output channels per block; false when the shape does not fit.
 static bool grp_plan(const DirectArgs& a, int KG, GrpPlan* p) {
     const int in_cols = (a.Wo - 1) * a.sw + (a.S - 1) * a.dw + 1;
@@ -1023,6 +1285,8 @@ hipError_t launch_direct(const DirectArgs& a, int xdt, int ydt, hipStream_t stre
     if (!std::getenv("CONV2D_DW_GENERIC")) {
         bool launched = false;
         hipError_t e = try_launch_dw(a, xdt, ydt, stream, &launched);
+        if (launched || e != hipSuccess) return e;
+        e = try_launch_grouped_strip(a, xdt, ydt, stream, &launched);
         if (launched || e != hipSuccess) return e;
         e = try_launch_grouped(a, xdt, ydt, stream, &launched);
         if (launched || e != hipSuccess) return e;

@@ -25,13 +25,13 @@ def test_export_configs_and_filters(tmp_path):
     rows = _rows(p)
     assert [r["name"] for r in rows] == list(datagen.CONFIGS)
     assert list(rows[0].keys()) == R.COLUMNS
-    grouped = {"dw", "grp_g64", "grp_g32"}
+    grouped = {"dw", "dw_bf16", "grp_g64", "grp_g32"}
     assert R.export("configs", str(p), ["no-grouped"]) == len(datagen.CONFIGS) - len(grouped)
     assert {r["name"] for r in _rows(p)} == set(datagen.CONFIGS) - grouped
     R.export("configs", str(p), ["pointwise"])
     assert {r["name"] for r in _rows(p)} == {"cfg3a", "cfg3b"}
     R.export("configs", str(p), ["bf16"])
-    assert {r["name"] for r in _rows(p)} == {"cfg4_bf16", "bf16_3x3"}
+    assert {r["name"] for r in _rows(p)} == {"cfg4_bf16", "dw_bf16", "bf16_3x3"}
     R.export("configs", str(p), ["regular", "no-strided", "f32"])
     assert {r["name"] for r in _rows(p)} == {"cfg1", "cfg2"}
     with pytest.raises(ValueError):

@@ -358,6 +358,35 @@ def test_tail_split_planned_cfg2_repeat():
     assert pt <= GATE["f32"]
 
 
+def test_tail_split_soak_cfg2():
+    """cfg2 as planned (its last 32 tiles each summed from 6 pieces that may run on different
+    XCDs, handed over through device-scope stores and an arrival counter) called 2000 times back
+    to back into a ring of outputs; each result is compared bit for bit with the first on the
+    stream itself, and the test stops at the first mismatch."""
+    import torch
+    cs = datagen.CONFIGS["cfg2"]
+    dc = DeviceConv(cs, "random")
+    try:
+        assert dc.plan(IMPLICIT).tail_tiles > 0
+        stream = torch.cuda.current_stream()
+        dc.run(IMPLICIT, stream)
+        torch.cuda.synchronize()
+        ref = dc.y.clone()
+        ring = [torch.empty_like(dc.y) for _ in range(8)]
+        bad = torch.zeros((), dtype=torch.int64, device=dc.y.device)
+        for i in range(2000):
+            y = ring[i % 8]
+            B.conv2d_fwd(dc.desc, dc.x, dc.w, dc.b, y, IMPLICIT, stream)
+            bad += (y != ref).any().to(torch.int64)
+            if i % 250 == 249:
+                torch.cuda.synchronize()
+                assert int(bad) == 0, f"a result differed from the first by call {i}"
+        torch.cuda.synchronize()
+        assert int(bad) == 0
+    finally:
+        dc.close()
+
+
 def test_descriptor_shared_across_streams():
     """One descriptor (cfg2 as planned: tail-split partials and arrival counters and the
     tap-major filter copy in its workspaces) called on two streams in turn without any
@@ -484,12 +513,57 @@ GROUPED = [
 ]
 
 
+class _Env:
+    def __init__(self, **env):
+        self.env, self.old = env, {}
+
+    def __enter__(self):
+        for k, v in self.env.items():
+            self.old[k] = os.environ.get(k)
+            os.environ[k] = v
+
+    def __exit__(self, *exc):
+        for k, v in self.old.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+
+
+# strip = "1": the row-strip kernel where it applies (square filters, strides 1/2, no dilation),
+# "0": the per-pixel grouped kernel for every shape
+@pytest.mark.parametrize("strip", ["1", "0"], ids=["strip", "perpixel"])
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 @pytest.mark.parametrize("idx", range(len(GROUPED)))
-def test_grouped_direct(idx, dt):
+def test_grouped_direct(idx, dt, strip):
     cs = GROUPED[idx].with_(x_dtype=dt, y_dtype=dt)
+    with _Env(CONV2D_GROUPED_STRIP=strip):
+        _check(cs, DIRECT)
+        _check(cs.with_(y_dtype="f32"), DIRECT, "integer")
+
+
+# the row-strip grouped kernel: every filter size and stride it takes, 1 to 8 output channels
+# per strip and chunks of 8 beyond, channels staged in chunks, rows that are not a multiple of
+# 4 (element-wise staging, ragged last strip), bands of rows, groups batched per block
+STRIP = [
+    _shape(2, 128, 56, 56, 128, 3, 3, pd=(1, 1), g=32, seed=380),           # C/g 4, K/g 4
+    _shape(1, 64, 30, 30, 64, 3, 3, st=(2, 2), pd=(1, 1), g=8, seed=381),   # 8, 8, stride 2
+    _shape(2, 24, 17, 19, 48, 5, 5, pd=(2, 2), g=6, seed=382),              # 4, 8, W % 4 != 0
+    _shape(1, 32, 28, 28, 96, 1, 1, g=8, seed=383),                         # 4, 12: two chunks of 8
+    _shape(1, 6, 40, 41, 9, 7, 7, st=(2, 2), pd=(3, 3), g=3, seed=384),     # 2, 3
+    _shape(2, 40, 23, 22, 20, 3, 3, pd=(1, 1), g=20, seed=385),             # 2, 1
+    _shape(1, 256, 14, 14, 32, 3, 3, pd=(1, 1), g=2, seed=386),             # 128 channels in chunks
+    _shape(3, 16, 9, 300, 16, 3, 3, pd=(1, 1), g=4, seed=387),              # wide rows, one row per band
+]
+
+
+@pytest.mark.parametrize("dt", [("f32", "f32"), ("bf16", "bf16"), ("bf16", "f32")], ids=lambda d: "-".join(d))
+@pytest.mark.parametrize("idx", range(len(STRIP)))
+def test_grouped_strip(idx, dt):
+    cs = STRIP[idx].with_(x_dtype=dt[0], y_dtype=dt[1])
     _check(cs, DIRECT)
-    _check(cs.with_(y_dtype="f32"), DIRECT, "integer")
+    if dt[1] == "f32":
+        _check(cs, DIRECT, "integer")
 
 
 # Winograd F(2x2, 3x3): 3x3, stride 1, dilation 1, one group, fp32; odd output sizes (clipped
