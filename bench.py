@@ -282,6 +282,12 @@ def time_launches(launch, reps, torch):
     return a.elapsed_time(b) / reps
 
 
+def kernel_label(plan, B):
+    """Microkernel name, with its tile where it has one (the direct kernels have none)."""
+    name = B.KERNEL_NAMES[plan.kernel]
+    return f"{name} {plan.tile_m}x{plan.tile_n}" if plan.tile_m > 0 else name
+
+
 def roofline(cs, nkhw, flops, kern_ms):
     """Which roofline bounds the operation (MFMA when the arithmetic intensity on algorithmic
     bytes reaches the dtype's ridge point; the vector ALU for direct grouped kernels whose
@@ -526,9 +532,10 @@ def config_gpu(name, args, B, torch):
         roof = roofline(cs, dc.out_nkhw, flops, kern_ms)
         roof["kernel_us"] = None if kern_ms is None else kern_ms * 1e3
         roof["kernel_source"] = src
+        roof["traffic"] = load_traffic(name, B.ALGO_NAMES[algo])
         _, _, bd = time_algo(dc, algo, 5, 1, B, torch, B.CONV2D_TIMING_PHASES)
         row = {"workload": describe(cs), "algo": B.ALGO_NAMES[algo],
-               "kernel": f"{B.KERNEL_NAMES[plan.kernel]} {plan.tile_m}x{plan.tile_n}",
+               "kernel": kernel_label(plan, B),
                "steps": steps, "ms_per_step": ms, "event_ms_per_step": ev_ms,
                "tflops": flops / (ms * 1e-3) / 1e12, "roofline": roof,
                "kernel_le_step": None if kern_ms is None else kern_ms <= max(ms, ev_ms) * 1.02,
@@ -628,11 +635,16 @@ def main():
                     data = json.load(f)
             except (OSError, ValueError):
                 data = {}
-            try:
-                with open(os.path.join(args.summarize_profiles, "bench.json")) as f:
-                    algo_name = json.loads(f.read().strip().splitlines()[-1])["config"]["algo"]
-            except (OSError, ValueError, KeyError, IndexError):
-                algo_name = "implicit_gemm"
+            # the bench line of the traced run (the profiler's own messages may follow it)
+            algo_name = None
+            with open(os.path.join(args.summarize_profiles, "bench.json")) as f:
+                for line in f:
+                    try:
+                        algo_name = json.loads(line)["config"]["algo"]
+                    except (ValueError, KeyError, TypeError):
+                        pass
+            if algo_name is None:
+                sys.exit(f"no bench line in {args.summarize_profiles}/bench.json")
             data[f"{args.workload}:{algo_name}"] = {
                 "kernel": key[0], "bytes_per_launch": traffic[key[0]],
                 "kernel_hash": kernel_hash(algo_name)}
@@ -681,7 +693,7 @@ def main():
 
     xdt = cs.x_dtype
     roof = roofline(cs, nkhw, flops, kern_ms)
-    roof["kernel"] = f"{algo_name} microkernel ({B.KERNEL_NAMES[plan.kernel]}, tile {plan.tile_m}x{plan.tile_n})"
+    roof["kernel"] = f"{algo_name} microkernel ({kernel_label(plan, B)})"
     roof["kernel_us_per_launch"] = None if kern_ms is None else kern_ms * 1e3
     roof["kernel_source"] = kern_src
     roof["traffic"] = load_traffic(args.workload, algo_name)

@@ -59,9 +59,11 @@ template <typename T> struct SliceTraits;
 template <> struct SliceTraits<float> { static constexpr int wpad = 4; };
 template <> struct SliceTraits<uint16_t> { static constexpr int wpad = 8; };
 
-// NW waves per block (4 or 8), tiles of 32*NW pixels.  The slice has one buffer: it is copied
-// between tiles, and a second resident block keeps the MFMAs busy meanwhile (a second buffer
-// would halve the resident blocks, which measured slower).
+// NW waves per block (4 or 8), tiles of 32*NW pixels.  The element-wise slice has one buffer:
+// it is copied between tiles, and a second resident block keeps the MFMAs busy meanwhile (a
+// second buffer would halve the resident blocks, which measured slower).  The packed-row slice
+// is half the size, so two buffers fit beside the filters at two blocks per CU (A.nbuf = 2):
+// the next tile's copy then goes out before the current tile's MFMAs.
 // PK (bf16 only): the packed-row layout.  The slice holds bf16 pairs, one 4-byte word per two
 // input columns (copied with dword loads), and the reduction runs over filter rows (c, r),
 // each padded to 8 taps with zero weights, two rows per MFMA step (lane half h takes row
