@@ -566,6 +566,39 @@ def test_grouped_strip(idx, dt):
         _check(cs, DIRECT, "integer")
 
 
+# the streamed-row depthwise kernel (stride 1; 3x3 at dilation 1 or 2, 5x5 and 7x7 at
+# dilation 1): bands of rows (ragged last band and strip), odd and even padding (bf16 words
+# start at the strip or one value before it), multiplier 2, asymmetric and zero padding, no
+# bias, wide rows with one unit per wave, first and last input planes (word-by-word loads);
+# shapes it does not take (odd W in bf16, 7x7 at dilation 2) go to the block-per-plane
+# kernel, through which every shape also runs with rows = "0"
+DW_ROWS = [
+    _shape(2, 16, 56, 56, 16, 3, 3, pd=(1, 1), g=16, seed=390),             # 4 bands of 14
+    _shape(1, 8, 37, 37, 8, 5, 5, pd=(2, 2), g=8, seed=391),                # Wo % 4 != 0, 32 KiB
+    _shape(2, 6, 30, 30, 12, 3, 3, pd=(1, 1), g=6, seed=392),               # multiplier 2
+    _shape(1, 4, 33, 64, 4, 7, 7, pd=(3, 3), g=4, seed=393),                # two copies per row
+    _shape(1, 4, 50, 60, 4, 3, 3, pd=(2, 2), dl=(2, 2), g=4, seed=394),     # dilation 2
+    _shape(1, 3, 45, 40, 3, 7, 7, pd=(6, 6), dl=(2, 2), g=3, seed=395),     # not taken (7x7 d2)
+    _shape(1, 2, 20, 250, 2, 3, 3, pd=(1, 1), g=2, seed=396),               # one unit per wave
+    _shape(2, 5, 29, 27, 5, 3, 3, g=5, seed=397, bias=False),               # no padding, no bias
+    _shape(1, 4, 21, 32, 4, 5, 5, pd=(1, 3), g=4, seed=398),                # ph != pw, Wo = 34
+    _shape(3, 8, 14, 14, 8, 3, 3, pd=(1, 1), g=8, seed=399),                # 16 units per wave
+    _shape(2, 4, 23, 31, 4, 3, 3, pd=(1, 1), g=4, seed=400),                # odd W (bf16: not taken)
+    _shape(1, 2, 26, 70, 2, 5, 5, pd=(2, 2), g=2, seed=401),                # 2 planes: all edge waves
+]
+
+
+@pytest.mark.parametrize("rows", ["1", "0"], ids=["rows", "block"])
+@pytest.mark.parametrize("dt", [("f32", "f32"), ("bf16", "bf16"), ("bf16", "f32")], ids=lambda d: "-".join(d))
+@pytest.mark.parametrize("idx", range(len(DW_ROWS)))
+def test_depthwise_rows(idx, dt, rows):
+    cs = DW_ROWS[idx].with_(x_dtype=dt[0], y_dtype=dt[1])
+    with _Env(CONV2D_DW_ROWS=rows):
+        _check(cs, DIRECT)
+        if dt[1] == "f32":
+            _check(cs, DIRECT, "integer")
+
+
 # Winograd F(2x2, 3x3): 3x3, stride 1, dilation 1, one group, fp32; odd output sizes (clipped
 # 2x2 tiles), paddings 0/1/2, channel counts across GEMM tiles, NHWC, chunked tiles
 WINOGRAD = B.CONV2D_ALGO_WINOGRAD
