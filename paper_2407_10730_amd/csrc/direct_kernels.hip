@@ -1010,10 +1010,14 @@ constexpr int GS_WF = 2048;    // LDS floats for the filters
 
 struct GsPlan {
     int32_t TR, GB, CC, IR, LDW, LPAD, ncb, nbands, kchunks, xfloats, lds_bytes;
+    FastDiv fd_cpl, fd_ldw, fd_ir, fd_cg;  // staging: chunks per line, line width, rows, channels per group
 };
 
+// Up to 4 output channels per strip the kernel fits in 73 registers, 7 blocks per CU; left to
+// itself the compiler took 100 (5 blocks per CU, 20 % slower on C/g = 4).
 template <int R, int ST, int KG, typename TX, typename TY>
-__global__ __launch_bounds__(DIRECT_THREADS) void grouped_strip_kernel(DirectArgs A, GsPlan P) {
+__global__ __launch_bounds__(DIRECT_THREADS) __attribute__((amdgpu_waves_per_eu(KG <= 4 ? 7 : 1))) void
+grouped_strip_kernel(DirectArgs A, GsPlan P) {
     constexpr int S = R;
     constexpr int RB = (GS_HC - 1) * ST + S;  // input columns under a strip
     extern __shared__ __attribute__((aligned(16))) float gsl[];
@@ -1061,17 +1065,19 @@ __global__ __launch_bounds__(DIRECT_THREADS) void grouped_strip_kernel(DirectArg
         __syncthreads();  // nobody reads the previous chunk any more
         // windows: line (lc, tr) holds input row hi_base + tr of channel chb + c0 + lc at
         // columns j = wi + LPAD
+        // (element offsets fit 32 bits: x is below 2 GiB)
+        const int cbase = (n * A.C + chb + c0) * A.H;  // row index of the chunk's first channel
         if ((A.W & 3) == 0) {
-            const int cpl = P.LDW / 4;  // 16-byte chunks per line
+            const int cpl = P.LDW / 4;  // 16-byte chunks per line (the odd last word is padding)
             const int total = ccn * P.IR * cpl;
             for (int i = t; i < total; i += DIRECT_THREADS) {
-                const int line = i / cpl;
+                const int line = (int)dk_fdiv((uint32_t)i, P.fd_cpl);
                 const int q = i - line * cpl;
-                const int lc = line / P.IR;
+                const int lc = (int)dk_fdiv((uint32_t)line, P.fd_ir);
                 const int tr = line - lc * P.IR;
                 const int hi = hi_base + tr, w0 = 4 * q - P.LPAD;
                 const bool ok = ((unsigned)hi < (unsigned)A.H) & ((unsigned)w0 < (unsigned)A.W);
-                const int64_t e = (((int64_t)n * A.C + chb + c0 + lc) * A.H + hi) * A.W + w0;
+                const int e = (cbase + lc * A.H + hi) * A.W + w0;
                 f32x4 v;
                 if constexpr (sizeof(TX) == 4) {
                     v = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
@@ -1083,18 +1089,22 @@ __global__ __launch_bounds__(DIRECT_THREADS) void grouped_strip_kernel(DirectArg
                     v = f32x4{__builtin_bit_cast(float, hh[0] << 16), __builtin_bit_cast(float, hh[0] & 0xFFFF0000u),
                               __builtin_bit_cast(float, hh[1] << 16), __builtin_bit_cast(float, hh[1] & 0xFFFF0000u)};
                 }
-                *reinterpret_cast<f32x4*>(&xs[line * P.LDW + 4 * q]) = v;
+                float* dst = &xs[line * P.LDW + 4 * q];  // 4-byte aligned (odd line width)
+                dst[0] = v[0];
+                dst[1] = v[1];
+                dst[2] = v[2];
+                dst[3] = v[3];
             }
         } else {
             const int total = ccn * P.IR * P.LDW;
             for (int i = t; i < total; i += DIRECT_THREADS) {
-                const int line = i / P.LDW;
+                const int line = (int)dk_fdiv((uint32_t)i, P.fd_ldw);
                 const int j = i - line * P.LDW;
-                const int lc = line / P.IR;
+                const int lc = (int)dk_fdiv((uint32_t)line, P.fd_ir);
                 const int tr = line - lc * P.IR;
                 const int hi = hi_base + tr, wi = j - P.LPAD;
                 const bool ok = ((unsigned)hi < (unsigned)A.H) & ((unsigned)wi < (unsigned)A.W);
-                xs[i] = dk_load(rx, ok, (((int64_t)n * A.C + chb + c0 + lc) * A.H + hi) * A.W + wi, (TX*)nullptr);
+                xs[i] = dk_load(rx, ok, ok ? (cbase + lc * A.H + hi) * A.W + wi : 0, (TX*)nullptr);
             }
         }
         // filters: ws[lc][tap][k] = w[group's output channel kq0 + k][channel within group][tap]
@@ -1103,7 +1113,7 @@ __global__ __launch_bounds__(DIRECT_THREADS) void grouped_strip_kernel(DirectArg
             const int tap = (i / KG) % (R * S);
             const int lc = i / (KG * R * S);
             const int ch = chb + c0 + lc;
-            const int gi = ch / A.Cg;
+            const int gi = (int)dk_fdiv((uint32_t)ch, P.fd_cg);
             float v = 0.0f;
             if (k < nk) {
                 const TX raw = wsrc[(((int64_t)gi * A.Kg + kq0 + k) * A.Cg + (ch - gi * A.Cg)) * (R * S) + tap];
@@ -1191,7 +1201,10 @@ static bool gs_plan(const DirectArgs& a, int KG, GsPlan* p) {
     const int LPAD = (a.pw + 3) / 4 * 4;
     const int maxcol = LPAD - a.pw + (ncb * GS_HC - 1) * a.sw + a.S - 1;
     int LDW = std::max(maxcol + 1, LPAD + a.W);
-    LDW = (LDW + 3) / 4 * 4;
+    // an odd line width (4m + 1 words, the last one never read) moves each row one LDS bank
+    // over: the lanes of a wave read 4 words apart within a row, so with a multiple-of-32
+    // width the rows of one wave met in the same 8 banks (up to 5-way conflicts at 56 columns)
+    LDW = (LDW + 3) / 4 * 4 + 1;
     const int RS = a.R * a.S;
     const int G = a.C / a.Cg;
     // rows per block: as many as the threads hold (one strip each), at most the plane
@@ -1204,6 +1217,8 @@ static bool gs_plan(const DirectArgs& a, int KG, GsPlan* p) {
     if (win > GS_XF || RS * KG > GS_WF) return false;
     const int fit = (int)std::min<int64_t>(GS_XF / win, GS_WF / (RS * KG));
     // groups per block: the threads left over by the rows, and whole groups' channels in LDS
+    // (filling the idle threads of 56-row planes with more groups in shorter bands measured
+    // slower: C/g 4, bands of 8 with two groups 64 us against 54 with bands of 14)
     int gb = std::max(1, std::min({G, DIRECT_THREADS / (ncb * tr), fit / a.Cg}));
     p->TR = tr;
     p->GB = gb;
@@ -1216,6 +1231,10 @@ static bool gs_plan(const DirectArgs& a, int KG, GsPlan* p) {
     p->kchunks = (a.Kg + KG - 1) / KG;
     p->xfloats = (int)(p->CC * win);
     p->lds_bytes = (p->xfloats + p->CC * RS * KG) * 4;
+    p->fd_cpl = make_fastdiv((uint32_t)(LDW / 4));
+    p->fd_ldw = make_fastdiv((uint32_t)LDW);
+    p->fd_ir = make_fastdiv((uint32_t)p->IR);
+    p->fd_cg = make_fastdiv((uint32_t)a.Cg);
     const int64_t blocks = (int64_t)a.N * ((G + gb - 1) / gb) * p->nbands * p->kchunks;
     return blocks <= 0x7fffffffLL && p->CC >= 1;
 }
