@@ -715,6 +715,14 @@ int run_slice(conv2d_desc* d, const SlicePlan& sp, const Ws& ws, const void* x, 
     a.pk_shift = sp.pk_shift;
     a.nbuf = sp.nbuf;
     a.xwords = sp.xwords;
+    // fp32 lines by 16-byte copies when every 4-word group of a line is wholly inside or
+    // outside the image and the shifted line still fits
+    // (CONV2D_SLICE_X1=1 keeps the 4-byte copies: tests run both)
+    const char* x1 = std::getenv("CONV2D_SLICE_X1");
+    a.xshift = (4 - a.pw % 4) % 4;
+    a.x4 = g.xdt == CONV2D_F32 && !sp.pk && a.W % 4 == 0 && ((uintptr_t)x & 15) == 0 &&
+           sp.pwp + a.xshift <= 256 && !(x1 && x1[0] == '1');
+    if (!a.x4) a.xshift = 0;
     a.fd_pergz = make_fastdiv((uint32_t)(a.N * a.tiles_px));
     a.fd_tpx = make_fastdiv((uint32_t)a.tiles_px);
     a.fd_gm = make_fastdiv((uint32_t)a.grid_m);
@@ -1269,13 +1277,25 @@ int conv2d_desc_create(const conv2d_params* params, conv2d_desc** out) {
     plan_split(d);
     plan_tail(d);
     {
-        // 8 waves (256-pixel tiles) unless an image has at most 128 output pixels;
-        // CONV2D_SLICE_WAVES = 4 or 8 overrides for tests and tuning
+        // 8 waves (256-pixel tiles) unless an image has at most 128 output pixels; fp32 layers
+        // with at least two rounds of 512-pixel tiles on one block per CU (256 CUs) take 16 waves
+        // and two slice buffers, so the next tile's copy overlaps this tile's MFMAs with 4 waves
+        // per SIMD (cfg4: 15 % faster than 8 waves, one buffer and two blocks per CU).
+        // CONV2D_SLICE_WAVES = 4, 8 or 16 (fp32) and CONV2D_SLICE_DB = 0 / 1 override.
+        const auto tiles = [&](int w) { return g.G * ceil_div(g.Kg, 64) * g.N * ceil_div(g.Ho * g.Wo, 32 * w); };
         int nw = g.Ho * g.Wo <= 128 ? 4 : 8;
+        if (g.xdt == CONV2D_F32 && g.Ho * g.Wo >= 512 && tiles(16) >= 512) nw = 16;
         const int64_t force_nw = env_int64("CONV2D_SLICE_WAVES", 0);
-        if (force_nw == 4 || force_nw == 8) nw = (int)force_nw;
+        if (force_nw == 4 || force_nw == 8 || (force_nw == 16 && g.xdt == CONV2D_F32)) nw = (int)force_nw;
+        const int64_t force_db = env_int64("CONV2D_SLICE_DB", -1);
+        const bool db = force_db < 0 ? tiles(nw) >= 512 : force_db != 0;
         d->slice = slice_plan(g.Cg, g.R, g.S, g.Ho, g.Wo, g.sh, g.sw, g.dh, g.dw, g.xdt, nw, g.W, g.pw,
-                              !std::getenv("CONV2D_SLICE_UNPACKED"));
+                              !std::getenv("CONV2D_SLICE_UNPACKED"), db);
+        if (!d->slice.ok && nw == 16 && force_nw != 16) {
+            nw = 8;
+            d->slice = slice_plan(g.Cg, g.R, g.S, g.Ho, g.Wo, g.sh, g.sw, g.dh, g.dw, g.xdt, nw, g.W, g.pw,
+                                  !std::getenv("CONV2D_SLICE_UNPACKED"), tiles(nw) >= 512);
+        }
         d->slice_u = slice_plan(g.Cg, g.R, g.S, g.Ho, g.Wo, g.sh, g.sw, g.dh, g.dw, g.xdt, nw);
     }
     // The sliced kernel replaces the table-driven gather (C/g not a multiple of the stage

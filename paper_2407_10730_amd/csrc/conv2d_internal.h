@@ -202,7 +202,8 @@ inline FastDiv make_fastdiv(uint32_t d) {
 // lds_k_off, then the slice at lds_x_off).  Persistent blocks walk the tiles
 // (group x channel tile, image, pixel tile).  NCHW x; NCHW or NHWC y.
 constexpr int64_t SLICE_MAX_KRED = 1024;
-constexpr int64_t SLICE_MAX_LDS = 80 * 1024;  // two blocks per CU
+constexpr int64_t SLICE_MAX_LDS = 80 * 1024;     // two blocks per CU
+constexpr int64_t SLICE_MAX_LDS_1 = 160 * 1024;  // one block per CU
 struct SliceArgs {
     const void* x;
     uint32_t x_bytes;
@@ -233,6 +234,10 @@ struct SliceArgs {
     int32_t pk, pk_shift;
     // slice buffers (1 or 2; with 2 the next tile's copy overlaps this tile's MFMAs), words each
     int32_t nbuf, xwords;
+    // fp32 lines copied 16 bytes per lane (x4 = 1; W % 4 == 0, x 16-byte aligned): input column
+    // wi sits at word wi + pw + xshift, xshift = (-pw) mod 4, so every 4-word group of a line is
+    // wholly inside or wholly outside the image; the pixel bases move by xshift
+    int32_t x4, xshift;
     // divisions of the tile and pixel decode and the filter load: by N*tiles_px, tiles_px,
     // grid_m, Wo and the filter row length 2*kh
     FastDiv fd_pergz, fd_tpx, fd_gm, fd_wo, fd_kw;
@@ -245,9 +250,10 @@ struct SlicePlan {
     int32_t pk_shift;
     int32_t nbuf, xwords;  // slice buffers and their size in 4-byte words
 };
-// pk: try the packed-row bf16 layout (falls back to one word per element when it does not apply)
+// pk: try the packed-row bf16 layout (falls back to one word per element when it does not apply);
+// db: fp32 may take two slice buffers and the whole LDS of a CU (enough tiles for that)
 SlicePlan slice_plan(int64_t Cg, int64_t R, int64_t S, int64_t Ho, int64_t Wo, int sh, int sw, int dh, int dw,
-                     int xdt, int nw, int64_t W = 0, int pw = 0, bool pk = false);
+                     int xdt, int nw, int64_t W = 0, int pw = 0, bool pk = false, bool db = false);
 hipError_t launch_slice(const SliceArgs& a, int xdt, int ydt, int nw, hipStream_t stream);
 
 // weight repack to tap-major order: w [K][C/g][R*S] -> wr [K][R*S][C/g].

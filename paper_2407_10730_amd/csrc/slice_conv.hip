@@ -48,6 +48,10 @@ constexpr int SLICE_LP = 256;   // slice line pitch in words (one column per thr
 __device__ __forceinline__ void lds_dma_b32(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t lds_addr) {
     asm volatile("buffer_load_dword %0, %1, 0 offen lds" ::"v"(voff), "s"(r), "{m0}"(lds_addr) : "memory");
 }
+// 16 bytes per lane: lane l writes LDS bytes lds_addr + 16*l .. + 15.
+__device__ __forceinline__ void lds_dma_b128(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t lds_addr) {
+    asm volatile("buffer_load_dwordx4 %0, %1, 0 offen lds" ::"v"(voff), "s"(r), "{m0}"(lds_addr) : "memory");
+}
 __device__ __forceinline__ void lds_dma_u16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t lds_addr) {
     asm volatile("buffer_load_ushort %0, %1, 0 offen lds" ::"v"(voff), "s"(r), "{m0}"(lds_addr) : "memory");
 }
@@ -70,8 +74,12 @@ template <> struct SliceTraits<uint16_t> { static constexpr int wpad = 8; };
 // 2*step + h).  The 8 values a lane feeds one MFMA are then 8 consecutive input columns of
 // one slice line starting at j0 = ow*sw + shift: 5 word reads and 4 funnel shifts (by 16 bits
 // when j0 is odd) instead of 8 single reads, a table lookup and the packing.
+// fp32 and packed-row kernels are held to 128 registers: the planner puts 16 waves on a CU
+// (4 per SIMD) and 129 registers would leave room for 3 (the element-wise bf16 kernels would
+// spill under that limit and keep their 136).
 template <typename T, typename TOut, int NW, bool PK>
-__global__ __launch_bounds__(64 * NW) void slice_conv_kernel(SliceArgs A) {
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(sizeof(T) == 4 || PK ? 4 : 1))) void
+slice_conv_kernel(SliceArgs A) {
     constexpr int SLICE_THREADS = 64 * NW;
     constexpr int SLICE_NPX = 32 * NW;
     extern __shared__ __attribute__((aligned(16))) char lds[];
@@ -195,6 +203,38 @@ __global__ __launch_bounds__(64 * NW) void slice_conv_kernel(SliceArgs A) {
             }
             return;
         }
+        if constexpr (ES == 4) {
+            if (A.x4) {
+                // 16 bytes per lane: wave w copies whole lines w, w + nwc, ...; lane l words
+                // 4l .. 4l + 3, input columns 4l - pw - xshift ..
+                const int wi = 4 * lane - A.pw - A.xshift;
+                const bool wok = (4 * lane < A.pwp + A.xshift) & ((unsigned)wi < (unsigned)A.W);
+                const uint32_t hw = (uint32_t)(A.H * A.W);
+                const uint32_t plane0 = (uint32_t)(tl.n * A.C + gi * A.Cg) * hw;
+                const uint32_t lds0 = __builtin_amdgcn_readfirstlane(
+                    (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint32_t*)buf);
+                const int lines = A.Cg * A.ph_max;
+                int c = 0, row = wave;
+                while (row >= A.ph_max) {
+                    row -= A.ph_max;
+                    ++c;
+                }
+                uint32_t plane = plane0 + (uint32_t)c * hw;
+                for (int u = wave; u < lines; u += nwc) {
+                    const int hi = tl.hi0 + row;
+                    const bool ok = wok & ((unsigned)hi < (unsigned)A.H);
+                    const uint32_t e = plane + (uint32_t)(hi * A.W + wi);
+                    lds_dma_b128(rx, ok ? e * 4u : OOB_OFF, lds0 + (uint32_t)(u * SLICE_LP * 4));
+                    row += nwc;
+                    while (row >= A.ph_max) {
+                        row -= A.ph_max;
+                        ++c;
+                        plane += hw;
+                    }
+                }
+                return;
+            }
+        }
         const int col = t & (SLICE_LP - 1);    // each group of 4 waves covers the 256 columns
         const int half = wave >> 2;            // ... of every (nwc/4)-th line
         const int rstep = nwc >> 2;
@@ -301,7 +341,7 @@ __global__ __launch_bounds__(64 * NW) void slice_conv_kernel(SliceArgs A) {
         // filters yet, so no barrier first).  The element-wise slice of 4-wave blocks needs
         // all four waves for a line: there every wave copies first.
         nxt = decode(0);
-        const bool split = PK || NW == 8;
+        const bool split = PK || NW >= 8;
         copy_slice(nxt, xs, split ? NW / 2 : NW);
         load_filters(nxt, split ? 32 * NW : 0, split ? 32 * NW : SLICE_THREADS);
         load_bias(nxt);
@@ -355,7 +395,7 @@ __global__ __launch_bounds__(64 * NW) void slice_conv_kernel(SliceArgs A) {
         if (p < howo) {
             const int oh = (int)fdiv((uint32_t)p, A.fd_wo);
             const int ow = p - oh * A.Wo;
-            pixbase = (oh - tl.oh0) * A.sh * SLICE_LP + ow * A.sw;
+            pixbase = (oh - tl.oh0) * A.sh * SLICE_LP + ow * A.sw + A.xshift;
         }
         const T* wa0 = wl + lcol * wpitch + lrow * A.kh;
         const T* wa1 = wa0 + 32 * wpitch;
@@ -582,7 +622,7 @@ __global__ __launch_bounds__(64 * NW) void slice_conv_kernel(SliceArgs A) {
 }
 
 SlicePlan slice_plan(int64_t Cg, int64_t R, int64_t S, int64_t Ho, int64_t Wo, int sh, int sw, int dh, int dw,
-                     int xdt, int nw, int64_t W, int pw, bool pk) {
+                     int xdt, int nw, int64_t W, int pw, bool pk, bool db) {
     SlicePlan sp{};
     const int64_t SLICE_NPX = 32 * nw;
     const int64_t es = xdt == CONV2D_BF16 ? 2 : 4;
@@ -627,11 +667,15 @@ SlicePlan slice_plan(int64_t Cg, int64_t R, int64_t S, int64_t Ho, int64_t Wo, i
     const int64_t pwp = (Wo - 1) * sw + (S - 1) * dw + 1;
     if (pwp > SLICE_LP) return sp;  // one column per thread
     const int64_t xbytes = Cg * ph_max * SLICE_LP * 4;
-    const int64_t total = wbytes + kbytes + xbytes;
-    if (total > SLICE_MAX_LDS) return sp;
+    // fp32 with many tiles: two slice buffers, one block per CU, when both fit beside the
+    // filters (the next tile's copy then overlaps this tile's MFMAs: cfg4 9 % faster than
+    // one buffer and two blocks per CU, whose copies and MFMAs did not overlap)
+    const bool two = db && es == 4 && wbytes + kbytes + 2 * xbytes <= SLICE_MAX_LDS_1;
+    const int64_t total = wbytes + kbytes + (two ? 2 : 1) * xbytes;
+    if (total > (two ? SLICE_MAX_LDS_1 : SLICE_MAX_LDS)) return sp;
     sp.ok = true;
     sp.nw = nw;
-    sp.nbuf = 1;
+    sp.nbuf = two ? 2 : 1;
     sp.xwords = (int32_t)(xbytes / 4);
     sp.kh = (int32_t)kh;
     sp.ph_max = (int32_t)ph_max;
@@ -661,6 +705,9 @@ hipError_t launch_slice(const SliceArgs& a, int xdt, int ydt, int nw, hipStream_
     if (a.nblocks < 1 || a.tiles_total < 1) return hipErrorInvalidValue;
     if (nw == 4) launch_slice_cfg<4>(a, xdt, ydt, stream);
     else if (nw == 8) launch_slice_cfg<8>(a, xdt, ydt, stream);
+    else if (nw == 16 && xdt == CONV2D_F32)
+        hipLaunchKernelGGL((slice_conv_kernel<float, float, 16, false>), dim3((unsigned)a.nblocks), dim3(1024),
+                           a.lds_bytes, stream, a);
     else return hipErrorInvalidValue;
     return hipGetLastError();
 }

@@ -49,7 +49,7 @@ class _Kernel:
     """Forces the implicit family's microkernel while descriptors are created: kernel None =
     planner's choice, "0" = tiled GEMM, "1" = sliced kernel (when it fits), "nhwc" = tiled
     GEMM with the bf16 NHWC gather (when C/g allows); waves = the sliced kernel's waves per
-    block ("4" or "8"; None = planner's choice)."""
+    block ("4", "8", or "16" for fp32; None = planner's choice)."""
 
     def __init__(self, force, waves=None):
         if force == "nhwc":
@@ -127,7 +127,8 @@ def test_config_parity(name, algo):
     _check(datagen.CONFIGS[name], algo)
 
 
-@pytest.mark.parametrize("kernel", [("0", None), ("1", "4"), ("1", "8")], ids=["gemm", "slice4", "slice8"])
+@pytest.mark.parametrize("kernel", [("0", None), ("1", "4"), ("1", "8"), ("1", "16")],
+                         ids=["gemm", "slice4", "slice8", "slice16"])
 @pytest.mark.parametrize("name", ["cfg1", "cfg4", "cfg4_bf16"])
 def test_config_parity_both_implicit_kernels(name, kernel):
     _check(datagen.CONFIGS[name], IMPLICIT, kernel=kernel[0], waves=kernel[1])
@@ -427,6 +428,33 @@ def test_slice_last_round_split(idx, dt):
     cs = SLICE_TAIL[idx].with_(x_dtype=dt[0], y_dtype=dt[1], layout=dt[2])
     _check(cs, IMPLICIT, "random", kernel="1", waves="8")
     _check(cs, IMPLICIT, "integer", kernel="1", waves="8")
+
+
+# the sliced kernel's fp32 slices copied 16 bytes per lane (W % 4 == 0): paddings 0 to 4 (slice
+# shift 3, 2, 1, 0), strides 1 and 2, row and column dilation, a line filled up to its last
+# word, two channel tiles; W % 4 != 0 keeps the 4-byte copies; each shape also with the
+# 4-byte copies forced (CONV2D_SLICE_X1), and with one and two slice buffers (CONV2D_SLICE_DB)
+X4 = [
+    _shape(2, 3, 32, 32, 16, 7, 7, st=(2, 2), pd=(3, 3), seed=370),
+    _shape(1, 5, 20, 24, 40, 3, 3, pd=(1, 1), seed=371),
+    _shape(1, 3, 16, 16, 8, 5, 5, pd=(2, 2), seed=372),
+    _shape(1, 4, 12, 20, 8, 3, 3, seed=373),
+    _shape(1, 3, 12, 16, 8, 5, 5, pd=(2, 4), seed=374),
+    _shape(2, 3, 20, 28, 70, 3, 3, st=(1, 2), pd=(2, 1), dl=(2, 1), seed=375),
+    _shape(1, 2, 6, 248, 8, 3, 5, pd=(1, 2), seed=376),
+    _shape(1, 3, 15, 18, 8, 3, 3, pd=(1, 1), seed=377),
+]
+
+
+@pytest.mark.parametrize("db", ["1", "0"], ids=["two-buffers", "one-buffer"])
+@pytest.mark.parametrize("copy", ["x4", "x1"])
+@pytest.mark.parametrize("waves", ["4", "8", "16"])
+@pytest.mark.parametrize("idx", range(len(X4)))
+def test_slice_x4_copies(idx, waves, copy, db):
+    cs = X4[idx]
+    with _Env(CONV2D_SLICE_X1="1" if copy == "x1" else "", CONV2D_SLICE_DB=db):
+        _check(cs, IMPLICIT, kernel="1", waves=waves)
+        _check(cs, IMPLICIT, "integer", kernel="1", waves=waves)
 
 
 # the sliced kernel's packed-row bf16 layout: input pairs per LDS word, filter rows padded to 8
