@@ -451,7 +451,20 @@ slice_conv_kernel(SliceArgs A) {
             float b0 = __builtin_bit_cast(float, xp[o.x]), b1 = __builtin_bit_cast(float, xp[o.y]),
                   b2 = __builtin_bit_cast(float, xp[o.z]), b3 = __builtin_bit_cast(float, xp[o.w]);
             o = *reinterpret_cast<const int4*>(kp + min(4, last));
-            for (int kk = 0; kk < A.kh; kk += 4) {
+            auto group = [&](const f32x4& x0, const f32x4& x1, float y0, float y1, float y2, float y3) {
+                acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(x0[0], y0, acc0, 0, 0, 0);
+                acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(x1[0], y0, acc1, 0, 0, 0);
+                acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(x0[1], y1, acc0, 0, 0, 0);
+                acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(x1[1], y1, acc1, 0, 0, 0);
+                acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(x0[2], y2, acc0, 0, 0, 0);
+                acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(x1[2], y2, acc1, 0, 0, 0);
+                acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(x0[3], y3, acc0, 0, 0, 0);
+                acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(x1[3], y3, acc1, 0, 0, 0);
+            };
+            // two groups per trip, the operands alternating between two register sets (a
+            // rotation at the end of every group cost 8 moves per 8 MFMAs, and the vector ALU
+            // does not run beside the MFMAs)
+            for (int kk = 0; kk < A.kh; kk += 8) {
                 const int kn = min(kk + 4, last);
                 const f32x4 a0n = *reinterpret_cast<const f32x4*>(wa0 + kn);
                 const f32x4 a1n = *reinterpret_cast<const f32x4*>(wa1 + kn);
@@ -460,17 +473,19 @@ slice_conv_kernel(SliceArgs A) {
                 o = *reinterpret_cast<const int4*>(kp + min(kk + 8, last));
                 // keep the next group's reads ahead of this group's MFMAs
                 __builtin_amdgcn_sched_barrier(0);
-                acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a0[0], b0, acc0, 0, 0, 0);
-                acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[0], b0, acc1, 0, 0, 0);
-                acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a0[1], b1, acc0, 0, 0, 0);
-                acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[1], b1, acc1, 0, 0, 0);
-                acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a0[2], b2, acc0, 0, 0, 0);
-                acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[2], b2, acc1, 0, 0, 0);
-                acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a0[3], b3, acc0, 0, 0, 0);
-                acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[3], b3, acc1, 0, 0, 0);
-                a0 = a0n;
-                a1 = a1n;
-                b0 = c0; b1 = c1; b2 = c2; b3 = c3;
+                group(a0, a1, b0, b1, b2, b3);
+                __builtin_amdgcn_sched_barrier(0);
+                if (kk + 4 >= A.kh) break;
+                const int km = min(kk + 8, last);
+                a0 = *reinterpret_cast<const f32x4*>(wa0 + km);
+                a1 = *reinterpret_cast<const f32x4*>(wa1 + km);
+                b0 = __builtin_bit_cast(float, xp[o.x]);
+                b1 = __builtin_bit_cast(float, xp[o.y]);
+                b2 = __builtin_bit_cast(float, xp[o.z]);
+                b3 = __builtin_bit_cast(float, xp[o.w]);
+                o = *reinterpret_cast<const int4*>(kp + min(kk + 12, last));
+                __builtin_amdgcn_sched_barrier(0);
+                group(a0n, a1n, c0, c1, c2, c3);
             }
         } else {
             // MFMA 32x32x16 bf16: a step takes 8 consecutive reduction indices of the lane's
@@ -605,6 +620,23 @@ slice_conv_kernel(SliceArgs A) {
                     store_out2<TOut>(ry, ybase + (uint32_t)(m + 32) * (uint32_t)howo, pok2 & (m + 32 < A.Kg),
                                      odd ? r : fa, odd ? fb : r);
                 }
+            }
+        } else if (sizeof(TOut) == 4 && m0 + 64 <= A.Kg) {
+            // NCHW fp32 with all 64 channels: one byte offset per lane plus a wave-uniform step
+            // per store (one add instead of a bounds test and an address per store; a lane past
+            // the plane starts in the out-of-range half and stays there)
+            const uint32_t lb = pok ? ((uint32_t)(tl.n * A.K + gi * A.Kg + m0 + 4 * lrow) * (uint32_t)howo +
+                                       (uint32_t)p) * 4u
+                                    : OOB_OFF;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const uint32_t c0 = (uint32_t)(8 * (v >> 2) + (v & 3)) * (uint32_t)howo * 4u;
+                const uint32_t c1 = c0 + 32u * (uint32_t)howo * 4u;
+                // (through float temporaries: this compiler turns a bit cast of an element of a
+                // 16-wide vector into element 0)
+                const float f0 = acc0[v], f1 = acc1[v];
+                st_f32(ry, lb + c0, f0);
+                st_f32(ry, lb + c1, f1);
             }
         } else {
             const uint32_t ybase = (uint32_t)(tl.n * A.K + gi * A.Kg) * (uint32_t)howo + (uint32_t)p;
