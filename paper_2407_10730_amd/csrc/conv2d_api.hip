@@ -1288,7 +1288,7 @@ int conv2d_desc_create(const conv2d_params* params, conv2d_desc** out) {
         const int64_t force_nw = env_int64("CONV2D_SLICE_WAVES", 0);
         if (force_nw == 4 || force_nw == 8 || (force_nw == 16 && g.xdt == CONV2D_F32)) nw = (int)force_nw;
         const int64_t force_db = env_int64("CONV2D_SLICE_DB", -1);
-        const bool db = force_db < 0 ? tiles(nw) >= 512 : force_db != 0;
+        const bool db = force_db < 0 ? g.xdt == CONV2D_F32 && tiles(nw) >= 512 : force_db != 0;
         d->slice = slice_plan(g.Cg, g.R, g.S, g.Ho, g.Wo, g.sh, g.sw, g.dh, g.dw, g.xdt, nw, g.W, g.pw,
                               !std::getenv("CONV2D_SLICE_UNPACKED"), db);
         if (!d->slice.ok && nw == 16 && force_nw != 16) {

@@ -469,6 +469,11 @@ PACKED = [
     _shape(2, 6, 15, 18, 24, 3, 2, st=(2, 1), pd=(2, 1), dl=(2, 1), seed=365),
     _shape(1, 8, 13, 16, 48, 3, 3, st=(1, 2), pd=(1, 1), g=2, seed=366),
     _shape(3, 1, 40, 46, 96, 7, 5, st=(2, 3), pd=(3, 2), seed=367),
+    # wider rows, paddings 2, 0, 3, 7, 8-tap rows
+    _shape(1, 3, 20, 32, 24, 5, 5, pd=(2, 2), seed=368),
+    _shape(2, 2, 18, 40, 16, 3, 3, seed=369),
+    _shape(1, 4, 15, 48, 40, 7, 7, st=(2, 2), pd=(3, 3), seed=402),
+    _shape(1, 3, 12, 24, 16, 8, 8, pd=(4, 7), seed=403),
 ]
 
 
