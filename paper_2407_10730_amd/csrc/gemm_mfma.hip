@@ -570,6 +570,45 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void ge
             areg[i] = __builtin_amdgcn_raw_buffer_load_b128(ra, ((m < A.M) & qa) ? (uint32_t)(e0 * 2) : OOB_OFF, 0, 0);
         }
     };
+    // NHWC gather with C/g >= BK: 32-bit byte offsets per load unit computed once, so a stage
+    // adds one wave-uniform offset per load (the 64-bit address arithmetic and the bounds tests
+    // per load had cost about 9 vector instructions per MFMA, and the vector ALU does not run
+    // beside the MFMAs).  nb_off: window origin + chunk of unit i (a window starting in the
+    // padding wraps; the offset of every tap inside the image comes out right modulo 2^32);
+    // vb_off: the same plus the current tap's offset, or out of range where that tap falls
+    // outside the image (recomputed when the tap changes); na_off: weight row + chunk.
+    uint32_t nb_off[NHWC ? BUNITS : 1], vb_off[NHWC ? BUNITS : 1], na_off[NHWC ? AUNITS : 1];
+    auto tap_offsets = [&]() {
+        if constexpr (NHWC) {
+            const int roff = cur_r * A.dh, soff = cur_s * A.dw;
+            const uint32_t tb = (uint32_t)((roff * A.W + soff) * A.Cx) * 2u;
+#pragma unroll
+            for (int i = 0; i < BUNITS; ++i) {
+                const bool ok = ((unsigned)(csn[i].hi0 + roff) < (unsigned)A.H) &
+                                ((unsigned)(csn[i].wi0 + soff) < (unsigned)A.W);
+                vb_off[i] = ok ? nb_off[i] + tb : OOB_OFF;
+            }
+        }
+    };
+    const bool nhwc_fast = NHWC && A.Cg >= BK;
+    if constexpr (NHWC) {
+        if (nhwc_fast) {
+#pragma unroll
+            for (int i = 0; i < BUNITS; ++i) {
+                const int kc = (t + i * 256) % CPR;
+                nb_off[i] = (uint32_t)(csn[i].base + kc * 8) * 2u;
+            }
+#pragma unroll
+            for (int i = 0; i < AUNITS; ++i) {
+                const int u = t + i * 256;
+                const bool qa = AQ % 256 == 0 || u < AQ;
+                const int m = m0 + u / CPR;
+                const int kc = u % CPR;
+                na_off[i] = ((m < A.M) & qa) ? (uint32_t)(a_base + (int64_t)m * A.lda + kc * 8) * 2u : OOB_OFF;
+            }
+            tap_offsets();
+        }
+    }
     auto advance_tap = [&]() {
         cur_c0 += BK;
         if (cur_c0 >= A.Cg) {
@@ -632,18 +671,15 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void ge
                     ra, (m < A.M) & (kr < A.Kred) & qa ? (uint32_t)(e0 * 2) : OOB_OFF, 0, 0);
             }
         } else if constexpr (NHWC) {
-            const int roff = cur_r * A.dh, soff = cur_s * A.dw;
-            const int64_t tapoff = ((int64_t)roff * A.W + soff) * A.Cx + cur_c0;
+            const uint32_t cb = (uint32_t)cur_c0 * 2u;
 #pragma unroll
-            for (int i = 0; i < BUNITS; ++i) {
-                const int kc = (t + i * 256) % CPR;
-                const int hi = csn[i].hi0 + roff, wi = csn[i].wi0 + soff;
-                const bool ok = ((unsigned)hi < (unsigned)A.H) & ((unsigned)wi < (unsigned)A.W);
-                const int64_t e = csn[i].base + tapoff + kc * 8;
-                breg[i] = __builtin_amdgcn_raw_buffer_load_b128(rb, ok ? (uint32_t)(e * 2) : OOB_OFF, 0, 0);
-            }
-            load_weights_tap();
+            for (int i = 0; i < BUNITS; ++i)
+                breg[i] = __builtin_amdgcn_raw_buffer_load_b128(rb, vb_off[i] + cb, 0, 0);
+            const uint32_t ab = (uint32_t)((cur_r * A.S + cur_s) * A.Cg + cur_c0) * 2u;
+#pragma unroll
+            for (int i = 0; i < AUNITS; ++i) areg[i] = __builtin_amdgcn_raw_buffer_load_b128(ra, na_off[i] + ab, 0, 0);
             advance_tap();
+            if (cur_c0 == 0) tap_offsets();
         } else if constexpr (BSRC == BSRC_IMPLICIT_TAP) {
             const int roff = cur_r * A.dh, soff = cur_s * A.dw;
             const int hi = cs.hi0 + roff, wi = cs.wi0 + soff;
