@@ -286,6 +286,16 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 16 ? 7 : 1)) void ge
 
     f32x4 breg0[BRUNS][BCOLS], breg1[BRUNS][BCOLS];
     f32x4 areg0[ARUNS], areg1[ARUNS];
+    // tap-major weights: byte offset of each A run's row and channel quad, computed once (a
+    // stage then adds one uniform offset per load instead of 64-bit index arithmetic)
+    uint32_t na_off[ARUNS];
+#pragma unroll
+    for (int g = 0; g < ARUNS; ++g) {
+        const int q = t + g * 256;
+        const bool qa = AQ % 256 == 0 || q < AQ;
+        const int m = m0 + q / (BK / 4);
+        na_off[g] = ((m < A.M) & qa) ? (uint32_t)(a_base + (int64_t)m * A.lda + 4 * (q % (BK / 4))) * 4u : OOB_OFF;
+    }
     // tap-major cursor of the next stage to load.  Channel blocks outermost, filter
     // taps innermost: the taps of one channel block re-read the same input lines,
     // which then hit in L1.
@@ -330,17 +340,12 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 16 ? 7 : 1)) void ge
                     }
             }
             // weights in tap-major order [K][R*S][C/g]: 4 consecutive channels per 16-byte load
-            const int tap = cur_r * A.S + cur_s;
+            const uint32_t ab = (uint32_t)((cur_r * A.S + cur_s) * A.Cg + cur_c0) * 4u;
 #pragma unroll
             for (int g = 0; g < ARUNS; ++g) {
-                const int q = t + g * 256;
-                const bool qa = AQ % 256 == 0 || q < AQ;
-                const int m = m0 + q / (BK / 4);
-                const int64_t e = a_base + (int64_t)m * A.lda + (int64_t)tap * A.Cg + cur_c0 + 4 * (q % (BK / 4));
                 // bit-cast the whole vector: casting its elements one by one made this
                 // compiler emit a single-dword load
-                areg[g] = __builtin_bit_cast(
-                    f32x4, __builtin_amdgcn_raw_buffer_load_b128(ra, ((m < A.M) & qa) ? (uint32_t)(e * 4) : OOB_OFF, 0, 0));
+                areg[g] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(ra, na_off[g] + ab, 0, 0));
             }
             if (++cur_s == A.S) {
                 cur_s = 0;
