@@ -351,6 +351,55 @@ __global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ in
     }
 }
 
+// The same transform with 64x64 tiles when rows and cols are multiples of 4: a thread moves
+// 4 consecutive elements per global access (8 bytes in bf16, 16 in fp32: the 32x32 kernel's
+// 2-byte accesses moved bf16 at about 3 TB/s).  The tile keeps one element per 4-byte LDS word
+// with a row pitch of 65 words, so the column reads of the write phase spread over all banks.
+// grid (ceil(cols/64), ceil(rows/64), n).
+template <typename T>
+__global__ __launch_bounds__(256) void transpose64_kernel(const T* __restrict__ in, T* __restrict__ out,
+                                                          int64_t rows, int64_t cols) {
+    typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+    typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+    __shared__ uint32_t tile[64][65];
+    const int64_t img = blockIdx.z;
+    const int64_t c0 = (int64_t)blockIdx.x * 64, r0 = (int64_t)blockIdx.y * 64;
+    const T* src = in + img * rows * cols;
+    T* dst = out + img * rows * cols;
+    const int tq = threadIdx.x & 15, tr = threadIdx.x >> 4;  // quad of 4 elements, row of 16
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int lr = tr + 16 * i;
+        const int64_t r = r0 + lr, c = c0 + 4 * tq;
+        uint32_t e[4] = {0, 0, 0, 0};
+        if (r < rows && c < cols) {  // cols % 4 == 0: the whole quad is inside
+            if constexpr (sizeof(T) == 2) {
+                const u32x2_t v = *reinterpret_cast<const u32x2_t*>(src + r * cols + c);
+                e[0] = v[0] & 0xFFFFu; e[1] = v[0] >> 16; e[2] = v[1] & 0xFFFFu; e[3] = v[1] >> 16;
+            } else {
+                const u32x4_t v = *reinterpret_cast<const u32x4_t*>(src + r * cols + c);
+                e[0] = v[0]; e[1] = v[1]; e[2] = v[2]; e[3] = v[3];
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) tile[lr][4 * tq + k] = e[k];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int lc = tr + 16 * i;
+        const int64_t c = c0 + lc, r = r0 + 4 * tq;
+        if (c < cols && r < rows) {  // rows % 4 == 0
+            const uint32_t e0 = tile[4 * tq][lc], e1 = tile[4 * tq + 1][lc], e2 = tile[4 * tq + 2][lc],
+                           e3 = tile[4 * tq + 3][lc];
+            if constexpr (sizeof(T) == 2)
+                *reinterpret_cast<u32x2_t*>(dst + c * rows + r) = u32x2_t{e0 | (e1 << 16), e2 | (e3 << 16)};
+            else
+                *reinterpret_cast<u32x4_t*>(dst + c * rows + r) = u32x4_t{e0, e1, e2, e3};
+        }
+    }
+}
+
 // The same transform when one side has at most NARROW_MAX entries (an image with few channels):
 // the 32x32 tiles would stay mostly empty, so a thread takes one index j of the long side and
 // moves its short row (reads or writes of consecutive threads are adjacent for every short
@@ -390,6 +439,19 @@ static hipError_t launch_transpose(const void* src, void* dst, int64_t n, int64_
     if (std::min(rows, cols) <= NARROW_MAX) {
         if (elem_bytes == 4) launch_narrow<uint32_t>(src, dst, n, rows, cols, stream);
         else launch_narrow<uint16_t>(src, dst, n, rows, cols, stream);
+        return hipGetLastError();
+    }
+    // (CONV2D_TRANSPOSE32=1 keeps the 32x32 kernel: tests run both)
+    const char* t32 = std::getenv("CONV2D_TRANSPOSE32");
+    if (rows % 4 == 0 && cols % 4 == 0 && ((uintptr_t)src & 15) == 0 && ((uintptr_t)dst & 15) == 0 &&
+        !(t32 && t32[0] == '1')) {
+        dim3 grid64((unsigned)((cols + 63) / 64), (unsigned)((rows + 63) / 64), (unsigned)n);
+        if (elem_bytes == 4)
+            hipLaunchKernelGGL(transpose64_kernel<uint32_t>, grid64, dim3(256), 0, stream, (const uint32_t*)src,
+                               (uint32_t*)dst, rows, cols);
+        else
+            hipLaunchKernelGGL(transpose64_kernel<uint16_t>, grid64, dim3(256), 0, stream, (const uint16_t*)src,
+                               (uint16_t*)dst, rows, cols);
         return hipGetLastError();
     }
     dim3 grid((unsigned)((cols + 31) / 32), (unsigned)((rows + 31) / 32), (unsigned)n);

@@ -632,6 +632,29 @@ def test_depthwise_rows(idx, dt, rows):
             _check(cs, DIRECT, "integer")
 
 
+# NHWC <-> NCHW copies: the 64x64 vector kernel (both sides multiples of 4, ragged tiles) and the
+# 32x32 element kernel (CONV2D_TRANSPOSE32, and sides that are not multiples of 4), through NHWC
+# convolutions that reorder x and y
+TRANSPOSE = [
+    _shape(2, 64, 14, 14, 64, 3, 3, pd=(1, 1), seed=410),
+    _shape(1, 36, 9, 20, 12, 3, 3, seed=411),
+    _shape(1, 12, 7, 9, 16, 1, 1, seed=412),
+    _shape(2, 200, 10, 10, 24, 3, 3, pd=(1, 1), seed=413),
+]
+
+
+@pytest.mark.parametrize("kernel", ["64", "32"])
+@pytest.mark.parametrize("dt", [("f32", "f32"), ("bf16", "bf16")], ids=lambda d: d[0])
+@pytest.mark.parametrize("idx", range(len(TRANSPOSE)))
+def test_layout_transposes(idx, dt, kernel):
+    cs = TRANSPOSE[idx].with_(layout="nhwc", x_dtype=dt[0], y_dtype=dt[1])
+    with _Env(CONV2D_TRANSPOSE32="1" if kernel == "32" else ""):
+        for algo in (IMPLICIT, IM2COL):
+            _check(cs, algo)
+            if dt[1] == "f32":
+                _check(cs, algo, "integer")
+
+
 # Winograd F(2x2, 3x3): 3x3, stride 1, dilation 1, one group, fp32; odd output sizes (clipped
 # 2x2 tiles), paddings 0/1/2, channel counts across GEMM tiles, NHWC, chunked tiles
 WINOGRAD = B.CONV2D_ALGO_WINOGRAD
