@@ -153,6 +153,12 @@ GemmPlan choose_tile(int64_t M, int64_t P, int64_t G, int64_t kred, int xdt, int
     }
     // (64-deep bf16 stages only on 64-row tiles: a 32 x 256 tile with them holds 83 KiB of LDS)
     if (best.kind == 0) best.bk = xdt == CONV2D_BF16 ? (nhwc && cg % 64 == 0 && best.bm > 32 ? 64 : 32) : 16;
+    // bf16 NHWC gather with 64-deep stages: two register sets, the loads two stages ahead
+    // (1-4 % on large layers; CONV2D_BF16_PF=1 takes one set)
+    if (xdt == CONV2D_BF16 && nhwc && best.bk == 64) {
+        const char* e = std::getenv("CONV2D_BF16_PF");
+        best.pf = e && e[0] == '1' ? 1 : 2;
+    }
     // fp32 64x64 tiles over a long tap-major reduction: 32-deep stages with the loads two
     // stages ahead (half the barriers per MFMA; cfg2 76 -> 72-74 us, N31 71.5 -> 69.4 us on
     // MI355X; no gain at reductions of 256)
@@ -171,7 +177,7 @@ GemmPlan choose_tile(int64_t M, int64_t P, int64_t G, int64_t kred, int xdt, int
             if (xdt == CONV2D_BF16 || gemm32_f32_supported(a, bk, pf)) {
                 best.kind = 0; best.tile = a; best.bm = kTileShapes[a].bm; best.bn = kTileShapes[a].bn;
                 best.bk = bk;
-                best.pf = xdt == CONV2D_BF16 ? 1 : pf;
+                best.pf = xdt == CONV2D_BF16 ? (nhwc && bk == 64 && pf == 2 ? 2 : 1) : pf;
             }
         }
     }
@@ -182,7 +188,9 @@ GemmPlan choose_tile(int64_t M, int64_t P, int64_t G, int64_t kred, int xdt, int
 hipError_t dispatch_gemm(const GemmPlan& gp, const GemmArgs& a_in, int bsrc, int epi, int xdt, int ydt,
                          int groups, hipStream_t s) {
     const GemmArgs& a = a_in;
-    return launch_gemm(a, gp.tile, gp.bk, gp.pf, bsrc, epi, xdt, ydt, groups, s);
+    // (bf16: the two-stage register prefetch exists for the NHWC gather only)
+    const int pf = xdt == CONV2D_BF16 && bsrc != BSRC_NHWC_TAP ? 1 : gp.pf;
+    return launch_gemm(a, gp.tile, gp.bk, pf, bsrc, epi, xdt, ydt, groups, s);
 }
 
 // Workspace slots of a descriptor (one use each).

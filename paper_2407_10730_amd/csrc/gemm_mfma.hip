@@ -74,6 +74,35 @@ __device__ __forceinline__ void store_tile(const GemmArgs& A, f32x16 (&acc)[TM][
         }
         return;
     }
+    if constexpr (EPI == EPI_NCHW && sizeof(TOut) == 2) {
+        if (mb + TM * 32 <= A.M) {
+            // bf16 NCHW, the wave's rows all inside M: one byte base per lane and column tile,
+            // the row offsets wave-uniform (the store's scalar offset), and one packed
+            // conversion for each two rows of a lane (the rows of v and v + 1, v even)
+            const int rs = A.HoWo * 2;  // bytes between output rows
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int p = pb + j * 32 + lcol;
+                uint32_t lb = OOB_OFF;
+                if (p < A.P) {
+                    const int n_img = p / A.HoWo;
+                    const int hw = p - n_img * A.HoWo;
+                    lb = (uint32_t)((int64_t)n_img * A.y_nstride + ((int64_t)gi * A.M + mb + 4 * lrow) * A.HoWo + hw) * 2u;
+                }
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int v = 0; v < 16; v += 2) {
+                        const uint32_t w = __builtin_bit_cast(
+                            uint32_t, __builtin_convertvector(f32x2{acc[i][j][v], acc[i][j][v + 1]}, bf16x2));
+                        const int r0 = i * 32 + 8 * (v >> 2) + (v & 3);
+                        __builtin_amdgcn_raw_buffer_store_b16((uint16_t)w, ry, lb, r0 * rs, 0);
+                        __builtin_amdgcn_raw_buffer_store_b16((uint16_t)(w >> 16), ry, lb, (r0 + 1) * rs, 0);
+                    }
+            }
+            return;
+        }
+    }
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
         const int p = pb + j * 32 + lcol;
@@ -455,19 +484,25 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 16 ? 7 : 1)) void ge
             __syncthreads();
         }
     } else {
+        // The loads past the block's last stage are issued too (except through the tap table,
+        // which they would read past): they read inside or past the tensors, where the buffer
+        // range check returns zero, and are never stored.  With a condition on them, the wait
+        // before the LDS stores would have to cover the path without them and so would wait
+        // for the loads just issued as well.
+        constexpr bool kAlways = BSRC != BSRC_IMPLICIT_NCHW;
         load_stage(s_begin, breg0, areg0);
         if (n > 1) load_stage(s_begin + 1, breg1, areg1);
         store_stage(0, breg0, areg0);
         __syncthreads();
         for (int j = 0; j < n; j += 2) {
             // even stage: set 0 is free, set 1 holds stage j+1
-            if (j + 2 < n) load_stage(s_begin + j + 2, breg0, areg0);
+            if (kAlways || j + 2 < n) load_stage(s_begin + j + 2, breg0, areg0);
             if (!A.loader_only) compute(0);
             if (j + 1 < n) store_stage(1, breg1, areg1);
             __syncthreads();
             if (j + 1 >= n) break;
             // odd stage: set 1 is free, set 0 holds stage j+2
-            if (j + 3 < n) load_stage(s_begin + j + 3, breg1, areg1);
+            if (kAlways || j + 3 < n) load_stage(s_begin + j + 3, breg1, areg1);
             if (!A.loader_only) compute(1);
             if (j + 2 < n) store_stage(0, breg0, areg0);
             __syncthreads();
@@ -494,7 +529,7 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 16 ? 7 : 1)) void ge
 // pixel's stage row come from consecutive threads (one 64- or 128-byte run).
 
 
-template <int BM, int BN, int WM, int WN, int BK, int BSRC, int EPI, typename TOut>
+template <int BM, int BN, int WM, int WN, int BK, int PF, int BSRC, int EPI, typename TOut>
 __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void gemm_bf16_kernel(GemmArgs A) {
     constexpr int LDK = BK + 8;
     constexpr int WTM = BM / WM, WTN = BN / WN;
@@ -549,20 +584,27 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void ge
     // A: unit u = t + i*256 -> row m = u / CPR, k chunk kc = u % CPR
     const int64_t a_base = (int64_t)gi * A.a_gstride;
 
-    u32x4 breg[BUNITS];
-    u32x4 areg[AUNITS];
+    // staging registers: PF sets, the loads of a stage issued PF stages before its compute
+    static_assert(PF == 1 || PF == 2, "prefetch distance");
+    u32x4 bset[PF][BUNITS];
+    u32x4 aset[PF][AUNITS];
     int cur_c0 = 0, cur_r = 0, cur_s = 0;  // tap-major cursor of the next stage
     if constexpr (BSRC == BSRC_IMPLICIT_TAP || BSRC == BSRC_NHWC_TAP) {
-        if (A.Cg >= BK) {  // (C/g < BK: the small-group NHWC gather indexes by stage)
+        if (A.Cg >= BK) {  // (C/g < BK, 32-deep stages only: the small-group NHWC gather indexes by stage)
             const int cblocks = A.Cg / BK;
             const int tap = s_begin / cblocks;
             cur_c0 = (s_begin - tap * cblocks) * BK;
             cur_r = tap / A.S;
             cur_s = tap - cur_r * A.S;
         }
+        // the divisions above run on the vector unit; the cursor is block-uniform, and taking
+        // it into scalar registers keeps its per-stage update off the vector ALU
+        cur_c0 = __builtin_amdgcn_readfirstlane(cur_c0);
+        cur_r = __builtin_amdgcn_readfirstlane(cur_r);
+        cur_s = __builtin_amdgcn_readfirstlane(cur_s);
     }
 
-    auto load_weights_tap = [&]() {
+    auto load_weights_tap = [&](u32x4 (&areg)[AUNITS]) {
         // weights in tap-major order [K][R*S][C/g]: 8 consecutive channels per 16-byte load
         const int tap = cur_r * A.S + cur_s;
 #pragma unroll
@@ -595,7 +637,7 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void ge
             }
         }
     };
-    const bool nhwc_fast = NHWC && A.Cg >= BK;
+    const bool nhwc_fast = NHWC && (BK == 64 || A.Cg >= BK);
     if constexpr (NHWC) {
         if (nhwc_fast) {
 #pragma unroll
@@ -625,7 +667,7 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void ge
         }
     };
 
-    auto load_stage = [&](int stage) {
+    auto load_stage = [&](int stage, u32x4 (&breg)[BUNITS], u32x4 (&areg)[AUNITS]) {
         const int k0 = stage * BK;
         uint16_t h[8];
         if constexpr (BSRC == BSRC_DENSE_T) {
@@ -649,7 +691,7 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void ge
                 areg[i] = __builtin_amdgcn_raw_buffer_load_b128(
                     ra, (m < A.M) & (kr < A.Kred) & qa ? (uint32_t)(e0 * 2) : OOB_OFF, 0, 0);
             }
-        } else if (NHWC && A.Cg < BK) {
+        } else if (NHWC && BK == 32 && A.Cg < BK) {
             // C/g = 8 or 16: a stage holds BK / (C/g) whole taps; chunk kc of a pixel is the
             // 8 channels (kc*8) % (C/g) .. +7 of tap k0/(C/g) + kc*8/(C/g) (zero past the last tap)
 #pragma unroll
@@ -676,13 +718,14 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void ge
                     ra, (m < A.M) & (kr < A.Kred) & qa ? (uint32_t)(e0 * 2) : OOB_OFF, 0, 0);
             }
         } else if constexpr (NHWC) {
-            const uint32_t cb = (uint32_t)cur_c0 * 2u;
+            // the stage's uniform part goes in the scalar offset: lanes whose vector offset is
+            // out of range stay out of range, the others address inside the tensor
+            const int cb = cur_c0 * 2;
 #pragma unroll
-            for (int i = 0; i < BUNITS; ++i)
-                breg[i] = __builtin_amdgcn_raw_buffer_load_b128(rb, vb_off[i] + cb, 0, 0);
-            const uint32_t ab = (uint32_t)((cur_r * A.S + cur_s) * A.Cg + cur_c0) * 2u;
+            for (int i = 0; i < BUNITS; ++i) breg[i] = __builtin_amdgcn_raw_buffer_load_b128(rb, vb_off[i], cb, 0);
+            const int ab = ((cur_r * A.S + cur_s) * A.Cg + cur_c0) * 2;
 #pragma unroll
-            for (int i = 0; i < AUNITS; ++i) areg[i] = __builtin_amdgcn_raw_buffer_load_b128(ra, na_off[i] + ab, 0, 0);
+            for (int i = 0; i < AUNITS; ++i) areg[i] = __builtin_amdgcn_raw_buffer_load_b128(ra, na_off[i], ab, 0);
             advance_tap();
             if (cur_c0 == 0) tap_offsets();
         } else if constexpr (BSRC == BSRC_IMPLICIT_TAP) {
@@ -699,7 +742,7 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void ge
 #pragma unroll
                 for (int q = 0; q < 4; ++q) breg[i][q] = (uint32_t)h[2 * q] | ((uint32_t)h[2 * q + 1] << 16);
             }
-            load_weights_tap();
+            load_weights_tap(areg);
             advance_tap();
         } else {
 #pragma unroll
@@ -739,12 +782,29 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void ge
             }
         }
     };
-    auto store_stage = [&](int buf) {
+    // LDS byte offsets of this thread's B chunks (K-contiguous sources), computed once and kept
+    // in registers (recomputing them per stage cost vector instructions)
+    uint32_t bs_off[KCONT ? BUNITS : 1];
+    if constexpr (KCONT) {
+#pragma unroll
+        for (int i = 0; i < BUNITS; ++i) {
+            const int u = t + i * 256;
+            bs_off[i] = (uint32_t)(((u / CPR) * LDK + (u % CPR) * 8) * 2);
+            asm volatile("" : "+v"(bs_off[i]));
+        }
+    }
+    uint32_t as_off[AUNITS];
+#pragma unroll
+    for (int i = 0; i < AUNITS; ++i) {
+        const int u = t + i * 256;
+        as_off[i] = (uint32_t)(((u / CPR) * LDK + (u % CPR) * 8) * 2);
+        asm volatile("" : "+v"(as_off[i]));
+    }
+    auto store_stage = [&](int buf, const u32x4 (&breg)[BUNITS], const u32x4 (&areg)[AUNITS]) {
 #pragma unroll
         for (int i = 0; i < BUNITS; ++i) {
             if constexpr (KCONT) {
-                const int u = t + i * 256;
-                *reinterpret_cast<u32x4*>(&Bs[buf][u / CPR][(u % CPR) * 8]) = breg[i];
+                *reinterpret_cast<u32x4*>(reinterpret_cast<char*>(&Bs[buf][0][0]) + bs_off[i]) = breg[i];
             } else {
                 const int kc = bkc0 + i * (256 / BN);
                 *reinterpret_cast<u32x4*>(&Bs[buf][bn][kc * 8]) = breg[i];
@@ -753,7 +813,8 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void ge
 #pragma unroll
         for (int i = 0; i < AUNITS; ++i) {
             const int u = t + i * 256;
-            if (AQ % 256 == 0 || u < AQ) *reinterpret_cast<u32x4*>(&As[buf][u / CPR][(u % CPR) * 8]) = areg[i];
+            if (AQ % 256 == 0 || u < AQ)
+                *reinterpret_cast<u32x4*>(reinterpret_cast<char*>(&As[buf][0][0]) + as_off[i]) = areg[i];
         }
     };
 
@@ -770,32 +831,92 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void ge
     const int lrow = lane >> 5;
     const int lcol = lane & 31;
 
-    load_stage(s_begin);
-    store_stage(0);
-    __syncthreads();
-    for (int st = s_begin; st < s_end; ++st) {
-        const int buf = (st - s_begin) & 1;
-        const bool more = st + 1 < s_end;
-        if (more) load_stage(st + 1);
-        if (!A.loader_only) {
+    auto compute = [&](int buf) {
 #pragma unroll
-            for (int ks = 0; ks < BK / 16; ++ks) {
-                bf16x8 a[TM], b[TN];
+        for (int ks = 0; ks < BK / 16; ++ks) {
+            bf16x8 a[TM], b[TN];
 #pragma unroll
-                for (int i = 0; i < TM; ++i)
-                    a[i] = *reinterpret_cast<const bf16x8*>(&As[buf][wm0 + i * 32 + lcol][ks * 16 + 8 * lrow]);
+            for (int i = 0; i < TM; ++i)
+                a[i] = *reinterpret_cast<const bf16x8*>(&As[buf][wm0 + i * 32 + lcol][ks * 16 + 8 * lrow]);
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                b[j] = *reinterpret_cast<const bf16x8*>(&Bs[buf][wn0 + j * 32 + lcol][ks * 16 + 8 * lrow]);
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    b[j] = *reinterpret_cast<const bf16x8*>(&Bs[buf][wn0 + j * 32 + lcol][ks * 16 + 8 * lrow]);
-#pragma unroll
-                for (int i = 0; i < TM; ++i)
-#pragma unroll
-                    for (int j = 0; j < TN; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-            }
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
         }
-        if (more) store_stage(buf ^ 1);
-        __syncthreads();
+    };
+
+    // The 128 x 128 tile's stage with 64-deep reduction in one scheduling region: the operand
+    // reads of k-step ks + 1 and the LDS stores of the next stage (set sb/sa into buffer wb)
+    // are issued between the MFMAs of k-step ks, in the order the group barriers below give,
+    // so that the matrix unit is not left waiting on LDS latency between k-steps.
+    auto compute_store = [&](int rb, int wb, const u32x4 (&sb)[BUNITS], const u32x4 (&sa)[AUNITS]) {
+        bf16x8 a[2][TM], b[2][TN];
+        auto rd = [&](int ks, int o) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+                a[o][i] = *reinterpret_cast<const bf16x8*>(&As[rb][wm0 + i * 32 + lcol][ks * 16 + 8 * lrow]);
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                b[o][j] = *reinterpret_cast<const bf16x8*>(&Bs[rb][wn0 + j * 32 + lcol][ks * 16 + 8 * lrow]);
+        };
+        rd(0, 0);
+#pragma unroll
+        for (int ks = 0; ks < BK / 16; ++ks) {
+            if (ks + 1 < BK / 16) rd(ks + 1, (ks + 1) & 1);
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks & 1][i], b[ks & 1][j], acc[i][j], 0, 0, 0);
+        }
+        store_stage(wb, sb, sa);
+        if constexpr (TM == 2 && TN == 2 && BK == 64 && BUNITS + AUNITS == 8) {
+#define CV_SG(mask, cnt) __builtin_amdgcn_sched_group_barrier(mask, cnt, 0)
+            CV_SG(0x100, 4);  // operands of k-step 0
+#pragma unroll
+            for (int r = 0; r < 3; ++r) {  // k-steps 0..2: 4 MFMAs, 4 reads, 2 LDS stores each
+                CV_SG(0x008, 1); CV_SG(0x100, 1); CV_SG(0x008, 1); CV_SG(0x100, 1); CV_SG(0x200, 1);
+                CV_SG(0x008, 1); CV_SG(0x100, 1); CV_SG(0x008, 1); CV_SG(0x100, 1); CV_SG(0x200, 1);
+            }
+            CV_SG(0x008, 1); CV_SG(0x200, 1); CV_SG(0x008, 1); CV_SG(0x008, 1); CV_SG(0x200, 1); CV_SG(0x008, 1);
+#undef CV_SG
+        }
+    };
+
+    // Stage jj is computed from LDS buffer jj & 1 while register set jj % PF (free since its
+    // stage went to LDS) takes the loads of stage jj + PF, and set (jj + 1) % PF, stage jj + 1,
+    // goes to the other buffer.  The loop body is unrolled over two stages so that every
+    // buffer and register set index is a constant.
+    constexpr int U = 2;
+    const int n = s_end - s_begin;
+#pragma unroll
+    for (int q = 0; q < PF; ++q)
+        if (q < n) load_stage(s_begin + q, bset[q], aset[q]);
+    store_stage(0, bset[0], aset[0]);
+    __syncthreads();
+    for (int j = 0; j < n; j += U) {
+#pragma unroll
+        for (int q = 0; q < U; ++q) {
+            const int jj = j + q;
+            if (jj >= n) break;
+            // Issued on every stage, also past the block's last one (those loads read inside or
+            // past the tensors, where the buffer range check returns zero, and are never
+            // stored): with a condition here, the wait before the LDS stores would have to cover
+            // the path without these loads and so wait for them too.
+            load_stage(s_begin + jj + PF, bset[q % PF], aset[q % PF]);
+            if (TM == 2 && TN == 2 && BK == 64 && PF == 2 && !A.loader_only) {
+                // (the last stage also stores a stale set into the buffer no stage reads)
+                compute_store(q & 1, (q + 1) & 1, bset[(q + 1) % PF], aset[(q + 1) % PF]);
+            } else {
+                if (!A.loader_only) compute(q & 1);
+                if (jj + 1 < n) store_stage((q + 1) & 1, bset[(q + 1) % PF], aset[(q + 1) % PF]);
+            }
+            __syncthreads();
+        }
     }
 
     if (A.loader_only) return;
@@ -828,19 +949,20 @@ static hipError_t launch_f32(const GemmArgs& a, int bsrc, int epi, int groups, h
     return hipGetLastError();
 }
 
-template <int BM, int BN, int WM, int WN, int BK>
+template <int BM, int BN, int WM, int WN, int BK, int PF>
 static hipError_t launch_bf16(const GemmArgs& a, int bsrc, int epi, int ydt, int groups, hipStream_t stream) {
     dim3 grid((unsigned)(a.grid_p * a.grid_m + a.tail_tiles * (a.tail_pieces - 1)), 1,
               (unsigned)(groups * (a.ksplit > 1 ? a.ksplit : 1)));
-    // NHWC gather: 16-byte channel runs, so C and C/g multiples of 8, and C/g a multiple or a
-    // divisor of the stage depth
-    if (bsrc == BSRC_NHWC_TAP && (a.Cg % 8 != 0 || a.Cx % 8 != 0 || (a.Cg >= BK ? a.Cg % BK : BK % a.Cg) != 0))
+    // NHWC gather: 16-byte channel runs, so C and C/g multiples of 8, and C/g a multiple of the
+    // stage depth or (32-deep stages) a divisor of it
+    if (bsrc == BSRC_NHWC_TAP && (a.Cg % 8 != 0 || a.Cx % 8 != 0 || (a.Cg >= BK ? a.Cg % BK : BK % a.Cg) != 0 ||
+                                  (BK == 64 && a.Cg < BK)))
         return hipErrorInvalidValue;
     // dense B^T: 16-byte rows of 8 reduction values
     if (bsrc == BSRC_DENSE_T && (a.Kred % 8 != 0 || a.ldb % 8 != 0 || a.lda % 8 != 0 || epi != EPI_DENSE))
         return hipErrorInvalidValue;
 #define CV_BF(BS, EP, TO) \
-    hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, BK, BS, EP, TO>), grid, dim3(256), 0, stream, a)
+    hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, BK, PF, BS, EP, TO>), grid, dim3(256), 0, stream, a)
     if (bsrc == BSRC_NHWC_TAP && epi == EPI_NCHW) {
         if (ydt == CONV2D_BF16) CV_BF(BSRC_NHWC_TAP, EPI_NCHW, uint16_t);
         else CV_BF(BSRC_NHWC_TAP, EPI_NCHW, float);
@@ -849,6 +971,8 @@ static hipError_t launch_bf16(const GemmArgs& a, int bsrc, int epi, int ydt, int
         else CV_BF(BSRC_NHWC_TAP, EPI_NHWC, float);
     } else if (bsrc == BSRC_NHWC_TAP && epi == EPI_DENSE) {
         CV_BF(BSRC_NHWC_TAP, EPI_DENSE, float);  // partial sums of a split reduction
+    } else if constexpr (PF != 1) {
+        return hipErrorInvalidValue;  // two register sets only with the NHWC gather
     } else if (bsrc == BSRC_DENSE_T) {
         CV_BF(BSRC_DENSE_T, EPI_DENSE, float);
     } else if (BK != 32) {
@@ -891,10 +1015,13 @@ hipError_t launch_gemm(const GemmArgs& a, int tile, int bk, int pf, int bsrc, in
             return hipErrorInvalidValue;
     }
     if (xdt == CONV2D_BF16) {
-        if (bk != 32 && bk != 64) return hipErrorInvalidValue;
+        // two register sets (pf 2): 64-deep stages with the NHWC gather only
+        if ((bk != 32 && bk != 64) || (pf != 1 && (pf != 2 || bk != 64 || bsrc != BSRC_NHWC_TAP)))
+            return hipErrorInvalidValue;
 #define CV_TB(BMV, BNV, WMV, WNV) \
-    return bk == 64 ? launch_bf16<BMV, BNV, WMV, WNV, 64>(a, bsrc, epi, ydt, groups, stream) \
-                    : launch_bf16<BMV, BNV, WMV, WNV, 32>(a, bsrc, epi, ydt, groups, stream)
+    return bk == 64 ? (pf == 2 ? launch_bf16<BMV, BNV, WMV, WNV, 64, 2>(a, bsrc, epi, ydt, groups, stream) \
+                               : launch_bf16<BMV, BNV, WMV, WNV, 64, 1>(a, bsrc, epi, ydt, groups, stream)) \
+                    : launch_bf16<BMV, BNV, WMV, WNV, 32, 1>(a, bsrc, epi, ydt, groups, stream)
         switch (tile) {
             case TILE_64x64: CV_TB(64, 64, 2, 2);
             case TILE_64x128: CV_TB(64, 128, 1, 4);
