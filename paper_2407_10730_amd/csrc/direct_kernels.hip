@@ -927,7 +927,14 @@ static bool dwr_plan(const DirectArgs& a, int xdt, DwrPlan* p) {
     const int upw = 64 / ncb;
     if (4 * upw * ncb < 3 * 64) return false;  // fewer than three quarters of the lanes busy
     const int64_t planes = (int64_t)a.N * a.K;
-    int64_t nb = (4096LL * upw + planes - 1) / planes;
+    // target wave count: 3x3 filters at dilation 1 split planes into more bands (their 2 halo
+    // rows cost less than the shorter row chains gain: N32 2048 28x28 bf16 51 -> 46 us); at
+    // dilation 2 (4 halo rows: N1 1024 224x224 40 -> 43 us) and for 5x5 and 7x7 (more
+    // arithmetic per row: N32 256 112x112 5x5 3 % slower) whole planes or long bands stay.
+    // CONV2D_DWR_WAVES overrides it.
+    const char* tw = std::getenv("CONV2D_DWR_WAVES");
+    const int64_t waves = tw && std::atoi(tw) > 0 ? std::atoi(tw) : (a.R == 3 && a.dh == 1 ? 16384 : 4096);
+    int64_t nb = (waves * upw + planes - 1) / planes;
     const int nb_max = (a.Ho + 7) / 8;
     if (nb > nb_max) nb = nb_max;
     if (nb < 1) nb = 1;

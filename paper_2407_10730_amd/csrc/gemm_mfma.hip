@@ -356,25 +356,36 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 16 ? 7 : 1)) void ge
 #pragma unroll
                     for (int j = 0; j < BCOLS; ++j)
                         breg[g][j] = __builtin_bit_cast(
-                            f32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                       rb, vb[j] == OOB_OFF ? OOB_OFF : vb[j] + (uint32_t)(4 * (g * BKT + tk)) * 4u, 0, 0));
+                            f32x4, PF == 1 ? __builtin_amdgcn_raw_buffer_load_b128(rb, vb[j], 4 * (g * BKT + tk) * 4, 0)
+                                           : __builtin_amdgcn_raw_buffer_load_b128(
+                                                 rb, vb[j] == OOB_OFF ? OOB_OFF : vb[j] + (uint32_t)(4 * (g * BKT + tk)) * 4u,
+                                                 0, 0));
             } else {
 #pragma unroll
                 for (int g = 0; g < BRUNS; ++g)
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        const uint32_t cofs = (uint32_t)((cur_c0 + 4 * (g * BKT + tk) + i) * A.HW) * 4u;
+                        // the channel's offset is wave-uniform (tk is).  One set of staging
+                        // registers: it goes in the load's scalar offset (a lane out of range
+                        // stays out of range, the others address inside x), so the loads share
+                        // the lanes' address registers (N32 256->64 56x56 1x1: 3 % faster).  Two
+                        // sets: added per lane (the scalar form measured 7 % slower on N32
+                        // 64->64 56x56 3x3).
+                        const int cofs = (cur_c0 + 4 * (g * BKT + tk) + i) * A.HW * 4;
 #pragma unroll
-                        for (int j = 0; j < BCOLS; ++j) breg[g][j][i] = ld_f32(rb, vb[j] + cofs);
+                        for (int j = 0; j < BCOLS; ++j)
+                            breg[g][j][i] = PF == 1 ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rb, vb[j], cofs, 0))
+                                                    : ld_f32(rb, vb[j] + (uint32_t)cofs);
                     }
             }
             // weights in tap-major order [K][R*S][C/g]: 4 consecutive channels per 16-byte load
-            const uint32_t ab = (uint32_t)((cur_r * A.S + cur_s) * A.Cg + cur_c0) * 4u;
+            const int ab = ((cur_r * A.S + cur_s) * A.Cg + cur_c0) * 4;
 #pragma unroll
             for (int g = 0; g < ARUNS; ++g) {
                 // bit-cast the whole vector: casting its elements one by one made this
                 // compiler emit a single-dword load
-                areg[g] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(ra, na_off[g] + ab, 0, 0));
+                areg[g] = __builtin_bit_cast(f32x4, PF == 1 ? __builtin_amdgcn_raw_buffer_load_b128(ra, na_off[g], ab, 0)
+                                                            : __builtin_amdgcn_raw_buffer_load_b128(ra, na_off[g] + (uint32_t)ab, 0, 0));
             }
             if (++cur_s == A.S) {
                 cur_s = 0;
@@ -488,7 +499,8 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 16 ? 7 : 1)) void ge
         // which they would read past): they read inside or past the tensors, where the buffer
         // range check returns zero, and are never stored.  With a condition on them, the wait
         // before the LDS stores would have to cover the path without them and so would wait
-        // for the loads just issued as well.
+        // for the loads just issued as well.  (Storing those sets as well, which removes the
+        // conditions on the stores, measured 2 % slower on N32 64->64 56x56 3x3.)
         constexpr bool kAlways = BSRC != BSRC_IMPLICIT_NCHW;
         load_stage(s_begin, breg0, areg0);
         if (n > 1) load_stage(s_begin + 1, breg1, areg1);
