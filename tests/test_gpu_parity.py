@@ -213,12 +213,18 @@ NHWC_BF16 = [
     _shape(1, 32, 15, 15, 64, 3, 3, st=(2, 2), pd=(2, 2), dl=(2, 2), g=2, seed=218),
     _shape(3, 16, 9, 9, 200, 1, 1, seed=219),
     _shape(1, 64, 13, 13, 40, 3, 3, pd=(1, 1), g=8, seed=220),
+    # one and three 64-deep stages (the two-set prefetch loop's shortest and odd lengths)
+    _shape(2, 64, 11, 13, 72, 1, 1, seed=221),
+    _shape(1, 192, 9, 10, 64, 1, 1, pd=(0, 0), seed=222),
 ]
 
 
+# pf: register sets of the 64-deep-stage kernels (2, the planner's choice, or 1)
+@pytest.mark.parametrize("pf", ["2", "1"])
 @pytest.mark.parametrize("layout", ["nchw", "nhwc"])
 @pytest.mark.parametrize("idx", range(len(NHWC_BF16)))
-def test_bf16_nhwc_gather(idx, layout):
+def test_bf16_nhwc_gather(idx, layout, pf, monkeypatch):
+    monkeypatch.setenv("CONV2D_BF16_PF", pf)
     cs = NHWC_BF16[idx].with_(layout=layout, x_dtype="bf16", y_dtype="bf16")
     with _Kernel("nhwc"):
         dc = DeviceConv(cs, "random")
