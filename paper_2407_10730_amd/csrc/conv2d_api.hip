@@ -1031,6 +1031,7 @@ int run_direct(conv2d_desc* d, Ws& ws, const void* x, const void* w, const float
     a.x = x; a.w = w; a.bias = g.has_bias ? bias : nullptr; a.y = y;
     a.x_bytes = (uint32_t)(g.x_elems * elem_size(g.xdt));
     a.y_bytes = (uint32_t)(g.y_elems * elem_size(g.ydt));
+    a.w_bytes = (uint32_t)std::min<int64_t>(g.w_elems * elem_size(g.xdt), kBufferLimit);
     a.C = (int32_t)g.C; a.H = (int32_t)g.H; a.W = (int32_t)g.W; a.K = (int32_t)g.K;
     a.Ho = (int32_t)g.Ho; a.Wo = (int32_t)g.Wo; a.R = (int32_t)g.R; a.S = (int32_t)g.S;
     a.sh = g.sh; a.sw = g.sw; a.ph = g.ph; a.pw = g.pw; a.dh = g.dh; a.dw = g.dw;

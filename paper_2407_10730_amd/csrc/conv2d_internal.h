@@ -135,6 +135,7 @@ struct DirectArgs {
     const float* bias;
     void* y;
     uint32_t x_bytes, y_bytes;
+    uint32_t w_bytes;  // filters (range of the grouped kernels' buffer loads)
     int32_t C, H, W, K, Ho, Wo, R, S, sh, sw, ph, pw, dh, dw, Cg, Kg;
     int32_t N;
 };

@@ -1055,7 +1055,7 @@ grouped_strip_kernel(DirectArgs A, GsPlan P) {
     const int ow0 = cb * GS_HC;
     const __amdgpu_buffer_rsrc_t rx = dk_rsrc(A.x, A.x_bytes);
     const __amdgpu_buffer_rsrc_t ry = dk_rsrc(A.y, A.y_bytes);
-    const TX* wsrc = reinterpret_cast<const TX*>(A.w);
+    const __amdgpu_buffer_rsrc_t rw = dk_rsrc(A.w, A.w_bytes);
 
     float acc[GS_HC][KG];
 #pragma unroll
@@ -1115,19 +1115,16 @@ grouped_strip_kernel(DirectArgs A, GsPlan P) {
             }
         }
         // filters: ws[lc][tap][k] = w[group's output channel kq0 + k][channel within group][tap]
+        // (32-bit element index and a range-checked buffer load: the 64-bit address arithmetic
+        // of a plain load cost about 45 vector instructions per element)
         for (int i = t; i < ccn * R * S * KG; i += DIRECT_THREADS) {
             const int k = i % KG;
             const int tap = (i / KG) % (R * S);
             const int lc = i / (KG * R * S);
             const int ch = chb + c0 + lc;
             const int gi = (int)dk_fdiv((uint32_t)ch, P.fd_cg);
-            float v = 0.0f;
-            if (k < nk) {
-                const TX raw = wsrc[(((int64_t)gi * A.Kg + kq0 + k) * A.Cg + (ch - gi * A.Cg)) * (R * S) + tap];
-                if constexpr (sizeof(TX) == 4) v = __builtin_bit_cast(float, raw);
-                else v = __builtin_bit_cast(float, (uint32_t)raw << 16);
-            }
-            ws[i] = v;
+            const int widx = ((gi * A.Kg + kq0 + k) * A.Cg + (ch - gi * A.Cg)) * (R * S) + tap;
+            ws[i] = dk_load(rw, k < nk, widx, (TX*)nullptr);
         }
         __syncthreads();
         if (act) {
@@ -1171,7 +1168,8 @@ grouped_strip_kernel(DirectArgs A, GsPlan P) {
     for (int k = 0; k < KG; ++k) {
         if (k >= nk) break;
         const float bv = A.bias ? A.bias[kglob0 + k] : 0.0f;
-        const int64_t o = (((int64_t)n * A.K + kglob0 + k) * A.Ho + oh) * A.Wo + ow0;
+        // (y holds fewer than 2^31 elements: 32-bit index arithmetic)
+        const int o = ((n * A.K + kglob0 + k) * A.Ho + oh) * A.Wo + ow0;
         if (vec) {
             if constexpr (sizeof(TY) == 4) {
                 const u32x4_t val = {__builtin_bit_cast(uint32_t, acc[0][k] + bv), __builtin_bit_cast(uint32_t, acc[1][k] + bv),
