@@ -918,8 +918,9 @@ __global__ __launch_bounds__(256, (BM * BN <= 4096 && BK == 32 ? 7 : 1)) void ge
             // Issued on every stage, also past the block's last one (those loads read inside or
             // past the tensors, where the buffer range check returns zero, and are never
             // stored): with a condition here, the wait before the LDS stores would have to cover
-            // the path without these loads and so wait for them too.
-            load_stage(s_begin + jj + PF, bset[q % PF], aset[q % PF]);
+            // the path without these loads and so wait for them too.  Not through the tap
+            // table, which the loads past the end would read past.
+            if (BSRC != BSRC_IMPLICIT_NCHW || jj + PF < n) load_stage(s_begin + jj + PF, bset[q % PF], aset[q % PF]);
             if (TM == 2 && TN == 2 && BK == 64 && PF == 2 && !A.loader_only) {
                 // (the last stage also stores a stale set into the buffer no stage reads)
                 compute_store(q & 1, (q + 1) & 1, bset[(q + 1) % PF], aset[(q + 1) % PF]);
