@@ -962,6 +962,7 @@ int run_explicit(conv2d_desc* d, Ws& ws, const void* x, const void* w, const flo
         {
             Im2colArgs a{};
             a.x = x;
+            a.x_bytes = g.x_elems * elem_size(g.xdt) <= kBufferLimit ? (uint32_t)(g.x_elems * elem_size(g.xdt)) : 0u;
             a.col = col;
             a.col_bytes = (uint32_t)(g.G * g.Kred * pc * elem_size(g.xdt));
             a.ktab = ktab;

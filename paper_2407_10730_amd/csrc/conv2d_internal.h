@@ -101,6 +101,8 @@ hipError_t launch_gemm(const GemmArgs& a, int tile, int bk, int pf, int bsrc, in
 // im2col of a chunk of output pixels [p_begin, p_begin + pc): col[g][kr][pl].
 struct Im2colArgs {
     const void* x;
+    uint32_t x_bytes;     // x below 2 GiB: the gathers use 32-bit offsets into a range-checked
+                          // buffer; 0: 64-bit addresses
     void* col;
     uint32_t col_bytes;
     const KTabEntry* ktab;

@@ -71,15 +71,38 @@ __global__ __launch_bounds__(256) void im2col_kernel(Im2colArgs A) {
 #pragma unroll
     for (int i = 0; i < KR_PER_BLOCK; ++i) e[i] = A.ktab[__builtin_amdgcn_readfirstlane(min(kr0 + i, A.Kred - 1))];
     T v[KR_PER_BLOCK][PIX_PER_THREAD];
+    if (A.x_bytes != 0) {
+        // x below 2 GiB: 32-bit element offsets into a range-checked buffer (a window position
+        // outside the image takes the out-of-range offset and reads zero), instead of 64-bit
+        // address arithmetic per gathered element
+        const __amdgpu_buffer_rsrc_t rx = pk_rsrc(A.x, A.x_bytes);
+        int32_t xb32[PIX_PER_THREAD];
 #pragma unroll
-    for (int i = 0; i < KR_PER_BLOCK; ++i)
+        for (int j = 0; j < PIX_PER_THREAD; ++j) xb32[j] = (int32_t)xb[j];
 #pragma unroll
-        for (int j = 0; j < PIX_PER_THREAD; ++j) {
-            const int hi = hi0[j] + e[i].roff;
-            const int wi = wi0[j] + e[i].soff;
-            const bool ok = pv[j] & ((unsigned)hi < (unsigned)A.H) & ((unsigned)wi < (unsigned)A.W);
-            v[i][j] = ok ? x[xb[j] + e[i].coff] : T(0);
-        }
+        for (int i = 0; i < KR_PER_BLOCK; ++i)
+#pragma unroll
+            for (int j = 0; j < PIX_PER_THREAD; ++j) {
+                const int hi = hi0[j] + e[i].roff;
+                const int wi = wi0[j] + e[i].soff;
+                const bool ok = pv[j] & ((unsigned)hi < (unsigned)A.H) & ((unsigned)wi < (unsigned)A.W);
+                const uint32_t off = ok ? (uint32_t)(xb32[j] + e[i].coff) * (uint32_t)sizeof(T) : OOB_OFF;
+                if constexpr (sizeof(T) == 4)
+                    v[i][j] = __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b32(rx, off, 0, 0));
+                else
+                    v[i][j] = (T)__builtin_amdgcn_raw_buffer_load_b16(rx, off, 0, 0);
+            }
+    } else {
+#pragma unroll
+        for (int i = 0; i < KR_PER_BLOCK; ++i)
+#pragma unroll
+            for (int j = 0; j < PIX_PER_THREAD; ++j) {
+                const int hi = hi0[j] + e[i].roff;
+                const int wi = wi0[j] + e[i].soff;
+                const bool ok = pv[j] & ((unsigned)hi < (unsigned)A.H) & ((unsigned)wi < (unsigned)A.W);
+                v[i][j] = ok ? x[xb[j] + e[i].coff] : T(0);
+            }
+    }
     const bool vec = ((A.pc & 3) == 0) & (pl0 + PIX_PER_THREAD <= A.pc);
 #pragma unroll
     for (int i = 0; i < KR_PER_BLOCK; ++i) {
