@@ -1268,12 +1268,18 @@ int conv2d_desc_create(const conv2d_params* params, conv2d_desc** out) {
     // bf16 with C/g a multiple of 32, or C/g = 8 or 16 (whole taps per 32-deep stage): gather
     // 16-byte channel runs from an NHWC copy of x.  The copy costs 2|x| of HBM traffic (nothing
     // when x is already NHWC), so it is taken when the convolution does at least 1000 flops per
-    // input byte; CONV2D_NHWC_GATHER=0 / 1 forces it.
+    // input byte, or at least 36 when a stride skips input columns: the element-wise gather then
+    // uses half of every line it fetches: 9 strided bf16 layers at 36 to 512 flops per byte ran
+    // 0.42-0.82x as long with the copy, one at 32 twice as long, and stride-1 layers at 147 to
+    // 800 flops per byte 1.1-1.4x as long.  CONV2D_NHWC_GATHER=0 / 1 forces it.
     if (g.xdt == CONV2D_BF16 && (g.Cg % 32 == 0 || g.Cg == 8 || g.Cg == 16)) {
         const double flops = 2.0 * (double)g.N * g.K * g.Cg * g.R * g.S * g.Ho * g.Wo;
         const double xbytes = (double)g.x_elems * 2;
+        const bool strided = g.sh > 1 || g.sw > 1;
         const int64_t force = env_int64("CONV2D_NHWC_GATHER", -1);
-        d->implicit_nhwc = force < 0 ? (g.layout == CONV2D_NHWC || flops >= 1000.0 * xbytes) : force != 0;
+        d->implicit_nhwc = force < 0 ? (g.layout == CONV2D_NHWC || flops >= 1000.0 * xbytes ||
+                                        (strided && flops >= 36.0 * xbytes))
+                                     : force != 0;
     }
     // fp32 NHWC x with C/g a multiple of 16: gather 4-channel runs with 16-byte loads straight
     // from x (no reorder of x); NCHW fp32 x keeps the NCHW gathers (a copy of x would cost more
