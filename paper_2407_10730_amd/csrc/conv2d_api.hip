@@ -1334,9 +1334,12 @@ int conv2d_desc_create(const conv2d_params* params, conv2d_desc** out) {
     // 64-row MFMA tile; the grouped direct kernel (one "group" of all channels) computes them on
     // the vector ALUs instead when its grid fills the chip (its blocks walk the whole reduction,
     // so a small grid leaves CUs idle) and the filter is not 1x1 (a pointwise layer is a plain
-    // GEMM with no gather, which the MFMA path runs well even with few rows).
+    // GEMM with no gather, which the MFMA path runs well even with few rows).  With 5..16 output
+    // channels only short reductions stay there: since the 32-row tiles, the implicit GEMM ran
+    // N32 64..512 -> 16 layers (reductions of 1152 to 4608) in 0.77-0.94x the time, while
+    // 3 -> 16 5x5 (75) took 1.8x as long.
     bool direct_small_k = false;
-    if (d->direct_ok && g.G == 1 && g.K <= 16 && g.R * g.S > 1) {
+    if (d->direct_ok && g.G == 1 && g.K <= 16 && g.R * g.S > 1 && (g.K <= 4 || g.Cg * g.R * g.S <= 256)) {
         DirectArgs da{};
         da.C = (int32_t)g.C; da.H = (int32_t)g.H; da.W = (int32_t)g.W; da.K = (int32_t)g.K;
         da.Ho = (int32_t)g.Ho; da.Wo = (int32_t)g.Wo; da.R = (int32_t)g.R; da.S = (int32_t)g.S;

@@ -237,8 +237,10 @@ def test_grouped_auto_choice():
     assert algo(groups=64, k=2048) == B.CONV2D_ALGO_DIRECT           # 4, 32
     assert algo(groups=1) == B.CONV2D_ALGO_WINOGRAD                  # 256 -> 256, 3x3, stride 1
     # ungrouped, K <= 16: the direct kernel when its grid fills the chip and the filter is not 1x1
+    # (for K = 5..16 only with a reduction of at most 256)
     assert algo(c=512, k=3, h=112, w=112) == B.CONV2D_ALGO_DIRECT        # 32 images x 13 bands
-    assert algo(c=512, k=16, h=112, w=112) == B.CONV2D_ALGO_DIRECT
+    assert algo(c=512, k=16, h=112, w=112) == B.CONV2D_ALGO_IMPLICIT_GEMM  # reduction 4608
+    assert algo(c=16, k=16, h=112, w=112) == B.CONV2D_ALGO_DIRECT         # reduction 144
     assert algo(c=512, k=32, h=112, w=112) == B.CONV2D_ALGO_IMPLICIT_GEMM
     # 26 grouped-kernel blocks; K <= 4: the few-output-channel kernel splits the channels instead
     assert algo(n=2, c=512, k=3, h=112, w=112) == B.CONV2D_ALGO_DIRECT
