@@ -1353,9 +1353,13 @@ int conv2d_desc_create(const conv2d_params* params, conv2d_desc** out) {
     // 3x3 stride-1 fp32 layers with at least 128 input and output channels and output planes of
     // at least 8x8: Winograd F(4x4,3x3) does 4x fewer multiplications, which outweighs its
     // transforms (measured 1.6-2.0x faster than the implicit GEMM for C, K = 128 .. 1024 on
-    // 14x14 to 112x112 planes on MI355X; 64 -> 64 channels on 56x56 gain under 10 %, 7x7 planes
-    // none)
-    else if (d->wino.ok && g.xdt == CONV2D_F32 && g.C >= 128 && g.K >= 128 && std::min(g.Ho, g.Wo) >= 8)
+    // 14x14 to 112x112 planes on MI355X; 64 -> 64 channels on 56x56 gain under 10 %).  On 7x7
+    // planes F(2x2,3x3) (2.25x fewer) pays off from about 4 GFLOP: 0.60-0.72x the time for N32
+    // 512 -> 512, 256 -> 1024, 1024 -> 1024 and N8 2048 -> 2048, but 1.1x for N8 512 -> 512 and
+    // 1.24x for N32 128 -> 128 (1.9 and 0.5 GFLOP), whose small per-position GEMMs stay inefficient.
+    else if (d->wino.ok && g.xdt == CONV2D_F32 && g.C >= 128 && g.K >= 128 &&
+             (std::min(g.Ho, g.Wo) >= 8 ||
+              (std::min(g.Ho, g.Wo) >= 7 && 2.0 * g.N * g.K * g.C * 9.0 * g.Ho * g.Wo >= 4e9)))
         d->auto_algo = CONV2D_ALGO_WINOGRAD;
     else if (d->implicit_ok)
         d->auto_algo = CONV2D_ALGO_IMPLICIT_GEMM;

@@ -281,7 +281,8 @@ def test_winograd_plan(monkeypatch):
             B.conv2d_desc_destroy(d)
     assert auto(cfg2) == B.CONV2D_ALGO_IMPLICIT_GEMM                       # 64 channels
     assert auto(cfg2.with_(c=128, k=256)) == B.CONV2D_ALGO_WINOGRAD
-    assert auto(cfg2.with_(c=512, k=512, h=7, w=7)) == B.CONV2D_ALGO_IMPLICIT_GEMM    # 7x7 planes
+    assert auto(cfg2.with_(c=512, k=512, h=7, w=7)) == B.CONV2D_ALGO_WINOGRAD         # 7x7, 7.4 GFLOP
+    assert auto(cfg2.with_(n=8, c=512, k=512, h=7, w=7)) == B.CONV2D_ALGO_IMPLICIT_GEMM  # 1.9 GFLOP
     # bf16: F(2x2) only, U and V in bf16, V from the NHWC copy of x; not taken by AUTO
     bf = cfg2.with_(x_dtype="bf16", y_dtype="bf16")
     info = plan(bf)
