@@ -1018,6 +1018,7 @@ constexpr int GS_WF = 2048;    // LDS floats for the filters
 struct GsPlan {
     int32_t TR, GB, CC, IR, LDW, LPAD, ncb, nbands, kchunks, xfloats, lds_bytes;
     FastDiv fd_cpl, fd_ldw, fd_ir, fd_cg;  // staging: chunks per line, line width, rows, channels per group
+    FastDiv fd_kch, fd_nb, fd_ngb, fd_ncb, fd_tr;  // block and thread decomposition
 };
 
 // Up to 4 output channels per strip the kernel fits in 73 registers, 7 blocks per CU; left to
@@ -1031,14 +1032,17 @@ grouped_strip_kernel(DirectArgs A, GsPlan P) {
     float* xs = gsl;                // [CC][IR][LDW]
     float* ws = gsl + P.xfloats;    // [CC][R*S][KG]
     const int G = A.C / A.Cg;
-    int b = blockIdx.x;
-    const int kc = b % P.kchunks;
-    b /= P.kchunks;
-    const int band = b % P.nbands;
-    b /= P.nbands;
+    // block -> (image, group batch, band, channel chunk) and thread -> (group, row, strip)
+    // with host-computed magic numbers (the compiler's divisions cost ~30 instructions each)
+    uint32_t b = blockIdx.x;
+    uint32_t b1 = dk_fdiv(b, P.fd_kch);
+    const int kc = (int)(b - b1 * (uint32_t)P.kchunks);
+    uint32_t b2 = dk_fdiv(b1, P.fd_nb);
+    const int band = (int)(b1 - b2 * (uint32_t)P.nbands);
     const int ngb = (G + P.GB - 1) / P.GB;
-    const int g0 = (b % ngb) * P.GB;
-    const int n = b / ngb;
+    const uint32_t b3 = dk_fdiv(b2, P.fd_ngb);
+    const int g0 = (int)(b2 - b3 * (uint32_t)ngb) * P.GB;
+    const int n = (int)b3;
     const int gn = min(P.GB, G - g0);
     const int kq0 = kc * KG;
     const int nk = min(KG, A.Kg - kq0);
@@ -1048,20 +1052,28 @@ grouped_strip_kernel(DirectArgs A, GsPlan P) {
     const int plane = P.IR * P.LDW;
     const int t = threadIdx.x;
     // the thread's strip: column block cb, output row rv of the band, group gg of the block
-    const int cb = t % P.ncb;
-    const int rv = (t / P.ncb) % P.TR;
-    const int gg = t / (P.ncb * P.TR);
+    const uint32_t t1 = dk_fdiv((uint32_t)t, P.fd_ncb);
+    const int cb = t - (int)t1 * P.ncb;
+    const uint32_t t2 = dk_fdiv(t1, P.fd_tr);
+    const int rv = (int)(t1 - t2 * (uint32_t)P.TR);
+    const int gg = (int)t2;
     const bool act = gg < gn && rv < rows;
     const int ow0 = cb * GS_HC;
     const __amdgpu_buffer_rsrc_t rx = dk_rsrc(A.x, A.x_bytes);
     const __amdgpu_buffer_rsrc_t ry = dk_rsrc(A.y, A.y_bytes);
     const __amdgpu_buffer_rsrc_t rw = dk_rsrc(A.w, A.w_bytes);
 
+    // the bias goes in first: the FMAs add the products to it
     float acc[GS_HC][KG];
+    {
+        const int kb = (g0 + gg) * A.Kg + kq0;
 #pragma unroll
-    for (int h = 0; h < GS_HC; ++h)
+        for (int k = 0; k < KG; ++k) {
+            const float bv = A.bias && act && k < nk ? A.bias[kb + k] : 0.0f;
 #pragma unroll
-        for (int k = 0; k < KG; ++k) acc[h][k] = 0.0f;
+            for (int h = 0; h < GS_HC; ++h) acc[h][k] = bv;
+        }
+    }
 
     // the block's channels: all channels of its gn groups (staged at once when GB > 1), or the
     // Cg channels of its one group, CC at a time
@@ -1163,22 +1175,23 @@ grouped_strip_kernel(DirectArgs A, GsPlan P) {
     if (!act) return;
     const int kglob0 = (g0 + gg) * A.Kg + kq0;
     const int oh = ho0 + rv;
+    const int howo = A.Ho * A.Wo;
+    const int o0 = ((n * A.K + kglob0) * A.Ho + oh) * A.Wo + ow0;
     const bool vec = (A.Wo & 3) == 0;
 #pragma unroll
     for (int k = 0; k < KG; ++k) {
         if (k >= nk) break;
-        const float bv = A.bias ? A.bias[kglob0 + k] : 0.0f;
         // (y holds fewer than 2^31 elements: 32-bit index arithmetic)
-        const int o = ((n * A.K + kglob0 + k) * A.Ho + oh) * A.Wo + ow0;
+        const int o = o0 + k * howo;
         if (vec) {
             if constexpr (sizeof(TY) == 4) {
-                const u32x4_t val = {__builtin_bit_cast(uint32_t, acc[0][k] + bv), __builtin_bit_cast(uint32_t, acc[1][k] + bv),
-                                     __builtin_bit_cast(uint32_t, acc[2][k] + bv), __builtin_bit_cast(uint32_t, acc[3][k] + bv)};
+                const u32x4_t val = {__builtin_bit_cast(uint32_t, acc[0][k]), __builtin_bit_cast(uint32_t, acc[1][k]),
+                                     __builtin_bit_cast(uint32_t, acc[2][k]), __builtin_bit_cast(uint32_t, acc[3][k])};
                 __builtin_amdgcn_raw_buffer_store_b128(val, ry, (uint32_t)(o * 4), 0, 0);
             } else {
                 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-                const u32x2 val = {(uint32_t)dk_f32_to_bf16(acc[0][k] + bv) | ((uint32_t)dk_f32_to_bf16(acc[1][k] + bv) << 16),
-                                   (uint32_t)dk_f32_to_bf16(acc[2][k] + bv) | ((uint32_t)dk_f32_to_bf16(acc[3][k] + bv) << 16)};
+                const u32x2 val = {(uint32_t)dk_f32_to_bf16(acc[0][k]) | ((uint32_t)dk_f32_to_bf16(acc[1][k]) << 16),
+                                   (uint32_t)dk_f32_to_bf16(acc[2][k]) | ((uint32_t)dk_f32_to_bf16(acc[3][k]) << 16)};
                 __builtin_amdgcn_raw_buffer_store_b64(val, ry, (uint32_t)(o * 2), 0, 0);
             }
         } else {
@@ -1186,10 +1199,10 @@ grouped_strip_kernel(DirectArgs A, GsPlan P) {
             for (int h = 0; h < GS_HC; ++h) {
                 const bool ok = ow0 + h < A.Wo;
                 if constexpr (sizeof(TY) == 4)
-                    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, acc[h][k] + bv), ry,
+                    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, acc[h][k]), ry,
                                                           ok ? (uint32_t)((o + h) * 4) : OOB_OFF, 0, 0);
                 else
-                    __builtin_amdgcn_raw_buffer_store_b16(dk_f32_to_bf16(acc[h][k] + bv), ry,
+                    __builtin_amdgcn_raw_buffer_store_b16(dk_f32_to_bf16(acc[h][k]), ry,
                                                           ok ? (uint32_t)((o + h) * 2) : OOB_OFF, 0, 0);
             }
         }
@@ -1240,6 +1253,11 @@ static bool gs_plan(const DirectArgs& a, int KG, GsPlan* p) {
     p->fd_ldw = make_fastdiv((uint32_t)LDW);
     p->fd_ir = make_fastdiv((uint32_t)p->IR);
     p->fd_cg = make_fastdiv((uint32_t)a.Cg);
+    p->fd_kch = make_fastdiv((uint32_t)p->kchunks);
+    p->fd_nb = make_fastdiv((uint32_t)p->nbands);
+    p->fd_ngb = make_fastdiv((uint32_t)((G + gb - 1) / gb));
+    p->fd_ncb = make_fastdiv((uint32_t)ncb);
+    p->fd_tr = make_fastdiv((uint32_t)tr);
     const int64_t blocks = (int64_t)a.N * ((G + gb - 1) / gb) * p->nbands * p->kchunks;
     return blocks <= 0x7fffffffLL && p->CC >= 1;
 }
