@@ -658,6 +658,7 @@ static hipError_t try_launch_dw(const DirectArgs& a, int xdt, int ydt, hipStream
 // top half of the first word).
 struct DwrPlan {
     int32_t ncb, upw, br, ir, nbands, units;
+    int32_t wpb;               // waves per block (independent; 1 or 4)
     uint32_t m_ncb;            // lane / ncb = (lane * m_ncb) >> 16 for lane < 64
     FastDiv fd_nb, fd_k, fd_kg;  // unit -> plane, plane -> image, channel -> input channel
 };
@@ -669,8 +670,8 @@ __host__ __device__ constexpr int dwr_words(int R, int DL, bool bf, bool odd) {
     return bf ? (4 + (R - 1) * DL + (odd ? 1 : 0) + 1) / 2 : 4 + (R - 1) * DL;
 }
 
-template <int R, int DL, bool ODD, typename TX, typename TY>
-__global__ __launch_bounds__(64) void dw_rows_kernel(DirectArgs A, DwrPlan P) {
+template <int R, int DL, bool ODD, int WPB, typename TX, typename TY>
+__global__ __launch_bounds__(64 * WPB) void dw_rows_kernel(DirectArgs A, DwrPlan P) {
     constexpr int HALO = (R - 1) * DL;
     constexpr int NS = HALO + 1;  // output rows in progress
     constexpr int RB = 4 + HALO;  // input values under a strip of 4 outputs
@@ -684,8 +685,9 @@ __global__ __launch_bounds__(64) void dw_rows_kernel(DirectArgs A, DwrPlan P) {
     typedef float f32x2_t __attribute__((ext_vector_type(2)));
     typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
     typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
-    const int l = threadIdx.x;
-    const int U0 = blockIdx.x * P.upw;
+    const int l = threadIdx.x & 63;
+    const int U0 = (int)(blockIdx.x * WPB + (WPB > 1 ? __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) : 0)) * P.upw;
+    if (WPB > 1 && U0 >= P.units) return;  // the whole wave: past the last unit
     const int nu = min(P.upw, P.units - U0);
     const __amdgpu_buffer_rsrc_t rx = dk_rsrc(A.x, A.x_bytes);
     const __amdgpu_buffer_rsrc_t ry = dk_rsrc(A.y, A.y_bytes);
@@ -932,8 +934,18 @@ static bool dwr_plan(const DirectArgs& a, int xdt, DwrPlan* p) {
     // dilation 2 (4 halo rows: N1 1024 224x224 40 -> 43 us) and for 5x5 and 7x7 (more
     // arithmetic per row: N32 256 112x112 5x5 3 % slower) whole planes or long bands stay.
     // CONV2D_DWR_WAVES overrides it.
+    // Many planes of up to 32 columns at 3x3 dilation 1 take blocks of 4 independent waves
+    // and twice the waves (bf16, us, one-wave -> 4-wave blocks: N32 2048 28x28 45.3 -> 43.7,
+    // N32 1024 14x14 15.5 either way; with fewer planes it loses: N32 256 28x28 8.07 -> 8.26,
+    // N8 96 32x32 5.35 -> 5.71; the 56x56 and 112x112 layers 0.5-1.5 % slower).
+    // CONV2D_DWR_WPB = 1 or 4 overrides the block size.
+    const bool small = a.R == 3 && a.dh == 1 && a.Wo <= 32 && planes >= 32768;
     const char* tw = std::getenv("CONV2D_DWR_WAVES");
-    const int64_t waves = tw && std::atoi(tw) > 0 ? std::atoi(tw) : (a.R == 3 && a.dh == 1 ? 16384 : 4096);
+    const int64_t waves = tw && std::atoi(tw) > 0 ? std::atoi(tw)
+                          : (a.R == 3 && a.dh == 1 ? (small ? 32768 : 16384) : 4096);
+    const char* tb = std::getenv("CONV2D_DWR_WPB");
+    p->wpb = tb && (tb[0] == '1' || tb[0] == '4') ? tb[0] - '0' : (small ? 4 : 1);
+    if (p->wpb == 4 && !(a.R == 3 && a.dh == 1)) p->wpb = 1;  // (instantiated for 3x3 at dilation 1)
     int64_t nb = (waves * upw + planes - 1) / planes;
     const int nb_max = (a.Ho + 7) / 8;
     if (nb > nb_max) nb = nb_max;
@@ -955,18 +967,19 @@ static bool dwr_plan(const DirectArgs& a, int xdt, DwrPlan* p) {
     return true;
 }
 
-template <int R, int DL>
+template <int R, int DL, int WPB>
 static hipError_t launch_dwr_t(const DirectArgs& a, const DwrPlan& p, int xdt, int ydt, hipStream_t stream) {
-    dim3 grid((unsigned)((p.units + p.upw - 1) / p.upw));
+    const int64_t wv = (p.units + p.upw - 1) / p.upw;
+    dim3 grid((unsigned)((wv + WPB - 1) / WPB)), block(64 * WPB);
     const bool odd = a.pw & 1;
     if (xdt == CONV2D_F32)
-        hipLaunchKernelGGL((dw_rows_kernel<R, DL, false, float, float>), grid, dim3(64), 0, stream, a, p);
+        hipLaunchKernelGGL((dw_rows_kernel<R, DL, false, WPB, float, float>), grid, block, 0, stream, a, p);
     else if (ydt == CONV2D_BF16) {
-        if (odd) hipLaunchKernelGGL((dw_rows_kernel<R, DL, true, uint16_t, uint16_t>), grid, dim3(64), 0, stream, a, p);
-        else hipLaunchKernelGGL((dw_rows_kernel<R, DL, false, uint16_t, uint16_t>), grid, dim3(64), 0, stream, a, p);
+        if (odd) hipLaunchKernelGGL((dw_rows_kernel<R, DL, true, WPB, uint16_t, uint16_t>), grid, block, 0, stream, a, p);
+        else hipLaunchKernelGGL((dw_rows_kernel<R, DL, false, WPB, uint16_t, uint16_t>), grid, block, 0, stream, a, p);
     } else {
-        if (odd) hipLaunchKernelGGL((dw_rows_kernel<R, DL, true, uint16_t, float>), grid, dim3(64), 0, stream, a, p);
-        else hipLaunchKernelGGL((dw_rows_kernel<R, DL, false, uint16_t, float>), grid, dim3(64), 0, stream, a, p);
+        if (odd) hipLaunchKernelGGL((dw_rows_kernel<R, DL, true, WPB, uint16_t, float>), grid, block, 0, stream, a, p);
+        else hipLaunchKernelGGL((dw_rows_kernel<R, DL, false, WPB, uint16_t, float>), grid, block, 0, stream, a, p);
     }
     return hipGetLastError();
 }
@@ -983,10 +996,11 @@ static hipError_t try_launch_dw_rows(const DirectArgs& a, int xdt, int ydt, hipS
     DwrPlan p;
     if (!dwr_plan(a, xdt, &p)) return hipSuccess;
     *launched = true;
-    if (a.R == 3 && a.dh == 1) return launch_dwr_t<3, 1>(a, p, xdt, ydt, stream);
-    if (a.R == 3 && a.dh == 2) return launch_dwr_t<3, 2>(a, p, xdt, ydt, stream);
-    if (a.R == 5 && a.dh == 1) return launch_dwr_t<5, 1>(a, p, xdt, ydt, stream);
-    if (a.R == 7 && a.dh == 1) return launch_dwr_t<7, 1>(a, p, xdt, ydt, stream);
+    if (a.R == 3 && a.dh == 1)
+        return p.wpb == 4 ? launch_dwr_t<3, 1, 4>(a, p, xdt, ydt, stream) : launch_dwr_t<3, 1, 1>(a, p, xdt, ydt, stream);
+    if (a.R == 3 && a.dh == 2) return launch_dwr_t<3, 2, 1>(a, p, xdt, ydt, stream);
+    if (a.R == 5 && a.dh == 1) return launch_dwr_t<5, 1, 1>(a, p, xdt, ydt, stream);
+    if (a.R == 7 && a.dh == 1) return launch_dwr_t<7, 1, 1>(a, p, xdt, ydt, stream);
     *launched = false;
     return hipSuccess;
 }

@@ -638,6 +638,18 @@ def test_depthwise_rows(idx, dt, rows):
             _check(cs, DIRECT, "integer")
 
 
+# the streamed-row kernel's block size: one wave per block or 4 independent waves (the plan takes
+# 4 for 3x3 planes up to 32 columns); forced both ways on every 3x3 dilation-1 shape, so the
+# last block's waves past the final unit are covered at several unit counts
+@pytest.mark.parametrize("wpb", ["1", "4"])
+@pytest.mark.parametrize("dt", [("f32", "f32"), ("bf16", "bf16")], ids=lambda d: "-".join(d))
+@pytest.mark.parametrize("idx", [i for i, c in enumerate(DW_ROWS) if c.r == 3 and c.dil == (1, 1)])
+def test_depthwise_rows_block_size(idx, dt, wpb):
+    cs = DW_ROWS[idx].with_(x_dtype=dt[0], y_dtype=dt[1])
+    with _Env(CONV2D_DW_ROWS="1", CONV2D_DWR_WPB=wpb):
+        _check(cs, DIRECT)
+
+
 # NHWC <-> NCHW copies: the 64x64 vector kernel (both sides multiples of 4, ragged tiles) and the
 # 32x32 element kernel (CONV2D_TRANSPOSE32, and sides that are not multiples of 4), through NHWC
 # convolutions that reorder x and y
