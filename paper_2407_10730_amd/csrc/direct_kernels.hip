@@ -1103,30 +1103,46 @@ grouped_strip_kernel(DirectArgs A, GsPlan P) {
         if ((A.W & 3) == 0) {
             const int cpl = P.LDW / 4;  // 16-byte chunks per line (the odd last word is padding)
             const int total = ccn * P.IR * cpl;
-            for (int i = t; i < total; i += DIRECT_THREADS) {
-                const int line = (int)dk_fdiv((uint32_t)i, P.fd_cpl);
-                const int q = i - line * cpl;
-                const int lc = (int)dk_fdiv((uint32_t)line, P.fd_ir);
-                const int tr = line - lc * P.IR;
-                const int hi = hi_base + tr, w0 = 4 * q - P.LPAD;
-                const bool ok = ((unsigned)hi < (unsigned)A.H) & ((unsigned)w0 < (unsigned)A.W);
-                const int e = (cbase + lc * A.H + hi) * A.W + w0;
-                f32x4 v;
-                if constexpr (sizeof(TX) == 4) {
-                    v = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                                      rx, ok ? (uint32_t)(e * 4) : OOB_OFF, 0, 0));
-                } else {
-                    typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-                    const u32x2 hh = __builtin_bit_cast(
-                        u32x2, __builtin_amdgcn_raw_buffer_load_b64(rx, ok ? (uint32_t)(e * 2) : OOB_OFF, 0, 0));
-                    v = f32x4{__builtin_bit_cast(float, hh[0] << 16), __builtin_bit_cast(float, hh[0] & 0xFFFF0000u),
-                              __builtin_bit_cast(float, hh[1] << 16), __builtin_bit_cast(float, hh[1] & 0xFFFF0000u)};
+            // up to 4 output channels per strip, two chunks per thread per trip: both loads go
+            // out before the first LDS write waits (one load round trip per two chunks; g=64
+            // 46.5 -> 44.9 us; four chunks spilled registers under the 7-wave cap, and the
+            // 8-channel kernel measured 3 % slower with two)
+            constexpr int UB = KG <= 4 ? 2 : 1;
+            for (int i0 = t; i0 < total; i0 += UB * DIRECT_THREADS) {
+                f32x4 v[UB];
+                int dst[UB];
+#pragma unroll
+                for (int u = 0; u < UB; ++u) {
+                    const int i = i0 + u * DIRECT_THREADS;
+                    const int line = (int)dk_fdiv((uint32_t)i, P.fd_cpl);
+                    const int q = i - line * cpl;
+                    const int lc = (int)dk_fdiv((uint32_t)line, P.fd_ir);
+                    const int tr = line - lc * P.IR;
+                    const int hi = hi_base + tr, w0 = 4 * q - P.LPAD;
+                    const bool ok = (i < total) & ((unsigned)hi < (unsigned)A.H) & ((unsigned)w0 < (unsigned)A.W);
+                    const int e = (cbase + lc * A.H + hi) * A.W + w0;
+                    if constexpr (sizeof(TX) == 4) {
+                        v[u] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                             rx, ok ? (uint32_t)(e * 4) : OOB_OFF, 0, 0));
+                    } else {
+                        typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+                        const u32x2 hh = __builtin_bit_cast(
+                            u32x2, __builtin_amdgcn_raw_buffer_load_b64(rx, ok ? (uint32_t)(e * 2) : OOB_OFF, 0, 0));
+                        v[u] = f32x4{__builtin_bit_cast(float, hh[0] << 16), __builtin_bit_cast(float, hh[0] & 0xFFFF0000u),
+                                     __builtin_bit_cast(float, hh[1] << 16), __builtin_bit_cast(float, hh[1] & 0xFFFF0000u)};
+                    }
+                    dst[u] = i < total ? line * P.LDW + 4 * q : -1;
                 }
-                float* dst = &xs[line * P.LDW + 4 * q];  // 4-byte aligned (odd line width)
-                dst[0] = v[0];
-                dst[1] = v[1];
-                dst[2] = v[2];
-                dst[3] = v[3];
+#pragma unroll
+                for (int u = 0; u < UB; ++u) {
+                    if (dst[u] >= 0) {
+                        float* d = &xs[dst[u]];  // 4-byte aligned (odd line width)
+                        d[0] = v[u][0];
+                        d[1] = v[u][1];
+                        d[2] = v[u][2];
+                        d[3] = v[u][3];
+                    }
+                }
             }
         } else {
             const int total = ccn * P.IR * P.LDW;
