@@ -1037,7 +1037,9 @@ struct GsPlan {
 
 // Up to 4 output channels per strip the kernel fits in 73 registers, 7 blocks per CU; left to
 // itself the compiler took 100 (5 blocks per CU, 20 % slower on C/g = 4).
-template <int R, int ST, int KG, typename TX, typename TY>
+// VW: rows of W % 4 == 0 columns, staged 16 bytes at a time (else element by element; the two
+// staging loops are separate instances, so neither one's registers weigh on the other)
+template <int R, int ST, int KG, bool VW, typename TX, typename TY>
 __global__ __launch_bounds__(DIRECT_THREADS) __attribute__((amdgpu_waves_per_eu(KG <= 4 ? 7 : 1))) void
 grouped_strip_kernel(DirectArgs A, GsPlan P) {
     constexpr int S = R;
@@ -1100,7 +1102,7 @@ grouped_strip_kernel(DirectArgs A, GsPlan P) {
         // columns j = wi + LPAD
         // (element offsets fit 32 bits: x is below 2 GiB)
         const int cbase = (n * A.C + chb + c0) * A.H;  // row index of the chunk's first channel
-        if ((A.W & 3) == 0) {
+        if constexpr (VW) {
             const int cpl = P.LDW / 4;  // 16-byte chunks per line (the odd last word is padding)
             const int total = ccn * P.IR * cpl;
             // up to 4 output channels per strip, two chunks per thread per trip: both loads go
@@ -1146,14 +1148,25 @@ grouped_strip_kernel(DirectArgs A, GsPlan P) {
             }
         } else {
             const int total = ccn * P.IR * P.LDW;
-            for (int i = t; i < total; i += DIRECT_THREADS) {
-                const int line = (int)dk_fdiv((uint32_t)i, P.fd_ldw);
-                const int j = i - line * P.LDW;
-                const int lc = (int)dk_fdiv((uint32_t)line, P.fd_ir);
-                const int tr = line - lc * P.IR;
-                const int hi = hi_base + tr, wi = j - P.LPAD;
-                const bool ok = ((unsigned)hi < (unsigned)A.H) & ((unsigned)wi < (unsigned)A.W);
-                xs[i] = dk_load(rx, ok, ok ? (cbase + lc * A.H + hi) * A.W + wi : 0, (TX*)nullptr);
+            // (as above: EB elements per thread per trip, their loads issued together; N32
+            // 1024 14x14 g=256 33.6 -> 24.4 us, 2048 7x7 g=512 27.9 -> 22.2 us)
+            constexpr int EB = KG <= 4 ? 4 : 1;
+            for (int i0 = t; i0 < total; i0 += EB * DIRECT_THREADS) {
+                float v[EB];
+#pragma unroll
+                for (int u = 0; u < EB; ++u) {
+                    const int i = i0 + u * DIRECT_THREADS;
+                    const int line = (int)dk_fdiv((uint32_t)i, P.fd_ldw);
+                    const int j = i - line * P.LDW;
+                    const int lc = (int)dk_fdiv((uint32_t)line, P.fd_ir);
+                    const int tr = line - lc * P.IR;
+                    const int hi = hi_base + tr, wi = j - P.LPAD;
+                    const bool ok = (i < total) & ((unsigned)hi < (unsigned)A.H) & ((unsigned)wi < (unsigned)A.W);
+                    v[u] = dk_load(rx, ok, ok ? (cbase + lc * A.H + hi) * A.W + wi : 0, (TX*)nullptr);
+                }
+#pragma unroll
+                for (int u = 0; u < EB; ++u)
+                    if (i0 + u * DIRECT_THREADS < total) xs[i0 + u * DIRECT_THREADS] = v[u];
             }
         }
         // filters: ws[lc][tap][k] = w[group's output channel kq0 + k][channel within group][tap]
@@ -1292,20 +1305,26 @@ static bool gs_plan(const DirectArgs& a, int KG, GsPlan* p) {
     return blocks <= 0x7fffffffLL && p->CC >= 1;
 }
 
-template <int R, int ST, int KG>
-static hipError_t launch_gs_t(const DirectArgs& a, const GsPlan& p, int xdt, int ydt, hipStream_t stream) {
+template <int R, int ST, int KG, bool VW>
+static hipError_t launch_gs_v(const DirectArgs& a, const GsPlan& p, int xdt, int ydt, hipStream_t stream) {
     const int G = a.C / a.Cg;
     dim3 grid((unsigned)((int64_t)a.N * ((G + p.GB - 1) / p.GB) * p.nbands * p.kchunks));
     if (xdt == CONV2D_F32)
-        hipLaunchKernelGGL((grouped_strip_kernel<R, ST, KG, float, float>), grid, dim3(DIRECT_THREADS), p.lds_bytes,
-                           stream, a, p);
+        hipLaunchKernelGGL((grouped_strip_kernel<R, ST, KG, VW, float, float>), grid, dim3(DIRECT_THREADS),
+                           p.lds_bytes, stream, a, p);
     else if (ydt == CONV2D_BF16)
-        hipLaunchKernelGGL((grouped_strip_kernel<R, ST, KG, uint16_t, uint16_t>), grid, dim3(DIRECT_THREADS),
+        hipLaunchKernelGGL((grouped_strip_kernel<R, ST, KG, VW, uint16_t, uint16_t>), grid, dim3(DIRECT_THREADS),
                            p.lds_bytes, stream, a, p);
     else
-        hipLaunchKernelGGL((grouped_strip_kernel<R, ST, KG, uint16_t, float>), grid, dim3(DIRECT_THREADS),
+        hipLaunchKernelGGL((grouped_strip_kernel<R, ST, KG, VW, uint16_t, float>), grid, dim3(DIRECT_THREADS),
                            p.lds_bytes, stream, a, p);
     return hipGetLastError();
+}
+
+template <int R, int ST, int KG>
+static hipError_t launch_gs_t(const DirectArgs& a, const GsPlan& p, int xdt, int ydt, hipStream_t stream) {
+    return (a.W & 3) == 0 ? launch_gs_v<R, ST, KG, true>(a, p, xdt, ydt, stream)
+                          : launch_gs_v<R, ST, KG, false>(a, p, xdt, ydt, stream);
 }
 
 // Row-strip fast path for grouped layers (G > 1, C/g > 1 or K/g > 1): KG = 1, 2, 4 or 8 output
